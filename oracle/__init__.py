@@ -1,0 +1,34 @@
+"""CPU oracle for the one-GPU share of a Dynamic Sequence Parallelism block.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports, calls or links
+this package: only the test suite, the smoke check and the CPU-baseline leg of
+the benchmark use it.  It shares no code with the HIP library and imports
+nothing from it.
+
+Everything here is plain, slow and written from the paper's definitions in
+float64 NumPy (library matmul and erf as the only primitives):
+
+* ``switch`` / ``unswitch`` / ``exchange_unpack`` -- the Switch primitive of
+  the primitive table in the Dynamic Primitives section (Eq. 10) restricted to
+  one GPU's share: a layout permute plus a pack into per-destination chunks,
+  done on raw bit patterns.
+* ``attention`` -- scaled dot-product attention, Eq. (3), applied per head
+  (Eq. 1-2) along one sequence dimension of a multi-dimensional sequence
+  (Eq. 7-8): ``spatial_attention`` over S within each frame and
+  ``temporal_attention`` over T at each location.
+* ``layernorm``, ``linear``, ``gelu`` and the composites ``st_block`` (the
+  full spatial-temporal block) and ``tiny_chain``.
+
+Pins: every function is checked in ``tests/test_oracle_pins.py`` against
+closed forms, invariants, hand-worked fixtures and brute force; see the header
+of each module for what pins it.
+"""
+from .switch import switch, unswitch, exchange_unpack, switch_index_map
+from .attention import attention, attention_rows, spatial_attention, temporal_attention, \
+    temporal_attention_strided
+from .block import layernorm, linear, gelu, st_block, tiny_chain, BLOCK_NO_MLP_LN
+
+__all__ = ["switch", "unswitch", "exchange_unpack", "switch_index_map", "attention",
+           "attention_rows", "spatial_attention", "temporal_attention",
+           "temporal_attention_strided", "layernorm", "linear", "gelu", "st_block", "tiny_chain",
+           "BLOCK_NO_MLP_LN"]

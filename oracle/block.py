@@ -1,0 +1,97 @@
+"""Oracle for the spatial-temporal transformer block (test infrastructure only).
+
+Building blocks, all float64:
+
+* ``layernorm`` -- normalisation over the hidden size, as used around every
+  sublayer (Eq. 4 and Eq. 6): (x - mean) / sqrt(var + eps) with the biased
+  variance.  The paper gives neither eps nor an affine part; the reading here
+  is eps as an argument (1e-6 by default) and no affine part.
+* ``linear`` -- y = x W (+ b) with W of shape [in, out], the x W_1 convention
+  of Eq. (5).
+* ``gelu`` -- x * Phi(x) with the exact error function.  The paper's FFN uses
+  ReLU (Eq. 5); the 720M-model block configuration uses GELU.
+* ``st_block`` -- one GPU's share of one layer of the 2D transformer (the two
+  per-dimension blocks of the model-details appendix): pre-LN spatial
+  attention with residual, the Switch T->S, pre-LN temporal attention with
+  residual, then a pre-LN GELU MLP with residual.  Output in (B, S, T, C).
+  ``BLOCK_NO_MLP_LN`` drops the LN before the MLP.
+* ``tiny_chain`` -- projection, spatial attention, output projection, switch,
+  projection, temporal attention, output projection, no LN, residual, MLP or
+  biases.
+
+Readings where the paper is silent: QKV columns ordered [Q | K | V], each C
+wide, head h at columns [h*d, (h+1)*d) of each (Eq. 1 concatenates heads in
+order); the residual stream is kept at full precision.
+
+Pinned by: hand-computed LayerNorm values and its moment identities, explicit
+loops for the linear map, GELU against the normal CDF of scipy.stats and its
+odd-part identity, and block identities (zero output projections leave only
+the switched residual; T=1 / S=1 reduce attention to the V path; the N-rank
+sharded evaluation equals the unsharded one).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+from scipy.special import erf
+
+from .attention import spatial_attention, temporal_attention
+from .switch import switch
+
+BLOCK_NO_MLP_LN = 1
+
+
+def layernorm(x: np.ndarray, eps: float = 1e-6) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + eps)
+
+
+def linear(x: np.ndarray, w: np.ndarray, b: np.ndarray | None = None) -> np.ndarray:
+    """x [..., in] times W [in, out] plus optional b [out]."""
+    y = np.matmul(np.asarray(x, dtype=np.float64), np.asarray(w, dtype=np.float64))
+    if b is not None:
+        y = y + np.asarray(b, dtype=np.float64)
+    return y
+
+
+def gelu(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    return 0.5 * x * (1.0 + erf(x / math.sqrt(2.0)))
+
+
+def _attn_sublayer(h, wqkv, bqkv, wo, bo, H, attn):
+    C = h.shape[-1]
+    qkv = linear(h, wqkv, bqkv)
+    q, k, v = qkv[..., :C], qkv[..., C:2 * C], qkv[..., 2 * C:]
+    return linear(attn(q, k, v, H), wo, bo)
+
+
+def st_block(x: np.ndarray, p: dict, H: int, eps: float = 1e-6, flags: int = 0) -> np.ndarray:
+    """x: (B, T, S, C) residual stream.  p: weights in the paper's [in, out] layout
+    (wqkv_s [C, 3C], wo_s [C, C], wqkv_t, wo_t, w1 [C, F], w2 [F, C]) and biases
+    (b*, may be None).  Returns the block output in (B, S, T, C)."""
+    x = np.asarray(x, dtype=np.float64)
+    # spatial half: attention over S inside each frame, residual
+    x = x + _attn_sublayer(layernorm(x, eps), p["wqkv_s"], p.get("bqkv_s"), p["wo_s"],
+                           p.get("bo_s"), H, spatial_attention)
+    # the Switch T -> S on one GPU (a single chunk): (B, T, S, C) -> (B, S, T, C)
+    y = switch(x, 1, 2, 1)[0]
+    # temporal half: attention over T at each location, residual
+    y = y + _attn_sublayer(layernorm(y, eps), p["wqkv_t"], p.get("bqkv_t"), p["wo_t"],
+                           p.get("bo_t"), H, temporal_attention)
+    # MLP with GELU, residual
+    h = y if (flags & BLOCK_NO_MLP_LN) else layernorm(y, eps)
+    y = y + linear(gelu(linear(h, p["w1"], p.get("b1"))), p["w2"], p.get("b2"))
+    return y
+
+
+def tiny_chain(x: np.ndarray, p: dict, H: int) -> np.ndarray:
+    """x (B, T, S, C) -> (B, S, T, C): Wqkv_s, spatial attention, Wo_s, switch,
+    Wqkv_t, temporal attention, Wo_t.  Weights in [in, out] layout."""
+    x = np.asarray(x, dtype=np.float64)
+    y = _attn_sublayer(x, p["wqkv_s"], None, p["wo_s"], None, H, spatial_attention)
+    y = switch(y, 1, 2, 1)[0]
+    return _attn_sublayer(y, p["wqkv_t"], None, p["wo_t"], None, H, temporal_attention)

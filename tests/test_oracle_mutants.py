@@ -1,0 +1,243 @@
+"""Each plausible mistake planted in the oracle (on the CPU) must make at least
+one pin fail.  This is what makes the pins worth trusting: a dropped term,
+a wrong sign, axis or index, or a transposed operand anywhere in the oracle
+is caught."""
+import math
+import sys
+import types
+
+import numpy as np
+import pytest
+
+import oracle  # noqa: F401  (loads the submodules)
+from tests import oracle_pins as P
+
+SW = sys.modules["oracle.switch"]
+AT = sys.modules["oracle.attention"]
+BL = sys.modules["oracle.block"]
+
+
+def _impl():
+    return types.SimpleNamespace(
+        switch=SW.switch, unswitch=SW.unswitch, exchange_unpack=SW.exchange_unpack,
+        index_map=SW.switch_index_map, attention=AT.attention, spatial=AT.spatial_attention,
+        temporal=AT.temporal_attention, strided=AT.temporal_attention_strided,
+        layernorm=BL.layernorm, linear=BL.linear, gelu=BL.gelu, st_block=BL.st_block,
+        tiny_chain=BL.tiny_chain)
+
+
+def _pins(i):
+    return [
+        lambda: P.pin_switch_golden(i.switch),
+        lambda: P.pin_switch_index_loops(i.switch, i.index_map),
+        lambda: P.pin_switch_round_trip(i.switch, i.unswitch),
+        lambda: P.pin_switch_b1_transpose(i.switch),
+        lambda: P.pin_switch_bits_and_copy(i.switch),
+        lambda: P.pin_switch_nrank_simulation(i.switch, i.exchange_unpack),
+        lambda: P.pin_attention_brute(i.attention),
+        lambda: P.pin_attention_l1_is_v(i.attention),
+        lambda: P.pin_attention_zero_q_mean(i.attention),
+        lambda: P.pin_attention_two_keys_closed_form(i.attention),
+        lambda: P.pin_attention_rows_stochastic(i.attention),
+        lambda: P.pin_attention_hard_max(i.attention),
+        lambda: P.pin_attention_permutations(i.attention),
+        lambda: P.pin_attention_scale_default(i.attention),
+        lambda: P.pin_spatial_temporal_units(i.spatial, i.temporal, i.strided, i.switch),
+        lambda: P.pin_layernorm(i.layernorm),
+        lambda: P.pin_linear(i.linear),
+        lambda: P.pin_gelu(i.gelu),
+        lambda: P.pin_block_identities(i.st_block, i.layernorm, i.linear, i.gelu, i.switch),
+        lambda: P.pin_block_t1_s1(i.st_block, i.layernorm, i.linear, i.gelu),
+        lambda: P.pin_block_sharded_equals_unsharded(i.st_block, i.layernorm, i.linear, i.gelu,
+                                                     i.switch, i.exchange_unpack, i.spatial,
+                                                     i.temporal),
+        lambda: P.pin_tiny_chain(i.tiny_chain, i.st_block),
+    ]
+
+
+def _n_failed():
+    failed = 0
+    for pin in _pins(_impl()):
+        try:
+            pin()
+        except Exception:
+            failed += 1
+    return failed
+
+
+# ---------------------------------------------------------------- mutants
+_orig_switch = SW.switch
+_orig_attention = AT.attention
+_orig_layernorm = BL.layernorm
+_orig_linear = BL.linear
+
+
+def sw_interleaved_chunks(x, f, t, n):
+    # chunks take every n-th index of the to-dim instead of contiguous slices
+    y = _orig_switch(x, f, t, 1)[0]
+    if f == t:
+        return y.copy()
+    B, D, F, C = y.shape
+    return np.ascontiguousarray(y.reshape(B, D // n, n, F, C).transpose(2, 0, 1, 3, 4))
+
+
+def sw_batch_outside(x, f, t, n):
+    # batch outermost: [b][n][...] instead of [n][b][...]
+    y = _orig_switch(x, f, t, n)
+    if f == t:
+        return y
+    return np.ascontiguousarray(y.transpose(1, 0, 2, 3, 4)).reshape(y.shape)
+
+
+def sw_no_transpose(x, f, t, n):
+    if f == t:
+        return x.copy()
+    B, D1, D2, C = x.shape
+    # slices the to-dim into chunks but keeps the from-dim outer inside each chunk
+    return np.ascontiguousarray(x.reshape(B, D1, n, D2 // n, C).transpose(2, 0, 1, 3, 4)
+                                .reshape(n, B, D2 // n, D1, C)) if t == 2 else _orig_switch(x, f, t, n)
+
+
+def sw_off_by_one(x, f, t, n):
+    y = _orig_switch(x, f, t, n)
+    return np.roll(y, 1, axis=3) if f != t else y
+
+
+def att_no_scale(q, k, v, scale=None):
+    return _orig_attention(q, k, v, 1.0 if scale is None else scale)
+
+
+def att_padded_scale(q, k, v, scale=None):
+    d = q.shape[-1]
+    dp = -(-d // 16) * 16 if d % 16 else d + 8
+    return _orig_attention(q, k, v, 1.0 / math.sqrt(dp) if scale is None else scale)
+
+
+def att_softmax_over_queries(q, k, v, scale=None):
+    q = np.asarray(q, float); k = np.asarray(k, float); v = np.asarray(v, float)
+    s = (1 / math.sqrt(q.shape[-1])) if scale is None else scale
+    z = np.matmul(q, np.swapaxes(k, -1, -2)) * s
+    p = np.exp(z - z.max(axis=-2, keepdims=True))
+    p = p / p.sum(axis=-2, keepdims=True)
+    return np.matmul(p, v)
+
+
+def att_k_for_v(q, k, v, scale=None):
+    if np.shape(k) != np.shape(v):
+        return _orig_attention(q, k, v, scale)
+    return _orig_attention(q, k, k, scale)
+
+
+def att_negated_scores(q, k, v, scale=None):
+    s = (1 / math.sqrt(np.shape(q)[-1])) if scale is None else scale
+    return _orig_attention(q, k, v, -s)
+
+
+def att_unnormalised(q, k, v, scale=None):
+    q = np.asarray(q, float); k = np.asarray(k, float); v = np.asarray(v, float)
+    s = (1 / math.sqrt(q.shape[-1])) if scale is None else scale
+    z = np.matmul(q, np.swapaxes(k, -1, -2)) * s
+    return np.matmul(np.exp(z - z.max(axis=-1, keepdims=True)), v)
+
+
+def ln_unbiased(x, eps=1e-6):
+    x = np.asarray(x, float)
+    return (x - x.mean(-1, keepdims=True)) / np.sqrt(x.var(-1, ddof=1, keepdims=True) + eps)
+
+
+def ln_eps_outside(x, eps=1e-6):
+    x = np.asarray(x, float)
+    return (x - x.mean(-1, keepdims=True)) / (np.sqrt(x.var(-1, keepdims=True)) + eps)
+
+
+def ln_no_centre(x, eps=1e-6):
+    x = np.asarray(x, float)
+    return x / np.sqrt(x.var(-1, keepdims=True) + eps)
+
+
+def gelu_tanh(x):
+    x = np.asarray(x, float)
+    return 0.5 * x * (1 + np.tanh(math.sqrt(2 / math.pi) * (x + 0.044715 * x ** 3)))
+
+
+def gelu_no_sqrt2(x):
+    from scipy.special import erf
+    x = np.asarray(x, float)
+    return 0.5 * x * (1 + erf(x))
+
+
+def lin_no_bias(x, w, b=None):
+    return _orig_linear(x, w, None)
+
+
+def lin_transposed(x, w, b=None):
+    w = np.asarray(w)
+    if w.shape[0] == w.shape[1]:
+        w = w.T
+    return _orig_linear(x, w, b)
+
+
+def block_wrong_axes(x, p, H, eps=1e-6, flags=0):
+    # spatial half attends over T instead of S
+    saved = BL.spatial_attention
+    BL.spatial_attention = lambda q, k, v, H_, scale=None: AT.temporal_attention_strided(q, k, v, H_, scale)
+    try:
+        return _orig_block(x, p, H, eps, flags)
+    finally:
+        BL.spatial_attention = saved
+
+
+def block_no_temporal_residual(x, p, H, eps=1e-6, flags=0):
+    saved = BL.temporal_attention
+    calls = {}
+
+    def t_attn(q, k, v, H_, scale=None):
+        return saved(q, k, v, H_, scale)
+    # drop the residual of the temporal half: subtract the switched input back out
+    y_in = BL.switch(x + BL._attn_sublayer(BL.layernorm(x, eps), p["wqkv_s"], p.get("bqkv_s"),
+                                           p["wo_s"], p.get("bo_s"), H, BL.spatial_attention),
+                     1, 2, 1)[0]
+    y = _orig_block(x, p, H, eps, flags)
+    return y - y_in
+
+
+def block_post_mlp_ln(x, p, H, eps=1e-6, flags=0):
+    y = _orig_block(x, p, H, eps, flags | BL.BLOCK_NO_MLP_LN)
+    return y
+
+
+_orig_block = BL.st_block
+
+MUTANTS = {
+    "switch: interleaved chunks": [(SW, "switch", sw_interleaved_chunks), (BL, "switch", sw_interleaved_chunks)],
+    "switch: batch outside chunks": [(SW, "switch", sw_batch_outside), (BL, "switch", sw_batch_outside)],
+    "switch: missing transpose": [(SW, "switch", sw_no_transpose), (BL, "switch", sw_no_transpose)],
+    "switch: off-by-one index": [(SW, "switch", sw_off_by_one), (BL, "switch", sw_off_by_one)],
+    "attention: no 1/sqrt(d)": [(AT, "attention", att_no_scale)],
+    "attention: padded-width scale": [(AT, "attention", att_padded_scale)],
+    "attention: softmax over queries": [(AT, "attention", att_softmax_over_queries)],
+    "attention: K used as V": [(AT, "attention", att_k_for_v)],
+    "attention: negated scores": [(AT, "attention", att_negated_scores)],
+    "attention: missing normalisation": [(AT, "attention", att_unnormalised)],
+    "layernorm: unbiased variance": [(BL, "layernorm", ln_unbiased)],
+    "layernorm: eps outside sqrt": [(BL, "layernorm", ln_eps_outside)],
+    "layernorm: no centring": [(BL, "layernorm", ln_no_centre)],
+    "gelu: tanh approximation": [(BL, "gelu", gelu_tanh)],
+    "gelu: erf(x) without 1/sqrt(2)": [(BL, "gelu", gelu_no_sqrt2)],
+    "linear: bias dropped": [(BL, "linear", lin_no_bias)],
+    "linear: square weight transposed": [(BL, "linear", lin_transposed)],
+    "block: spatial half over T": [(BL, "st_block", block_wrong_axes)],
+    "block: temporal residual dropped": [(BL, "st_block", block_no_temporal_residual)],
+    "block: no LN before the MLP": [(BL, "st_block", block_post_mlp_ln)],
+}
+
+
+def test_unmutated_oracle_passes_every_pin():
+    assert _n_failed() == 0
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    for mod, attr, fn in MUTANTS[name]:
+        monkeypatch.setattr(mod, attr, fn)
+    assert _n_failed() >= 1, f"no pin catches the planted mistake: {name}"

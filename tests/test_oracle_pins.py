@@ -1,0 +1,100 @@
+"""The oracle against its pins (CPU only)."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import attention as oatt
+from tests import oracle_pins as P
+
+
+def test_switch_golden():
+    P.pin_switch_golden(oracle.switch)
+
+
+def test_switch_index_loops():
+    P.pin_switch_index_loops(oracle.switch, oracle.switch_index_map)
+
+
+def test_switch_round_trip():
+    P.pin_switch_round_trip(oracle.switch, oracle.unswitch)
+
+
+def test_switch_b1_is_transpose():
+    P.pin_switch_b1_transpose(oracle.switch)
+
+
+def test_switch_bits_and_copy():
+    P.pin_switch_bits_and_copy(oracle.switch)
+
+
+def test_switch_nrank_simulation():
+    P.pin_switch_nrank_simulation(oracle.switch, oracle.exchange_unpack)
+
+
+def test_switch_rejects_bad_args():
+    x = np.zeros((1, 4, 6, 2), np.float32)
+    with pytest.raises(ValueError):
+        oracle.switch(x, 1, 2, 4)          # 6 % 4 != 0
+    with pytest.raises(ValueError):
+        oracle.switch(x[0], 1, 2, 1)       # not 4-D
+    with pytest.raises(ValueError):
+        oracle.switch(x, 0, 2, 1)
+
+
+@pytest.mark.parametrize("pin", [P.pin_attention_brute, P.pin_attention_l1_is_v,
+                                 P.pin_attention_zero_q_mean, P.pin_attention_two_keys_closed_form,
+                                 P.pin_attention_rows_stochastic, P.pin_attention_hard_max,
+                                 P.pin_attention_permutations, P.pin_attention_scale_default])
+def test_attention(pin):
+    pin(oracle.attention)
+
+
+def test_spatial_temporal_units():
+    P.pin_spatial_temporal_units(oracle.spatial_attention, oracle.temporal_attention,
+                                 oracle.temporal_attention_strided, oracle.switch)
+
+
+def test_layernorm():
+    P.pin_layernorm(oracle.layernorm)
+
+
+def test_linear():
+    P.pin_linear(oracle.linear)
+
+
+def test_gelu():
+    P.pin_gelu(oracle.gelu)
+
+
+def test_block_identities():
+    P.pin_block_identities(oracle.st_block, oracle.layernorm, oracle.linear, oracle.gelu,
+                           oracle.switch)
+
+
+def test_block_t1_s1():
+    P.pin_block_t1_s1(oracle.st_block, oracle.layernorm, oracle.linear, oracle.gelu)
+
+
+def test_block_sharded_equals_unsharded():
+    P.pin_block_sharded_equals_unsharded(oracle.st_block, oracle.layernorm, oracle.linear,
+                                         oracle.gelu, oracle.switch, oracle.exchange_unpack,
+                                         oracle.spatial_attention, oracle.temporal_attention)
+
+
+def test_tiny_chain():
+    P.pin_tiny_chain(oracle.tiny_chain, oracle.st_block)
+
+
+def test_block_no_mlp_ln_flag():
+    rng = np.random.default_rng(3)
+    C, F, H = 8, 8, 2
+    x = rng.standard_normal((1, 2, 3, C))
+    p = {n: rng.standard_normal(s) * 0.3 for n, s in
+         (("wqkv_s", (C, 3 * C)), ("wo_s", (C, C)), ("wqkv_t", (C, 3 * C)), ("wo_t", (C, C)),
+          ("w1", (C, F)), ("w2", (F, C)))}
+    a = oracle.st_block(x, p, H)
+    b = oracle.st_block(x, p, H, flags=oracle.BLOCK_NO_MLP_LN)
+    zc = np.zeros((F, C))
+    base = oracle.st_block(x, dict(p, w2=zc), H)
+    assert np.allclose(b, base + oracle.linear(oracle.gelu(oracle.linear(base, p["w1"])), p["w2"]))
+    assert not np.allclose(a, b)
