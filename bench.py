@@ -1,0 +1,249 @@
+#!/usr/bin/env python3
+"""Benchmark of one GPU's share of a DSP spatial-temporal block on MI355X.
+
+One step is one pass over the whole hot path, each piece at its own synthetic
+workload (video-latent shapes of the 720M model: C=1152, 16 heads of 72):
+
+  switch    dsp_switch of a 1 x 64 x 4096 x 1152 bf16 T-shard into 8 chunks
+  spatial   dsp_spatial_attn,  B=2, T=16,  S=4096 (attention over S)
+  temporal  dsp_temporal_attn, B=2, S=512, T=128  (attention over T)
+  block     dsp_st_block_forward, B=1, T=32, S=1024, MLP 4608 (LN, QKV,
+            spatial attention, out-proj, switch, LN, QKV, temporal attention,
+            out-proj, LN, MLP with GELU, residuals)
+
+The headline value is the combined attention throughput
+(F_spatial + F_temporal) / (t_spatial + t_temporal) in TFLOP/s with
+F = 4 L^2 D per (unit) -- useful flops only, no padding, no softmax.  The
+switch is reported in GB/s of bytes read + written.  Per-kernel times are HIP
+events recorded on the stream the kernels run on, averaged over the timed
+steps.  Inputs are resident in HBM before timing starts.
+
+Prints ONE JSON line.  Only one GPU is used; --gpus N with N > 1 exits.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0           # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+
+METRIC = "spatial+temporal attn TFLOP/s (% MFMA peak); dsp_switch GB/s (% HBM peak)"
+
+
+def attn_flops(units: int, L: int, D: int) -> float:
+    return 4.0 * units * L * L * D
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0,
+                    help="approximate seconds of oracle work for the CPU baseline")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file with measured HBM bytes per launch of the spatial kernel")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the inter-GPU exchange of the switch is out of scope)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2403_10266_amd as dsp
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    def to_dev(a, dt):
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+        return (t.to(torch.bfloat16) if dt == "bf16" else t).to(dev)
+
+    W = synth.WORKLOADS
+    # ---- inputs (seeded, synthetic), resident in HBM
+    ws = W["switch_bf16_T64_S4096"]
+    x_sw = to_dev(synth.switch_input(ws), "bf16")
+    y_sw = torch.empty((ws.n_chunks, ws.B, ws.S // ws.n_chunks, ws.T, ws.C), dtype=torch.bfloat16, device=dev)
+
+    wsp = W["spatial_bf16_B2_T16_S4096"]
+    q_sp, k_sp, v_sp = (to_dev(a, "bf16") for a in synth.qkv_inputs(wsp, "BTSC"))
+    o_sp = torch.empty_like(q_sp)
+
+    wtp = W["temporal_bf16_B2_S512_T128"]
+    q_tp, k_tp, v_tp = (to_dev(a, "bf16") for a in synth.qkv_inputs(wtp, "BSTC"))
+    o_tp = torch.empty_like(q_tp)
+
+    wbl = W["block_bf16_B1_T32_S1024"]
+    x_bl_np, p_bl = synth.block_inputs(wbl)
+    x_bl = to_dev(x_bl_np, "f32")
+    w_bl = {n: (None if v is None else to_dev(v, "bf16")) for n, v in p_bl.items()}
+    y_bl = torch.empty((wbl.B, wbl.S, wbl.T, wbl.C), dtype=torch.float32, device=dev)
+    ws_bytes = dsp.block_workspace_bytes(wbl.B, wbl.T, wbl.S, wbl.C, wbl.H, wbl.F, dsp.DSP_BF16)
+    ws_bl = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    del x_bl_np, p_bl
+    torch.cuda.synchronize()
+
+    def run_switch():
+        dsp.dsp_switch(x_sw, 1, 2, ws.n_chunks, out=y_sw)
+
+    def run_spatial():
+        dsp.dsp_spatial_attn(q_sp, k_sp, v_sp, wsp.H, out=o_sp)
+
+    def run_temporal():
+        dsp.dsp_temporal_attn(q_tp, k_tp, v_tp, wtp.H, out=o_tp)
+
+    def run_block():
+        dsp.dsp_st_block_forward(x_bl, w_bl, wbl.H, out=y_bl, workspace=ws_bl)
+
+    parts = [("switch", run_switch), ("spatial", run_spatial), ("temporal", run_temporal),
+             ("block", run_block)]
+
+    for _ in range(args.warmup):
+        for _, fn in parts:
+            fn()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(parts) + 1)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(K):
+        ev[s][0].record(stream)
+        for i, (_, fn) in enumerate(parts):
+            fn()
+            ev[s][i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = {name: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(K)]))
+          for i, (name, _) in enumerate(parts)}
+
+    # ---- accounting
+    sw_bytes = 2.0 * x_sw.numel() * x_sw.element_size()
+    F_sp = attn_flops(wsp.B * wsp.T * wsp.H, wsp.S, wsp.D)
+    F_tp = attn_flops(wtp.B * wtp.S * wtp.H, wtp.T, wtp.D)
+    tp_bytes = 4.0 * q_tp.numel() * 2
+    sp_bytes = 4.0 * q_sp.numel() * 2
+    tok = wbl.B * wbl.T * wbl.S
+    C, F = wbl.C, wbl.F
+    F_bl = (2.0 * tok * C * (3 * C) * 2 + 2.0 * tok * C * C * 2 + 2.0 * tok * C * F * 2
+            + attn_flops(wbl.B * wbl.T * wbl.H, wbl.S, wbl.D) + attn_flops(wbl.B * wbl.S * wbl.H, wbl.T, wbl.D))
+
+    sp_tflops = F_sp / (ms["spatial"] * 1e-3) / 1e12
+    tp_tflops = F_tp / (ms["temporal"] * 1e-3) / 1e12
+    attn_tflops = (F_sp + F_tp) / ((ms["spatial"] + ms["temporal"]) * 1e-3) / 1e12
+    sw_gbps = sw_bytes / (ms["switch"] * 1e-3) / 1e9
+    tp_gbps = tp_bytes / (ms["temporal"] * 1e-3) / 1e9
+
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            traffic = json.load(f).get("spatial_bytes_per_launch")
+
+    out = {
+        "metric": METRIC,
+        "value": round(attn_tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / K, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "dsp_switch 1x64x4096x1152 bf16 -> 8 chunks; spatial attn B2 T16 S4096 H16 D72; "
+                        "temporal attn B2 S512 T128 H16 D72; ST block B1 T32 S1024 C1152 H16 F4608",
+            "attn_frac_mfma_peak": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "switch_GBps": round(sw_gbps, 1),
+            "switch_frac_hbm_peak": round(sw_gbps / HBM_PEAK_GBPS, 4),
+            "spatial_TFLOPs": round(sp_tflops, 2),
+            "temporal_TFLOPs": round(tp_tflops, 2),
+            "temporal_GBps": round(tp_gbps, 1),
+            "temporal_frac_hbm_peak": round(tp_gbps / HBM_PEAK_GBPS, 4),
+            "block_TFLOPs": round(F_bl / (ms["block"] * 1e-3) / 1e12, 2),
+            "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
+        },
+        "roofline": {
+            "kernel": "spatial attention (attn_fwd_kernel<72,4,2>)",
+            "bound": "mfma",
+            "achieved": round(sp_tflops, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(sp_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(budget_s: float) -> dict:
+    """The fp64 oracle on this host's cores, on a bounded sample of the same
+    attention workloads (independent units, so throughput is per-unit exact)."""
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    W = synth.WORKLOADS
+    wsp, wtp = W["spatial_bf16_B2_T16_S4096"], W["temporal_bf16_B2_S512_T128"]
+    rng = np.random.default_rng(0)
+    D = wsp.D
+
+    def unit_set(w, L, n):
+        g = synth.rng(w.seed)
+        q = synth.bf16_round(synth.normal_f32(g, (n, L, D))).astype(np.float64)
+        k = synth.bf16_round(synth.normal_f32(g, (n, L, D))).astype(np.float64)
+        v = synth.bf16_round(synth.normal_f32(g, (n, L, D))).astype(np.float64)
+        return q, k, v
+
+    # spatial: whole units of L = 4096, as many as fit in half the budget
+    t_sp = f_sp = 0.0
+    n_sp = 0
+    q, k, v = unit_set(wsp, wsp.S, 1)
+    while t_sp < budget_s / 2 and n_sp < 64:
+        t0 = time.perf_counter()
+        oracle.attention(q[0], k[0], v[0])
+        t_sp += time.perf_counter() - t0
+        f_sp += attn_flops(1, wsp.S, D)
+        n_sp += 1
+    # temporal: batches of 256 units of L = 128
+    t_tp = f_tp = 0.0
+    n_tp = 0
+    q, k, v = unit_set(wtp, wtp.T, 256)
+    while t_tp < budget_s / 2 and n_tp < 16384:
+        t0 = time.perf_counter()
+        oracle.attention(q, k, v)
+        t_tp += time.perf_counter() - t0
+        f_tp += attn_flops(256, wtp.T, D)
+        n_tp += 256
+    return {
+        "value": round((f_sp + f_tp) / (t_sp + t_tp) / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"fp64 NumPy oracle attention: {n_sp} of 512 spatial units (L=4096, D=72) and "
+                  f"{n_tp} of 16384 temporal units (L=128, D=72), same 4*L^2*D accounting; "
+                  f"{t_sp + t_tp:.1f} s of host time",
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * dsp.h -- C ABI of libdsp: one GPU's share of a Dynamic Sequence Parallelism
+ * (DSP) spatial-temporal transformer block on AMD MI355X (gfx950).
+ *
+ * The operations follow "DSP: Dynamic Sequence Parallelism for
+ * Multi-Dimensional Transformers" (Zhao et al., ICML 2025):
+ *   - the Switch primitive (primitive table, row s_i -> s_j; Eq. 10), here
+ *     the local permute + pack of one GPU's shard that precedes the exchange;
+ *   - scaled dot-product attention (Eq. 3), per head (Eq. 1-2), run along one
+ *     sequence dimension of a multi-dimensional sequence (Eq. 7-8): spatial
+ *     attention over S inside each frame, temporal attention over T at each
+ *     spatial location;
+ *   - the LayerNorm (Eq. 4, 6), linear maps and MLP (Eq. 5) of the block.
+ *
+ * Conventions shared by every entry point
+ *   - All tensor arguments are DEVICE pointers owned by the caller.  The
+ *     library allocates nothing, keeps no pointer after returning and holds no
+ *     mutable global state; calls are thread-safe.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t passed as an
+ *     opaque pointer; NULL means the default stream).  Device faults surface at
+ *     the caller's next synchronisation.
+ *   - Arguments are validated on the host before anything is launched; a
+ *     failed check returns a nonzero dsp_status_t and launches nothing.  A
+ *     launch failure returns DSP_ERR_HIP.  No C++ exception crosses the ABI.
+ *   - Tensors are dense row-major.  Sequence tensors are [B, S_1, S_2, C]
+ *     (C innermost); dimension numbers follow that order: 0 = batch,
+ *     1 and 2 = the two sequence dimensions, 3 = hidden.
+ *   - Weights of linear maps are stored [out][in] (row-major, the reduction
+ *     index contiguous), i.e. y = x * W with W = stored^T.
+ */
+#ifndef DSP_H_
+#define DSP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DSP_OK = 0,
+  DSP_ERR_NULL = 1,      /* a required pointer is NULL */
+  DSP_ERR_DIM = 2,       /* bad ndim or dimension index */
+  DSP_ERR_SHAPE = 3,     /* nonpositive / non-divisible / unsupported size */
+  DSP_ERR_DTYPE = 4,     /* unknown or unsupported dtype */
+  DSP_ERR_ALIGN = 5,     /* pointer or stride alignment the kernel requires */
+  DSP_ERR_HIP = 6,       /* a HIP runtime call or kernel launch failed */
+  DSP_ERR_WORKSPACE = 7, /* workspace missing or too small */
+  DSP_ERR_ARG = 8        /* any other invalid argument (flags, eps, ...) */
+} dsp_status_t;
+
+typedef enum { DSP_F32 = 0, DSP_BF16 = 1 } dsp_dtype_t;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* dsp_status_str(int status);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int dsp_version(void);
+
+/* ------------------------------------------------------------------------
+ * dsp_switch -- one GPU's share of DynamicSwitch(X, i, j)
+ * (primitive table, row s_i -> s_j; Eq. 10; system overview figure).
+ *
+ * x:      [B, D1, D2, C] (ndim must be 4: two sequence dimensions), the local
+ *         shard, currently sharded on `from_dim`.
+ * y:      output, same number of elements as x, written as `n_chunks`
+ *         contiguous per-destination chunks.  With from_dim=1, to_dim=2:
+ *             y[n][b][j'][i][c] = x[b][i][n*D2/n_chunks + j'][c]
+ *         (chunk n has shape [B, D2/n_chunks, D1, C]: the to-dim slice
+ *         outermost, the from-dim -- the dimension the next stage computes
+ *         over -- innermost before C).  With from_dim=2, to_dim=1:
+ *             y[n][b][i'][j][c] = x[b][n*D1/n_chunks + i'][j][c].
+ *         For (B,T,S,C) with T sharded, from=1 (T), to=2 (S) and n_chunks=1
+ *         this is the permute to (B,S,T,C).  Chunk n is what rank n receives
+ *         in the all-to-all; the exchange itself is not part of this call.
+ * from_dim == to_dim is the "no primitive" row of the table: y = copy of x.
+ * Errors: DSP_ERR_NULL (x, y or shape NULL), DSP_ERR_DIM (ndim != 4 or a dim
+ *   not in {1,2}), DSP_ERR_SHAPE (a size < 0, n_chunks < 1, the to-dim not
+ *   divisible by n_chunks, or more than 2^31 rows / 16-byte vectors),
+ *   DSP_ERR_DTYPE, DSP_ERR_ARG (x and y overlap).  A tensor with a zero size
+ *   is accepted and launches nothing.
+ * The data are moved as raw bits (bit-exact for any payload, NaNs included).
+ * ------------------------------------------------------------------------ */
+int dsp_switch(const void* x, void* y, const int64_t* shape, int ndim, int from_dim, int to_dim,
+               int n_chunks, int dtype, void* stream);
+
+/* Same as dsp_switch with an explicit kernel choice: 0 = automatic,
+ * 1 = direct 128-bit row copy (requires 16-byte aligned pointers and rows),
+ * 2 = LDS-staged tile transpose.  Any other value -> DSP_ERR_ARG. */
+int dsp_switch_variant(const void* x, void* y, const int64_t* shape, int ndim, int from_dim,
+                       int to_dim, int n_chunks, int dtype, int variant, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Attention along one sequence dimension (Eq. 3 per head, Eq. 1-2; the
+ * per-dimension reshape of Eq. 7-8).  Non-causal softmax(q k^T * scale) v.
+ *
+ * dsp_spatial_attn:  q, k, v, o laid out (B, T, S, *), attention over L = S
+ *   inside each (b, t) frame, independently per head h.
+ * dsp_temporal_attn: q, k, v, o laid out (B, S, T, *), attention over L = T at
+ *   each (b, s) location, independently per head.
+ *
+ * Head h of a token occupies elements [h*D, (h+1)*D) of that token's row.
+ * ld_in:  elements between consecutive token rows of q, k and v (C = H*D for
+ *         separate tensors, 3C when q/k/v point into one packed [Q|K|V] buffer).
+ * ld_out: elements between consecutive token rows of o (>= H*D).
+ * scale:  softmax scale; scale <= 0 selects 1/sqrt(D) with the true D.
+ * dtype:  DSP_BF16 (bf16 storage, bf16 MFMA, fp32 softmax and accumulation)
+ *         or DSP_F32 (fp32 storage and fp32 arithmetic throughout).
+ * Supported D: DSP_BF16 -- D in {16, 32, 64, 72, 80, 96}; DSP_F32 --
+ *   1 <= D <= 256.  bf16 needs 16-byte aligned q/k/v/o and ld_in, ld_out
+ *   multiples of 8 (DSP_ERR_ALIGN otherwise).
+ * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE (a size < 1, H*D > ld, unsupported D),
+ *   DSP_ERR_DTYPE, DSP_ERR_ALIGN, DSP_ERR_HIP.  An empty batch (B, T or S
+ *   equal to 0) is accepted and launches nothing.
+ * ------------------------------------------------------------------------ */
+int dsp_spatial_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t T,
+                     int64_t S, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
+                     int dtype, void* stream);
+int dsp_temporal_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t S,
+                      int64_t T, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
+                      int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * dsp_layernorm -- per-row normalisation over C (Eq. 4, 6):
+ *   y = (x - mean) / sqrt(var + eps), biased variance, no affine part,
+ *   statistics in fp32.
+ * x: [rows, C] of x_dtype; y: [rows, C] of y_dtype (DSP_F32 or DSP_BF16).
+ * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE (rows < 0, C < 1), DSP_ERR_DTYPE,
+ *   DSP_ERR_ARG (eps < 0 or not finite).
+ * ------------------------------------------------------------------------ */
+int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows, int C, float eps,
+                  void* stream);
+
+/* ------------------------------------------------------------------------
+ * dsp_linear -- out = epilogue(a * W + bias)  (Eq. 1 W^O, Eq. 5 W_1/W_2)
+ *
+ * a:        [M, K] of dtype.
+ * w:        [N, K] of dtype (stored [out][in]).
+ * bias:     [N] of dtype, or NULL.
+ * residual: [M, N] fp32 or NULL; required iff DSP_EPI_RESID.  May equal out.
+ * out:      [M, N]; dtype for DSP_EPI_NONE / DSP_EPI_GELU, fp32 for
+ *           DSP_EPI_F32 (out = a*W + bias) and DSP_EPI_RESID
+ *           (out = residual + a*W + bias).
+ * epilogue: DSP_EPI_NONE, DSP_EPI_GELU (exact-erf GELU: x*Phi(x)),
+ *           DSP_EPI_RESID, DSP_EPI_F32.
+ * dtype:    DSP_BF16 (bf16 MFMA, fp32 accumulation) or DSP_F32 (fp32 FMA).
+ * bf16 needs K % 8 == 0 and 16-byte aligned a, w, out and residual
+ * (DSP_ERR_ALIGN).  out must not overlap a, w or bias.
+ * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE (M < 0, N < 1, K < 1), DSP_ERR_DTYPE,
+ *   DSP_ERR_ALIGN, DSP_ERR_ARG (unknown epilogue, residual missing).
+ * ------------------------------------------------------------------------ */
+enum { DSP_EPI_NONE = 0, DSP_EPI_GELU = 1, DSP_EPI_RESID = 2, DSP_EPI_F32 = 3 };
+int dsp_linear(const void* a, const void* w, const void* bias, const float* residual, void* out,
+               int64_t M, int N, int K, int epilogue, int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * The spatial-temporal block: one GPU's share of one layer of the 2D
+ * transformer of the model-details appendix (a spatial block, then a temporal
+ * block), with one Switch between them.
+ *
+ *   x  += Wo_s * SpatialAttn(LN(x) * Wqkv_s)          x in (B,T,S,C)
+ *   y   = Switch_{T->S}(x)                             y in (B,S,T,C)
+ *   y  += Wo_t * TemporalAttn(LN(y) * Wqkv_t)
+ *   y  += W2 * GELU(LN(y) * W1)
+ *
+ * Weights (dtype, stored [out][in]): wqkv_* [3C][C] with output columns
+ * [Q | K | V], wo_* [C][C], w1 [F][C], w2 [C][F]; biases ([out], dtype) may be
+ * NULL.  x_BTSC and y_BSTC are fp32 (the residual stream); they must not
+ * overlap.  Flags:
+ *   DSP_BLOCK_NO_MLP_LN -- no LayerNorm before the MLP;
+ *   DSP_BLOCK_ATTN_ONLY -- projections and attention only: no LayerNorm, no
+ *     residual adds and no MLP (w1/w2 unused):
+ *       y = Wo_t * TemporalAttn(Switch(Wo_s * SpatialAttn(x * Wqkv_s)) * Wqkv_t).
+ * workspace: device buffer of at least dsp_st_block_workspace_bytes(...)
+ * bytes, 256-byte aligned, owned by the caller; contents are scratch.
+ * dsp_st_block_workspace_bytes returns 0 for invalid sizes.
+ * Errors: those of the pieces plus DSP_ERR_WORKSPACE and DSP_ERR_ARG.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  const void *wqkv_s, *bqkv_s, *wo_s, *bo_s;
+  const void *wqkv_t, *bqkv_t, *wo_t, *bo_t;
+  const void *w1, *b1, *w2, *b2;
+} dsp_block_weights_t;
+
+enum { DSP_BLOCK_NO_MLP_LN = 1, DSP_BLOCK_ATTN_ONLY = 2 };
+
+size_t dsp_st_block_workspace_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F,
+                                    int dtype);
+int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_weights_t* w,
+                         void* workspace, size_t ws_bytes, int64_t B, int64_t T, int64_t S, int C,
+                         int H, int F, float ln_eps, int flags, int dtype, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSP_H_ */

@@ -1,0 +1,243 @@
+"""Python binding of libdsp: one GPU's share of a Dynamic Sequence Parallelism
+spatial-temporal block on MI355X.
+
+Argument marshalling only.  Every computation runs in the HIP kernels of
+``libdsp.so`` (built in-tree by ``paper_2403_10266_amd.build``); this module
+turns torch tensors into device pointers, sizes and the current HIP stream,
+calls the C entry point of the same name and raises ``DspError`` on a nonzero
+status.  There is no fallback: if the library is missing, importing the
+binding's functions raises.
+
+Entry points (see ``include/dsp.h`` for the exact contracts):
+``dsp_switch``, ``dsp_spatial_attn``, ``dsp_temporal_attn``,
+``dsp_layernorm``, ``dsp_linear``, ``dsp_st_block_forward``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from pathlib import Path
+
+_PKG = Path(__file__).resolve().parent
+LIB_PATH = _PKG / "libdsp.so"
+
+# status codes and enums of include/dsp.h
+DSP_OK, DSP_ERR_NULL, DSP_ERR_DIM, DSP_ERR_SHAPE, DSP_ERR_DTYPE, DSP_ERR_ALIGN, DSP_ERR_HIP, \
+    DSP_ERR_WORKSPACE, DSP_ERR_ARG = range(9)
+DSP_F32, DSP_BF16 = 0, 1
+DSP_EPI_NONE, DSP_EPI_GELU, DSP_EPI_RESID, DSP_EPI_F32 = 0, 1, 2, 3
+DSP_BLOCK_NO_MLP_LN, DSP_BLOCK_ATTN_ONLY = 1, 2
+
+BLOCK_WEIGHT_FIELDS = ("wqkv_s", "bqkv_s", "wo_s", "bo_s", "wqkv_t", "bqkv_t", "wo_t", "bo_t",
+                       "w1", "b1", "w2", "b2")
+
+
+class DspError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} (status {status})")
+
+
+class BlockWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_WEIGHT_FIELDS]
+
+
+_lib = None
+
+_c = ctypes
+_P, _I, _I64, _F, _SZ = _c.c_void_p, _c.c_int, _c.c_int64, _c.c_float, _c.c_size_t
+_SIGNATURES = {
+    "dsp_status_str": (_c.c_char_p, [_I]),
+    "dsp_version": (_I, []),
+    "dsp_switch": (_I, [_P, _P, _c.POINTER(_I64), _I, _I, _I, _I, _I, _P]),
+    "dsp_switch_variant": (_I, [_P, _P, _c.POINTER(_I64), _I, _I, _I, _I, _I, _I, _P]),
+    "dsp_spatial_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
+    "dsp_temporal_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
+    "dsp_layernorm": (_I, [_P, _I, _P, _I, _I64, _I, _F, _P]),
+    "dsp_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
+    "dsp_st_block_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
+    "dsp_st_block_forward": (_I, [_P, _P, _c.POINTER(BlockWeights), _P, _SZ, _I64, _I64, _I64, _I,
+                                  _I, _I, _F, _I, _I, _P]),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libdsp.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not LIB_PATH.exists():
+            raise RuntimeError(f"libdsp.so not found at {LIB_PATH}; build it with "
+                               "`python -m paper_2403_10266_amd.build`")
+        L = ctypes.CDLL(str(LIB_PATH))
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_str(status: int) -> str:
+    return lib().dsp_status_str(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != DSP_OK:
+        raise DspError(status, where)
+
+
+# --------------------------------------------------------------------------- torch marshalling
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return DSP_F32
+    if t.dtype == torch.bfloat16:
+        return DSP_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _require_device(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("libdsp operates on device tensors only")
+
+
+def dsp_switch(x, from_dim: int, to_dim: int, n_chunks: int, out=None, variant: int = 0,
+               stream=None):
+    """Permute + pack of a [B, D1, D2, C] shard (see dsp.h).  Returns ``out`` as a
+    tensor of shape [n_chunks, B, D_to/n_chunks, D_from, C] (or x's shape when
+    from_dim == to_dim)."""
+    torch = _torch()
+    _require_device(x)
+    if x.dim() != 4:
+        raise ValueError("x must be [B, D1, D2, C]")
+    x = x.contiguous()
+    B, D1, D2, C = x.shape
+    if from_dim == to_dim:
+        oshape = tuple(x.shape)
+    else:
+        d_to, d_from = (D2, D1) if to_dim == 2 else (D1, D2)
+        oshape = (n_chunks, B, d_to // max(n_chunks, 1), d_from, C)
+    if out is None:
+        out = torch.empty(oshape, dtype=x.dtype, device=x.device)
+    shape = (ctypes.c_int64 * 4)(B, D1, D2, C)
+    st = lib().dsp_switch_variant(_ptr(x), _ptr(out), shape, 4, from_dim, to_dim, n_chunks,
+                                  _dtype_code(x), variant, _stream(stream))
+    _check(st, "dsp_switch")
+    return out
+
+
+def _attn(name, q, k, v, B, X, L, H, out, ld_in, ld_out, scale, stream, C):
+    torch = _torch()
+    _require_device(q, k, v, out)
+    D = C // H
+    if out is None:
+        out = torch.empty((B, X, L, C), dtype=q.dtype, device=q.device)
+    fn = getattr(lib(), name)
+    st = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, X, L, H, D, ld_in, ld_out, float(scale),
+            _dtype_code(q), _stream(stream))
+    _check(st, name)
+    return out
+
+
+def dsp_spatial_attn(q, k, v, H: int, out=None, scale: float = 0.0, C: int | None = None,
+                     ld_in: int | None = None, ld_out: int | None = None, stream=None):
+    """Attention over S within each frame.  q, k, v: (B, T, S, ld_in) views whose
+    first C = H*D columns hold the heads (pass C explicitly for packed QKV views)."""
+    B, T, S = q.shape[0], q.shape[1], q.shape[2]
+    C = C if C is not None else q.shape[3]
+    ld_in = ld_in if ld_in is not None else q.stride(2)
+    ld_out = ld_out if ld_out is not None else (out.stride(2) if out is not None else C)
+    return _attn("dsp_spatial_attn", q, k, v, B, T, S, H, out, ld_in, ld_out, scale, stream, C)
+
+
+def dsp_temporal_attn(q, k, v, H: int, out=None, scale: float = 0.0, C: int | None = None,
+                      ld_in: int | None = None, ld_out: int | None = None, stream=None):
+    """Attention over T at each spatial location.  q, k, v: (B, S, T, ld_in) views."""
+    B, S, T = q.shape[0], q.shape[1], q.shape[2]
+    C = C if C is not None else q.shape[3]
+    ld_in = ld_in if ld_in is not None else q.stride(2)
+    ld_out = ld_out if ld_out is not None else (out.stride(2) if out is not None else C)
+    return _attn("dsp_temporal_attn", q, k, v, B, S, T, H, out, ld_in, ld_out, scale, stream, C)
+
+
+def dsp_layernorm(x, eps: float = 1e-6, out=None, out_dtype=None, stream=None):
+    torch = _torch()
+    _require_device(x, out)
+    x = x.contiguous()
+    C = x.shape[-1]
+    rows = x.numel() // C
+    if out is None:
+        out = torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    st = lib().dsp_layernorm(_ptr(x), _dtype_code(x), _ptr(out), _dtype_code(out), rows, C,
+                             float(eps), _stream(stream))
+    _check(st, "dsp_layernorm")
+    return out
+
+
+def dsp_linear(a, w, bias=None, residual=None, epilogue: int = DSP_EPI_NONE, out=None,
+               stream=None):
+    """out = epilogue(a @ w.T + bias); w stored [N, K]."""
+    torch = _torch()
+    _require_device(a, w, bias, residual, out)
+    a = a.contiguous()
+    K = a.shape[-1]
+    M = a.numel() // K
+    N = w.shape[0]
+    if out is None:
+        odt = torch.float32 if epilogue in (DSP_EPI_RESID, DSP_EPI_F32) else a.dtype
+        out = torch.empty((*a.shape[:-1], N), dtype=odt, device=a.device)
+    st = lib().dsp_linear(_ptr(a), _ptr(w), _ptr(bias), _ptr(residual), _ptr(out), M, N, K,
+                          epilogue, _dtype_code(a), _stream(stream))
+    _check(st, "dsp_linear")
+    return out
+
+
+def block_workspace_bytes(B, T, S, C, H, F, dtype_code) -> int:
+    return int(lib().dsp_st_block_workspace_bytes(B, T, S, C, H, F, dtype_code))
+
+
+def dsp_st_block_forward(x, weights: dict, H: int, eps: float = 1e-6, flags: int = 0,
+                         out=None, workspace=None, dtype=None, stream=None):
+    """One spatial-temporal block on x (B, T, S, C) fp32; returns (B, S, T, C) fp32.
+    ``weights`` maps the dsp_block_weights_t field names to device tensors (or None)."""
+    torch = _torch()
+    _require_device(x, out, workspace, *weights.values())
+    B, T, S, C = x.shape
+    wdt = weights["wqkv_s"].dtype
+    code = DSP_BF16 if (dtype or wdt) == torch.bfloat16 else DSP_F32
+    F = weights["w1"].shape[0] if weights.get("w1") is not None else 0
+    if out is None:
+        out = torch.empty((B, S, T, C), dtype=torch.float32, device=x.device)
+    need = block_workspace_bytes(B, T, S, C, H, F, code)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    wt = BlockWeights(**{n: (weights[n].data_ptr() if weights.get(n) is not None else None)
+                         for n in BLOCK_WEIGHT_FIELDS})
+    st = lib().dsp_st_block_forward(_ptr(x), _ptr(out), ctypes.byref(wt), _ptr(workspace),
+                                    workspace.numel(), B, T, S, C, H, F, float(eps), flags, code,
+                                    _stream(stream))
+    _check(st, "dsp_st_block_forward")
+    return out
+
+
+__all__ = ["lib", "status_str", "DspError", "BlockWeights", "dsp_switch", "dsp_spatial_attn",
+           "dsp_temporal_attn", "dsp_layernorm", "dsp_linear", "dsp_st_block_forward",
+           "block_workspace_bytes", "LIB_PATH"]

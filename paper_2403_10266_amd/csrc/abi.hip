@@ -1,0 +1,300 @@
+// C ABI of libdsp: host-side argument validation and launches on the caller's
+// stream.  Every entry point validates all of its arguments before it enqueues
+// anything, so a nonzero status means nothing was launched (except
+// DSP_ERR_HIP from a launch, or from a later step of the block composite).
+#include <math.h>
+#include <string.h>
+
+#include "dsp_internal.h"
+
+using namespace dsp;
+
+namespace {
+
+constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
+
+bool valid_dtype(int dt) { return dt == DSP_F32 || dt == DSP_BF16; }
+int elem_size(int dt) { return dt == DSP_F32 ? 4 : 2; }
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+  return na && nb && pa < pb + nb && pb < pa + na;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+int switch_impl(const void* x, void* y, const int64_t* shape, int ndim, int from_dim, int to_dim,
+                int n_chunks, int dtype, int variant, void* stream) {
+  if (!x || !y || !shape) return DSP_ERR_NULL;
+  if (ndim != 4) return DSP_ERR_DIM;
+  if (from_dim < 1 || from_dim > 2 || to_dim < 1 || to_dim > 2) return DSP_ERR_DIM;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (variant < 0 || variant > 2) return DSP_ERR_ARG;
+  const int64_t B = shape[0], D1 = shape[1], D2 = shape[2], C = shape[3];
+  if (B < 0 || D1 < 0 || D2 < 0 || C < 0 || n_chunks < 1) return DSP_ERR_SHAPE;
+  const int64_t d_to = to_dim == 2 ? D2 : D1;
+  if (from_dim != to_dim && d_to % n_chunks != 0) return DSP_ERR_SHAPE;
+  int64_t rows, elems, bytes;
+  if (!mul_ok(B, D1, &rows) || !mul_ok(rows, D2, &rows) || !mul_ok(rows, C, &elems) ||
+      !mul_ok(elems, elem_size(dtype), &bytes))
+    return DSP_ERR_SHAPE;
+  if (overlap(x, (size_t)bytes, y, (size_t)bytes)) return DSP_ERR_ARG;
+  if (bytes == 0) return DSP_OK;
+  const int64_t row_bytes = C * elem_size(dtype);
+  const bool rows_ok = row_bytes % 16 == 0 && aligned(x, 16) && aligned(y, 16);
+  if (variant == 1 && !rows_ok) return DSP_ERR_ALIGN;
+  const bool use_rows = variant == 1 || (variant == 0 && rows_ok && row_bytes >= 64);
+  hipStream_t s = as_stream(stream);
+  if (use_rows) return launch_switch_rows(x, y, B, D1, D2, row_bytes, from_dim, to_dim, n_chunks, s);
+  return launch_switch_tiles(x, y, B, D1, D2, C, elem_size(dtype), from_dim, to_dim, n_chunks, s);
+}
+
+int attn_impl(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X, int64_t L,
+              int H, int D, int64_t ld_in, int64_t ld_out, float scale, int dtype, void* stream,
+              bool spatial) {
+  if (!q || !k || !v || !o) return DSP_ERR_NULL;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
+  if ((int64_t)H * D > ld_in || (int64_t)H * D > ld_out) return DSP_ERR_SHAPE;
+  if (isnan(scale) || isinf(scale)) return DSP_ERR_ARG;
+  if (dtype == DSP_BF16) {
+    if (!attn_bf16_supports(D)) return DSP_ERR_SHAPE;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return DSP_ERR_ALIGN;
+    if (ld_in % 8 || ld_out % 8) return DSP_ERR_ALIGN;
+  } else if (D > 256) {
+    return DSP_ERR_SHAPE;
+  }
+  int64_t tokens;
+  if (!mul_ok(B, X, &tokens) || !mul_ok(tokens, L, &tokens)) return DSP_ERR_SHAPE;
+  int64_t span_in, span_out;
+  if (!mul_ok(tokens, ld_in, &span_in) || !mul_ok(tokens, ld_out, &span_out)) return DSP_ERR_SHAPE;
+  if (tokens == 0) return DSP_OK;
+  AttnArgs a;
+  a.q = q; a.k = k; a.v = v; a.o = o;
+  a.B = B; a.X = X; a.L = L; a.H = H; a.D = D;
+  // spatial (B,T,S,*): unit (b, t), positions s.  temporal (B,S,T,*): unit (b, s), positions t.
+  // Both: position r of unit (b, x) is row (b*X + x)*L + r.
+  (void)spatial;
+  a.r_stride_in = ld_in;
+  a.x_stride_in = L * ld_in;
+  a.b_stride_in = X * L * ld_in;
+  a.r_stride_out = ld_out;
+  a.x_stride_out = L * ld_out;
+  a.b_stride_out = X * L * ld_out;
+  a.scale = scale > 0.0f ? scale : (float)(1.0 / sqrt((double)D));
+  hipStream_t s = as_stream(stream);
+  return dtype == DSP_BF16 ? launch_attn_bf16(a, s) : launch_attn_f32(a, s);
+}
+
+int linear_impl(const void* a, const void* w, const void* bias, const float* residual, void* out,
+                int64_t M, int N, int K, int epilogue, int dtype, hipStream_t s) {
+  if (!a || !w || !out) return DSP_ERR_NULL;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
+  if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_F32) return DSP_ERR_ARG;
+  if (epilogue == DSP_EPI_RESID && !residual) return DSP_ERR_NULL;
+  int64_t mk, mn;
+  if (!mul_ok(M, K, &mk) || !mul_ok(M, N, &mn)) return DSP_ERR_SHAPE;
+  const int es = elem_size(dtype);
+  const int out_es = (epilogue == DSP_EPI_RESID || epilogue == DSP_EPI_F32) ? 4 : es;
+  const size_t out_bytes = (size_t)mn * out_es;
+  if (overlap(out, out_bytes, a, (size_t)mk * es) || overlap(out, out_bytes, w, (size_t)N * K * es) ||
+      (bias && overlap(out, out_bytes, bias, (size_t)N * es)))
+    return DSP_ERR_ARG;
+  if (residual && epilogue == DSP_EPI_RESID && residual != out &&
+      overlap(out, out_bytes, residual, (size_t)mn * 4))
+    return DSP_ERR_ARG;
+  if (dtype == DSP_BF16) {
+    if (K % 8 || !aligned(a, 16) || !aligned(w, 16) || !aligned(out, 16)) return DSP_ERR_ALIGN;
+    if (epilogue == DSP_EPI_RESID && !aligned(residual, 16)) return DSP_ERR_ALIGN;
+    return launch_linear_bf16(a, w, bias, epilogue == DSP_EPI_RESID ? residual : nullptr, out, M, N,
+                              K, epilogue, s);
+  }
+  return launch_linear_f32(static_cast<const float*>(a), static_cast<const float*>(w),
+                           static_cast<const float*>(bias),
+                           epilogue == DSP_EPI_RESID ? residual : nullptr,
+                           static_cast<float*>(out), M, N, K, epilogue, s);
+}
+
+// Workspace regions of the block (each 256-byte aligned).
+struct BlockWs {
+  size_t h, qkv, o, f, x1, total;
+};
+
+bool block_ws_layout(int64_t B, int64_t T, int64_t S, int C, int F, int dtype, BlockWs* ws) {
+  int64_t tokens;
+  if (!mul_ok(B, T, &tokens) || !mul_ok(tokens, S, &tokens)) return false;
+  const int es = elem_size(dtype);
+  auto up = [](size_t v) { return (v + 255) & ~size_t(255); };
+  int64_t tc, t3c, tf;
+  if (!mul_ok(tokens, C, &tc) || !mul_ok(tokens, 3 * (int64_t)C, &t3c) || !mul_ok(tokens, F, &tf))
+    return false;
+  size_t off = 0;
+  ws->h = off;   off += up((size_t)tc * es);
+  ws->qkv = off; off += up((size_t)t3c * es);
+  ws->o = off;   off += up((size_t)tc * es);
+  ws->f = off;   off += up((size_t)tf * es);
+  ws->x1 = off;  off += up((size_t)tc * 4);
+  ws->total = off;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dsp_status_str(int status) {
+  switch (status) {
+    case DSP_OK: return "DSP_OK";
+    case DSP_ERR_NULL: return "DSP_ERR_NULL: a required pointer is NULL";
+    case DSP_ERR_DIM: return "DSP_ERR_DIM: bad ndim or dimension index";
+    case DSP_ERR_SHAPE: return "DSP_ERR_SHAPE: invalid or unsupported size";
+    case DSP_ERR_DTYPE: return "DSP_ERR_DTYPE: unknown or unsupported dtype";
+    case DSP_ERR_ALIGN: return "DSP_ERR_ALIGN: pointer or stride alignment not met";
+    case DSP_ERR_HIP: return "DSP_ERR_HIP: HIP runtime or launch failure";
+    case DSP_ERR_WORKSPACE: return "DSP_ERR_WORKSPACE: workspace missing or too small";
+    case DSP_ERR_ARG: return "DSP_ERR_ARG: invalid argument";
+    default: return "unknown dsp status";
+  }
+}
+
+int dsp_version(void) { return kVersion; }
+
+int dsp_switch(const void* x, void* y, const int64_t* shape, int ndim, int from_dim, int to_dim,
+               int n_chunks, int dtype, void* stream) {
+  return switch_impl(x, y, shape, ndim, from_dim, to_dim, n_chunks, dtype, 0, stream);
+}
+
+int dsp_switch_variant(const void* x, void* y, const int64_t* shape, int ndim, int from_dim,
+                       int to_dim, int n_chunks, int dtype, int variant, void* stream) {
+  return switch_impl(x, y, shape, ndim, from_dim, to_dim, n_chunks, dtype, variant, stream);
+}
+
+int dsp_spatial_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t T,
+                     int64_t S, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
+                     int dtype, void* stream) {
+  return attn_impl(q, k, v, o, B, T, S, H, D, ld_in, ld_out, scale, dtype, stream, true);
+}
+
+int dsp_temporal_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t S,
+                      int64_t T, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
+                      int dtype, void* stream) {
+  return attn_impl(q, k, v, o, B, S, T, H, D, ld_in, ld_out, scale, dtype, stream, false);
+}
+
+int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows, int C, float eps,
+                  void* stream) {
+  if (!x || !y) return DSP_ERR_NULL;
+  if (!valid_dtype(x_dtype) || !valid_dtype(y_dtype)) return DSP_ERR_DTYPE;
+  if (rows < 0 || C < 1) return DSP_ERR_SHAPE;
+  if (!(eps >= 0.0f) || isinf(eps)) return DSP_ERR_ARG;
+  int64_t n;
+  if (!mul_ok(rows, C, &n)) return DSP_ERR_SHAPE;
+  if (overlap(x, (size_t)n * elem_size(x_dtype), y, (size_t)n * elem_size(y_dtype))) return DSP_ERR_ARG;
+  return launch_layernorm(x, x_dtype == DSP_BF16, y, y_dtype == DSP_BF16, rows, C, eps,
+                          as_stream(stream));
+}
+
+int dsp_linear(const void* a, const void* w, const void* bias, const float* residual, void* out,
+               int64_t M, int N, int K, int epilogue, int dtype, void* stream) {
+  return linear_impl(a, w, bias, residual, out, M, N, K, epilogue, dtype, as_stream(stream));
+}
+
+size_t dsp_st_block_workspace_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F,
+                                    int dtype) {
+  if (!valid_dtype(dtype) || B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || F < 0 || C % H)
+    return 0;
+  BlockWs ws;
+  if (!block_ws_layout(B, T, S, C, F, dtype, &ws)) return 0;
+  return ws.total;
+}
+
+int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_weights_t* w,
+                         void* workspace, size_t ws_bytes, int64_t B, int64_t T, int64_t S, int C,
+                         int H, int F, float ln_eps, int flags, int dtype, void* stream) {
+  if (!x_BTSC || !y_BSTC || !w) return DSP_ERR_NULL;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (flags & ~(DSP_BLOCK_NO_MLP_LN | DSP_BLOCK_ATTN_ONLY)) return DSP_ERR_ARG;
+  const bool attn_only = (flags & DSP_BLOCK_ATTN_ONLY) != 0;
+  if (B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || C % H || F < 0) return DSP_ERR_SHAPE;
+  if (!attn_only && F < 1) return DSP_ERR_SHAPE;
+  const int D = C / H;
+  if (dtype == DSP_BF16 && (!attn_bf16_supports(D) || C % 8 || F % 8)) return DSP_ERR_SHAPE;
+  if (!(ln_eps >= 0.0f) || isinf(ln_eps)) return DSP_ERR_ARG;
+  if (!w->wqkv_s || !w->wo_s || !w->wqkv_t || !w->wo_t) return DSP_ERR_NULL;
+  if (!attn_only && (!w->w1 || !w->w2)) return DSP_ERR_NULL;
+  BlockWs ws;
+  if (!block_ws_layout(B, T, S, C, F, dtype, &ws)) return DSP_ERR_SHAPE;
+  if (!workspace || ws_bytes < ws.total) return DSP_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return DSP_ERR_ALIGN;
+  const int64_t tokens = B * T * S;
+  const size_t act_bytes = (size_t)tokens * C * 4;
+  if (overlap(x_BTSC, act_bytes, y_BSTC, act_bytes) ||
+      overlap(x_BTSC, act_bytes, workspace, ws_bytes) ||
+      overlap(y_BSTC, act_bytes, workspace, ws_bytes))
+    return DSP_ERR_ARG;
+  if (dtype == DSP_BF16) {
+    const void* ws_[] = {w->wqkv_s, w->wo_s, w->wqkv_t, w->wo_t, w->w1, w->w2};
+    for (const void* p : ws_)
+      if (p && !aligned(p, 16)) return DSP_ERR_ALIGN;
+    if (!aligned(x_BTSC, 16) || !aligned(y_BSTC, 16)) return DSP_ERR_ALIGN;
+  }
+  if (tokens == 0) return DSP_OK;
+
+  hipStream_t s = as_stream(stream);
+  char* base = static_cast<char*>(workspace);
+  void* h = base + ws.h;
+  void* qkv = base + ws.qkv;
+  void* o = base + ws.o;
+  void* f = base + ws.f;
+  float* x1 = reinterpret_cast<float*>(base + ws.x1);
+  const int bf = dtype == DSP_BF16;
+  const int es = elem_size(dtype);
+  const int64_t ld3 = 3 * (int64_t)C;
+  char* qkvc = static_cast<char*>(qkv);
+  int st;
+#define DSP_TRY(expr)            \
+  do {                           \
+    st = (expr);                 \
+    if (st != DSP_OK) return st; \
+  } while (0)
+
+  // ---- spatial half on (B, T, S, C): attention over S inside each frame
+  if (attn_only) DSP_TRY(launch_cast(x_BTSC, 0, h, bf, tokens * C, s));
+  else DSP_TRY(launch_layernorm(x_BTSC, 0, h, bf, tokens, C, ln_eps, s));
+  DSP_TRY(linear_impl(h, w->wqkv_s, w->bqkv_s, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s));
+  DSP_TRY(attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, T, S, H, D, ld3, C,
+                    0.0f, dtype, s, true));
+  DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, attn_only ? nullptr : x_BTSC, x1, tokens, C, C,
+                      attn_only ? DSP_EPI_F32 : DSP_EPI_RESID, dtype, s));
+  // ---- the Switch T -> S on one GPU: (B, T, S, C) -> (B, S, T, C)
+  const int64_t shp[4] = {B, T, S, C};
+  DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+  // ---- temporal half on (B, S, T, C): attention over T at each location
+  if (attn_only) DSP_TRY(launch_cast(y_BSTC, 0, h, bf, tokens * C, s));
+  else DSP_TRY(launch_layernorm(y_BSTC, 0, h, bf, tokens, C, ln_eps, s));
+  DSP_TRY(linear_impl(h, w->wqkv_t, w->bqkv_t, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s));
+  DSP_TRY(attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, S, T, H, D, ld3, C,
+                    0.0f, dtype, s, false));
+  if (attn_only) {
+    DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, nullptr, y_BSTC, tokens, C, C, DSP_EPI_F32, dtype, s));
+    return DSP_OK;
+  }
+  DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, y_BSTC, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s));
+  // ---- MLP with GELU (Eq. 5 with the configuration's activation), residual
+  if (flags & DSP_BLOCK_NO_MLP_LN) DSP_TRY(launch_cast(y_BSTC, 0, h, bf, tokens * C, s));
+  else DSP_TRY(launch_layernorm(y_BSTC, 0, h, bf, tokens, C, ln_eps, s));
+  DSP_TRY(linear_impl(h, w->w1, w->b1, nullptr, f, tokens, F, C, DSP_EPI_GELU, dtype, s));
+  DSP_TRY(linear_impl(f, w->w2, w->b2, y_BSTC, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
+#undef DSP_TRY
+  return DSP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,102 @@
+// fp32 attention along one sequence dimension (Eq. 3 per head), the exact
+// path: fp32 storage, fp32 FMA arithmetic, no reduced-precision operand
+// anywhere.  One thread owns one (unit, query, 32-column slice of the output):
+// a first pass over the keys finds the row maximum of the scaled scores, a
+// second pass accumulates exp(score - max) and the weighted values of its
+// slice.  Meant for small problems and for checking; the bf16 MFMA kernel is
+// the fast path.
+#include <math.h>
+
+#include "dsp_internal.h"
+
+namespace dsp {
+namespace {
+
+constexpr int DC = 32;  // output columns per thread
+
+struct ParamsF {
+  const float* q;
+  const float* k;
+  const float* v;
+  float* o;
+  int64_t b_in, x_in, r_in, b_out, x_out, r_out;
+  int64_t X, H, L, D, n_dc, total;
+  float scale;
+};
+
+__global__ __launch_bounds__(256) void attn_f32_kernel(ParamsF p) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= p.total) return;
+  // tid -> (unit, query, column slice), slice fastest
+  const int64_t dc = tid % p.n_dc;
+  const int64_t uq = tid / p.n_dc;
+  const int64_t qi = uq % p.L;
+  const int64_t unit = uq / p.L;
+  const int64_t h = unit % p.H;
+  const int64_t bx = unit / p.H;
+  const int64_t xx = bx % p.X;
+  const int64_t bb = bx / p.X;
+  const int64_t in_base = bb * p.b_in + xx * p.x_in + h * p.D;
+  const float* qrow = p.q + in_base + qi * p.r_in;
+  const float* kb = p.k + in_base;
+  const float* vb = p.v + in_base;
+  float m = -INFINITY;
+  for (int64_t j = 0; j < p.L; ++j) {
+    const float* krow = kb + j * p.r_in;
+    float s = 0.0f;
+    for (int64_t d = 0; d < p.D; ++d) s = fmaf(qrow[d], krow[d], s);
+    m = fmaxf(m, s * p.scale);
+  }
+  const int64_t c0 = dc * DC;
+  const int64_t nc = min((int64_t)DC, p.D - c0);
+  float acc[DC];
+#pragma unroll
+  for (int c = 0; c < DC; ++c) acc[c] = 0.0f;
+  float l = 0.0f;
+  for (int64_t j = 0; j < p.L; ++j) {
+    const float* krow = kb + j * p.r_in;
+    float s = 0.0f;
+    for (int64_t d = 0; d < p.D; ++d) s = fmaf(qrow[d], krow[d], s);
+    const float e = expf(s * p.scale - m);
+    l += e;
+    const float* vrow = vb + j * p.r_in + c0;
+#pragma unroll
+    for (int c = 0; c < DC; ++c)
+      if (c < nc) acc[c] = fmaf(e, vrow[c], acc[c]);
+  }
+  float* orow = p.o + bb * p.b_out + xx * p.x_out + h * p.D + qi * p.r_out + c0;
+  const float inv = 1.0f / l;
+#pragma unroll
+  for (int c = 0; c < DC; ++c)
+    if (c < nc) orow[c] = acc[c] * inv;
+}
+
+}  // namespace
+
+int launch_attn_f32(const AttnArgs& a, hipStream_t s) {
+  ParamsF p;
+  p.q = static_cast<const float*>(a.q);
+  p.k = static_cast<const float*>(a.k);
+  p.v = static_cast<const float*>(a.v);
+  p.o = static_cast<float*>(a.o);
+  p.b_in = a.b_stride_in;
+  p.x_in = a.x_stride_in;
+  p.r_in = a.r_stride_in;
+  p.b_out = a.b_stride_out;
+  p.x_out = a.x_stride_out;
+  p.r_out = a.r_stride_out;
+  p.X = a.X;
+  p.H = a.H;
+  p.L = a.L;
+  p.D = a.D;
+  p.n_dc = (a.D + DC - 1) / DC;
+  p.total = a.B * a.X * a.H * a.L * p.n_dc;
+  p.scale = a.scale;
+  if (p.total == 0) return DSP_OK;
+  const int64_t blocks = (p.total + 255) / 256;
+  if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
+  hipLaunchKernelGGL(attn_f32_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p);
+  return last_launch_status();
+}
+
+}  // namespace dsp

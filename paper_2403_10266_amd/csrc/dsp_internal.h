@@ -1,0 +1,50 @@
+// Internal declarations shared by the libdsp translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/dsp.h"
+
+namespace dsp {
+
+// Launch wrappers implemented in the kernel translation units.  Arguments have
+// been validated by the ABI layer; each returns a dsp_status_t.
+int launch_switch_rows(const void* x, void* y, int64_t B, int64_t D1, int64_t D2, int64_t row_bytes,
+                       int from_dim, int to_dim, int64_t n_chunks, hipStream_t s);
+int launch_switch_tiles(const void* x, void* y, int64_t B, int64_t D1, int64_t D2, int64_t C,
+                        int elem_bytes, int from_dim, int to_dim, int64_t n_chunks, hipStream_t s);
+
+// Attention over units of L consecutive sequence positions.  Unit u decomposes
+// as u = (b * X + x) * H + h; position r of unit (b, x, h) sits at element
+//   b * b_stride + x * x_stride + r * r_stride + h * D
+// of q/k/v (strides *_in) and of o (strides *_out).
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  int64_t B, X, L;
+  int H, D;
+  int64_t b_stride_in, x_stride_in, r_stride_in;
+  int64_t b_stride_out, x_stride_out, r_stride_out;
+  float scale;
+};
+int launch_attn_bf16(const AttnArgs& a, hipStream_t s);
+int launch_attn_f32(const AttnArgs& a, hipStream_t s);
+bool attn_bf16_supports(int D);
+
+int launch_layernorm(const void* x, int x_bf16, void* y, int y_bf16, int64_t rows, int C, float eps,
+                     hipStream_t s);
+
+int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s);
+
+int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
+                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s);
+int launch_linear_f32(const float* a, const float* w, const float* bias, const float* residual,
+                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s);
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? DSP_OK : DSP_ERR_HIP; }
+inline int last_launch_status() { return hip_status(hipGetLastError()); }
+
+}  // namespace dsp

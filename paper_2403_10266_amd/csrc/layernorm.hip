@@ -1,0 +1,131 @@
+// LayerNorm over the hidden size (Eq. 4 and Eq. 6 normalise every sublayer):
+// y = (x - mean) / sqrt(var + eps), biased variance, no affine part.
+// One wave per row; the row is held in registers (up to 64*VPL elements),
+// statistics are computed in fp32 in two passes over the registers (mean,
+// then centred sum of squares), and reductions use cross-lane adds.
+// HBM-bound: one read of x and one write of y per row.
+#include <math.h>
+
+#include <algorithm>
+
+#include "dsp_internal.h"
+
+namespace dsp {
+namespace {
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ float load_elem(const void* p, int64_t i, int bf) {
+  if (bf) {
+    const uint16_t u = static_cast<const uint16_t*>(p)[i];
+    return __uint_as_float(((uint32_t)u) << 16);
+  }
+  return static_cast<const float*>(p)[i];
+}
+
+__device__ __forceinline__ void store_elem(void* p, int64_t i, float v, int bf) {
+  if (bf) {
+    static_cast<__bf16*>(p)[i] = (__bf16)v;
+  } else {
+    static_cast<float*>(p)[i] = v;
+  }
+}
+
+constexpr int kRowsPerBlock = 4;  // one wave per row
+
+template <int VPL>
+__global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_kernel(
+    const void* __restrict__ x, int x_bf, void* __restrict__ y, int y_bf, int64_t rows, int C,
+    float eps) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int64_t base = row * C;
+  float v[VPL];
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int c = lane + 64 * i;
+    v[i] = c < C ? load_elem(x, base + c, x_bf) : 0.0f;
+    s += v[i];
+  }
+  const float mean = wave_sum(s) / (float)C;
+  float ss = 0.0f;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int c = lane + 64 * i;
+    const float d = c < C ? v[i] - mean : 0.0f;
+    ss = fmaf(d, d, ss);
+  }
+  const float var = wave_sum(ss) / (float)C;
+  const float rstd = 1.0f / sqrtf(var + eps);
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int c = lane + 64 * i;
+    if (c < C) store_elem(y, base + c, (v[i] - mean) * rstd, y_bf);
+  }
+}
+
+// Rows longer than the register budget: three passes over global memory.
+__global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_long_kernel(
+    const void* __restrict__ x, int x_bf, void* __restrict__ y, int y_bf, int64_t rows, int C,
+    float eps) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int64_t base = row * C;
+  float s = 0.0f;
+  for (int c = lane; c < C; c += 64) s += load_elem(x, base + c, x_bf);
+  const float mean = wave_sum(s) / (float)C;
+  float ss = 0.0f;
+  for (int c = lane; c < C; c += 64) {
+    const float d = load_elem(x, base + c, x_bf) - mean;
+    ss = fmaf(d, d, ss);
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(ss) / (float)C + eps);
+  for (int c = lane; c < C; c += 64) store_elem(y, base + c, (load_elem(x, base + c, x_bf) - mean) * rstd, y_bf);
+}
+
+__global__ __launch_bounds__(256) void cast_kernel(const void* __restrict__ x, int x_bf,
+                                                   void* __restrict__ y, int y_bf, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    store_elem(y, i, load_elem(x, i, x_bf), y_bf);
+}
+
+}  // namespace
+
+// Element-wise format conversion (fp32 <-> bf16, round to nearest even).
+int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s) {
+  if (n == 0) return DSP_OK;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
+  hipLaunchKernelGGL(cast_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, x, x_bf16, y, y_bf16, n);
+  return last_launch_status();
+}
+
+int launch_layernorm(const void* x, int x_bf16, void* y, int y_bf16, int64_t rows, int C, float eps,
+                     hipStream_t s) {
+  if (rows == 0) return DSP_OK;
+  const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
+  if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
+  const dim3 grid((uint32_t)blocks), block(64 * kRowsPerBlock);
+  const int vpl = (C + 63) / 64;
+  if (vpl <= 4) {
+    hipLaunchKernelGGL(layernorm_kernel<4>, grid, block, 0, s, x, x_bf16, y, y_bf16, rows, C, eps);
+  } else if (vpl <= 8) {
+    hipLaunchKernelGGL(layernorm_kernel<8>, grid, block, 0, s, x, x_bf16, y, y_bf16, rows, C, eps);
+  } else if (vpl <= 18) {
+    hipLaunchKernelGGL(layernorm_kernel<18>, grid, block, 0, s, x, x_bf16, y, y_bf16, rows, C, eps);
+  } else if (vpl <= 32) {
+    hipLaunchKernelGGL(layernorm_kernel<32>, grid, block, 0, s, x, x_bf16, y, y_bf16, rows, C, eps);
+  } else {
+    hipLaunchKernelGGL(layernorm_long_kernel, grid, block, 0, s, x, x_bf16, y, y_bf16, rows, C, eps);
+  }
+  return last_launch_status();
+}
+
+}  // namespace dsp

@@ -1,0 +1,163 @@
+"""The C ABI without a GPU: the library loads, exports every symbol that
+include/*.h declares, and rejects bad arguments with the documented status
+before touching the device (only calls that fail validation are made)."""
+import ctypes
+import re
+from pathlib import Path
+
+import pytest
+
+import paper_2403_10266_amd as dsp
+
+ROOT = Path(__file__).resolve().parent.parent
+FAKE = 0x10000          # a 256-byte aligned address that is never dereferenced
+FAKE2 = 0x20000000
+MIS = FAKE + 2          # misaligned
+
+
+def _declared():
+    names = set()
+    for h in (ROOT / "include").glob("*.h"):
+        text = re.sub(r"/\*.*?\*/", "", h.read_text(), flags=re.S)
+        for m in re.finditer(r"^[A-Za-z_][\w \t\*]*?\b(dsp_\w+)\s*\(", text, flags=re.M):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+def test_header_declares_entry_points():
+    names = _declared()
+    for n in ("dsp_switch", "dsp_spatial_attn", "dsp_temporal_attn", "dsp_layernorm", "dsp_linear",
+              "dsp_st_block_forward", "dsp_st_block_workspace_bytes", "dsp_status_str"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(str(dsp.LIB_PATH))
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_signatures_cover_header():
+    assert set(_declared()) <= set(dsp._SIGNATURES)
+
+
+def test_status_strings():
+    for code in range(9):
+        s = dsp.status_str(code)
+        assert s.startswith("DSP_")
+    assert "unknown" in dsp.status_str(99)
+    assert dsp.lib().dsp_version() >= 10000
+
+
+def _shape(*v):
+    return (ctypes.c_int64 * len(v))(*v)
+
+
+L = None
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return dsp.lib()
+
+
+def test_switch_validation(lib):
+    sw = lambda x, y, shape, ndim, f, t, n, dt, var=0: lib.dsp_switch_variant(
+        x, y, shape, ndim, f, t, n, dt, var, None)
+    s = _shape(1, 4, 6, 8)
+    assert sw(None, FAKE2, s, 4, 1, 2, 2, 1) == dsp.DSP_ERR_NULL
+    assert sw(FAKE, None, s, 4, 1, 2, 2, 1) == dsp.DSP_ERR_NULL
+    assert sw(FAKE, FAKE2, None, 4, 1, 2, 2, 1) == dsp.DSP_ERR_NULL
+    assert sw(FAKE, FAKE2, s, 3, 1, 2, 2, 1) == dsp.DSP_ERR_DIM
+    assert sw(FAKE, FAKE2, s, 4, 0, 2, 2, 1) == dsp.DSP_ERR_DIM
+    assert sw(FAKE, FAKE2, s, 4, 1, 3, 2, 1) == dsp.DSP_ERR_DIM
+    assert sw(FAKE, FAKE2, s, 4, 1, 2, 4, 1) == dsp.DSP_ERR_SHAPE      # 6 % 4
+    assert sw(FAKE, FAKE2, s, 4, 1, 2, 0, 1) == dsp.DSP_ERR_SHAPE
+    assert sw(FAKE, FAKE2, _shape(1, -1, 6, 8), 4, 1, 2, 1, 1) == dsp.DSP_ERR_SHAPE
+    assert sw(FAKE, FAKE2, s, 4, 1, 2, 2, 7) == dsp.DSP_ERR_DTYPE
+    assert sw(FAKE, FAKE + 16, s, 4, 1, 2, 2, 1) == dsp.DSP_ERR_ARG      # overlapping buffers
+    assert sw(FAKE, FAKE2, s, 4, 1, 2, 2, 1, 3) == dsp.DSP_ERR_ARG     # unknown variant
+    assert sw(MIS, FAKE2, s, 4, 1, 2, 2, 1, 1) == dsp.DSP_ERR_ALIGN    # rows variant needs 16 B
+    # empty tensors are accepted and launch nothing
+    assert sw(FAKE, FAKE2, _shape(0, 4, 6, 8), 4, 1, 2, 2, 1) == dsp.DSP_OK
+    assert sw(FAKE, FAKE2, _shape(1, 4, 6, 0), 4, 1, 2, 2, 1) == dsp.DSP_OK
+
+
+@pytest.mark.parametrize("fn", ["dsp_spatial_attn", "dsp_temporal_attn"])
+def test_attention_validation(lib, fn):
+    f = getattr(lib, fn)
+    call = lambda q=FAKE, k=FAKE, v=FAKE, o=FAKE2, B=2, X=3, L=5, H=16, D=72, ldi=1152, ldo=1152, \
+        sc=0.0, dt=1: f(q, k, v, o, B, X, L, H, D, ldi, ldo, sc, dt, None)
+    assert call(q=None) == dsp.DSP_ERR_NULL
+    assert call(o=None) == dsp.DSP_ERR_NULL
+    assert call(dt=5) == dsp.DSP_ERR_DTYPE
+    assert call(H=0) == dsp.DSP_ERR_SHAPE
+    assert call(B=-1) == dsp.DSP_ERR_SHAPE
+    assert call(ldi=1000) == dsp.DSP_ERR_SHAPE            # H*D > ld
+    assert call(D=70, ldi=1120, ldo=1120) == dsp.DSP_ERR_SHAPE   # unsupported bf16 head width
+    assert call(q=MIS) == dsp.DSP_ERR_ALIGN
+    assert call(ldi=1156) == dsp.DSP_ERR_ALIGN
+    assert call(sc=float("nan")) == dsp.DSP_ERR_ARG
+    assert call(dt=0, D=300, H=1, ldi=300, ldo=300) == dsp.DSP_ERR_SHAPE
+    assert call(B=0) == dsp.DSP_OK                         # empty: nothing launched
+    assert call(L=0) == dsp.DSP_OK
+
+
+def test_layernorm_validation(lib):
+    f = lambda x=FAKE, xd=1, y=FAKE2, yd=1, rows=4, C=8, eps=1e-6: lib.dsp_layernorm(
+        x, xd, y, yd, rows, C, eps, None)
+    assert f(x=None) == dsp.DSP_ERR_NULL
+    assert f(xd=3) == dsp.DSP_ERR_DTYPE
+    assert f(C=0) == dsp.DSP_ERR_SHAPE
+    assert f(rows=-2) == dsp.DSP_ERR_SHAPE
+    assert f(eps=-1.0) == dsp.DSP_ERR_ARG
+    assert f(eps=float("inf")) == dsp.DSP_ERR_ARG
+    assert f(y=FAKE + 4) == dsp.DSP_ERR_ARG
+    assert f(rows=0) == dsp.DSP_OK
+
+
+def test_linear_validation(lib):
+    f = lambda a=FAKE, w=FAKE2, b=None, r=None, o=0x40000000, M=4, N=8, K=16, epi=0, dt=1: \
+        lib.dsp_linear(a, w, b, r, o, M, N, K, epi, dt, None)
+    assert f(a=None) == dsp.DSP_ERR_NULL
+    assert f(epi=2) == dsp.DSP_ERR_NULL                    # residual required
+    assert f(epi=9) == dsp.DSP_ERR_ARG
+    assert f(dt=9) == dsp.DSP_ERR_DTYPE
+    assert f(N=0) == dsp.DSP_ERR_SHAPE
+    assert f(K=12) == dsp.DSP_ERR_ALIGN                    # bf16 needs K % 8 == 0
+    assert f(a=MIS) == dsp.DSP_ERR_ALIGN
+    assert f(o=FAKE + 8) == dsp.DSP_ERR_ARG                # out overlaps a
+    assert f(M=0) == dsp.DSP_OK
+
+
+def test_block_validation_and_workspace(lib):
+    B, T, S, C, H, F = 1, 4, 16, 64, 4, 256
+    need = lib.dsp_st_block_workspace_bytes(B, T, S, C, H, F, 1)
+    tokens = B * T * S
+    up = lambda v: (v + 255) // 256 * 256
+    assert need == up(tokens * C * 2) + up(tokens * 3 * C * 2) + up(tokens * C * 2) + \
+        up(tokens * F * 2) + up(tokens * C * 4)
+    assert lib.dsp_st_block_workspace_bytes(B, T, S, C, 5, F, 1) == 0     # C % H != 0
+    w = dsp.BlockWeights(wqkv_s=FAKE, wo_s=FAKE, wqkv_t=FAKE, wo_t=FAKE, w1=FAKE, w2=FAKE)
+    f = lambda x=0x100000, y=0x200000, wp=ctypes.byref(w), ws=0x40000000, wsb=need, flags=0, \
+        dt=1, eps=1e-6, F_=F: lib.dsp_st_block_forward(x, y, wp, ws, wsb, B, T, S, C, H, F_, eps,
+                                                     flags, dt, None)
+    assert f(x=None) == dsp.DSP_ERR_NULL
+    assert f(wp=None) == dsp.DSP_ERR_NULL
+    assert f(ws=None) == dsp.DSP_ERR_WORKSPACE
+    assert f(wsb=need - 1) == dsp.DSP_ERR_WORKSPACE
+    assert f(ws=0x40000010) == dsp.DSP_ERR_ALIGN
+    assert f(flags=8) == dsp.DSP_ERR_ARG
+    assert f(dt=4) == dsp.DSP_ERR_DTYPE
+    assert f(eps=-1.0) == dsp.DSP_ERR_ARG
+    assert f(F_=0) == dsp.DSP_ERR_SHAPE                     # the MLP needs F >= 1
+    assert f(y=0x100000 + 64) == dsp.DSP_ERR_ARG            # x and y overlap
+    w2 = dsp.BlockWeights(wqkv_s=FAKE, wo_s=FAKE, wqkv_t=FAKE, wo_t=None)
+    assert f(wp=ctypes.byref(w2)) == dsp.DSP_ERR_NULL
+
+
+def test_binding_rejects_host_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 2, 2, 8), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        dsp.dsp_switch(x, 1, 2, 1)

@@ -1,0 +1,119 @@
+"""Spatial and temporal attention on the GPU against the fp64 oracle."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import assert_close, dev, host, say, bits16
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    return torch
+
+
+def _inputs(shape, dtype, seed):
+    rng = np.random.default_rng(seed)
+    arrs = [rng.standard_normal(shape, dtype=np.float32) for _ in range(3)]
+    if dtype == "bf16":
+        arrs = [synth.bf16_round(a) for a in arrs]
+    return arrs
+
+
+@pytest.mark.parametrize("kind", ["spatial", "temporal"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("B,X,L,H,D", [
+    (1, 4, 16, 4, 16),      # the tiny configuration's shape
+    (2, 3, 1, 2, 72),       # L = 1
+    (1, 2, 7, 3, 72),       # L below one tile
+    (1, 2, 64, 2, 72),      # exactly one tile
+    (2, 2, 65, 2, 72),      # one past a tile
+    (1, 1, 300, 4, 72),     # several tiles + ragged tail, several query blocks
+    (1, 2, 130, 2, 64),     # D a multiple of 32: VALU row sums
+    (1, 2, 97, 2, 80),
+    (1, 2, 50, 2, 96),
+    (1, 2, 33, 2, 32),
+])
+def test_attention_small(torch, kind, dtype, B, X, L, H, D):
+    import paper_2403_10266_amd as dsp
+    C = H * D
+    q, k, v = _inputs((B, X, L, C), dtype, seed=B * 1000 + L * 7 + D)
+    say(f"{kind} {dtype} B={B} X={X} L={L} H={H} D={D}")
+    fn = dsp.dsp_spatial_attn if kind == "spatial" else dsp.dsp_temporal_attn
+    o = fn(dev(q, dtype), dev(k, dtype), dev(v, dtype), H)
+    torch.cuda.synchronize()
+    want = (oracle.spatial_attention if kind == "spatial" else oracle.temporal_attention)(q, k, v, H)
+    assert_close(host(o), want, dtype, f"{kind} L={L} D={D}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_packed_qkv_and_scale(torch, dtype):
+    """q/k/v as column slices of one packed [Q|K|V] buffer (row stride 3C) and an
+    explicit softmax scale."""
+    import paper_2403_10266_amd as dsp
+    B, T, S, H, D = 1, 3, 70, 4, 72
+    C = H * D
+    rng = np.random.default_rng(42)
+    qkv = rng.standard_normal((B, T, S, 3 * C), dtype=np.float32)
+    if dtype == "bf16":
+        qkv = synth.bf16_round(qkv)
+    t = dev(qkv, dtype)
+    q, k, v = t[..., :C], t[..., C:2 * C], t[..., 2 * C:]
+    o = dsp.dsp_spatial_attn(q, k, v, H, C=C, ld_in=3 * C, scale=0.05)
+    torch.cuda.synchronize()
+    want = oracle.spatial_attention(qkv[..., :C], qkv[..., C:2 * C], qkv[..., 2 * C:], H, scale=0.05)
+    assert_close(host(o), want, dtype, "packed qkv")
+
+
+def test_l1_returns_v_exactly(torch):
+    import paper_2403_10266_amd as dsp
+    q, k, v = _inputs((2, 5, 1, 1152), "bf16", seed=9)
+    o = dsp.dsp_temporal_attn(dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16"), 16)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits16(o), bits16(dev(v, "bf16")))
+
+
+def _sampled_check(torch, kind, w, n_units, n_rows, seed):
+    import paper_2403_10266_amd as dsp
+    layout = "BTSC" if kind == "spatial" else "BSTC"
+    q, k, v = synth.qkv_inputs(w, layout)
+    X, L = (w.T, w.S) if kind == "spatial" else (w.S, w.T)
+    say(f"{kind} full size {q.shape} H={w.H}")
+    fn = dsp.dsp_spatial_attn if kind == "spatial" else dsp.dsp_temporal_attn
+    o = fn(dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16"), w.H)
+    torch.cuda.synchronize()
+    o = o.float().cpu().numpy()
+    rng = np.random.default_rng(seed)
+    D = w.D
+    got, want = [], []
+    for _ in range(n_units):
+        b, x, h = rng.integers(w.B), rng.integers(X), rng.integers(w.H)
+        rows = rng.choice(L, size=min(n_rows, L), replace=False)
+        cs = slice(h * D, (h + 1) * D)
+        want.append(oracle.attention_rows(q[b, x, rows, cs], k[b, x, :, cs], v[b, x, :, cs]))
+        got.append(o[b, x, rows, cs])
+    assert_close(np.concatenate(got), np.concatenate(want), "bf16", f"{kind} sampled")
+    assert np.isfinite(o).all()
+    return o
+
+
+def test_spatial_full_size_sampled(torch):
+    _sampled_check(torch, "spatial", synth.WORKLOADS["spatial_bf16_B2_T16_S4096"], 24, 96, 1)
+
+
+def test_temporal_full_size_sampled(torch):
+    _sampled_check(torch, "temporal", synth.WORKLOADS["temporal_bf16_B2_S512_T128"], 256, 128, 2)
+
+
+def test_deterministic(torch):
+    import paper_2403_10266_amd as dsp
+    q, k, v = _inputs((1, 2, 200, 1152), "bf16", seed=3)
+    a = dsp.dsp_spatial_attn(dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16"), 16)
+    b = dsp.dsp_spatial_attn(dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16"), 16)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits16(a), bits16(b))

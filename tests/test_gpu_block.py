@@ -1,0 +1,60 @@
+"""The spatial-temporal block composite on the GPU against the fp64 oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import assert_close, dev, host, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    return torch
+
+
+def _oracle_params(stored):
+    """Stored [out][in] weights -> the paper's [in, out] matrices for the oracle."""
+    return {n: (None if v is None else (v.T if n.startswith("w") else v)) for n, v in stored.items()}
+
+
+def test_tiny_chain_fp32(torch):
+    import paper_2403_10266_amd as dsp
+    w = synth.WORKLOADS["tiny_chain_f32"]
+    x, p = synth.chain_inputs(w)
+    say(f"tiny chain {x.shape}")
+    wd = {n: dev(v, "f32") for n, v in p.items()}
+    y = dsp.dsp_st_block_forward(dev(x, "f32"), wd, w.H, flags=dsp.DSP_BLOCK_ATTN_ONLY)
+    torch.cuda.synchronize()
+    want = oracle.tiny_chain(x, _oracle_params(p), w.H)
+    assert_close(host(y), want, "f32", "tiny chain")
+
+
+def _block_case(torch, w, with_bias, flags=0):
+    import paper_2403_10266_amd as dsp
+    x, p = synth.block_inputs(w, with_bias=with_bias)
+    say(f"block {w.name} {x.shape} bias={with_bias} flags={flags}")
+    wd = {n: (None if v is None else dev(v, w.dtype)) for n, v in p.items()}
+    y = dsp.dsp_st_block_forward(dev(x, "f32"), wd, w.H, flags=flags)
+    torch.cuda.synchronize()
+    want = oracle.st_block(x, _oracle_params(p), w.H, flags=flags)
+    assert_close(host(y), want, w.dtype, w.name)
+
+
+@pytest.mark.parametrize("with_bias", [False, True])
+@pytest.mark.parametrize("flags", [0, 1])
+def test_small_block_bf16(torch, with_bias, flags):
+    w = synth.Workload("block_small", "block", "bf16", B=2, T=5, S=24, C=144, H=2, F=576, seed=11)
+    _block_case(torch, w, with_bias, flags)
+
+
+def test_small_block_f32(torch):
+    w = synth.Workload("block_small_f32", "block", "f32", B=1, T=4, S=9, C=64, H=4, F=128, seed=12)
+    _block_case(torch, w, True)
+
+
+def test_full_block_bf16(torch):
+    """The 720M-model block at B=1, T=32, S=1024 (C=1152, 16 heads, MLP 4608)."""
+    _block_case(torch, synth.WORKLOADS["block_bf16_B1_T32_S1024"], False)
