@@ -75,7 +75,8 @@ int dsp_version(void);
  *         this is the permute to (B,S,T,C).  Chunk n is what rank n receives
  *         in the all-to-all; the exchange itself is not part of this call.
  * from_dim == to_dim is the "no primitive" row of the table: y = copy of x.
- * Errors: DSP_ERR_NULL (x, y or shape NULL), DSP_ERR_DIM (ndim != 4 or a dim
+ * Errors: DSP_ERR_NULL (shape NULL, or x / y NULL for a non-empty tensor;
+ *   an empty tensor may come with NULL pointers), DSP_ERR_DIM (ndim != 4 or a dim
  *   not in {1,2}), DSP_ERR_SHAPE (a size < 0, n_chunks < 1, the to-dim not
  *   divisible by n_chunks, or more than 2^31 rows / 16-byte vectors),
  *   DSP_ERR_DTYPE, DSP_ERR_ARG (x and y overlap).  A tensor with a zero size
@@ -110,9 +111,10 @@ int dsp_switch_variant(const void* x, void* y, const int64_t* shape, int ndim, i
  * Supported D: DSP_BF16 -- D in {16, 32, 64, 72, 80, 96}; DSP_F32 --
  *   1 <= D <= 256.  bf16 needs 16-byte aligned q/k/v/o and ld_in, ld_out
  *   multiples of 8 (DSP_ERR_ALIGN otherwise).
- * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE (a size < 1, H*D > ld, unsupported D),
- *   DSP_ERR_DTYPE, DSP_ERR_ALIGN, DSP_ERR_HIP.  An empty batch (B, T or S
- *   equal to 0) is accepted and launches nothing.
+ * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE (a size < 0, H < 1, D < 1, H*D > ld,
+ *   unsupported D), DSP_ERR_DTYPE, DSP_ERR_ALIGN, DSP_ERR_ARG (scale NaN or
+ *   infinite), DSP_ERR_HIP.  An empty input (B, T or S equal to 0) is
+ *   accepted, may come with NULL pointers, and launches nothing.
  * ------------------------------------------------------------------------ */
 int dsp_spatial_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t T,
                      int64_t S, int H, int D, int64_t ld_in, int64_t ld_out, float scale,

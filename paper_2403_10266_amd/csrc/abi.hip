@@ -32,7 +32,7 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 
 int switch_impl(const void* x, void* y, const int64_t* shape, int ndim, int from_dim, int to_dim,
                 int n_chunks, int dtype, int variant, void* stream) {
-  if (!x || !y || !shape) return DSP_ERR_NULL;
+  if (!shape) return DSP_ERR_NULL;
   if (ndim != 4) return DSP_ERR_DIM;
   if (from_dim < 1 || from_dim > 2 || to_dim < 1 || to_dim > 2) return DSP_ERR_DIM;
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
@@ -45,8 +45,9 @@ int switch_impl(const void* x, void* y, const int64_t* shape, int ndim, int from
   if (!mul_ok(B, D1, &rows) || !mul_ok(rows, D2, &rows) || !mul_ok(rows, C, &elems) ||
       !mul_ok(elems, elem_size(dtype), &bytes))
     return DSP_ERR_SHAPE;
+  if (bytes == 0) return DSP_OK;  // empty: NULL pointers allowed, nothing launched
+  if (!x || !y) return DSP_ERR_NULL;
   if (overlap(x, (size_t)bytes, y, (size_t)bytes)) return DSP_ERR_ARG;
-  if (bytes == 0) return DSP_OK;
   const int64_t row_bytes = C * elem_size(dtype);
   const bool rows_ok = row_bytes % 16 == 0 && aligned(x, 16) && aligned(y, 16);
   if (variant == 1 && !rows_ok) return DSP_ERR_ALIGN;
@@ -59,9 +60,9 @@ int switch_impl(const void* x, void* y, const int64_t* shape, int ndim, int from
 int attn_impl(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X, int64_t L,
               int H, int D, int64_t ld_in, int64_t ld_out, float scale, int dtype, void* stream,
               bool spatial) {
-  if (!q || !k || !v || !o) return DSP_ERR_NULL;
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
   if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
+  if ((!q || !k || !v || !o) && B != 0 && X != 0 && L != 0) return DSP_ERR_NULL;
   if ((int64_t)H * D > ld_in || (int64_t)H * D > ld_out) return DSP_ERR_SHAPE;
   if (isnan(scale) || isinf(scale)) return DSP_ERR_ARG;
   if (dtype == DSP_BF16) {
@@ -95,10 +96,12 @@ int attn_impl(const void* q, const void* k, const void* v, void* o, int64_t B, i
 
 int linear_impl(const void* a, const void* w, const void* bias, const float* residual, void* out,
                 int64_t M, int N, int K, int epilogue, int dtype, hipStream_t s) {
-  if (!a || !w || !out) return DSP_ERR_NULL;
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
   if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
   if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_F32) return DSP_ERR_ARG;
+  if (!w) return DSP_ERR_NULL;
+  if (M == 0) return DSP_OK;
+  if (!a || !out) return DSP_ERR_NULL;
   if (epilogue == DSP_EPI_RESID && !residual) return DSP_ERR_NULL;
   int64_t mk, mn;
   if (!mul_ok(M, K, &mk) || !mul_ok(M, N, &mn)) return DSP_ERR_SHAPE;
@@ -191,9 +194,10 @@ int dsp_temporal_attn(const void* q, const void* k, const void* v, void* o, int6
 
 int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows, int C, float eps,
                   void* stream) {
-  if (!x || !y) return DSP_ERR_NULL;
   if (!valid_dtype(x_dtype) || !valid_dtype(y_dtype)) return DSP_ERR_DTYPE;
   if (rows < 0 || C < 1) return DSP_ERR_SHAPE;
+  if (rows == 0) return DSP_OK;
+  if (!x || !y) return DSP_ERR_NULL;
   if (!(eps >= 0.0f) || isinf(eps)) return DSP_ERR_ARG;
   int64_t n;
   if (!mul_ok(rows, C, &n)) return DSP_ERR_SHAPE;
