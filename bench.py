@@ -48,8 +48,15 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="approximate seconds of oracle work for the CPU baseline")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per launch of the spatial kernel")
+    ap.add_argument("--traffic", default=os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                      "profiles", "attention_hbm_traffic.txt"),
+                    help="rocprofv3 summary with the measured HBM bytes per launch of the "
+                         "spatial kernel; used only while the kernel source is unchanged")
+    ap.add_argument("--only", default=None,
+                    choices=["switch", "spatial", "temporal", "block", "copy"],
+                    help="run a single part (for profiling); prints per-kernel times only. "
+                         "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
+                         "plain 604 MB copy used to calibrate traffic counters")
     return ap.parse_args()
 
 
@@ -72,43 +79,52 @@ def main():
         return (t.to(torch.bfloat16) if dt == "bf16" else t).to(dev)
 
     W = synth.WORKLOADS
-    # ---- inputs (seeded, synthetic), resident in HBM
-    ws = W["switch_bf16_T64_S4096"]
-    x_sw = to_dev(synth.switch_input(ws), "bf16")
-    y_sw = torch.empty((ws.n_chunks, ws.B, ws.S // ws.n_chunks, ws.T, ws.C), dtype=torch.bfloat16, device=dev)
-
-    wsp = W["spatial_bf16_B2_T16_S4096"]
-    q_sp, k_sp, v_sp = (to_dev(a, "bf16") for a in synth.qkv_inputs(wsp, "BTSC"))
-    o_sp = torch.empty_like(q_sp)
-
-    wtp = W["temporal_bf16_B2_S512_T128"]
-    q_tp, k_tp, v_tp = (to_dev(a, "bf16") for a in synth.qkv_inputs(wtp, "BSTC"))
-    o_tp = torch.empty_like(q_tp)
-
-    wbl = W["block_bf16_B1_T32_S1024"]
-    x_bl_np, p_bl = synth.block_inputs(wbl)
-    x_bl = to_dev(x_bl_np, "f32")
-    w_bl = {n: (None if v is None else to_dev(v, "bf16")) for n, v in p_bl.items()}
-    y_bl = torch.empty((wbl.B, wbl.S, wbl.T, wbl.C), dtype=torch.float32, device=dev)
-    ws_bytes = dsp.block_workspace_bytes(wbl.B, wbl.T, wbl.S, wbl.C, wbl.H, wbl.F, dsp.DSP_BF16)
-    ws_bl = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    del x_bl_np, p_bl
+    ws, wsp, wtp, wbl = (W["switch_bf16_T64_S4096"], W["spatial_bf16_B2_T16_S4096"],
+                         W["temporal_bf16_B2_S512_T128"], W["block_bf16_B1_T32_S1024"])
+    wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block"}
+    if "copy" in wanted:
+        wanted.add("switch")
+    t = {}
+    # ---- inputs (seeded, synthetic), resident in HBM before timing
+    if "switch" in wanted:
+        t["x_sw"] = to_dev(synth.switch_input(ws), "bf16")
+        t["y_sw"] = torch.empty((ws.n_chunks, ws.B, ws.S // ws.n_chunks, ws.T, ws.C),
+                                dtype=torch.bfloat16, device=dev)
+    if "spatial" in wanted:
+        t["q_sp"], t["k_sp"], t["v_sp"] = (to_dev(a, "bf16") for a in synth.qkv_inputs(wsp, "BTSC"))
+        t["o_sp"] = torch.empty_like(t["q_sp"])
+    if "temporal" in wanted:
+        t["q_tp"], t["k_tp"], t["v_tp"] = (to_dev(a, "bf16") for a in synth.qkv_inputs(wtp, "BSTC"))
+        t["o_tp"] = torch.empty_like(t["q_tp"])
+    if "block" in wanted:
+        x_bl_np, p_bl = synth.block_inputs(wbl)
+        t["x_bl"] = to_dev(x_bl_np, "f32")
+        t["w_bl"] = {n: (None if v is None else to_dev(v, "bf16")) for n, v in p_bl.items()}
+        t["y_bl"] = torch.empty((wbl.B, wbl.S, wbl.T, wbl.C), dtype=torch.float32, device=dev)
+        ws_bytes = dsp.block_workspace_bytes(wbl.B, wbl.T, wbl.S, wbl.C, wbl.H, wbl.F, dsp.DSP_BF16)
+        t["ws_bl"] = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        del x_bl_np, p_bl
     torch.cuda.synchronize()
 
     def run_switch():
-        dsp.dsp_switch(x_sw, 1, 2, ws.n_chunks, out=y_sw)
+        dsp.dsp_switch(t["x_sw"], 1, 2, ws.n_chunks, out=t["y_sw"])
 
     def run_spatial():
-        dsp.dsp_spatial_attn(q_sp, k_sp, v_sp, wsp.H, out=o_sp)
+        dsp.dsp_spatial_attn(t["q_sp"], t["k_sp"], t["v_sp"], wsp.H, out=t["o_sp"])
 
     def run_temporal():
-        dsp.dsp_temporal_attn(q_tp, k_tp, v_tp, wtp.H, out=o_tp)
+        dsp.dsp_temporal_attn(t["q_tp"], t["k_tp"], t["v_tp"], wtp.H, out=t["o_tp"])
 
     def run_block():
-        dsp.dsp_st_block_forward(x_bl, w_bl, wbl.H, out=y_bl, workspace=ws_bl)
+        dsp.dsp_st_block_forward(t["x_bl"], t["w_bl"], wbl.H, out=t["y_bl"], workspace=t["ws_bl"])
+
+    def run_copy():
+        dsp.dsp_switch(t["x_sw"], 1, 1, 1, out=t["y_sw"].view(t["x_sw"].shape))
 
     parts = [("switch", run_switch), ("spatial", run_spatial), ("temporal", run_temporal),
              ("block", run_block)]
+    if args.only:
+        parts = [(args.only, run_copy if args.only == "copy" else dict(parts)[args.only])]
 
     for _ in range(args.warmup):
         for _, fn in parts:
@@ -128,13 +144,15 @@ def main():
     wall = time.perf_counter() - t0
     ms = {name: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(K)]))
           for i, (name, _) in enumerate(parts)}
+    if args.only:
+        print(json.dumps({"only": args.only, "steps": K, "kernel_ms": ms}), flush=True)
+        return
 
     # ---- accounting
-    sw_bytes = 2.0 * x_sw.numel() * x_sw.element_size()
+    sw_bytes = 2.0 * t["x_sw"].numel() * t["x_sw"].element_size()
     F_sp = attn_flops(wsp.B * wsp.T * wsp.H, wsp.S, wsp.D)
     F_tp = attn_flops(wtp.B * wtp.S * wtp.H, wtp.T, wtp.D)
-    tp_bytes = 4.0 * q_tp.numel() * 2
-    sp_bytes = 4.0 * q_sp.numel() * 2
+    tp_bytes = 4.0 * t["q_tp"].numel() * 2
     tok = wbl.B * wbl.T * wbl.S
     C, F = wbl.C, wbl.F
     F_bl = (2.0 * tok * C * (3 * C) * 2 + 2.0 * tok * C * C * 2 + 2.0 * tok * C * F * 2
@@ -146,10 +164,7 @@ def main():
     sw_gbps = sw_bytes / (ms["switch"] * 1e-3) / 1e9
     tp_gbps = tp_bytes / (ms["temporal"] * 1e-3) / 1e9
 
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            traffic = json.load(f).get("spatial_bytes_per_launch")
+    traffic = measured_traffic(args.traffic)
 
     out = {
         "metric": METRIC,
@@ -178,7 +193,7 @@ def main():
             "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
         },
         "roofline": {
-            "kernel": "spatial attention (attn_fwd_kernel<72,4,2>)",
+            "kernel": "spatial attention attn_fwd_kernel<72,8,2,64,2,2> (B2 T16 S4096 H16 D72)",
             "bound": "mfma",
             "achieved": round(sp_tflops, 2),
             "peak": MFMA_BF16_PEAK_TFLOPS,
@@ -190,6 +205,28 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_budget)
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic(path):
+    """HBM bytes per launch of the spatial kernel from the committed counter
+    summary, or None when the summary is missing or the kernel source has
+    changed since the counters were taken."""
+    import hashlib
+    if not path or not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2403_10266_amd", "csrc",
+                       "attn_bf16.hip")
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    if kv.get("spatial_source_sha256_16") != sha or "spatial_bytes_per_launch" not in kv:
+        return None
+    return int(kv["spatial_bytes_per_launch"])
 
 
 def cpu_baseline(budget_s: float) -> dict:

@@ -3,7 +3,7 @@
 // (Eq. 7-8): every (batch, other-dimension index, head) triple is an
 // independent problem over L consecutive sequence positions.  Spatial
 // attention (L = S) and temporal attention (L = T) are the same kernel with
-// different L and strides.
+// different L, strides and tiling.
 //
 // Design for gfx950 (CDNA4):
 //  * Both products run on v_mfma_f32_32x32x16_bf16 and are computed
@@ -16,24 +16,66 @@
 //    16-key step is permuted identically on both operands), so P never goes
 //    through LDS.
 //  * Head width D is padded to 16 for Q K^T (D=72 -> 80, 90% useful) and to
-//    32 for P V (72 -> 96).  Padding columns of K in LDS are zero; for D not
-//    a multiple of 32, padding column D of V is 1.0, so the P V product also
-//    yields the softmax row sum from the bf16 probabilities actually used.
-//  * K and V tiles of 64 keys are staged in LDS, double-buffered, with
-//    register prefetch of the next tile overlapping the current tile's math.
-//    K rows are read as 16-byte MFMA A fragments (row pitch an odd multiple
-//    of 16 bytes: conflict-free); V fragments come straight from row-major
-//    LDS through ds_read_b64_tr_b16, so V is never transposed in memory.
-//  * Online softmax in the exp2 domain with the running maximum updated
-//    lazily: a wave only rescales its O accumulators when some query's block
-//    maximum exceeds its running maximum by more than 2^8, which after the
-//    first blocks is rare; exactness does not depend on the reference point.
+//    32 for P V (72 -> 96).  For D not a multiple of 32, padding column D of
+//    V is 1.0 in LDS, so the P V product also yields the softmax row sum from
+//    the bf16 probabilities actually used.
+//  * The softmax scale and log2(e) are folded into Q once (Q' = Q * scale *
+//    log2 e, rounded to bf16), so the MFMA produces scores in the exp2
+//    domain.  When D leaves a spare column in the Q K^T contraction (D % 16
+//    == 8, e.g. 72), K's padding column D is 1.0 and Q's is -m (the running
+//    reference maximum, as bf16): the MFMA then also subtracts the maximum
+//    and the VALU only evaluates exp2 -- no per-score FMA.
+//  * Online softmax with a lazily moved reference maximum: a lane moves it
+//    only when a tile maximum exceeds it by more than 2^8, and O is rescaled
+//    only when some lane of the wave moved; the result does not depend on
+//    the reference point (the row sum uses the same reference).
+//  * K and V tiles of 64 keys are staged in LDS, double-buffered, with the
+//    next tile prefetched into registers during the current tile's math.
+//    Tiles are fetched with buffer loads through a per-tile buffer resource:
+//    rows past L fall outside the resource's range and read as zero, so there
+//    are no per-lane bounds checks or address computations in the loop.  Half
+//    of the work-group's waves fetch K, the other half V (the resource is
+//    wave-uniform).  K rows are read as 16-byte MFMA A fragments (row pitch
+//    an odd multiple of 16 bytes: conflict-free); V fragments come straight
+//    from row-major LDS through ds_read_b64_tr_b16, so V is never transposed.
 //  * Work-group index -> (unit, query block) is remapped so that consecutive
 //    units land on the same XCD: the query blocks of a unit, and neighbouring
 //    heads of a token row, then share that XCD's L2.
 #include <math.h>
 
 #include "dsp_internal.h"
+
+// Compile-time tiling of the long-sequence (spatial) and short-sequence
+// (temporal) launches: waves per work-group, 32-query tiles per wave, keys per
+// LDS tile, minimum waves per SIMD the register allocation must allow.
+#ifndef DSP_SATTN_NW
+#define DSP_SATTN_NW 8
+#endif
+#ifndef DSP_SATTN_QT
+#define DSP_SATTN_QT 2
+#endif
+#ifndef DSP_SATTN_KB
+#define DSP_SATTN_KB 64
+#endif
+#ifndef DSP_SATTN_MINW
+#define DSP_SATTN_MINW 2
+#endif
+#ifndef DSP_TATTN_NW
+#define DSP_TATTN_NW 4
+#endif
+#ifndef DSP_TATTN_QT
+#define DSP_TATTN_QT 1
+#endif
+#ifndef DSP_TATTN_KB
+#define DSP_TATTN_KB 64
+#endif
+#ifndef DSP_TATTN_MINW
+#define DSP_TATTN_MINW 2
+#endif
+// Fold the running maximum into the Q K^T contraction when D allows it.
+#ifndef DSP_ATTN_BIAS_COLUMN
+#define DSP_ATTN_BIAS_COLUMN 1
+#endif
 
 namespace dsp {
 namespace {
@@ -44,9 +86,10 @@ typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short shortx8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int KB = 64;          // keys per LDS tile (two 32-key MFMA tiles)
-constexpr float kLazyRescale = 8.0f;  // log2 headroom before the running max is moved
+constexpr float kLazyRescale = 8.0f;       // log2 headroom before the reference moves
+constexpr int kRsrcWord3 = 0x00020000;     // buffer resource flags, gfx9 family
 
 __device__ __forceinline__ float swap_halves(float v) {
   // value held by lane (l ^ 32)
@@ -59,15 +102,17 @@ __device__ __forceinline__ shortx4 lds_read_tr(const bf16* p) {
       (__attribute__((address_space(3))) shortx4*)(p));
 }
 
-template <int D>
+template <int D, int KB>
 struct Geo {
   static constexpr int NDK = (D + 15) / 16;       // 16-wide d steps of Q K^T
   static constexpr int NDV = (D + 31) / 32;       // 32-row d tiles of P V
   static constexpr bool ONES = (D % 32) != 0;     // spare V column carries the row sum
+  static constexpr bool BIAS = DSP_ATTN_BIAS_COLUMN && (D % 16) == 8;  // spare Q K^T column
   static constexpr int KP = NDK * 16 + 8;         // K row pitch (elements)
   static constexpr int VP = NDV * 32 + 16;        // V row pitch (elements)
   static constexpr int CH = D / 8;                // 16-byte chunks per row
   static constexpr int TILE_ELEMS = KB * (KP + VP);
+  static constexpr int NKT = KB / 32;             // 32-key MFMA tiles per LDS tile
 };
 
 struct Params {
@@ -80,48 +125,64 @@ struct Params {
   float c;  // scale * log2(e)
 };
 
-template <int D, int NW, int QT>
-__global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(Params p) {
-  using G = Geo<D>;
+// Work-group -> unit and query block (XCD-aware), and the unit's base offsets.
+struct UnitMap {
+  uint32_t qb;
+  int64_t in_base, out_base;
+};
+
+__device__ __forceinline__ UnitMap map_unit(const Params& p, int D) {
+  uint32_t bid = blockIdx.x;
+  // hardware places block i on XCD i % 8; give each XCD a contiguous range
+  if ((p.n_blocks & 7u) == 0) bid = (bid & 7u) * (p.n_blocks >> 3) + (bid >> 3);
+  const uint32_t unit = bid / p.n_qb;
+  UnitMap m;
+  m.qb = bid - unit * p.n_qb;
+  const uint32_t h = unit % p.H;
+  const uint32_t bx = unit / p.H;
+  const uint32_t xx = bx % p.X;
+  const uint32_t bb = bx / p.X;
+  m.in_base = (int64_t)bb * p.b_in + (int64_t)xx * p.x_in + (int64_t)h * D;
+  m.out_base = (int64_t)bb * p.b_out + (int64_t)xx * p.x_out + (int64_t)h * D;
+  return m;
+}
+
+template <int D, int NW, int QT, int KB, int MINW, int NBUF>
+__global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
+  // NBUF == 1: the launcher guarantees L <= KB (one tile, nothing to prefetch)
+  using G = Geo<D, KB>;
   constexpr int NT = NW * 64;
-  constexpr int QW = 32 * QT;                      // queries per wave
-  constexpr int QB = NW * QW;                      // queries per work-group
-  constexpr int NCHUNK = 2 * KB * G::CH;           // 16-byte chunks per K+V tile
-  constexpr int NLOAD = (NCHUNK + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) bf16 lds[2 * G::TILE_ELEMS];
+  constexpr int QB = NW * 32 * QT;
+  constexpr int NKT = G::NKT;
+  constexpr bool SPLIT = NW > 1;                       // K and V fetched by separate waves
+  constexpr int FT = SPLIT ? NT / 2 : NT;              // threads fetching one tensor
+  constexpr int TCH = KB * G::CH;                      // 16-byte chunks of one tensor tile
+  constexpr int NLOAD = (TCH + FT - 1) / FT;
+  static_assert(NW == 1 || NW % 2 == 0, "K/V fetch split needs an even wave count");
+  __shared__ __attribute__((aligned(16))) bf16 lds[NBUF * G::TILE_ELEMS];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int l32 = lane & 31;
   const int g = lane >> 5;
-
-  // XCD-aware block order: hardware places block i on XCD i % 8.
-  uint32_t bid = blockIdx.x;
-  if ((p.n_blocks & 7u) == 0) bid = (bid & 7u) * (p.n_blocks >> 3) + (bid >> 3);
-  const uint32_t unit = bid / p.n_qb;
-  const uint32_t qb = bid - unit * p.n_qb;
-  const uint32_t h = unit % p.H;
-  const uint32_t bx = unit / p.H;
-  const uint32_t xx = bx % p.X;
-  const uint32_t bb = bx / p.X;
-  const int64_t in_base = (int64_t)bb * p.b_in + (int64_t)xx * p.x_in + (int64_t)h * D;
-  const int64_t out_base = (int64_t)bb * p.b_out + (int64_t)xx * p.x_out + (int64_t)h * D;
-  const bf16* __restrict__ qg = p.q + in_base;
-  const bf16* __restrict__ kg = p.k + in_base;
-  const bf16* __restrict__ vg = p.v + in_base;
+  const UnitMap um = map_unit(p, D);
   const uint32_t L = p.L;
 
-  // ---- padding columns of both LDS buffers: K pad = 0, V pad = [1 (row sum), 0...]
-  for (int e = threadIdx.x; e < 2 * KB; e += NT) {
+  // ---- padding columns of the LDS buffers.  K: column D is 1.0 when it
+  // carries the bias, the rest 0.  V: column D is 1.0 (row sum), the rest 0.
+  for (int e = threadIdx.x; e < NBUF * KB; e += NT) {
     bf16* t = lds + (e / KB) * G::TILE_ELEMS;
     const int r = e % KB;
-    for (int c = D; c < G::KP; ++c) t[r * G::KP + c] = (bf16)0.0f;
+    for (int c = D; c < G::KP; ++c) t[r * G::KP + c] = (bf16)((G::BIAS && c == D) ? 1.0f : 0.0f);
     bf16* vt = t + KB * G::KP;
     for (int c = D; c < G::VP; ++c) vt[r * G::VP + c] = (bf16)((G::ONES && c == D) ? 1.0f : 0.0f);
   }
 
-  // ---- Q fragments (B operand of S^T = K Q^T): lane (n + 32g) holds Q[q][16s + 8g .. +7]
-  const uint32_t q_wave = qb * QB + wave * QW;
+  // ---- Q' = Q * scale * log2(e) as bf16 B fragments: lane (n + 32g) holds
+  // Q'[q][16s + 8g .. +7].  With the bias column, element D of Q' is the
+  // negated reference maximum (0 until the first tile sets it).
+  const uint32_t q_wave = um.qb * QB + wave * 32 * QT;
+  const bf16* qg = p.q + um.in_base;
   bf16x8 qf[QT][G::NDK];
 #pragma unroll
   for (int j = 0; j < QT; ++j) {
@@ -129,45 +190,68 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(Params p) {
 #pragma unroll
     for (int s = 0; s < G::NDK; ++s) {
       const int d = 16 * s + 8 * g;
+      bf16x8 v;
       if (q < L && d < D) {
-        qf[j][s] = *reinterpret_cast<const bf16x8*>(qg + (int64_t)q * p.r_in + d);
+        v = *reinterpret_cast<const bf16x8*>(qg + (int64_t)q * p.r_in + d);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (bf16)((float)v[e] * p.c);
       } else {
-        for (int e = 0; e < 8; ++e) qf[j][s][e] = (bf16)0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (bf16)0.0f;
       }
+      qf[j][s] = v;
     }
   }
+  constexpr int BS = G::NDK - 1;  // the d step holding column D (lanes g == 1)
 
-  // ---- tile loader: chunk c -> (tensor, row, column chunk)
-  uint4 pre[NLOAD];
-  auto load_tile = [&](uint32_t kb) {
+  // ---- tile fetch through buffer resources covering rows [kb, L) of the
+  // unit (rows past L read as zero).  With several waves, waves [0, NW/2)
+  // fetch K and the others V; a single wave fetches both.
+  const bool fetch_v = SPLIT && wave >= NW / 2;
+  const int ft = SPLIT ? threadIdx.x % FT : threadIdx.x;
+  const uint32_t row_bytes = (uint32_t)p.r_in * 2u;
+  uint32_t voff[NLOAD];
+  int lofs[NLOAD];
 #pragma unroll
-    for (int i = 0; i < NLOAD; ++i) {
-      const int c = threadIdx.x + i * NT;
-      pre[i] = make_uint4(0, 0, 0, 0);
-      if (c < NCHUNK) {
-        const int tsr = c / (KB * G::CH);
-        const int rc = c - tsr * (KB * G::CH);
-        const int row = rc / G::CH;
-        const int col = rc - row * G::CH;
-        if (kb + row < L) {
-          const bf16* src = (tsr ? vg : kg) + (int64_t)(kb + row) * p.r_in + col * 8;
-          pre[i] = *reinterpret_cast<const uint4*>(src);
-        }
-      }
-    }
+  for (int i = 0; i < NLOAD; ++i) {
+    const int c = ft + i * FT;
+    const int row = c / G::CH, col = c - row * G::CH;
+    voff[i] = (uint32_t)row * row_bytes + (uint32_t)col * 16u;
+    lofs[i] = row * G::KP + col * 8;                 // K layout; V adds its own base/pitch
+    if (fetch_v) lofs[i] = KB * G::KP + row * G::VP + col * 8;
+  }
+  auto rsrc = [&](const bf16* tensor, uint32_t kb) {
+    const uint32_t rows_left = kb < L ? L - kb : 0u;
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(tensor + um.in_base + (int64_t)kb * p.r_in),
+                                             (short)0, (int)(rows_left * row_bytes), kRsrcWord3);
   };
-  auto store_tile = [&](int buf) {
+  u32x4 pre[SPLIT ? NLOAD : 1];
+  auto fetch = [&](uint32_t kb) {  // SPLIT: one tensor into registers
+    const __amdgpu_buffer_rsrc_t rs = rsrc(fetch_v ? p.v : p.k, kb);
+#pragma unroll
+    for (int i = 0; i < NLOAD; ++i)
+      if (ft + i * FT < TCH) pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
+  };
+  auto stash = [&](int buf) {  // SPLIT: registers into LDS buffer `buf`
     bf16* t = lds + buf * G::TILE_ELEMS;
 #pragma unroll
-    for (int i = 0; i < NLOAD; ++i) {
-      const int c = threadIdx.x + i * NT;
-      if (c < NCHUNK) {
-        const int tsr = c / (KB * G::CH);
-        const int rc = c - tsr * (KB * G::CH);
-        const int row = rc / G::CH;
-        const int col = rc - row * G::CH;
-        bf16* dst = tsr ? (t + KB * G::KP + row * G::VP + col * 8) : (t + row * G::KP + col * 8);
-        *reinterpret_cast<uint4*>(dst) = pre[i];
+    for (int i = 0; i < NLOAD; ++i)
+      if (ft + i * FT < TCH) *reinterpret_cast<u32x4*>(t + lofs[i]) = pre[i];
+  };
+  auto fetch_single = [&](uint32_t kb, int buf) {  // one wave: both tensors straight to LDS
+    bf16* t = lds + buf * G::TILE_ELEMS;
+#pragma unroll
+    for (int tsr = 0; tsr < 2; ++tsr) {
+      const __amdgpu_buffer_rsrc_t rs = rsrc(tsr ? p.v : p.k, kb);
+#pragma unroll
+      for (int i = 0; i < NLOAD; ++i) {
+        const int c = ft + i * FT;
+        if (c < TCH) {
+          const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
+          const int row = c / G::CH, col = c - row * G::CH;
+          bf16* dst = tsr ? t + KB * G::KP + row * G::VP + col * 8 : t + lofs[i];
+          *reinterpret_cast<u32x4*>(dst) = v;
+        }
       }
     }
   };
@@ -179,110 +263,133 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(Params p) {
     for (int j = 0; j < QT; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[t][j][r] = 0.0f;
-  float m_run[QT], l_run[QT];
+  // m_ref: reference maximum currently applied (exp2 domain); -inf before the first tile
+  float m_ref[QT], l_run[QT];
 #pragma unroll
-  for (int j = 0; j < QT; ++j) { m_run[j] = -INFINITY; l_run[j] = 0.0f; }
+  for (int j = 0; j < QT; ++j) { m_ref[j] = -INFINITY; l_run[j] = 0.0f; }
 
   const uint32_t n_kb = (L + KB - 1) / KB;
-  load_tile(0);
-  __syncthreads();  // padding columns written before tile rows land beside them
-  store_tile(0);
+  if (SPLIT) {
+    fetch(0);
+    stash(0);
+  } else {
+    fetch_single(0, 0);
+  }
   __syncthreads();
 
   for (uint32_t it = 0; it < n_kb; ++it) {
     const uint32_t kb = it * KB;
-    if (it + 1 < n_kb) load_tile(kb + KB);
-    const bf16* kt_lds = lds + (it & 1) * G::TILE_ELEMS;
-    const bf16* vt_lds = kt_lds + KB * G::KP;
+    const bool more = NBUF > 1 && it + 1 < n_kb;
+    if (SPLIT && more) fetch(kb + KB);
+    const bf16* k_lds = lds + (NBUF > 1 ? (it & 1) : 0) * G::TILE_ELEMS;
 
-    // S^T = K Q^T for two 32-key tiles
-    floatx16 sacc[2][QT];
+    // ---- S'^T = K Q'^T (exp2-domain scores, minus the reference with BIAS)
+    floatx16 s[NKT][QT];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
+    for (int kt = 0; kt < NKT; ++kt) {
 #pragma unroll
       for (int j = 0; j < QT; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[kt][j][r] = 0.0f;
+        for (int r = 0; r < 16; ++r) s[kt][j][r] = 0.0f;
 #pragma unroll
-      for (int s = 0; s < G::NDK; ++s) {
+      for (int st = 0; st < G::NDK; ++st) {
         const bf16x8 a =
-            *reinterpret_cast<const bf16x8*>(kt_lds + (32 * kt + l32) * G::KP + 16 * s + 8 * g);
+            *reinterpret_cast<const bf16x8*>(k_lds + (32 * kt + l32) * G::KP + 16 * st + 8 * g);
 #pragma unroll
         for (int j = 0; j < QT; ++j)
-          sacc[kt][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[j][s], sacc[kt][j], 0, 0, 0);
+          s[kt][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[j][st], s[kt][j], 0, 0, 0);
       }
     }
-
-    // mask keys past L (only the last tile can hold any)
-    if (kb + KB > L) {
+    if (kb + KB > L) {  // keys past L: score -inf (only the last tile can hold any)
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const uint32_t key = kb + 32 * kt + (r / 4) * 8 + 4 * g + (r % 4);
           if (key >= L) {
 #pragma unroll
-            for (int j = 0; j < QT; ++j) sacc[kt][j][r] = -INFINITY;
+            for (int j = 0; j < QT; ++j) s[kt][j][r] = -INFINITY;
           }
         }
     }
 
-    // online softmax (exp2 domain), lazily moved reference maximum
-    float mblk[QT];
+    // ---- online softmax with a lazily moved reference
+    float mx[QT];
     bool need = false;
 #pragma unroll
     for (int j = 0; j < QT; ++j) {
-      float mx = sacc[0][j][0];
+      float m = s[0][j][0];
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[0][j][r]);
+      for (int r = 1; r < 16; ++r) m = fmaxf(m, s[0][j][r]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[1][j][r]);
-      mx = fmaxf(mx, swap_halves(mx));
-      mblk[j] = mx * p.c;
-      need |= mblk[j] > m_run[j] + kLazyRescale;
+      for (int kt = 1; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[kt][j][r]);
+      m = fmaxf(m, swap_halves(m));
+      // with BIAS the scores are relative to the reference the MFMA applied
+      // (0 before the first tile); mx is the absolute tile maximum
+      const float applied = m_ref[j] == -INFINITY ? 0.0f : m_ref[j];
+      mx[j] = G::BIAS ? m + applied : m;
+      need |= !(mx[j] <= m_ref[j] + kLazyRescale);
     }
     if (__any(need)) {
+      // rare path (the first tile, occasionally later): move the references,
+      // rescale O, and re-base this tile's scores on the new reference
 #pragma unroll
       for (int j = 0; j < QT; ++j) {
-        const float mnew = fmaxf(m_run[j], mblk[j]);
-        const float alpha = __builtin_amdgcn_exp2f(m_run[j] - mnew);
-        m_run[j] = mnew;
+        const bool mv = !(mx[j] <= m_ref[j] + kLazyRescale);
+        float m_new = mv ? mx[j] : m_ref[j];
+        if (G::BIAS) m_new = -(float)(bf16)(-m_new);  // the applied reference is a bf16 value
+        const float alpha = m_ref[j] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_ref[j] - m_new);
+        const float applied = m_ref[j] == -INFINITY ? 0.0f : m_ref[j];
+        m_ref[j] = m_new;
         l_run[j] *= alpha;
 #pragma unroll
         for (int t = 0; t < G::NDV; ++t)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[t][j][r] *= alpha;
+        if (G::BIAS) {
+          const float sub = m_new - applied;
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s[kt][j][r] -= sub;
+          if (g == 1) qf[j][BS][0] = (bf16)(-m_new);
+        }
       }
     }
-    bf16x8 pf[2][2][QT];  // [key tile][16-key step][query tile]
+    // probabilities as bf16 B fragments (with BIAS the scores are already
+    // relative to the reference; otherwise subtract it here)
+    bf16x8 pf[NKT][2][QT];
 #pragma unroll
     for (int j = 0; j < QT; ++j) {
-      const float mc = m_run[j];
       float ls = 0.0f;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(sacc[kt][j][r], p.c, -mc));
+          const float e = G::BIAS ? __builtin_amdgcn_exp2f(s[kt][j][r])
+                                  : __builtin_amdgcn_exp2f(s[kt][j][r] - m_ref[j]);
           if (!G::ONES) ls += e;
           pf[kt][r / 8][j][r % 8] = (bf16)e;
         }
       if (!G::ONES) l_run[j] += ls;
     }
 
-    // O^T += V^T P^T: A fragment of V^T via transposing LDS reads
+    // ---- O^T += V^T P^T, V fragments read transposed from row-major LDS
+    const bf16* v_lds = k_lds + KB * G::KP;
     const int j16 = lane & 15;
     const int mbase = 16 * ((lane >> 4) & 1);
 #pragma unroll
     for (int t = 0; t < G::NDV; ++t) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           const int row = 32 * kt + 16 * kk + 4 * g + (j16 >> 2);
           const int col = 32 * t + mbase + 4 * (j16 & 3);
-          const shortx4 lo = lds_read_tr(vt_lds + row * G::VP + col);
-          const shortx4 hi = lds_read_tr(vt_lds + (row + 8) * G::VP + col);
+          const shortx4 lo = lds_read_tr(v_lds + row * G::VP + col);
+          const shortx4 hi = lds_read_tr(v_lds + (row + 8) * G::VP + col);
           const shortx8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
           const bf16x8 a = __builtin_bit_cast(bf16x8, both);
 #pragma unroll
@@ -291,12 +398,18 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(Params p) {
         }
     }
 
-    if (it + 1 < n_kb) store_tile((it + 1) & 1);
+    if (more) {
+      if (SPLIT) {
+        stash((it + 1) & 1);
+      } else {
+        fetch_single(kb + KB, (it + 1) & 1);
+      }
+    }
     __syncthreads();
   }
 
   // ---- normalise and store: lane (n + 32g) holds O^T[32t + 8(r/4) + 4g + r%4][q]
-  bf16* __restrict__ og = p.o + out_base;
+  bf16* og = p.o + um.out_base;
 #pragma unroll
   for (int j = 0; j < QT; ++j) {
     float l;
@@ -331,8 +444,9 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(Params p) {
   }
 }
 
-template <int D, int NW, int QT>
+template <int D, int NW, int QT, int KB, int MINW, int NBUF = 2>
 int launch_cfg(const AttnArgs& a, hipStream_t s) {
+  if (NBUF == 1 && a.L > KB) return DSP_ERR_SHAPE;
   constexpr int QB = NW * 32 * QT;
   Params p;
   p.q = static_cast<const bf16*>(a.q);
@@ -352,21 +466,30 @@ int launch_cfg(const AttnArgs& a, hipStream_t s) {
   const int64_t n_qb = (a.L + QB - 1) / QB;
   const int64_t blocks = units * n_qb;
   if (blocks == 0) return DSP_OK;
-  if (blocks >= (int64_t(1) << 31) || a.L >= (int64_t(1) << 30)) return DSP_ERR_SHAPE;
+  // buffer resources address one unit's rows with 32-bit byte offsets
+  if (blocks >= (int64_t(1) << 31) || a.L * a.r_stride_in * 2 >= (int64_t(1) << 31))
+    return DSP_ERR_SHAPE;
   p.n_units = (uint32_t)units;
   p.n_qb = (uint32_t)n_qb;
   p.n_blocks = (uint32_t)blocks;
   p.c = a.scale * 1.4426950408889634f;
-  hipLaunchKernelGGL((attn_fwd_kernel<D, NW, QT>), dim3((uint32_t)blocks), dim3(NW * 64), 0, s, p);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, NW, QT, KB, MINW, NBUF>), dim3((uint32_t)blocks),
+                     dim3(NW * 64), 0, s, p);
   return last_launch_status();
 }
 
 template <int D>
 int launch_d(const AttnArgs& a, hipStream_t s) {
-  if (a.L <= 32) return launch_cfg<D, 1, 1>(a, s);
-  if (a.L <= 64) return launch_cfg<D, 2, 1>(a, s);
-  if (a.L <= 128) return launch_cfg<D, 2, 2>(a, s);
-  return launch_cfg<D, 4, 2>(a, s);
+  // short sequences: the whole unit is one tile, fetched at once
+  if (a.L <= 32) return launch_cfg<D, 1, 1, 32, 1, 1>(a, s);
+  if (a.L <= 64) return launch_cfg<D, 2, 1, 64, 2, 1>(a, s);
+  if (a.L <= 128) {
+    if constexpr (DSP_TATTN_KB >= 128)
+      return launch_cfg<D, DSP_TATTN_NW, DSP_TATTN_QT, 128, DSP_TATTN_MINW, 1>(a, s);
+    else
+      return launch_cfg<D, DSP_TATTN_NW, DSP_TATTN_QT, DSP_TATTN_KB, DSP_TATTN_MINW>(a, s);
+  }
+  return launch_cfg<D, DSP_SATTN_NW, DSP_SATTN_QT, DSP_SATTN_KB, DSP_SATTN_MINW>(a, s);
 }
 
 }  // namespace

@@ -60,8 +60,23 @@ struct RowMap {
   }
 };
 
-constexpr int kRowThreads = 256;
-constexpr int kRowVecPerThread = 8;
+// Tuning knobs (compile time): 16-byte vectors per thread, and whether loads
+// and stores carry the non-temporal hint.
+#ifndef DSP_SWITCH_VPT
+#define DSP_SWITCH_VPT 4
+#endif
+#ifndef DSP_SWITCH_NT_LOAD
+#define DSP_SWITCH_NT_LOAD 1
+#endif
+#ifndef DSP_SWITCH_NT_STORE
+#define DSP_SWITCH_NT_STORE 1
+#endif
+#ifndef DSP_SWITCH_THREADS
+#define DSP_SWITCH_THREADS 512
+#endif
+
+constexpr int kRowThreads = DSP_SWITCH_THREADS;
+constexpr int kRowVecPerThread = DSP_SWITCH_VPT;
 
 // Moves 16-byte vectors.  Vector v of the output is (row ro = v / V, column
 // c = v % V) and comes from vector src_row(ro) * V + c of the input.
@@ -82,12 +97,16 @@ __global__ __launch_bounds__(kRowThreads) void switch_rows_kernel(
         const uint32_t c = v - ro * V;
         src = map.src_row(ro) * V + c;
       }
-      buf[u] = __builtin_nontemporal_load(x + src);
+      if (DSP_SWITCH_NT_LOAD) buf[u] = __builtin_nontemporal_load(x + src);
+      else buf[u] = x[src];
     }
   }
 #pragma unroll
   for (int u = 0; u < kRowVecPerThread; ++u) {
-    if (dst[u] < n_vec) __builtin_nontemporal_store(buf[u], y + dst[u]);
+    if (dst[u] < n_vec) {
+      if (DSP_SWITCH_NT_STORE) __builtin_nontemporal_store(buf[u], y + dst[u]);
+      else y[dst[u]] = buf[u];
+    }
   }
 }
 
