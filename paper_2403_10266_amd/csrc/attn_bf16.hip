@@ -97,6 +97,17 @@ __device__ __forceinline__ float swap_halves(float v) {
   return __uint_as_float(threadIdx.x & 32 ? r[0] : r[1]);
 }
 
+// Buffer resource over [base, base + bytes): all inputs are wave-uniform, and are
+// passed through readfirstlane so the descriptor is built in scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  const uint32_t n = __builtin_amdgcn_readfirstlane(bytes);
+  void* p = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)n, kRsrcWord3);
+}
+
 __device__ __forceinline__ shortx4 lds_read_tr(const bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (__attribute__((address_space(3))) shortx4*)(p));
@@ -162,7 +173,9 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   __shared__ __attribute__((aligned(16))) bf16 lds[NBUF * G::TILE_ELEMS];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  // wave index as a scalar: the K/V choice of the tile fetch must be provably
+  // wave-uniform, or the buffer resource would need a waterfall loop
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31;
   const int g = lane >> 5;
   const UnitMap um = map_unit(p, D);
@@ -222,8 +235,7 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   }
   auto rsrc = [&](const bf16* tensor, uint32_t kb) {
     const uint32_t rows_left = kb < L ? L - kb : 0u;
-    return __builtin_amdgcn_make_buffer_rsrc((void*)(tensor + um.in_base + (int64_t)kb * p.r_in),
-                                             (short)0, (int)(rows_left * row_bytes), kRsrcWord3);
+    return make_rsrc(tensor + um.in_base + (int64_t)kb * p.r_in, rows_left * row_bytes);
   };
   u32x4 pre[SPLIT ? NLOAD : 1];
   auto fetch = [&](uint32_t kb) {  // SPLIT: one tensor into registers
