@@ -72,6 +72,11 @@
 #ifndef DSP_TATTN_MINW
 #define DSP_TATTN_MINW 2
 #endif
+// D % 32 == 8 (e.g. 72): the last 16 rows of O^T = V^T P^T (d = D - 8 .. D + 7,
+// holding the row-sum column) on 16x16x32 MFMAs instead of a padded 32-row tile.
+#ifndef DSP_ATTN_PV_SLAB
+#define DSP_ATTN_PV_SLAB 1
+#endif
 // Fold the running maximum into the Q K^T contraction when D allows it.
 #ifndef DSP_ATTN_BIAS_COLUMN
 #define DSP_ATTN_BIAS_COLUMN 1
@@ -85,6 +90,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short shortx8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4;
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -268,13 +274,24 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
     }
   };
 
-  floatx16 o[G::NDV][QT];
+  // O^T accumulators: NT32 tiles of 32 rows of d (32x32 MFMA layout), plus
+  // with SLAB the last 16 rows per 16-query half (16x16 MFMA layout)
+  constexpr bool SLAB = DSP_ATTN_PV_SLAB && (D % 32) == 8;
+  constexpr int NT32 = SLAB ? D / 32 : G::NDV;
+  floatx16 o[NT32 > 0 ? NT32 : 1][QT];
+  floatx4 os[QT][2];
 #pragma unroll
-  for (int t = 0; t < G::NDV; ++t)
+  for (int t = 0; t < NT32; ++t)
 #pragma unroll
     for (int j = 0; j < QT; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[t][j][r] = 0.0f;
+#pragma unroll
+  for (int j = 0; j < QT; ++j)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) os[j][h][r] = 0.0f;
   // m_ref: reference maximum currently applied (exp2 domain); -inf before the first tile
   float m_ref[QT], l_run[QT];
 #pragma unroll
@@ -357,9 +374,15 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
         m_ref[j] = m_new;
         l_run[j] *= alpha;
 #pragma unroll
-        for (int t = 0; t < G::NDV; ++t)
+        for (int t = 0; t < NT32; ++t)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[t][j][r] *= alpha;
+        if (SLAB) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) os[j][h][r] *= alpha;
+        }
         if (G::BIAS) {
           const float sub = m_new - applied;
 #pragma unroll
@@ -393,7 +416,7 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
     const int j16 = lane & 15;
     const int mbase = 16 * ((lane >> 4) & 1);
 #pragma unroll
-    for (int t = 0; t < G::NDV; ++t) {
+    for (int t = 0; t < NT32; ++t) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
@@ -408,6 +431,39 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
           for (int j = 0; j < QT; ++j)
             o[t][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[kt][kk][j], o[t][j], 0, 0, 0);
         }
+    }
+    if constexpr (SLAB) {
+      // rows d = 32 NT32 .. + 15 over each 32-key tile with 16x16x32 MFMAs.
+      // B operand (keys x 16 queries): lane group c = lane / 16 holds 8 keys
+      // for queries lane % 16.  One permlane16 swap of the two 16-key halves
+      // of a 32x32 probability tile yields it: group c then holds keys
+      // kb(c) + {0..3, 8..11} with kb = {0, 16, 4, 20}, for queries 0-15 of
+      // the tile in the first register and 16-31 in the second.
+      const int c = lane >> 4;
+      const int kbase = ((c & 1) ? 16 : 0) + ((c & 2) ? 4 : 0);
+      const int col = 32 * NT32 + 4 * (j16 & 3);
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        // A operand: lane (d + 16 c) holds V^T[d][keys of group c]
+        const int row = 32 * kt + kbase + (j16 >> 2);
+        const shortx4 lo = lds_read_tr(v_lds + row * G::VP + col);
+        const shortx4 hi = lds_read_tr(v_lds + (row + 8) * G::VP + col);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int j = 0; j < QT; ++j) {
+          u32x4 x = __builtin_bit_cast(u32x4, pf[kt][0][j]);
+          u32x4 y = __builtin_bit_cast(u32x4, pf[kt][1][j]);
+          u32x4 b0, b1;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
+            b0[w] = r[0];
+            b1[w] = r[1];
+          }
+          os[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, b0), os[j][0], 0, 0, 0);
+          os[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, b1), os[j][1], 0, 0, 0);
+        }
+      }
     }
 
     if (more) {
@@ -425,7 +481,14 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
 #pragma unroll
   for (int j = 0; j < QT; ++j) {
     float l;
-    if (G::ONES) {
+    if constexpr (SLAB) {
+      // row sum (d = D) of query l32: 16x16 slab of half l32 / 16, lane
+      // 32 + l32 % 16 (rows 8..11 of the slab), register 0
+      const int src_lane = 32 + (l32 & 15);
+      const float s0 = __shfl(os[j][0][0], src_lane);
+      const float s1 = __shfl(os[j][1][0], src_lane);
+      l = (l32 & 16) ? s1 : s0;
+    } else if constexpr (G::ONES) {
       constexpr int tl = D / 32, ml = D % 32;
       constexpr int gl = (ml / 4) % 2, rl = (ml / 8) * 4 + ml % 4;
       const float vsum = o[tl][j][rl];
@@ -435,11 +498,30 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
       l = l_run[j] + swap_halves(l_run[j]);
     }
     const float inv = 1.0f / l;
+    if constexpr (SLAB) {
+      // slab rows d < D: lanes 0-31 hold d = 32 NT32 + 4 (lane / 16) + r for
+      // query 16 h + lane % 16; their row sum is that query's
+      const int sl = (lane & 15);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float inv_h = __shfl(inv, 16 * h + sl);
+        const uint32_t qs = q_wave + 32 * j + 16 * h + sl;
+        if (lane < 32 && qs < L) {
+          const int d0 = 32 * NT32 + 4 * (lane >> 4);
+          bf16x2 lo = {(bf16)(os[j][h][0] * inv_h), (bf16)(os[j][h][1] * inv_h)};
+          bf16x2 hi = {(bf16)(os[j][h][2] * inv_h), (bf16)(os[j][h][3] * inv_h)};
+          uint2 w;
+          w.x = __builtin_bit_cast(uint32_t, lo);
+          w.y = __builtin_bit_cast(uint32_t, hi);
+          *reinterpret_cast<uint2*>(og + (int64_t)qs * p.r_out + d0) = w;
+        }
+      }
+    }
     const uint32_t q = q_wave + 32 * j + l32;
     if (q < L) {
       bf16* orow = og + (int64_t)q * p.r_out;
 #pragma unroll
-      for (int t = 0; t < G::NDV; ++t)
+      for (int t = 0; t < NT32; ++t)
 #pragma unroll
         for (int r4 = 0; r4 < 4; ++r4) {
           const int d0 = 32 * t + 8 * r4 + 4 * g;
@@ -456,11 +538,9 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   }
 }
 
-template <int D, int NW, int QT, int KB, int MINW, int NBUF = 2>
-int launch_cfg(const AttnArgs& a, hipStream_t s) {
-  if (NBUF == 1 && a.L > KB) return DSP_ERR_SHAPE;
-  constexpr int QB = NW * 32 * QT;
-  Params p;
+// Kernel parameters for a launch with QB queries per work-group; returns the
+// number of work-groups (0: nothing to do) or -1 when the shape is out of range.
+int64_t make_params(const AttnArgs& a, int QB, Params& p) {
   p.q = static_cast<const bf16*>(a.q);
   p.k = static_cast<const bf16*>(a.k);
   p.v = static_cast<const bf16*>(a.v);
@@ -477,14 +557,22 @@ int launch_cfg(const AttnArgs& a, hipStream_t s) {
   const int64_t units = a.B * a.X * a.H;
   const int64_t n_qb = (a.L + QB - 1) / QB;
   const int64_t blocks = units * n_qb;
-  if (blocks == 0) return DSP_OK;
+  if (blocks == 0) return 0;
   // buffer resources address one unit's rows with 32-bit byte offsets
-  if (blocks >= (int64_t(1) << 31) || a.L * a.r_stride_in * 2 >= (int64_t(1) << 31))
-    return DSP_ERR_SHAPE;
+  if (blocks >= (int64_t(1) << 31) || a.L * a.r_stride_in * 2 >= (int64_t(1) << 31)) return -1;
   p.n_units = (uint32_t)units;
   p.n_qb = (uint32_t)n_qb;
   p.n_blocks = (uint32_t)blocks;
   p.c = a.scale * 1.4426950408889634f;
+  return blocks;
+}
+
+template <int D, int NW, int QT, int KB, int MINW, int NBUF = 2>
+int launch_cfg(const AttnArgs& a, hipStream_t s) {
+  if (NBUF == 1 && a.L > KB) return DSP_ERR_SHAPE;
+  Params p;
+  const int64_t blocks = make_params(a, NW * 32 * QT, p);
+  if (blocks <= 0) return blocks == 0 ? DSP_OK : DSP_ERR_SHAPE;
   hipLaunchKernelGGL((attn_fwd_kernel<D, NW, QT, KB, MINW, NBUF>), dim3((uint32_t)blocks),
                      dim3(NW * 64), 0, s, p);
   return last_launch_status();

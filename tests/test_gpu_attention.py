@@ -78,6 +78,26 @@ def test_l1_returns_v_exactly(torch):
     assert np.array_equal(bits16(o), bits16(dev(v, "bf16")))
 
 
+@pytest.mark.parametrize("B,X,L,H,D", [
+    (1, 150, 128, 4, 72),   # 600 units: several per persistent work-group, count not a multiple of 8
+    (2, 37, 100, 3, 72),    # ragged L, 222 units
+    (1, 3, 128, 1, 72),     # 3 units: most XCD ranges empty
+    (1, 64, 128, 2, 64),    # D a multiple of 32: VALU row sums
+    (1, 40, 77, 2, 16),
+    (1, 40, 127, 2, 96),
+])
+def test_temporal_stream_many_units(torch, B, X, L, H, D):
+    """64 < L <= 128 runs the persistent streaming kernel: many units per work-group."""
+    import paper_2403_10266_amd as dsp
+    C = H * D
+    q, k, v = _inputs((B, X, L, C), "bf16", seed=B * 77 + X + L * 3 + D)
+    say(f"temporal stream B={B} X={X} L={L} H={H} D={D}")
+    o = dsp.dsp_temporal_attn(dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16"), H)
+    torch.cuda.synchronize()
+    want = oracle.temporal_attention(q, k, v, H)
+    assert_close(host(o), want, "bf16", f"temporal stream L={L} D={D}")
+
+
 def _sampled_check(torch, kind, w, n_units, n_rows, seed):
     import paper_2403_10266_amd as dsp
     layout = "BTSC" if kind == "spatial" else "BSTC"

@@ -28,8 +28,11 @@ def test_layernorm(torch, rows, C, out):
     assert_close(host(y), oracle.layernorm(x, 1e-6), out, "layernorm")
 
 
+# (M >= 256 and N >= 192 run the 256 x 192 pipelined kernel: ragged M, N and K
+# tails, a single partial K slice, and the block's own N = 3C)
 @pytest.mark.parametrize("M,N,K", [(1, 8, 8), (300, 200, 72), (513, 1152, 1152), (64, 4608, 1152),
-                                   (257, 136, 4608)])
+                                   (257, 136, 4608), (256, 192, 8), (777, 385, 104),
+                                   (512, 3456, 1152)])
 @pytest.mark.parametrize("epi", [0, 1, 2, 3])
 @pytest.mark.parametrize("bias", [False, True])
 def test_linear_bf16(torch, M, N, K, epi, bias):
@@ -52,10 +55,10 @@ def test_linear_bf16(torch, M, N, K, epi, bias):
     assert_close(host(out), want, "bf16", f"linear epi={epi}")
 
 
-def test_linear_resid_in_place(torch):
+@pytest.mark.parametrize("M,N,K", [(130, 96, 64), (300, 200, 72)])
+def test_linear_resid_in_place(torch, M, N, K):
     import paper_2403_10266_amd as dsp
     rng = np.random.default_rng(1)
-    M, N, K = 130, 96, 64
     a = synth.bf16_round(rng.standard_normal((M, K), dtype=np.float32))
     w = synth.bf16_round(rng.standard_normal((N, K), dtype=np.float32) * np.float32(0.1))
     r = rng.standard_normal((M, N), dtype=np.float32)
