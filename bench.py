@@ -5,11 +5,16 @@ One step is one pass over the whole hot path, each piece at its own synthetic
 workload (video-latent shapes of the 720M model: C=1152, 16 heads of 72):
 
   switch    dsp_switch of a 1 x 64 x 4096 x 1152 bf16 T-shard into 8 chunks
+  switch_inv  the inverse switch: the 1 x 4096 x 64 x 1152 (B,S,T,C) tensor into
+            8 chunks along T
   spatial   dsp_spatial_attn,  B=2, T=16,  S=4096 (attention over S)
   temporal  dsp_temporal_attn, B=2, S=512, T=128  (attention over T)
   block     dsp_st_block_forward, B=1, T=32, S=1024, MLP 4608 (LN, QKV,
             spatial attention, out-proj, switch, LN, QKV, temporal attention,
             out-proj, LN, MLP with GELU, residuals)
+and, timed separately after the steps (not part of a step):
+  exchange  dsp_exchange_unpack among 8 ranks simulated on this GPU, each rank
+            holding one such shard's packed switch output (8 x 604 MB in and out)
 
 The headline value is the combined attention throughput
 (F_spatial + F_temporal) / (t_spatial + t_temporal) in TFLOP/s with
@@ -53,7 +58,7 @@ def parse():
                     help="rocprofv3 summary with the measured HBM bytes per launch of the "
                          "spatial kernel; used only while the kernel source is unchanged")
     ap.add_argument("--only", default=None,
-                    choices=["switch", "spatial", "temporal", "block", "copy"],
+                    choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange", "copy"],
                     help="run a single part (for profiling); prints per-kernel times only. "
                          "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
                          "plain 604 MB copy used to calibrate traffic counters")
@@ -81,8 +86,8 @@ def main():
     W = synth.WORKLOADS
     ws, wsp, wtp, wbl = (W["switch_bf16_T64_S4096"], W["spatial_bf16_B2_T16_S4096"],
                          W["temporal_bf16_B2_S512_T128"], W["block_bf16_B1_T32_S1024"])
-    wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block"}
-    if "copy" in wanted:
+    wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block", "exchange"}
+    if wanted & {"copy", "switch_inv", "exchange"}:
         wanted.add("switch")
     t = {}
     # ---- inputs (seeded, synthetic), resident in HBM before timing
@@ -90,6 +95,17 @@ def main():
         t["x_sw"] = to_dev(synth.switch_input(ws), "bf16")
         t["y_sw"] = torch.empty((ws.n_chunks, ws.B, ws.S // ws.n_chunks, ws.T, ws.C),
                                 dtype=torch.bfloat16, device=dev)
+        # the inverse switch (S -> T): the (B, S, T, C) tensor into chunks along T
+        t["x_inv"] = t["x_sw"].permute(0, 2, 1, 3).contiguous()
+        t["y_inv"] = torch.empty((ws.n_chunks, ws.B, ws.T // ws.n_chunks, ws.S, ws.C),
+                                 dtype=torch.bfloat16, device=dev)
+    if "exchange" in wanted:
+        # N = n_chunks ranks, each holding one switch-shard's packed output
+        # (distinct contents; a copy's speed does not depend on the values)
+        dsp.dsp_switch(t["x_sw"], 1, 2, ws.n_chunks, out=t["y_sw"])
+        t["ex_in"] = [t["y_sw"] + m for m in range(ws.n_chunks)]
+        t["ex_out"] = [torch.empty((ws.B, ws.S // ws.n_chunks, ws.T * ws.n_chunks, ws.C),
+                                   dtype=torch.bfloat16, device=dev) for _ in range(ws.n_chunks)]
     if "spatial" in wanted:
         t["q_sp"], t["k_sp"], t["v_sp"] = (to_dev(a, "bf16") for a in synth.qkv_inputs(wsp, "BTSC"))
         t["o_sp"] = torch.empty_like(t["q_sp"])
@@ -109,6 +125,12 @@ def main():
     def run_switch():
         dsp.dsp_switch(t["x_sw"], 1, 2, ws.n_chunks, out=t["y_sw"])
 
+    def run_switch_inv():
+        dsp.dsp_switch(t["x_inv"], 1, 2, ws.n_chunks, out=t["y_inv"])
+
+    def run_exchange():
+        dsp.dsp_exchange_unpack(t["ex_in"], out=t["ex_out"])
+
     def run_spatial():
         dsp.dsp_spatial_attn(t["q_sp"], t["k_sp"], t["v_sp"], wsp.H, out=t["o_sp"])
 
@@ -121,10 +143,13 @@ def main():
     def run_copy():
         dsp.dsp_switch(t["x_sw"], 1, 1, 1, out=t["y_sw"].view(t["x_sw"].shape))
 
-    parts = [("switch", run_switch), ("spatial", run_spatial), ("temporal", run_temporal),
-             ("block", run_block)]
+    parts = [("switch", run_switch), ("switch_inv", run_switch_inv), ("spatial", run_spatial),
+             ("temporal", run_temporal), ("block", run_block)]
+    # timed on its own after the steps: not a step of the single-GPU hot path
+    extras = [("exchange", run_exchange)]
     if args.only:
-        parts = [(args.only, run_copy if args.only == "copy" else dict(parts)[args.only])]
+        every = dict(parts + extras)
+        parts, extras = [(args.only, run_copy if args.only == "copy" else every[args.only])], []
 
     for _ in range(args.warmup):
         for _, fn in parts:
@@ -144,6 +169,17 @@ def main():
     wall = time.perf_counter() - t0
     ms = {name: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(K)]))
           for i, (name, _) in enumerate(parts)}
+    for name, fn in extras:
+        for _ in range(args.warmup):
+            fn()
+        xev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+        torch.cuda.synchronize()
+        xev[0].record(stream)
+        for s in range(K):
+            fn()
+            xev[s + 1].record(stream)
+        torch.cuda.synchronize()
+        ms[name] = float(np.mean([xev[s].elapsed_time(xev[s + 1]) for s in range(K)]))
     if args.only:
         print(json.dumps({"only": args.only, "steps": K, "kernel_ms": ms}), flush=True)
         return
@@ -162,6 +198,8 @@ def main():
     tp_tflops = F_tp / (ms["temporal"] * 1e-3) / 1e12
     attn_tflops = (F_sp + F_tp) / ((ms["spatial"] + ms["temporal"]) * 1e-3) / 1e12
     sw_gbps = sw_bytes / (ms["switch"] * 1e-3) / 1e9
+    sw_inv_gbps = sw_bytes / (ms["switch_inv"] * 1e-3) / 1e9
+    ex_gbps = ws.n_chunks * sw_bytes / (ms["exchange"] * 1e-3) / 1e9
     tp_gbps = tp_bytes / (ms["temporal"] * 1e-3) / 1e9
 
     traffic = measured_traffic(args.traffic)
@@ -180,11 +218,16 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "dsp_switch 1x64x4096x1152 bf16 -> 8 chunks; spatial attn B2 T16 S4096 H16 D72; "
+            "workload": "dsp_switch 1x64x4096x1152 bf16 -> 8 chunks and its inverse 1x4096x64x1152 -> 8 "
+                        "chunks; 8-rank exchange+unpack of such shards; spatial attn B2 T16 S4096 H16 D72; "
                         "temporal attn B2 S512 T128 H16 D72; ST block B1 T32 S1024 C1152 H16 F4608",
             "attn_frac_mfma_peak": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
             "switch_GBps": round(sw_gbps, 1),
             "switch_frac_hbm_peak": round(sw_gbps / HBM_PEAK_GBPS, 4),
+            "switch_inverse_GBps": round(sw_inv_gbps, 1),
+            "switch_inverse_frac_hbm_peak": round(sw_inv_gbps / HBM_PEAK_GBPS, 4),
+            "exchange_unpack_GBps": round(ex_gbps, 1),
+            "exchange_unpack_frac_hbm_peak": round(ex_gbps / HBM_PEAK_GBPS, 4),
             "spatial_TFLOPs": round(sp_tflops, 2),
             "temporal_TFLOPs": round(tp_tflops, 2),
             "temporal_GBps": round(tp_gbps, 1),

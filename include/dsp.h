@@ -93,6 +93,32 @@ int dsp_switch_variant(const void* x, void* y, const int64_t* shape, int ndim, i
                        int to_dim, int n_chunks, int dtype, int variant, void* stream);
 
 /* ------------------------------------------------------------------------
+ * dsp_exchange_unpack -- the exchange of DynamicSwitch among N ranks (the
+ * all-to-all of the primitive table's row s_i -> s_j, Eq. 10), run on one GPU
+ * with one buffer per rank, fused with every receiver's unpack.
+ *
+ * packed: host array of N device pointers; packed[m] is rank m's dsp_switch
+ *         output, shape [N][B][P][F][C] (P = D_to / N, F = rank m's length of
+ *         the from-dimension).  Read only; the N buffers may alias each other.
+ * out:    host array of N device pointers; out[n] receives rank n's result,
+ *         shape [B][P][N*F][C]:
+ *             out[n][b][p][m*F + f][c] = packed[m][n][b][p][f][c]
+ *         i.e. chunk n of every rank, concatenated along the from-dimension
+ *         in rank order.  For the (B,T,S,C) -> (B,S,T,C) switch of T-shards
+ *         this is S-shard n of the permuted tensor (Eq. 7-8, i = T).
+ * shape:  {N, B, P, F, C}.  dtype: element type (only its size matters; the
+ *         data move as raw bits).
+ * The caller owns all buffers; N*(B*P*F*C) elements per buffer.
+ * Errors: DSP_ERR_NULL (shape NULL, or a pointer array / pointer NULL for a
+ *   non-empty exchange), DSP_ERR_SHAPE (N < 1, N > 64, a negative size, or a
+ *   size overflow), DSP_ERR_DTYPE, DSP_ERR_ARG (an output buffer overlaps a
+ *   packed buffer or another output buffer).  An empty exchange launches
+ *   nothing.
+ * ------------------------------------------------------------------------ */
+int dsp_exchange_unpack(const void* const* packed, void* const* out, const int64_t* shape,
+                        int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
  * Attention along one sequence dimension (Eq. 3 per head, Eq. 1-2; the
  * per-dimension reshape of Eq. 7-8).  Non-causal softmax(q k^T * scale) v.
  *

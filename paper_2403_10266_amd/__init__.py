@@ -9,7 +9,7 @@ status.  There is no fallback: if the library is missing, importing the
 binding's functions raises.
 
 Entry points (see ``include/dsp.h`` for the exact contracts):
-``dsp_switch``, ``dsp_spatial_attn``, ``dsp_temporal_attn``,
+``dsp_switch``, ``dsp_exchange_unpack``, ``dsp_spatial_attn``, ``dsp_temporal_attn``,
 ``dsp_layernorm``, ``dsp_linear``, ``dsp_st_block_forward``.
 """
 from __future__ import annotations
@@ -51,6 +51,7 @@ _SIGNATURES = {
     "dsp_version": (_I, []),
     "dsp_switch": (_I, [_P, _P, _c.POINTER(_I64), _I, _I, _I, _I, _I, _P]),
     "dsp_switch_variant": (_I, [_P, _P, _c.POINTER(_I64), _I, _I, _I, _I, _I, _I, _P]),
+    "dsp_exchange_unpack": (_I, [_c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_I64), _I, _P]),
     "dsp_spatial_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
     "dsp_temporal_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
     "dsp_layernorm": (_I, [_P, _I, _P, _I, _I64, _I, _F, _P]),
@@ -154,6 +155,38 @@ def _attn(name, q, k, v, B, X, L, H, out, ld_in, ld_out, scale, stream, C):
     st = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, X, L, H, D, ld_in, ld_out, float(scale),
             _dtype_code(q), _stream(stream))
     _check(st, name)
+    return out
+
+
+def dsp_exchange_unpack(packed, out=None, stream=None):
+    """Exchange + unpack of N ranks' packed switch outputs on one GPU (see
+    dsp.h).  ``packed``: N tensors of shape [N, B, P, F, C] (same dtype).
+    Returns N tensors of shape [B, P, N*F, C]: rank n's result."""
+    torch = _torch()
+    packed = list(packed)
+    N = len(packed)
+    if N == 0:
+        raise ValueError("dsp_exchange_unpack: no ranks")
+    shape = tuple(packed[0].shape)
+    if len(shape) != 5 or shape[0] != N:
+        raise ValueError(f"dsp_exchange_unpack: packed[0] has shape {shape}, want [N={N}, B, P, F, C]")
+    _require_device(*packed)
+    for t in packed:
+        if tuple(t.shape) != shape or t.dtype != packed[0].dtype or not t.is_contiguous():
+            raise ValueError("dsp_exchange_unpack: packed tensors must share one contiguous shape and dtype")
+    _, B, P, F, C = shape
+    if out is None:
+        out = [torch.empty((B, P, N * F, C), dtype=packed[0].dtype, device=packed[0].device)
+               for _ in range(N)]
+    out = list(out)
+    _require_device(*out)
+    if len(out) != N or any(tuple(o.shape) != (B, P, N * F, C) or not o.is_contiguous() for o in out):
+        raise ValueError("dsp_exchange_unpack: out must be N contiguous tensors of shape [B, P, N*F, C]")
+    src = (ctypes.c_void_p * N)(*[t.data_ptr() for t in packed])
+    dst = (ctypes.c_void_p * N)(*[o.data_ptr() for o in out])
+    shp = (ctypes.c_int64 * 5)(N, B, P, F, C)
+    _check(lib().dsp_exchange_unpack(src, dst, shp, _dtype_code(packed[0]), _stream(stream)),
+           "dsp_exchange_unpack")
     return out
 
 

@@ -180,6 +180,32 @@ int dsp_switch_variant(const void* x, void* y, const int64_t* shape, int ndim, i
   return switch_impl(x, y, shape, ndim, from_dim, to_dim, n_chunks, dtype, variant, stream);
 }
 
+int dsp_exchange_unpack(const void* const* packed, void* const* out, const int64_t* shape,
+                        int dtype, void* stream) {
+  if (!shape) return DSP_ERR_NULL;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  const int64_t N = shape[0], B = shape[1], P = shape[2], F = shape[3], C = shape[4];
+  if (N < 1 || N > kMaxExchangeRanks || B < 0 || P < 0 || F < 0 || C < 0) return DSP_ERR_SHAPE;
+  int64_t run, per_rank, run_bytes;
+  if (!mul_ok(F, C, &run) || !mul_ok(run, elem_size(dtype), &run_bytes) ||
+      !mul_ok(N, B, &per_rank) || !mul_ok(per_rank, P, &per_rank) ||
+      !mul_ok(per_rank, run_bytes, &per_rank))
+    return DSP_ERR_SHAPE;
+  if (per_rank == 0) return DSP_OK;
+  if (!packed || !out) return DSP_ERR_NULL;
+  for (int64_t i = 0; i < N; ++i)
+    if (!packed[i] || !out[i]) return DSP_ERR_NULL;
+  // every destination is written by N sources: it must not overlap a source or
+  // another destination (sources may alias each other: they are only read)
+  for (int64_t i = 0; i < N; ++i) {
+    for (int64_t j = 0; j < N; ++j) {
+      if (overlap(out[i], (size_t)per_rank, packed[j], (size_t)per_rank)) return DSP_ERR_ARG;
+      if (j != i && overlap(out[i], (size_t)per_rank, out[j], (size_t)per_rank)) return DSP_ERR_ARG;
+    }
+  }
+  return launch_exchange_unpack(packed, out, N, B, P, run_bytes, static_cast<hipStream_t>(stream));
+}
+
 int dsp_spatial_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t T,
                      int64_t S, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
                      int dtype, void* stream) {

@@ -10,6 +10,10 @@ namespace dsp {
 
 // Launch wrappers implemented in the kernel translation units.  Arguments have
 // been validated by the ABI layer; each returns a dsp_status_t.
+// N-rank exchange + unpack (exchange.hip); N <= kMaxExchangeRanks.
+constexpr int kMaxExchangeRanks = 64;
+int launch_exchange_unpack(const void* const* packed, void* const* out, int64_t N, int64_t B,
+                           int64_t P, int64_t run_bytes, hipStream_t s);
 int launch_switch_rows(const void* x, void* y, int64_t B, int64_t D1, int64_t D2, int64_t row_bytes,
                        int from_dim, int to_dim, int64_t n_chunks, hipStream_t s);
 int launch_switch_tiles(const void* x, void* y, int64_t B, int64_t D1, int64_t D2, int64_t C,

@@ -83,6 +83,29 @@ def test_switch_validation(lib):
     assert sw(FAKE, FAKE2, _shape(1, 4, 6, 0), 4, 1, 2, 2, 1) == dsp.DSP_OK
 
 
+def test_exchange_validation(lib):
+    P = ctypes.c_void_p
+    def call(srcs, dsts, shape, dt=1):
+        s = (P * len(srcs))(*srcs) if srcs is not None else None
+        d = (P * len(dsts))(*dsts) if dsts is not None else None
+        return lib.dsp_exchange_unpack(s, d, shape, dt, None)
+    ok = _shape(2, 1, 4, 3, 8)                  # N=2 ranks, 2*1*4*3*8 = 192 elements each
+    a, b, c, d = 0x100000, 0x200000, 0x300000, 0x400000
+    assert call([a, b], [c, d], None) == dsp.DSP_ERR_NULL
+    assert call(None, [c, d], ok) == dsp.DSP_ERR_NULL
+    assert call([a, b], None, ok) == dsp.DSP_ERR_NULL
+    assert call([a, None], [c, d], ok) == dsp.DSP_ERR_NULL
+    assert call([a, b], [c, d], _shape(0, 1, 4, 3, 8)) == dsp.DSP_ERR_SHAPE
+    assert call([a] * 65, [c] * 65, _shape(65, 1, 1, 1, 1)) == dsp.DSP_ERR_SHAPE
+    assert call([a, b], [c, d], _shape(2, 1, -4, 3, 8)) == dsp.DSP_ERR_SHAPE
+    assert call([a, b], [c, d], _shape(2, 1, 2 ** 40, 2 ** 20, 8)) == dsp.DSP_ERR_SHAPE
+    assert call([a, b], [c, d], ok, dt=7) == dsp.DSP_ERR_DTYPE
+    assert call([a, b], [b + 64, d], ok) == dsp.DSP_ERR_ARG     # an output overlaps a source
+    assert call([a, b], [c, c + 256], ok) == dsp.DSP_ERR_ARG    # two outputs overlap
+    # an empty exchange launches nothing (pointers are not looked at)
+    assert call([a, b], [c, d], _shape(2, 0, 4, 3, 8)) == dsp.DSP_OK
+
+
 @pytest.mark.parametrize("fn", ["dsp_spatial_attn", "dsp_temporal_attn"])
 def test_attention_validation(lib, fn):
     f = getattr(lib, fn)
