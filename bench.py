@@ -15,6 +15,8 @@ workload (video-latent shapes of the 720M model: C=1152, 16 heads of 72):
 and, timed separately after the steps (not part of a step):
   exchange  dsp_exchange_unpack among 8 ranks simulated on this GPU, each rank
             holding one such shard's packed switch output (8 x 604 MB in and out)
+  temporal_strided  the temporal workload read and written in the unswitched
+            (B, T, S, C) layout through dsp_attn_strided
 
 The headline value is the combined attention throughput
 (F_spatial + F_temporal) / (t_spatial + t_temporal) in TFLOP/s with
@@ -58,7 +60,8 @@ def parse():
                     help="rocprofv3 summary with the measured HBM bytes per launch of the "
                          "spatial kernel; used only while the kernel source is unchanged")
     ap.add_argument("--only", default=None,
-                    choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange", "copy"],
+                    choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange",
+                             "temporal_strided", "copy"],
                     help="run a single part (for profiling); prints per-kernel times only. "
                          "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
                          "plain 604 MB copy used to calibrate traffic counters")
@@ -86,9 +89,12 @@ def main():
     W = synth.WORKLOADS
     ws, wsp, wtp, wbl = (W["switch_bf16_T64_S4096"], W["spatial_bf16_B2_T16_S4096"],
                          W["temporal_bf16_B2_S512_T128"], W["block_bf16_B1_T32_S1024"])
-    wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block", "exchange"}
+    wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block", "exchange",
+                                            "temporal_strided"}
     if wanted & {"copy", "switch_inv", "exchange"}:
         wanted.add("switch")
+    if "temporal_strided" in wanted:
+        wanted.add("temporal")
     t = {}
     # ---- inputs (seeded, synthetic), resident in HBM before timing
     if "switch" in wanted:
@@ -112,6 +118,10 @@ def main():
     if "temporal" in wanted:
         t["q_tp"], t["k_tp"], t["v_tp"] = (to_dev(a, "bf16") for a in synth.qkv_inputs(wtp, "BSTC"))
         t["o_tp"] = torch.empty_like(t["q_tp"])
+    if "temporal_strided" in wanted:
+        # the same tensors left in the unswitched (B, T, S, C) layout
+        t["tq_tsc"] = [a.permute(0, 2, 1, 3).contiguous() for a in (t["q_tp"], t["k_tp"], t["v_tp"])]
+        t["to_tsc"] = torch.empty_like(t["tq_tsc"][0])
     if "block" in wanted:
         x_bl_np, p_bl = synth.block_inputs(wbl)
         t["x_bl"] = to_dev(x_bl_np, "f32")
@@ -131,6 +141,10 @@ def main():
     def run_exchange():
         dsp.dsp_exchange_unpack(t["ex_in"], out=t["ex_out"])
 
+    def run_temporal_strided():
+        v = [a.permute(0, 2, 1, 3) for a in t["tq_tsc"]]
+        dsp.dsp_attn_strided(*v, wtp.H, out=t["to_tsc"].permute(0, 2, 1, 3))
+
     def run_spatial():
         dsp.dsp_spatial_attn(t["q_sp"], t["k_sp"], t["v_sp"], wsp.H, out=t["o_sp"])
 
@@ -146,7 +160,7 @@ def main():
     parts = [("switch", run_switch), ("switch_inv", run_switch_inv), ("spatial", run_spatial),
              ("temporal", run_temporal), ("block", run_block)]
     # timed on its own after the steps: not a step of the single-GPU hot path
-    extras = [("exchange", run_exchange)]
+    extras = [("exchange", run_exchange), ("temporal_strided", run_temporal_strided)]
     if args.only:
         every = dict(parts + extras)
         parts, extras = [(args.only, run_copy if args.only == "copy" else every[args.only])], []
@@ -189,6 +203,7 @@ def main():
     F_sp = attn_flops(wsp.B * wsp.T * wsp.H, wsp.S, wsp.D)
     F_tp = attn_flops(wtp.B * wtp.S * wtp.H, wtp.T, wtp.D)
     tp_bytes = 4.0 * t["q_tp"].numel() * 2
+    tp_bytes_all = tp_bytes
     tok = wbl.B * wbl.T * wbl.S
     C, F = wbl.C, wbl.F
     F_bl = (2.0 * tok * C * (3 * C) * 2 + 2.0 * tok * C * C * 2 + 2.0 * tok * C * F * 2
@@ -200,6 +215,7 @@ def main():
     sw_gbps = sw_bytes / (ms["switch"] * 1e-3) / 1e9
     sw_inv_gbps = sw_bytes / (ms["switch_inv"] * 1e-3) / 1e9
     ex_gbps = ws.n_chunks * sw_bytes / (ms["exchange"] * 1e-3) / 1e9
+    tps_gbps = tp_bytes_all / (ms["temporal_strided"] * 1e-3) / 1e9
     tp_gbps = tp_bytes / (ms["temporal"] * 1e-3) / 1e9
 
     traffic = measured_traffic(args.traffic)
@@ -228,6 +244,7 @@ def main():
             "switch_inverse_frac_hbm_peak": round(sw_inv_gbps / HBM_PEAK_GBPS, 4),
             "exchange_unpack_GBps": round(ex_gbps, 1),
             "exchange_unpack_frac_hbm_peak": round(ex_gbps / HBM_PEAK_GBPS, 4),
+            "temporal_unswitched_layout_GBps": round(tps_gbps, 1),
             "spatial_TFLOPs": round(sp_tflops, 2),
             "temporal_TFLOPs": round(tp_tflops, 2),
             "temporal_GBps": round(tp_gbps, 1),

@@ -149,6 +149,23 @@ int dsp_temporal_attn(const void* q, const void* k, const void* v, void* o, int6
                       int64_t T, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
                       int dtype, void* stream);
 
+/* Attention with explicit layouts: the same operation over L positions of
+ * each (b, x, h) unit, element (b, x, l, h*D + d) of q/k/v at
+ *     b*in_strides[0] + x*in_strides[1] + l*in_strides[2] + h*D + d
+ * and of o at the same offsets with out_strides (strides in elements).  This
+ * reads a layout the previous stage left behind without a switch, e.g.
+ * temporal attention straight from (B, T, S, C): X = S, L = T, in_strides =
+ * {T*S*C, C, S*C} (Eq. 7-8 with i = T, computed on the unswitched tensor).
+ * dsp_spatial_attn and dsp_temporal_attn are this call with the strides of
+ * their dense layouts.  Requirements and errors as for dsp_spatial_attn, plus:
+ * strides must be >= 0 (DSP_ERR_SHAPE), the output rows must not overlap
+ * (checked: DSP_ERR_ARG), and for DSP_BF16 every stride a multiple of 8
+ * elements and min(L, 64) * in_strides[2] * 2 < 2^31 (DSP_ERR_ALIGN /
+ * DSP_ERR_SHAPE).  o must not overlap q, k or v. */
+int dsp_attn_strided(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X,
+                     int64_t L, int H, int D, const int64_t* in_strides, const int64_t* out_strides,
+                     float scale, int dtype, void* stream);
+
 /* ------------------------------------------------------------------------
  * dsp_layernorm -- per-row normalisation over C (Eq. 4, 6):
  *   y = (x - mean) / sqrt(var + eps), biased variance, no affine part,

@@ -10,6 +10,7 @@ binding's functions raises.
 
 Entry points (see ``include/dsp.h`` for the exact contracts):
 ``dsp_switch``, ``dsp_exchange_unpack``, ``dsp_spatial_attn``, ``dsp_temporal_attn``,
+``dsp_attn_strided``,
 ``dsp_layernorm``, ``dsp_linear``, ``dsp_st_block_forward``.
 """
 from __future__ import annotations
@@ -54,6 +55,8 @@ _SIGNATURES = {
     "dsp_exchange_unpack": (_I, [_c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_I64), _I, _P]),
     "dsp_spatial_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
     "dsp_temporal_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
+    "dsp_attn_strided": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _c.POINTER(_I64),
+                              _c.POINTER(_I64), _F, _I, _P]),
     "dsp_layernorm": (_I, [_P, _I, _P, _I, _I64, _I, _F, _P]),
     "dsp_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
     "dsp_st_block_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
@@ -209,6 +212,32 @@ def dsp_temporal_attn(q, k, v, H: int, out=None, scale: float = 0.0, C: int | No
     ld_in = ld_in if ld_in is not None else q.stride(2)
     ld_out = ld_out if ld_out is not None else (out.stride(2) if out is not None else C)
     return _attn("dsp_temporal_attn", q, k, v, B, S, T, H, out, ld_in, ld_out, scale, stream, C)
+
+
+def dsp_attn_strided(q, k, v, H: int, out=None, scale: float = 0.0, stream=None):
+    """Attention over dim 2 of the 4-D views q, k, v [B, X, L, >=H*D] (any
+    strides, last one 1, the same for q, k and v), per (b, x, head): e.g.
+    temporal attention on a (B, T, S, C) tensor x is ``q = x.permute(0, 2, 1, 3)``.
+    The output is a new contiguous [B, X, L, C] tensor, or ``out`` (any 4-D
+    view with last stride 1)."""
+    torch = _torch()
+    _require_device(q, k, v, out)
+    if q.dim() != 4 or q.shape != k.shape or q.shape != v.shape:
+        raise ValueError("q, k, v must be 4-D views of one shape [B, X, L, C]")
+    if q.stride() != k.stride() or q.stride() != v.stride() or q.stride(3) != 1:
+        raise ValueError("q, k, v must share strides, with a unit last stride")
+    B, X, L, C = q.shape
+    if C % H:
+        raise ValueError("C must be a multiple of H")
+    if out is None:
+        out = torch.empty((B, X, L, C), dtype=q.dtype, device=q.device)
+    if out.shape != q.shape or out.stride(3) != 1:
+        raise ValueError("out must be a view of shape [B, X, L, C] with a unit last stride")
+    ins = (ctypes.c_int64 * 3)(*q.stride()[:3])
+    outs = (ctypes.c_int64 * 3)(*out.stride()[:3])
+    _check(lib().dsp_attn_strided(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, X, L, H, C // H, ins, outs,
+                                  float(scale), _dtype_code(q), _stream(stream)), "dsp_attn_strided")
+    return out
 
 
 def dsp_layernorm(x, eps: float = 1e-6, out=None, out_dtype=None, stream=None):

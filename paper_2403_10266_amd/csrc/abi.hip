@@ -5,6 +5,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <utility>
+
 #include "dsp_internal.h"
 
 using namespace dsp;
@@ -57,41 +59,84 @@ int switch_impl(const void* x, void* y, const int64_t* shape, int ndim, int from
   return launch_switch_tiles(x, y, B, D1, D2, C, elem_size(dtype), from_dim, to_dim, n_chunks, s);
 }
 
-int attn_impl(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X, int64_t L,
-              int H, int D, int64_t ld_in, int64_t ld_out, float scale, int dtype, void* stream,
-              bool spatial) {
+// Rows of a (B, X, L) grid with element strides st = {b, x, l}, each `width`
+// elements wide, do not overlap when, taking the dimensions of extent > 1 by
+// increasing stride, every stride is at least the span of the smaller ones.
+bool rows_disjoint(int64_t B, int64_t X, int64_t L, const int64_t* st, int64_t width) {
+  int64_t e[3] = {B, X, L}, s[3] = {st[0], st[1], st[2]};
+  for (int i = 0; i < 3; ++i)
+    for (int j = i + 1; j < 3; ++j)
+      if (s[j] < s[i]) { std::swap(s[i], s[j]); std::swap(e[i], e[j]); }
+  int64_t span = width;
+  for (int i = 0; i < 3; ++i) {
+    if (e[i] <= 1) continue;
+    if (s[i] < span) return false;
+    if (!mul_ok(s[i], e[i] - 1, &span) || span > INT64_MAX - width) return false;
+    span += width;
+  }
+  return true;
+}
+
+int attn_impl_strided(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X,
+                      int64_t L, int H, int D, const int64_t* in_st, const int64_t* out_st,
+                      float scale, int dtype, void* stream) {
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (!in_st || !out_st) return DSP_ERR_NULL;
   if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
   if ((!q || !k || !v || !o) && B != 0 && X != 0 && L != 0) return DSP_ERR_NULL;
-  if ((int64_t)H * D > ld_in || (int64_t)H * D > ld_out) return DSP_ERR_SHAPE;
+  for (int i = 0; i < 3; ++i)
+    if (in_st[i] < 0 || out_st[i] < 0) return DSP_ERR_SHAPE;
   if (isnan(scale) || isinf(scale)) return DSP_ERR_ARG;
+  int64_t width;
+  if (!mul_ok(H, D, &width)) return DSP_ERR_SHAPE;
   if (dtype == DSP_BF16) {
     if (!attn_bf16_supports(D)) return DSP_ERR_SHAPE;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return DSP_ERR_ALIGN;
-    if (ld_in % 8 || ld_out % 8) return DSP_ERR_ALIGN;
+    for (int i = 0; i < 3; ++i)
+      if (in_st[i] % 8 || out_st[i] % 8) return DSP_ERR_ALIGN;
   } else if (D > 256) {
     return DSP_ERR_SHAPE;
   }
-  int64_t tokens;
-  if (!mul_ok(B, X, &tokens) || !mul_ok(tokens, L, &tokens)) return DSP_ERR_SHAPE;
-  int64_t span_in, span_out;
-  if (!mul_ok(tokens, ld_in, &span_in) || !mul_ok(tokens, ld_out, &span_out)) return DSP_ERR_SHAPE;
-  if (tokens == 0) return DSP_OK;
+  if (B == 0 || X == 0 || L == 0) return DSP_OK;
+  // every output row is written by exactly one unit
+  if (!rows_disjoint(B, X, L, out_st, width)) return DSP_ERR_ARG;
+  // the largest element offset of either side must be addressable
+  for (const int64_t* st : {in_st, out_st}) {
+    int64_t tb, tx, tl;
+    if (!mul_ok(B - 1, st[0], &tb) || !mul_ok(X - 1, st[1], &tx) || !mul_ok(L - 1, st[2], &tl) ||
+        tb > INT64_MAX / 4 || tx > INT64_MAX / 4 || tl > INT64_MAX / 4)
+      return DSP_ERR_SHAPE;
+  }
   AttnArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.B = B; a.X = X; a.L = L; a.H = H; a.D = D;
-  // spatial (B,T,S,*): unit (b, t), positions s.  temporal (B,S,T,*): unit (b, s), positions t.
-  // Both: position r of unit (b, x) is row (b*X + x)*L + r.
-  (void)spatial;
-  a.r_stride_in = ld_in;
-  a.x_stride_in = L * ld_in;
-  a.b_stride_in = X * L * ld_in;
-  a.r_stride_out = ld_out;
-  a.x_stride_out = L * ld_out;
-  a.b_stride_out = X * L * ld_out;
+  a.b_stride_in = in_st[0];
+  a.x_stride_in = in_st[1];
+  a.r_stride_in = in_st[2];
+  a.b_stride_out = out_st[0];
+  a.x_stride_out = out_st[1];
+  a.r_stride_out = out_st[2];
   a.scale = scale > 0.0f ? scale : (float)(1.0 / sqrt((double)D));
   hipStream_t s = as_stream(stream);
   return dtype == DSP_BF16 ? launch_attn_bf16(a, s) : launch_attn_f32(a, s);
+}
+
+// Spatial (B,T,S,*): unit (b, t), positions s.  Temporal (B,S,T,*): unit
+// (b, s), positions t.  Both: position r of unit (b, x) is row (b*X + x)*L + r.
+int attn_impl(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X, int64_t L,
+              int H, int D, int64_t ld_in, int64_t ld_out, float scale, int dtype, void* stream) {
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
+  if ((int64_t)H * D > ld_in || (int64_t)H * D > ld_out) return DSP_ERR_SHAPE;
+  int64_t tokens, xl_in, xl_out, bl_in, bl_out;
+  if (!mul_ok(B, X, &tokens) || !mul_ok(tokens, L, &tokens)) return DSP_ERR_SHAPE;
+  int64_t span_in, span_out;
+  if (!mul_ok(tokens, ld_in, &span_in) || !mul_ok(tokens, ld_out, &span_out)) return DSP_ERR_SHAPE;
+  if (!mul_ok(L, ld_in, &xl_in) || !mul_ok(L, ld_out, &xl_out) || !mul_ok(X, xl_in, &bl_in) ||
+      !mul_ok(X, xl_out, &bl_out))
+    return DSP_ERR_SHAPE;
+  const int64_t in_st[3] = {bl_in, xl_in, ld_in}, out_st[3] = {bl_out, xl_out, ld_out};
+  return attn_impl_strided(q, k, v, o, B, X, L, H, D, in_st, out_st, scale, dtype, stream);
 }
 
 int linear_impl(const void* a, const void* w, const void* bias, const float* residual, void* out,
@@ -209,13 +254,19 @@ int dsp_exchange_unpack(const void* const* packed, void* const* out, const int64
 int dsp_spatial_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t T,
                      int64_t S, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
                      int dtype, void* stream) {
-  return attn_impl(q, k, v, o, B, T, S, H, D, ld_in, ld_out, scale, dtype, stream, true);
+  return attn_impl(q, k, v, o, B, T, S, H, D, ld_in, ld_out, scale, dtype, stream);
 }
 
 int dsp_temporal_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t S,
                       int64_t T, int H, int D, int64_t ld_in, int64_t ld_out, float scale,
                       int dtype, void* stream) {
-  return attn_impl(q, k, v, o, B, S, T, H, D, ld_in, ld_out, scale, dtype, stream, false);
+  return attn_impl(q, k, v, o, B, S, T, H, D, ld_in, ld_out, scale, dtype, stream);
+}
+
+int dsp_attn_strided(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X,
+                     int64_t L, int H, int D, const int64_t* in_strides, const int64_t* out_strides,
+                     float scale, int dtype, void* stream) {
+  return attn_impl_strided(q, k, v, o, B, X, L, H, D, in_strides, out_strides, scale, dtype, stream);
 }
 
 int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows, int C, float eps,
@@ -301,7 +352,7 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
   else DSP_TRY(launch_layernorm(x_BTSC, 0, h, bf, tokens, C, ln_eps, s));
   DSP_TRY(linear_impl(h, w->wqkv_s, w->bqkv_s, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s));
   DSP_TRY(attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, T, S, H, D, ld3, C,
-                    0.0f, dtype, s, true));
+                    0.0f, dtype, s));
   DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, attn_only ? nullptr : x_BTSC, x1, tokens, C, C,
                       attn_only ? DSP_EPI_F32 : DSP_EPI_RESID, dtype, s));
   // ---- the Switch T -> S on one GPU: (B, T, S, C) -> (B, S, T, C)
@@ -312,7 +363,7 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
   else DSP_TRY(launch_layernorm(y_BSTC, 0, h, bf, tokens, C, ln_eps, s));
   DSP_TRY(linear_impl(h, w->wqkv_t, w->bqkv_t, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s));
   DSP_TRY(attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, S, T, H, D, ld3, C,
-                    0.0f, dtype, s, false));
+                    0.0f, dtype, s));
   if (attn_only) {
     DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, nullptr, y_BSTC, tokens, C, C, DSP_EPI_F32, dtype, s));
     return DSP_OK;

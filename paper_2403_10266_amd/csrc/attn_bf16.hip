@@ -43,6 +43,8 @@
 //    heads of a token row, then share that XCD's L2.
 #include <math.h>
 
+#include <algorithm>
+
 #include "dsp_internal.h"
 
 // Compile-time tiling of the long-sequence (spatial) and short-sequence
@@ -239,8 +241,10 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
     lofs[i] = row * G::KP + col * 8;                 // K layout; V adds its own base/pitch
     if (fetch_v) lofs[i] = KB * G::KP + row * G::VP + col * 8;
   }
+  // the range covers the tile's own rows only, so that widely strided rows
+  // (a row stride of many megabytes) still fit a 32-bit byte range
   auto rsrc = [&](const bf16* tensor, uint32_t kb) {
-    const uint32_t rows_left = kb < L ? L - kb : 0u;
+    const uint32_t rows_left = kb < L ? min(L - kb, (uint32_t)KB) : 0u;
     return make_rsrc(tensor + um.in_base + (int64_t)kb * p.r_in, rows_left * row_bytes);
   };
   u32x4 pre[SPLIT ? NLOAD : 1];
@@ -538,9 +542,10 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   }
 }
 
-// Kernel parameters for a launch with QB queries per work-group; returns the
-// number of work-groups (0: nothing to do) or -1 when the shape is out of range.
-int64_t make_params(const AttnArgs& a, int QB, Params& p) {
+// Kernel parameters for a launch with QB queries per work-group and KB keys
+// per tile; returns the number of work-groups (0: nothing to do) or -1 when
+// the shape is out of range.
+int64_t make_params(const AttnArgs& a, int QB, int KB, Params& p) {
   p.q = static_cast<const bf16*>(a.q);
   p.k = static_cast<const bf16*>(a.k);
   p.v = static_cast<const bf16*>(a.v);
@@ -558,8 +563,9 @@ int64_t make_params(const AttnArgs& a, int QB, Params& p) {
   const int64_t n_qb = (a.L + QB - 1) / QB;
   const int64_t blocks = units * n_qb;
   if (blocks == 0) return 0;
-  // buffer resources address one unit's rows with 32-bit byte offsets
-  if (blocks >= (int64_t(1) << 31) || a.L * a.r_stride_in * 2 >= (int64_t(1) << 31)) return -1;
+  // a tile's buffer resource addresses its rows with 32-bit byte offsets
+  if (blocks >= (int64_t(1) << 31) || std::min<int64_t>(a.L, KB) * a.r_stride_in * 2 >= (int64_t(1) << 31))
+    return -1;
   p.n_units = (uint32_t)units;
   p.n_qb = (uint32_t)n_qb;
   p.n_blocks = (uint32_t)blocks;
@@ -571,7 +577,7 @@ template <int D, int NW, int QT, int KB, int MINW, int NBUF = 2>
 int launch_cfg(const AttnArgs& a, hipStream_t s) {
   if (NBUF == 1 && a.L > KB) return DSP_ERR_SHAPE;
   Params p;
-  const int64_t blocks = make_params(a, NW * 32 * QT, p);
+  const int64_t blocks = make_params(a, NW * 32 * QT, KB, p);
   if (blocks <= 0) return blocks == 0 ? DSP_OK : DSP_ERR_SHAPE;
   hipLaunchKernelGGL((attn_fwd_kernel<D, NW, QT, KB, MINW, NBUF>), dim3((uint32_t)blocks),
                      dim3(NW * 64), 0, s, p);

@@ -126,6 +126,22 @@ def test_attention_validation(lib, fn):
     assert call(L=0) == dsp.DSP_OK
 
 
+def test_attn_strided_validation(lib):
+    ok_in, ok_out = _shape(8 * 1152 * 5, 1152, 8 * 1152), _shape(3 * 5 * 1152, 5 * 1152, 1152)
+    call = lambda q=FAKE, o=FAKE2, B=2, X=3, L=5, H=16, D=72, si=ok_in, so=ok_out, sc=0.0, dt=1: \
+        lib.dsp_attn_strided(q, q, q, o, B, X, L, H, D, si, so, sc, dt, None)
+    assert call(si=None) == dsp.DSP_ERR_NULL
+    assert call(q=None) == dsp.DSP_ERR_NULL
+    assert call(si=_shape(-8, 1152, 9216)) == dsp.DSP_ERR_SHAPE
+    assert call(so=_shape(0, 0, 1152), B=2) == dsp.DSP_ERR_ARG          # rows of different b coincide
+    assert call(so=_shape(3 * 5 * 1152, 5 * 1152, 576)) == dsp.DSP_ERR_ARG   # rows narrower than H*D
+    assert call(si=_shape(8 * 1152 * 5, 1152, 8 * 1152 + 4)) == dsp.DSP_ERR_ALIGN
+    assert call(dt=9) == dsp.DSP_ERR_DTYPE
+    assert call(D=70) == dsp.DSP_ERR_SHAPE
+    assert call(si=_shape(0, 0, 2 ** 28)) == dsp.DSP_ERR_SHAPE          # 64 rows exceed a 2^31-byte range
+    assert call(B=0) == dsp.DSP_OK
+
+
 def test_layernorm_validation(lib):
     f = lambda x=FAKE, xd=1, y=FAKE2, yd=1, rows=4, C=8, eps=1e-6: lib.dsp_layernorm(
         x, xd, y, yd, rows, C, eps, None)

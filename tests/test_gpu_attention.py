@@ -137,3 +137,58 @@ def test_deterministic(torch):
     b = dsp.dsp_spatial_attn(dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16"), 16)
     torch.cuda.synchronize()
     assert np.array_equal(bits16(a), bits16(b))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,T,S,H,D", [(1, 40, 12, 2, 72), (2, 130, 6, 3, 72), (1, 17, 9, 2, 64),
+                                       (1, 300, 4, 1, 72)])
+def test_temporal_attention_on_unswitched_layout(torch, dtype, B, T, S, H, D):
+    """dsp_attn_strided reads (B, T, S, C) directly (no switch): equal to the
+    oracle's strided temporal attention, output also written in (B, T, S, C)."""
+    import paper_2403_10266_amd as dsp
+    C = H * D
+    q, k, v = _inputs((B, T, S, C), dtype, seed=T * 11 + S + D)
+    say(f"temporal strided {dtype} B={B} T={T} S={S} H={H} D={D}")
+    qd, kd, vd = (dev(a, dtype).permute(0, 2, 1, 3) for a in (q, k, v))     # views (B, S, T, C)
+    out_full = torch.zeros((B, T, S, C), dtype=qd.dtype, device=qd.device)
+    o = dsp.dsp_attn_strided(qd, kd, vd, H, out=out_full.permute(0, 2, 1, 3))
+    torch.cuda.synchronize()
+    want = oracle.temporal_attention_strided(q, k, v, H)
+    assert_close(host(out_full), want, dtype, f"temporal strided T={T}")
+    assert o.data_ptr() == out_full.data_ptr()
+
+
+def test_strided_equals_dense_temporal(torch):
+    """Reading the unswitched layout gives bit-identical results to switching
+    first and reading the dense (B, S, T, C) layout (same kernel, same order)."""
+    import paper_2403_10266_amd as dsp
+    B, T, S, H, D = 1, 128, 8, 16, 72
+    C = H * D
+    q, k, v = _inputs((B, T, S, C), "bf16", seed=7)
+    qd, kd, vd = (dev(a, "bf16") for a in (q, k, v))
+    a = dsp.dsp_attn_strided(qd.permute(0, 2, 1, 3), kd.permute(0, 2, 1, 3), vd.permute(0, 2, 1, 3), H)
+    dense = [t.permute(0, 2, 1, 3).contiguous() for t in (qd, kd, vd)]
+    b = dsp.dsp_temporal_attn(*dense, H)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits16(a), bits16(b))
+
+
+def test_temporal_strided_full_size_sampled(torch):
+    """The temporal workload (B2 S512 T128 H16 D72) read straight from (B, T, S, C)."""
+    import paper_2403_10266_amd as dsp
+    w = synth.WORKLOADS["temporal_bf16_B2_S512_T128"]
+    q, k, v = synth.qkv_inputs(w, "BSTC")
+    q, k, v = (np.ascontiguousarray(a.transpose(0, 2, 1, 3)) for a in (q, k, v))     # (B, T, S, C)
+    say(f"temporal strided full size {q.shape}")
+    o = dsp.dsp_attn_strided(*(dev(a, "bf16").permute(0, 2, 1, 3) for a in (q, k, v)), w.H)
+    torch.cuda.synchronize()
+    o = o.float().cpu().numpy()                                                        # (B, S, T, C)
+    rng = np.random.default_rng(4)
+    D = w.D
+    got, want = [], []
+    for _ in range(128):
+        b, s, h = rng.integers(w.B), rng.integers(w.S), rng.integers(w.H)
+        cs = slice(h * D, (h + 1) * D)
+        want.append(oracle.attention_rows(q[b, :, s, cs], k[b, :, s, cs], v[b, :, s, cs]))
+        got.append(o[b, s, :, cs])
+    assert_close(np.concatenate(got), np.concatenate(want), "bf16", "temporal strided sampled")
