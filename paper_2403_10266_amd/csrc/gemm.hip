@@ -13,7 +13,8 @@
 //    output row and four consecutive output columns per register group: the
 //    epilogue reads bias/residual and writes results as 8- or 16-byte
 //    vectors.
-//  * Epilogues: none, exact-erf GELU (bf16 out), fp32 output, residual add
+//  * Epilogues: none, erf GELU (bf16 out; erf evaluated by Abramowitz-Stegun
+//    7.1.26, abs. error <= 1.5e-7), fp32 output, residual add
 //    (fp32 out, may be in place).
 // fp32 path: LDS-tiled FMA kernel, 64 x 64 tile, 4 x 4 outputs per thread.
 #include <math.h>
@@ -27,6 +28,7 @@ typedef __bf16 bf16;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 256, BN = 128, BK = 64;
 constexpr int PITCH = BK + 8;                 // 144-byte rows
@@ -38,8 +40,37 @@ static_assert((A_CHUNKS + W_CHUNKS) % NTHR == 0, "loader shape");
 
 __device__ __forceinline__ float bf2f(bf16 v) { return (float)v; }
 
-__device__ __forceinline__ float gelu_erf(float v) {
-  return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+// Buffer resource over [base, base + bytes) built from wave-uniform values in
+// scalar registers; out-of-range loads return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  const uint32_t n = __builtin_amdgcn_readfirstlane(bytes);
+  void* p = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)n, 0x00020000);
+}
+
+// erf(z) by Abramowitz and Stegun, Handbook of Mathematical Functions, 7.1.26:
+// 1 - (a1 t + ... + a5 t^5) exp(-z^2) with t = 1 / (1 + p |z|), |error| <=
+// 1.5e-7 -- far below the bf16 rounding of the GEMM output, and a reciprocal,
+// an exp2 and five FMAs instead of a general erf.
+__device__ __forceinline__ float erf_as7126(float z) {
+  const float a = fabsf(z);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  poly *= t;
+  // exp(-a^2) = exp2(-a^2 log2 e); the raw exp2 flushes tiny results to 0
+  const float e = __builtin_amdgcn_exp2f(-a * a * 1.4426950408889634f);
+  return copysignf(1.0f - poly * e, z);
+}
+
+// GELU x * Phi(x) for the bf16 path (output rounded to bf16)
+__device__ __forceinline__ float gelu_bf16out(float v) {
+  return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f));
 }
 
 template <int EPI>
@@ -62,37 +93,38 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
   const int wm = wave & 1, wn = wave >> 1;
   const int l32 = lane & 31, g = lane >> 5;
 
-  uint4 pre[NLOAD];
+  // Loader: thread t moves 16-byte chunk (row t/8 + 32 i, column 8 (t % 8)) of
+  // the A slice (i < 8) and of the W slice (i < 4), through buffer resources
+  // whose range ends at the last valid row (rows past M or N read as zero).
+  // The per-thread offsets are fixed; a slice only adds its K offset.
+  const int lrow = threadIdx.x >> 3, lcol = threadIdx.x & 7;
+  const uint32_t row_bytes = (uint32_t)K * 2u;
+  const uint32_t a_rows = (uint32_t)min(BM, M - m0), w_rows = (uint32_t)min(BN, N - n0);
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + (int64_t)m0 * K, a_rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(W + (int64_t)n0 * K, w_rows * row_bytes);
+  const uint32_t off0 = (uint32_t)lrow * row_bytes + (uint32_t)lcol * 16u;
+  const uint32_t step32 = 32u * row_bytes;            // 32 rows further
+  constexpr int A_LOADS = A_CHUNKS / NTHR, W_LOADS = W_CHUNKS / NTHR;
+  u32x4 pre[NLOAD];
   auto load_regs = [&](int k0) {
+    // columns past K: an offset past every range reads zero
+    const bool kin = k0 + 8 * lcol < K;
+    const uint32_t off = off0 + (uint32_t)k0 * 2u;
 #pragma unroll
-    for (int i = 0; i < NLOAD; ++i) {
-      const int c = threadIdx.x + i * NTHR;
-      pre[i] = make_uint4(0, 0, 0, 0);
-      if (c < A_CHUNKS) {
-        const int row = c / (BK / 8), col = c % (BK / 8);
-        const int gm = m0 + row, gk = k0 + col * 8;
-        if (gm < M && gk < K) pre[i] = *reinterpret_cast<const uint4*>(A + (int64_t)gm * K + gk);
-      } else {
-        const int cc = c - A_CHUNKS;
-        const int row = cc / (BK / 8), col = cc % (BK / 8);
-        const int gn = n0 + row, gk = k0 + col * 8;
-        if (gn < N && gk < K) pre[i] = *reinterpret_cast<const uint4*>(W + (int64_t)gn * K + gk);
-      }
-    }
+    for (int i = 0; i < A_LOADS; ++i)
+      pre[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, kin ? off + i * step32 : 0xFFFFFFF0u, 0, 0);
+#pragma unroll
+    for (int i = 0; i < W_LOADS; ++i)
+      pre[A_LOADS + i] =
+          __builtin_amdgcn_raw_buffer_load_b128(rw, kin ? off + i * step32 : 0xFFFFFFF0u, 0, 0);
   };
   auto store_lds = [&]() {
 #pragma unroll
-    for (int i = 0; i < NLOAD; ++i) {
-      const int c = threadIdx.x + i * NTHR;
-      if (c < A_CHUNKS) {
-        const int row = c / (BK / 8), col = c % (BK / 8);
-        *reinterpret_cast<uint4*>(As + row * PITCH + col * 8) = pre[i];
-      } else {
-        const int cc = c - A_CHUNKS;
-        const int row = cc / (BK / 8), col = cc % (BK / 8);
-        *reinterpret_cast<uint4*>(Ws + row * PITCH + col * 8) = pre[i];
-      }
-    }
+    for (int i = 0; i < A_LOADS; ++i)
+      *reinterpret_cast<u32x4*>(As + (lrow + 32 * i) * PITCH + lcol * 8) = pre[i];
+#pragma unroll
+    for (int i = 0; i < W_LOADS; ++i)
+      *reinterpret_cast<u32x4*>(Ws + (lrow + 32 * i) * PITCH + lcol * 8) = pre[A_LOADS + i];
   };
 
   floatx16 acc[2][4];
@@ -153,7 +185,7 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
         }
         if (EPI == DSP_EPI_GELU) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = gelu_erf(v[i]);
+          for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
         }
         const int64_t off = (int64_t)m * N + n;
         if (EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32) {
@@ -252,7 +284,9 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
   if (M == 0) return DSP_OK;
   const int64_t n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN;
   const int64_t tiles = n_mt * n_nt;
-  if (tiles >= (int64_t(1) << 31) || M >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
+  // a tile's buffer resources address BM rows of K bf16 with 32-bit offsets
+  if (tiles >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) || (int64_t)BM * K * 2 >= (int64_t(1) << 31))
+    return DSP_ERR_SHAPE;
   const dim3 grid((uint32_t)tiles), block(NTHR);
   const bf16* A = static_cast<const bf16*>(a);
   const bf16* Wt = static_cast<const bf16*>(w);
