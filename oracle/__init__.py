@@ -26,9 +26,10 @@ of each module for what pins it.
 from .switch import switch, unswitch, exchange_unpack, switch_index_map
 from .attention import attention, attention_rows, spatial_attention, temporal_attention, \
     temporal_attention_strided
-from .block import layernorm, linear, gelu, st_block, tiny_chain, BLOCK_NO_MLP_LN
+from .block import layernorm, linear, gelu, relu, st_block, tiny_chain, BLOCK_NO_MLP_LN, BLOCK_POST_LN, \
+    BLOCK_RELU
 
 __all__ = ["switch", "unswitch", "exchange_unpack", "switch_index_map", "attention",
            "attention_rows", "spatial_attention", "temporal_attention",
            "temporal_attention_strided", "layernorm", "linear", "gelu", "st_block", "tiny_chain",
-           "BLOCK_NO_MLP_LN"]
+           "BLOCK_NO_MLP_LN", "BLOCK_POST_LN", "BLOCK_RELU", "relu"]

@@ -244,6 +244,15 @@ def pin_gelu(gelu):
     assert math.isclose(gelu(np.array([1.0]))[0], 0.8413447460685429, rel_tol=1e-15)
 
 
+def pin_relu(relu):
+    """Eq. (5): max(0, x).  relu(x) - relu(-x) = x and relu(x) + relu(-x) = |x|."""
+    x = np.linspace(-5, 5, 101)
+    assert np.array_equal(relu(x) - relu(-x), x)
+    assert np.array_equal(relu(x) + relu(-x), np.abs(x))
+    assert relu(np.array([0.0]))[0] == 0.0
+    assert np.array_equal(relu(np.array([-2.5, 3.25])), np.array([0.0, 3.25]))
+
+
 # ----------------------------------------------------------------------------- block
 def _block_params(rng, C, F, scale=0.3, bias=False):
     p = {"wqkv_s": rng.standard_normal((C, 3 * C)) * scale, "wo_s": rng.standard_normal((C, C)) * scale,
@@ -331,6 +340,35 @@ def pin_block_sharded_equals_unsharded(st_block, layernorm, linear, gelu, switch
         y = y + linear(gelu(linear(layernorm(y), p["w1"], p["b1"])), p["w2"], p["b2"])
         outs.append(y)
     assert np.allclose(np.concatenate(outs, axis=1), want, rtol=1e-12, atol=1e-12)
+
+
+def pin_block_post_ln_relu(st_block, layernorm, linear, relu, switch, post_flag, relu_flag):
+    """The paper's own block, Eq. (4)-(6): x <- LN(x + sublayer(x)) with a ReLU FFN.
+    * Every output row is LN's: mean 0 and (with eps = 0) variance 1.
+    * Zero output projections leave LN(LN(LN(switch(x)))) = switch(LN(x)).
+    * The MLP path alone is LN(y + ReLU(y W1) W2) with y = LN(switch(x))."""
+    rng = np.random.default_rng(26)
+    B, T, S, C, H, F = 1, 3, 4, 8, 2, 16
+    x = rng.standard_normal((B, T, S, C)) * 2.0 + 0.5
+    p = _block_params(rng, C, F)
+    flags = post_flag | relu_flag
+    out = st_block(x, p, H, 0.0, flags)
+    assert np.allclose(out.mean(axis=-1), 0.0, atol=1e-12)
+    assert np.allclose(out.var(axis=-1), 1.0, atol=1e-12)
+    zc, zf = np.zeros((C, C)), np.zeros((F, C))
+    xt = np.ascontiguousarray(switch(x, 1, 2, 1)[0])
+    y0 = layernorm(xt, 0.0)
+    assert np.allclose(st_block(x, dict(p, wo_s=zc, wo_t=zc, w2=zf), H, 0.0, flags), y0,
+                       rtol=1e-12, atol=1e-12)
+    want = layernorm(y0 + linear(relu(linear(y0, p["w1"])), p["w2"]), 0.0)
+    assert np.allclose(st_block(x, dict(p, wo_s=zc, wo_t=zc), H, 0.0, flags), want,
+                       rtol=1e-12, atol=1e-12)
+    # post-LN alone keeps the GELU MLP; ReLU alone keeps the pre-LN placement
+    g = st_block(x, dict(p, wo_s=zc, wo_t=zc), H, 0.0, post_flag)
+    assert not np.allclose(g, want)
+    r = st_block(x, dict(p, wo_s=zc, wo_t=zc), H, 0.0, relu_flag)
+    assert np.allclose(r, xt + linear(relu(linear(layernorm(xt, 0.0), p["w1"])), p["w2"]),
+                       rtol=1e-12, atol=1e-12)
 
 
 def pin_tiny_chain(tiny_chain, st_block):

@@ -22,7 +22,7 @@ def _impl():
         switch=SW.switch, unswitch=SW.unswitch, exchange_unpack=SW.exchange_unpack,
         index_map=SW.switch_index_map, attention=AT.attention, spatial=AT.spatial_attention,
         temporal=AT.temporal_attention, strided=AT.temporal_attention_strided,
-        layernorm=BL.layernorm, linear=BL.linear, gelu=BL.gelu, st_block=BL.st_block,
+        layernorm=BL.layernorm, linear=BL.linear, gelu=BL.gelu, relu=BL.relu, st_block=BL.st_block,
         tiny_chain=BL.tiny_chain)
 
 
@@ -46,6 +46,9 @@ def _pins(i):
         lambda: P.pin_layernorm(i.layernorm),
         lambda: P.pin_linear(i.linear),
         lambda: P.pin_gelu(i.gelu),
+        lambda: P.pin_relu(i.relu),
+        lambda: P.pin_block_post_ln_relu(i.st_block, i.layernorm, i.linear, i.relu, i.switch,
+                                         BL.BLOCK_POST_LN, BL.BLOCK_RELU),
         lambda: P.pin_block_identities(i.st_block, i.layernorm, i.linear, i.gelu, i.switch),
         lambda: P.pin_block_t1_s1(i.st_block, i.layernorm, i.linear, i.gelu),
         lambda: P.pin_block_sharded_equals_unsharded(i.st_block, i.layernorm, i.linear, i.gelu,
@@ -206,6 +209,35 @@ def block_post_mlp_ln(x, p, H, eps=1e-6, flags=0):
     return y
 
 
+def relu_leaky(x):
+    x = np.asarray(x, float)
+    return np.where(x > 0, x, 0.01 * x)
+
+
+def block_post_ln_inside(x, p, H, eps=1e-6, flags=0):
+    # post-LN placed on the sublayer output instead of the sum: x + LN(F(x))
+    if not flags & BL.BLOCK_POST_LN:
+        return _orig_block(x, p, H, eps, flags)
+    saved = BL.layernorm
+    f = flags & ~BL.BLOCK_POST_LN
+
+    def attn_sub(h, wq, bq, wo, bo, attn):
+        return saved(BL._attn_sublayer(h, wq, bq, wo, bo, H, attn), eps)
+    act = BL.relu if flags & BL.BLOCK_RELU else BL.gelu
+    x = np.asarray(x, float)
+    x = x + attn_sub(x, p["wqkv_s"], p.get("bqkv_s"), p["wo_s"], p.get("bo_s"), BL.spatial_attention)
+    y = BL.switch(x, 1, 2, 1)[0]
+    y = y + attn_sub(y, p["wqkv_t"], p.get("bqkv_t"), p["wo_t"], p.get("bo_t"), BL.temporal_attention)
+    return y + saved(BL.linear(act(BL.linear(y, p["w1"], p.get("b1"))), p["w2"], p.get("b2")), eps)
+
+
+def block_post_ln_no_final(x, p, H, eps=1e-6, flags=0):
+    # post-LN without the LN after the MLP's residual add
+    if not flags & BL.BLOCK_POST_LN:
+        return _orig_block(x, p, H, eps, flags)
+    return _orig_block(x, p, H, eps, flags | BL.BLOCK_NO_MLP_LN)
+
+
 _orig_block = BL.st_block
 
 MUTANTS = {
@@ -229,6 +261,9 @@ MUTANTS = {
     "block: spatial half over T": [(BL, "st_block", block_wrong_axes)],
     "block: temporal residual dropped": [(BL, "st_block", block_no_temporal_residual)],
     "block: no LN before the MLP": [(BL, "st_block", block_post_mlp_ln)],
+    "relu: leaky negative slope": [(BL, "relu", relu_leaky)],
+    "block: post-LN on the sublayer, not the sum": [(BL, "st_block", block_post_ln_inside)],
+    "block: post-LN without the MLP's LN": [(BL, "st_block", block_post_ln_no_final)],
 }
 
 

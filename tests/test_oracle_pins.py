@@ -66,6 +66,15 @@ def test_gelu():
     P.pin_gelu(oracle.gelu)
 
 
+def test_relu():
+    P.pin_relu(oracle.relu)
+
+
+def test_block_post_ln_relu():
+    P.pin_block_post_ln_relu(oracle.st_block, oracle.layernorm, oracle.linear, oracle.relu,
+                             oracle.switch, oracle.BLOCK_POST_LN, oracle.BLOCK_RELU)
+
+
 def test_block_identities():
     P.pin_block_identities(oracle.st_block, oracle.layernorm, oracle.linear, oracle.gelu,
                            oracle.switch)
