@@ -184,18 +184,18 @@ int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows
  * w:        [N, K] of dtype (stored [out][in]).
  * bias:     [N] of dtype, or NULL.
  * residual: [M, N] fp32 or NULL; required iff DSP_EPI_RESID.  May equal out.
- * out:      [M, N]; dtype for DSP_EPI_NONE / DSP_EPI_GELU, fp32 for
- *           DSP_EPI_F32 (out = a*W + bias) and DSP_EPI_RESID
+ * out:      [M, N]; dtype for DSP_EPI_NONE / DSP_EPI_GELU / DSP_EPI_RELU,
+ *           fp32 for DSP_EPI_F32 (out = a*W + bias) and DSP_EPI_RESID
  *           (out = residual + a*W + bias).
- * epilogue: DSP_EPI_NONE, DSP_EPI_GELU (exact-erf GELU: x*Phi(x)),
- *           DSP_EPI_RESID, DSP_EPI_F32.
+ * epilogue: DSP_EPI_NONE, DSP_EPI_GELU (erf GELU: x*Phi(x)), DSP_EPI_RESID,
+ *           DSP_EPI_F32, DSP_EPI_RELU (max(0, x): the FFN activation of Eq. 5).
  * dtype:    DSP_BF16 (bf16 MFMA, fp32 accumulation) or DSP_F32 (fp32 FMA).
  * bf16 needs K % 8 == 0 and 16-byte aligned a, w, out and residual
  * (DSP_ERR_ALIGN).  out must not overlap a, w or bias.
  * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE (M < 0, N < 1, K < 1), DSP_ERR_DTYPE,
  *   DSP_ERR_ALIGN, DSP_ERR_ARG (unknown epilogue, residual missing).
  * ------------------------------------------------------------------------ */
-enum { DSP_EPI_NONE = 0, DSP_EPI_GELU = 1, DSP_EPI_RESID = 2, DSP_EPI_F32 = 3 };
+enum { DSP_EPI_NONE = 0, DSP_EPI_GELU = 1, DSP_EPI_RESID = 2, DSP_EPI_F32 = 3, DSP_EPI_RELU = 4 };
 int dsp_linear(const void* a, const void* w, const void* bias, const float* residual, void* out,
                int64_t M, int N, int K, int epilogue, int dtype, void* stream);
 
@@ -213,10 +213,15 @@ int dsp_linear(const void* a, const void* w, const void* bias, const float* resi
  * [Q | K | V], wo_* [C][C], w1 [F][C], w2 [C][F]; biases ([out], dtype) may be
  * NULL.  x_BTSC and y_BSTC are fp32 (the residual stream); they must not
  * overlap.  Flags:
- *   DSP_BLOCK_NO_MLP_LN -- no LayerNorm before the MLP;
+ *   DSP_BLOCK_NO_MLP_LN -- no LayerNorm for the MLP;
  *   DSP_BLOCK_ATTN_ONLY -- projections and attention only: no LayerNorm, no
  *     residual adds and no MLP (w1/w2 unused):
- *       y = Wo_t * TemporalAttn(Switch(Wo_s * SpatialAttn(x * Wqkv_s)) * Wqkv_t).
+ *       y = Wo_t * TemporalAttn(Switch(Wo_s * SpatialAttn(x * Wqkv_s)) * Wqkv_t);
+ *   DSP_BLOCK_POST_LN -- every LayerNorm after its residual add, the form of
+ *     Eq. 4 and Eq. 6:  x = LN(x + Wo_s * SpatialAttn(x * Wqkv_s)), ...,
+ *     y = LN(y + W2 * act(y * W1));
+ *   DSP_BLOCK_RELU -- the FFN activation is ReLU (Eq. 5) instead of GELU.
+ *   DSP_BLOCK_POST_LN | DSP_BLOCK_RELU is the paper's own block.
  * workspace: device buffer of at least dsp_st_block_workspace_bytes(...)
  * bytes, 256-byte aligned, owned by the caller; contents are scratch.
  * dsp_st_block_workspace_bytes returns 0 for invalid sizes.
@@ -228,7 +233,7 @@ typedef struct {
   const void *w1, *b1, *w2, *b2;
 } dsp_block_weights_t;
 
-enum { DSP_BLOCK_NO_MLP_LN = 1, DSP_BLOCK_ATTN_ONLY = 2 };
+enum { DSP_BLOCK_NO_MLP_LN = 1, DSP_BLOCK_ATTN_ONLY = 2, DSP_BLOCK_POST_LN = 4, DSP_BLOCK_RELU = 8 };
 
 size_t dsp_st_block_workspace_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F,
                                     int dtype);

@@ -26,8 +26,8 @@ LIB_PATH = _PKG / "libdsp.so"
 DSP_OK, DSP_ERR_NULL, DSP_ERR_DIM, DSP_ERR_SHAPE, DSP_ERR_DTYPE, DSP_ERR_ALIGN, DSP_ERR_HIP, \
     DSP_ERR_WORKSPACE, DSP_ERR_ARG = range(9)
 DSP_F32, DSP_BF16 = 0, 1
-DSP_EPI_NONE, DSP_EPI_GELU, DSP_EPI_RESID, DSP_EPI_F32 = 0, 1, 2, 3
-DSP_BLOCK_NO_MLP_LN, DSP_BLOCK_ATTN_ONLY = 1, 2
+DSP_EPI_NONE, DSP_EPI_GELU, DSP_EPI_RESID, DSP_EPI_F32, DSP_EPI_RELU = 0, 1, 2, 3, 4
+DSP_BLOCK_NO_MLP_LN, DSP_BLOCK_ATTN_ONLY, DSP_BLOCK_POST_LN, DSP_BLOCK_RELU = 1, 2, 4, 8
 
 BLOCK_WEIGHT_FIELDS = ("wqkv_s", "bqkv_s", "wo_s", "bo_s", "wqkv_t", "bqkv_t", "wo_t", "bo_t",
                        "w1", "b1", "w2", "b2")

@@ -143,7 +143,7 @@ int linear_impl(const void* a, const void* w, const void* bias, const float* res
                 int64_t M, int N, int K, int epilogue, int dtype, hipStream_t s) {
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
   if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
-  if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_F32) return DSP_ERR_ARG;
+  if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_RELU) return DSP_ERR_ARG;
   if (!w) return DSP_ERR_NULL;
   if (M == 0) return DSP_OK;
   if (!a || !out) return DSP_ERR_NULL;
@@ -302,7 +302,8 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
                          int H, int F, float ln_eps, int flags, int dtype, void* stream) {
   if (!x_BTSC || !y_BSTC || !w) return DSP_ERR_NULL;
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
-  if (flags & ~(DSP_BLOCK_NO_MLP_LN | DSP_BLOCK_ATTN_ONLY)) return DSP_ERR_ARG;
+  if (flags & ~(DSP_BLOCK_NO_MLP_LN | DSP_BLOCK_ATTN_ONLY | DSP_BLOCK_POST_LN | DSP_BLOCK_RELU))
+    return DSP_ERR_ARG;
   const bool attn_only = (flags & DSP_BLOCK_ATTN_ONLY) != 0;
   if (B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || C % H || F < 0) return DSP_ERR_SHAPE;
   if (!attn_only && F < 1) return DSP_ERR_SHAPE;
@@ -347,35 +348,72 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
     if (st != DSP_OK) return st; \
   } while (0)
 
-  // ---- spatial half on (B, T, S, C): attention over S inside each frame
-  if (attn_only) DSP_TRY(launch_cast(x_BTSC, 0, h, bf, tokens * C, s));
-  else DSP_TRY(launch_layernorm(x_BTSC, 0, h, bf, tokens, C, ln_eps, s));
-  DSP_TRY(linear_impl(h, w->wqkv_s, w->bqkv_s, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s));
-  DSP_TRY(attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, T, S, H, D, ld3, C,
-                    0.0f, dtype, s));
-  DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, attn_only ? nullptr : x_BTSC, x1, tokens, C, C,
-                      attn_only ? DSP_EPI_F32 : DSP_EPI_RESID, dtype, s));
-  // ---- the Switch T -> S on one GPU: (B, T, S, C) -> (B, S, T, C)
+  const bool post = (flags & DSP_BLOCK_POST_LN) != 0 && !attn_only;
+  const int act = (flags & DSP_BLOCK_RELU) ? DSP_EPI_RELU : DSP_EPI_GELU;
   const int64_t shp[4] = {B, T, S, C};
-  DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
-  // ---- temporal half on (B, S, T, C): attention over T at each location
-  if (attn_only) DSP_TRY(launch_cast(y_BSTC, 0, h, bf, tokens * C, s));
-  else DSP_TRY(launch_layernorm(y_BSTC, 0, h, bf, tokens, C, ln_eps, s));
-  DSP_TRY(linear_impl(h, w->wqkv_t, w->bqkv_t, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s));
-  DSP_TRY(attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, S, T, H, D, ld3, C,
-                    0.0f, dtype, s));
+  // the bf16 (or fp32) operand of a projection: LN of the residual stream, or
+  // (post-LN, projection-only chain) the stream itself
+  auto operand = [&](const float* r, bool norm) {
+    return norm ? launch_layernorm(r, 0, h, bf, tokens, C, ln_eps, s)
+                : launch_cast(r, 0, h, bf, tokens * C, s);
+  };
+  auto attn_sublayer = [&](const void* wqkv, const void* bqkv, int64_t X, int64_t L) {
+    int r = linear_impl(h, wqkv, bqkv, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s);
+    if (r != DSP_OK) return r;
+    return attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, X, L, H, D, ld3, C,
+                     0.0f, dtype, s);
+  };
   if (attn_only) {
+    // y = Wo_t * TemporalAttn(Switch(Wo_s * SpatialAttn(x * Wqkv_s)) * Wqkv_t)
+    DSP_TRY(operand(x_BTSC, false));
+    DSP_TRY(attn_sublayer(w->wqkv_s, w->bqkv_s, T, S));
+    DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, nullptr, x1, tokens, C, C, DSP_EPI_F32, dtype, s));
+    DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+    DSP_TRY(operand(y_BSTC, false));
+    DSP_TRY(attn_sublayer(w->wqkv_t, w->bqkv_t, S, T));
     DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, nullptr, y_BSTC, tokens, C, C, DSP_EPI_F32, dtype, s));
     return DSP_OK;
   }
-  DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, y_BSTC, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s));
-  // ---- MLP with GELU (Eq. 5 with the configuration's activation), residual
-  if (flags & DSP_BLOCK_NO_MLP_LN) DSP_TRY(launch_cast(y_BSTC, 0, h, bf, tokens * C, s));
-  else DSP_TRY(launch_layernorm(y_BSTC, 0, h, bf, tokens, C, ln_eps, s));
-  DSP_TRY(linear_impl(h, w->w1, w->b1, nullptr, f, tokens, F, C, DSP_EPI_GELU, dtype, s));
-  DSP_TRY(linear_impl(f, w->w2, w->b2, y_BSTC, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
-#undef DSP_TRY
+  if (!post) {
+    // pre-LN: x += F(LN(x)) for each sublayer
+    // ---- spatial half on (B, T, S, C): attention over S inside each frame
+    DSP_TRY(operand(x_BTSC, true));
+    DSP_TRY(attn_sublayer(w->wqkv_s, w->bqkv_s, T, S));
+    DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, x_BTSC, x1, tokens, C, C, DSP_EPI_RESID, dtype, s));
+    // ---- the Switch T -> S on one GPU: (B, T, S, C) -> (B, S, T, C)
+    DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+    // ---- temporal half on (B, S, T, C): attention over T at each location
+    DSP_TRY(operand(y_BSTC, true));
+    DSP_TRY(attn_sublayer(w->wqkv_t, w->bqkv_t, S, T));
+    DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, y_BSTC, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s));
+    // ---- MLP (Eq. 5 with GELU or ReLU), residual
+    DSP_TRY(operand(y_BSTC, !(flags & DSP_BLOCK_NO_MLP_LN)));
+    DSP_TRY(linear_impl(h, w->w1, w->b1, nullptr, f, tokens, F, C, act, dtype, s));
+    DSP_TRY(linear_impl(f, w->w2, w->b2, y_BSTC, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
+    return DSP_OK;
+  }
+  // post-LN (Eq. 4, 6): x = LN(x + F(x)) for each sublayer.  The residual
+  // stream alternates between x1 and y_BSTC (LN is never run in place).
+  DSP_TRY(operand(x_BTSC, false));
+  DSP_TRY(attn_sublayer(w->wqkv_s, w->bqkv_s, T, S));
+  DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, x_BTSC, x1, tokens, C, C, DSP_EPI_RESID, dtype, s));
+  // switch first, then LN: LN acts per token, so LN(Switch(v)) = Switch(LN(v))
+  DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+  DSP_TRY(launch_layernorm(y_BSTC, 0, x1, 0, tokens, C, ln_eps, s));           // x1 = r1 (B,S,T,C)
+  DSP_TRY(operand(x1, false));
+  DSP_TRY(attn_sublayer(w->wqkv_t, w->bqkv_t, S, T));
+  DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, x1, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s));
+  DSP_TRY(launch_layernorm(y_BSTC, 0, x1, 0, tokens, C, ln_eps, s));           // x1 = r2
+  DSP_TRY(operand(x1, false));
+  DSP_TRY(linear_impl(h, w->w1, w->b1, nullptr, f, tokens, F, C, act, dtype, s));
+  if (flags & DSP_BLOCK_NO_MLP_LN) {
+    DSP_TRY(linear_impl(f, w->w2, w->b2, x1, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
+    return DSP_OK;
+  }
+  DSP_TRY(linear_impl(f, w->w2, w->b2, x1, x1, tokens, C, F, DSP_EPI_RESID, dtype, s));
+  DSP_TRY(launch_layernorm(x1, 0, y_BSTC, 0, tokens, C, ln_eps, s));
   return DSP_OK;
+#undef DSP_TRY
 }
 
 }  // extern "C"

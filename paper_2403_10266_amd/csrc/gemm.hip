@@ -14,7 +14,7 @@
 //    epilogue reads bias/residual and writes results as 8- or 16-byte
 //    vectors.
 //  * Epilogues: none, erf GELU (bf16 out; erf evaluated by Abramowitz-Stegun
-//    7.1.26, abs. error <= 1.5e-7), fp32 output, residual add
+//    7.1.26, abs. error <= 1.5e-7), ReLU (Eq. 5), fp32 output, residual add
 //    (fp32 out, may be in place).
 // fp32 path: LDS-tiled FMA kernel, 64 x 64 tile, 4 x 4 outputs per thread.
 #include <math.h>
@@ -187,6 +187,10 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
 #pragma unroll
           for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
         }
+        if (EPI == DSP_EPI_RELU) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
+        }
         const int64_t off = (int64_t)m * N + n;
         if (EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32) {
           float* o = static_cast<float*>(out);
@@ -270,6 +274,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
       float v = acc[i][j];
       if (bias) v += bias[n];
       if (EPI == DSP_EPI_GELU) v = 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+      if (EPI == DSP_EPI_RELU) v = fmaxf(v, 0.0f);
       const int64_t off = (int64_t)m * N + n;
       if (EPI == DSP_EPI_RESID) v += resid[off];
       out[off] = v;
@@ -308,6 +313,10 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
       hipLaunchKernelGGL(gemm_bf16_kernel<DSP_EPI_F32>, grid, block, 0, s, A, Wt, bs, residual,
                          out, (int)M, N, K, (int)n_nt, (int)tiles);
       break;
+    case DSP_EPI_RELU:
+      hipLaunchKernelGGL(gemm_bf16_kernel<DSP_EPI_RELU>, grid, block, 0, s, A, Wt, bs, residual,
+                         out, (int)M, N, K, (int)n_nt, (int)tiles);
+      break;
     default:
       return DSP_ERR_ARG;
   }
@@ -335,6 +344,10 @@ int launch_linear_f32(const float* a, const float* w, const float* bias, const f
       break;
     case DSP_EPI_F32:
       hipLaunchKernelGGL(gemm_f32_kernel<DSP_EPI_NONE>, grid, block, 0, s, a, w, bias, residual, out,
+                         (int)M, N, K);
+      break;
+    case DSP_EPI_RELU:
+      hipLaunchKernelGGL(gemm_f32_kernel<DSP_EPI_RELU>, grid, block, 0, s, a, w, bias, residual, out,
                          (int)M, N, K);
       break;
     default:

@@ -161,6 +161,7 @@ def test_linear_validation(lib):
     assert f(a=None) == dsp.DSP_ERR_NULL
     assert f(epi=2) == dsp.DSP_ERR_NULL                    # residual required
     assert f(epi=9) == dsp.DSP_ERR_ARG
+    assert f(epi=5) == dsp.DSP_ERR_ARG                      # one past DSP_EPI_RELU
     assert f(dt=9) == dsp.DSP_ERR_DTYPE
     assert f(N=0) == dsp.DSP_ERR_SHAPE
     assert f(K=12) == dsp.DSP_ERR_ALIGN                    # bf16 needs K % 8 == 0
@@ -186,7 +187,7 @@ def test_block_validation_and_workspace(lib):
     assert f(ws=None) == dsp.DSP_ERR_WORKSPACE
     assert f(wsb=need - 1) == dsp.DSP_ERR_WORKSPACE
     assert f(ws=0x40000010) == dsp.DSP_ERR_ALIGN
-    assert f(flags=8) == dsp.DSP_ERR_ARG
+    assert f(flags=16) == dsp.DSP_ERR_ARG                   # unknown flag bit
     assert f(dt=4) == dsp.DSP_ERR_DTYPE
     assert f(eps=-1.0) == dsp.DSP_ERR_ARG
     assert f(F_=0) == dsp.DSP_ERR_SHAPE                     # the MLP needs F >= 1

@@ -43,18 +43,28 @@ def _block_case(torch, w, with_bias, flags=0):
     assert_close(host(y), want, w.dtype, w.name)
 
 
+# flags: 0 pre-LN GELU, 1 no MLP LayerNorm, 4 post-LN (Eq. 4, 6), 8 ReLU FFN
+# (Eq. 5), 12 the paper's post-LN ReLU block, 13 post-LN without the last LN
 @pytest.mark.parametrize("with_bias", [False, True])
-@pytest.mark.parametrize("flags", [0, 1])
+@pytest.mark.parametrize("flags", [0, 1, 4, 8, 12, 13])
 def test_small_block_bf16(torch, with_bias, flags):
     w = synth.Workload("block_small", "block", "bf16", B=2, T=5, S=24, C=144, H=2, F=576, seed=11)
     _block_case(torch, w, with_bias, flags)
 
 
-def test_small_block_f32(torch):
+@pytest.mark.parametrize("flags", [0, 12, 13])
+def test_small_block_f32(torch, flags):
     w = synth.Workload("block_small_f32", "block", "f32", B=1, T=4, S=9, C=64, H=4, F=128, seed=12)
-    _block_case(torch, w, True)
+    _block_case(torch, w, True, flags)
 
 
 def test_full_block_bf16(torch):
     """The 720M-model block at B=1, T=32, S=1024 (C=1152, 16 heads, MLP 4608)."""
     _block_case(torch, synth.WORKLOADS["block_bf16_B1_T32_S1024"], False)
+
+
+def test_full_block_bf16_post_ln_relu(torch):
+    """The same block in the paper's post-LN form with a ReLU FFN."""
+    import paper_2403_10266_amd as dsp
+    _block_case(torch, synth.WORKLOADS["block_bf16_B1_T32_S1024"], False,
+                dsp.DSP_BLOCK_POST_LN | dsp.DSP_BLOCK_RELU)

@@ -33,7 +33,7 @@ def test_layernorm(torch, rows, C, out):
 @pytest.mark.parametrize("M,N,K", [(1, 8, 8), (300, 200, 72), (513, 1152, 1152), (64, 4608, 1152),
                                    (257, 136, 4608), (256, 192, 8), (777, 385, 104),
                                    (512, 3456, 1152)])
-@pytest.mark.parametrize("epi", [0, 1, 2, 3])
+@pytest.mark.parametrize("epi", [0, 1, 2, 3, 4])
 @pytest.mark.parametrize("bias", [False, True])
 def test_linear_bf16(torch, M, N, K, epi, bias):
     import paper_2403_10266_amd as dsp
@@ -49,6 +49,8 @@ def test_linear_bf16(torch, M, N, K, epi, bias):
     want = oracle.linear(a, w.T, b)
     if epi == 1:
         want = oracle.gelu(want)
+    if epi == 4:
+        want = oracle.relu(want)
     if epi == 2:
         want = want + r
     # bf16 outputs carry a bf16 rounding; fp32 outputs only accumulation error
@@ -69,7 +71,7 @@ def test_linear_resid_in_place(torch, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(3, 5, 7), (100, 70, 64), (65, 192, 64)])
-@pytest.mark.parametrize("epi", [0, 1, 2])
+@pytest.mark.parametrize("epi", [0, 1, 2, 4])
 def test_linear_f32(torch, M, N, K, epi):
     import paper_2403_10266_amd as dsp
     rng = np.random.default_rng(M + N + K)
@@ -82,6 +84,8 @@ def test_linear_f32(torch, M, N, K, epi):
     want = oracle.linear(a, w.T, b)
     if epi == 1:
         want = oracle.gelu(want)
+    if epi == 4:
+        want = oracle.relu(want)
     if epi == 2:
         want = want + r
     assert_close(host(out), want, "f32", f"linear f32 epi={epi}")
