@@ -11,7 +11,9 @@ float64 NumPy (library matmul and erf as the only primitives):
 * ``switch`` / ``unswitch`` / ``exchange_unpack`` -- the Switch primitive of
   the primitive table in the Dynamic Primitives section (Eq. 10) restricted to
   one GPU's share: a layout permute plus a pack into per-destination chunks,
-  done on raw bit patterns.
+  done on raw bit patterns, for K = 2 or 3 sequence dimensions.
+* ``split`` / ``gather`` -- the table's Split and Gather rows (one rank's
+  slice; the concatenation of every rank's slice).
 * ``attention`` -- scaled dot-product attention, Eq. (3), applied per head
   (Eq. 1-2) along one sequence dimension of a multi-dimensional sequence
   (Eq. 7-8): ``spatial_attention`` over S within each frame and
@@ -23,13 +25,13 @@ Pins: every function is checked in ``tests/test_oracle_pins.py`` against
 closed forms, invariants, hand-worked fixtures and brute force; see the header
 of each module for what pins it.
 """
-from .switch import switch, unswitch, exchange_unpack, switch_index_map
+from .switch import switch, unswitch, exchange_unpack, switch_index_map, split, gather
 from .attention import attention, attention_rows, spatial_attention, temporal_attention, \
     temporal_attention_strided
 from .block import layernorm, linear, gelu, relu, st_block, tiny_chain, BLOCK_NO_MLP_LN, BLOCK_POST_LN, \
     BLOCK_RELU
 
-__all__ = ["switch", "unswitch", "exchange_unpack", "switch_index_map", "attention",
+__all__ = ["switch", "unswitch", "exchange_unpack", "switch_index_map", "split", "gather", "attention",
            "attention_rows", "spatial_attention", "temporal_attention",
            "temporal_attention_strided", "layernorm", "linear", "gelu", "st_block", "tiny_chain",
            "BLOCK_NO_MLP_LN", "BLOCK_POST_LN", "BLOCK_RELU", "relu"]

@@ -86,6 +86,98 @@ def pin_switch_nrank_simulation(switch, exchange_unpack):
                 assert np.array_equal(got[n], want[n])
 
 
+def _k3_source(shape, f, t, n_chunks, out_idx):
+    """Input index of packed element out_idx = (n, b, o_1, o_2, i, c) for a K = 3
+    switch, by the definition: the other two sequence dims in their order (the
+    to-dim's index offset by its chunk), the from-dim index i, then c."""
+    n, b, o1, o2, i, c = out_idx
+    others = [d for d in (1, 2, 3) if d != f]
+    src = [b, 0, 0, 0, c]
+    for d, o in zip(others, (o1, o2)):
+        src[d] = o + (n * (shape[t] // n_chunks) if d == t else 0)
+    src[f] = i
+    return tuple(src)
+
+
+def pin_switch_k3_index_loops(switch):
+    rng = np.random.default_rng(11)
+    for shape in [(2, 2, 3, 4, 2), (1, 4, 2, 2, 3)]:
+        x = rng.integers(0, 60000, size=shape).astype(np.uint16)
+        for f, t in itertools.permutations((1, 2, 3), 2):
+            for n in [d for d in (1, 2, 4) if shape[t] % d == 0]:
+                y = switch(x, f, t, n)
+                assert y.size == x.size
+                for out_idx in itertools.product(*(range(e) for e in y.shape)):
+                    assert y[out_idx] == x[_k3_source(shape, f, t, n, out_idx)]
+
+
+def pin_switch_k3_unit_dim(switch):
+    """A K = 3 tensor with a unit sequence dimension switches as the K = 2 tensor."""
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((2, 4, 6, 3)).astype(np.float32)
+    for n in (1, 2, 3):
+        want = switch(x, 1, 2, n)                                   # [n, B, 6/n, 4, C]
+        got = switch(x[:, :, :, None, :], 1, 2, n)                  # [n, B, 6/n, 1, 4, C]
+        assert np.array_equal(got.reshape(want.shape), want)
+        got = switch(x[:, None], 2, 3, n)                           # unit dim in front
+        assert np.array_equal(got.reshape(want.shape), want)
+        got = switch(x[:, :, None], 1, 3, n)                        # unit dim between
+        assert np.array_equal(got.reshape(want.shape), want)
+    want = switch(x, 2, 1, 2)
+    assert np.array_equal(switch(x[:, :, :, None], 2, 1, 2).reshape(want.shape), want)
+
+
+def pin_switch_nrank_simulation_k3(switch, exchange_unpack):
+    """K = 3: N ranks hold the from-dim shards of X; after switch + all-to-all +
+    unpack rank n holds shard n of the to-dim of X with the from-dim next to C
+    (the layout of Eq. 7 for the from-dim)."""
+    rng = np.random.default_rng(13)
+    X = rng.standard_normal((2, 4, 2, 4, 3)).astype(np.float32)
+    for f, t in itertools.permutations((1, 2, 3), 2):
+        for N_ in (1, 2):
+            shards = np.split(X, N_, axis=f)
+            got = exchange_unpack([switch(s, f, t, N_) for s in shards])
+            G = np.moveaxis(X, f, -2)
+            want = np.split(G, N_, axis=t if t < f else t - 1)
+            for n in range(N_):
+                assert np.array_equal(got[n], want[n])
+
+
+def pin_split_gather(split, gather):
+    rng = np.random.default_rng(14)
+    for shape in [(2, 4, 6, 3), (1, 2, 4, 6, 2)]:
+        x = rng.integers(0, 60000, size=shape).astype(np.uint16)
+        for d in range(1, len(shape) - 1):
+            for N_ in [k for k in (1, 2, 3, 4) if shape[d] % k == 0]:
+                per = shape[d] // N_
+                parts = [split(x, d, N_, r) for r in range(N_)]
+                for r, part in enumerate(parts):
+                    idx = [slice(None)] * len(shape)
+                    idx[d] = slice(r * per, (r + 1) * per)
+                    assert np.array_equal(part, x[tuple(idx)])
+                assert np.array_equal(gather(parts, d), x)
+                # gather by explicit loops: element e of shard m lands at m*per + e on d
+                y = gather(parts, d)
+                for m in range(N_):
+                    for e in range(per):
+                        assert np.array_equal(np.take(y, m * per + e, axis=d),
+                                              np.take(parts[m], e, axis=d))
+
+
+def pin_switch_is_gather_then_split(switch, exchange_unpack, split, gather):
+    """The Switch's all-to-all moves what a Gather on the from-dim followed by a
+    Split on the to-dim would leave on each rank (primitive table), laid out with
+    the from-dim next to C."""
+    rng = np.random.default_rng(15)
+    X = rng.standard_normal((1, 4, 6, 2)).astype(np.float32)
+    N_ = 2
+    shards = [split(X, 1, N_, r) for r in range(N_)]
+    got = exchange_unpack([switch(s, 1, 2, N_) for s in shards])
+    for n in range(N_):
+        want = split(gather(shards, 1), 2, N_, n)                    # [B, T, S/N, C]
+        assert np.array_equal(got[n], np.moveaxis(want, 1, -2))
+
+
 # ----------------------------------------------------------------------------- attention
 def _brute_attention(q, k, v, scale):
     Lq, d = q.shape

@@ -20,7 +20,7 @@ BL = sys.modules["oracle.block"]
 def _impl():
     return types.SimpleNamespace(
         switch=SW.switch, unswitch=SW.unswitch, exchange_unpack=SW.exchange_unpack,
-        index_map=SW.switch_index_map, attention=AT.attention, spatial=AT.spatial_attention,
+        index_map=SW.switch_index_map, split=SW.split, gather=SW.gather, attention=AT.attention, spatial=AT.spatial_attention,
         temporal=AT.temporal_attention, strided=AT.temporal_attention_strided,
         layernorm=BL.layernorm, linear=BL.linear, gelu=BL.gelu, relu=BL.relu, st_block=BL.st_block,
         tiny_chain=BL.tiny_chain)
@@ -34,6 +34,11 @@ def _pins(i):
         lambda: P.pin_switch_b1_transpose(i.switch),
         lambda: P.pin_switch_bits_and_copy(i.switch),
         lambda: P.pin_switch_nrank_simulation(i.switch, i.exchange_unpack),
+        lambda: P.pin_switch_k3_index_loops(i.switch),
+        lambda: P.pin_switch_k3_unit_dim(i.switch),
+        lambda: P.pin_switch_nrank_simulation_k3(i.switch, i.exchange_unpack),
+        lambda: P.pin_split_gather(i.split, i.gather),
+        lambda: P.pin_switch_is_gather_then_split(i.switch, i.exchange_unpack, i.split, i.gather),
         lambda: P.pin_attention_brute(i.attention),
         lambda: P.pin_attention_l1_is_v(i.attention),
         lambda: P.pin_attention_zero_q_mean(i.attention),
@@ -104,6 +109,40 @@ def sw_no_transpose(x, f, t, n):
 def sw_off_by_one(x, f, t, n):
     y = _orig_switch(x, f, t, n)
     return np.roll(y, 1, axis=3) if f != t else y
+
+
+def sw_k3_others_reversed(x, f, t, n):
+    # K = 3: the two other sequence dims swapped inside each chunk
+    y = _orig_switch(x, f, t, n)
+    if x.ndim != 5 or f == t:
+        return y
+    return np.ascontiguousarray(np.swapaxes(y, 2, 3))
+
+
+def sw_k3_from_dim_outer(x, f, t, n):
+    # K = 3: the from-dim placed first instead of next to C
+    y = _orig_switch(x, f, t, n)
+    if x.ndim != 5 or f == t:
+        return y
+    return np.ascontiguousarray(np.moveaxis(y, -2, 2))
+
+
+_orig_split = SW.split
+_orig_gather = SW.gather
+
+
+def split_from_end(x, dim, n_chunks, rank):
+    return _orig_split(x, dim, n_chunks, n_chunks - 1 - rank)
+
+
+def gather_reversed(shards, dim):
+    return _orig_gather(list(shards)[::-1], dim)
+
+
+def exchange_outer_axis(packed_per_rank):
+    # the received chunks joined on the outermost sequence axis, not the from-dim
+    N = len(packed_per_rank)
+    return [np.concatenate([p[n] for p in packed_per_rank], axis=1) for n in range(N)]
 
 
 def att_no_scale(q, k, v, scale=None):
@@ -245,6 +284,11 @@ MUTANTS = {
     "switch: batch outside chunks": [(SW, "switch", sw_batch_outside), (BL, "switch", sw_batch_outside)],
     "switch: missing transpose": [(SW, "switch", sw_no_transpose), (BL, "switch", sw_no_transpose)],
     "switch: off-by-one index": [(SW, "switch", sw_off_by_one), (BL, "switch", sw_off_by_one)],
+    "switch K=3: other dims swapped": [(SW, "switch", sw_k3_others_reversed)],
+    "switch K=3: from-dim outermost": [(SW, "switch", sw_k3_from_dim_outer)],
+    "split: slices counted from the end": [(SW, "split", split_from_end)],
+    "gather: shards in reverse order": [(SW, "gather", gather_reversed)],
+    "exchange: joined on the outer axis": [(SW, "exchange_unpack", exchange_outer_axis)],
     "attention: no 1/sqrt(d)": [(AT, "attention", att_no_scale)],
     "attention: padded-width scale": [(AT, "attention", att_padded_scale)],
     "attention: softmax over queries": [(AT, "attention", att_softmax_over_queries)],

@@ -31,6 +31,27 @@ def test_switch_nrank_simulation():
     P.pin_switch_nrank_simulation(oracle.switch, oracle.exchange_unpack)
 
 
+def test_switch_k3_index_loops():
+    P.pin_switch_k3_index_loops(oracle.switch)
+
+
+def test_switch_k3_unit_dim():
+    P.pin_switch_k3_unit_dim(oracle.switch)
+
+
+def test_switch_nrank_simulation_k3():
+    P.pin_switch_nrank_simulation_k3(oracle.switch, oracle.exchange_unpack)
+
+
+def test_split_gather():
+    P.pin_split_gather(oracle.split, oracle.gather)
+
+
+def test_switch_is_gather_then_split():
+    P.pin_switch_is_gather_then_split(oracle.switch, oracle.exchange_unpack, oracle.split,
+                                      oracle.gather)
+
+
 def test_switch_rejects_bad_args():
     x = np.zeros((1, 4, 6, 2), np.float32)
     with pytest.raises(ValueError):
@@ -39,6 +60,14 @@ def test_switch_rejects_bad_args():
         oracle.switch(x[0], 1, 2, 1)       # not 4-D
     with pytest.raises(ValueError):
         oracle.switch(x, 0, 2, 1)
+    with pytest.raises(ValueError):
+        oracle.switch(np.zeros((1, 2, 2, 2, 2, 2)), 1, 2, 1)       # K = 4
+    with pytest.raises(ValueError):
+        oracle.switch(np.zeros((1, 2, 2, 2, 2)), 1, 4, 1)          # 4 is C for K = 3
+    with pytest.raises(ValueError):
+        oracle.split(x, 2, 4, 0)                                    # 6 % 4 != 0
+    with pytest.raises(ValueError):
+        oracle.split(x, 2, 2, 2)                                    # rank out of range
 
 
 @pytest.mark.parametrize("pin", [P.pin_attention_brute, P.pin_attention_l1_is_v,
