@@ -17,6 +17,10 @@ and, timed separately after the steps (not part of a step):
             holding one such shard's packed switch output (8 x 604 MB in and out)
   temporal_strided  the temporal workload read and written in the unswitched
             (B, T, S, C) layout through dsp_attn_strided
+  switch_k3 dsp_switch of the same shard seen as K = 3 sequence dims,
+            1 x 64 x 64 x 64 x 1152 (T x H x W), T -> H into 8 chunks
+  split     dsp_split of that shard along S into 8, one rank's slice
+  gather    dsp_gather of 8 shards 1 x 512 x 64 x 1152 along T (604 MB out)
 
 The headline value is the combined attention throughput
 (F_spatial + F_temporal) / (t_spatial + t_temporal) in TFLOP/s with
@@ -61,7 +65,7 @@ def parse():
                          "spatial kernel; used only while the kernel source is unchanged")
     ap.add_argument("--only", default=None,
                     choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange",
-                             "temporal_strided", "copy"],
+                             "temporal_strided", "switch_k3", "split", "gather", "copy"],
                     help="run a single part (for profiling); prints per-kernel times only. "
                          "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
                          "plain 604 MB copy used to calibrate traffic counters")
@@ -90,8 +94,8 @@ def main():
     ws, wsp, wtp, wbl = (W["switch_bf16_T64_S4096"], W["spatial_bf16_B2_T16_S4096"],
                          W["temporal_bf16_B2_S512_T128"], W["block_bf16_B1_T32_S1024"])
     wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block", "exchange",
-                                            "temporal_strided"}
-    if wanted & {"copy", "switch_inv", "exchange"}:
+                                            "temporal_strided", "switch_k3", "split", "gather"}
+    if wanted & {"copy", "switch_inv", "exchange", "switch_k3", "split", "gather"}:
         wanted.add("switch")
     if "temporal_strided" in wanted:
         wanted.add("temporal")
@@ -112,6 +116,18 @@ def main():
         t["ex_in"] = [t["y_sw"] + m for m in range(ws.n_chunks)]
         t["ex_out"] = [torch.empty((ws.B, ws.S // ws.n_chunks, ws.T * ws.n_chunks, ws.C),
                                    dtype=torch.bfloat16, device=dev) for _ in range(ws.n_chunks)]
+    if "switch_k3" in wanted:
+        t["x_k3"] = t["x_sw"].view(ws.B, ws.T, 64, ws.S // 64, ws.C)
+        t["y_k3"] = torch.empty((ws.n_chunks, ws.B, 64 // ws.n_chunks, ws.S // 64, ws.T, ws.C),
+                                dtype=torch.bfloat16, device=dev)
+    if "split" in wanted:
+        t["y_split"] = torch.empty((ws.B, ws.T, ws.S // ws.n_chunks, ws.C), dtype=torch.bfloat16,
+                                   device=dev)
+    if "gather" in wanted:
+        dsp.dsp_switch(t["x_sw"], 1, 2, ws.n_chunks, out=t["y_sw"])
+        t["g_in"] = [t["y_sw"][m] for m in range(ws.n_chunks)]        # [B, S/8, T, C] each
+        t["g_out"] = torch.empty((ws.B, ws.S // ws.n_chunks, ws.T * ws.n_chunks, ws.C),
+                                 dtype=torch.bfloat16, device=dev)
     if "spatial" in wanted:
         t["q_sp"], t["k_sp"], t["v_sp"] = (to_dev(a, "bf16") for a in synth.qkv_inputs(wsp, "BTSC"))
         t["o_sp"] = torch.empty_like(t["q_sp"])
@@ -145,6 +161,15 @@ def main():
         v = [a.permute(0, 2, 1, 3) for a in t["tq_tsc"]]
         dsp.dsp_attn_strided(*v, wtp.H, out=t["to_tsc"].permute(0, 2, 1, 3))
 
+    def run_switch_k3():
+        dsp.dsp_switch(t["x_k3"], 1, 2, ws.n_chunks, out=t["y_k3"])
+
+    def run_split():
+        dsp.dsp_split(t["x_sw"], 2, ws.n_chunks, 3, out=t["y_split"])
+
+    def run_gather():
+        dsp.dsp_gather(t["g_in"], 2, out=t["g_out"])
+
     def run_spatial():
         dsp.dsp_spatial_attn(t["q_sp"], t["k_sp"], t["v_sp"], wsp.H, out=t["o_sp"])
 
@@ -160,7 +185,8 @@ def main():
     parts = [("switch", run_switch), ("switch_inv", run_switch_inv), ("spatial", run_spatial),
              ("temporal", run_temporal), ("block", run_block)]
     # timed on its own after the steps: not a step of the single-GPU hot path
-    extras = [("exchange", run_exchange), ("temporal_strided", run_temporal_strided)]
+    extras = [("exchange", run_exchange), ("temporal_strided", run_temporal_strided),
+              ("switch_k3", run_switch_k3), ("split", run_split), ("gather", run_gather)]
     if args.only:
         every = dict(parts + extras)
         parts, extras = [(args.only, run_copy if args.only == "copy" else every[args.only])], []
@@ -217,6 +243,9 @@ def main():
     ex_gbps = ws.n_chunks * sw_bytes / (ms["exchange"] * 1e-3) / 1e9
     tps_gbps = tp_bytes_all / (ms["temporal_strided"] * 1e-3) / 1e9
     tp_gbps = tp_bytes / (ms["temporal"] * 1e-3) / 1e9
+    k3_gbps = sw_bytes / (ms["switch_k3"] * 1e-3) / 1e9
+    split_gbps = sw_bytes / ws.n_chunks / (ms["split"] * 1e-3) / 1e9
+    gather_gbps = sw_bytes / (ms["gather"] * 1e-3) / 1e9
 
     traffic = measured_traffic(args.traffic)
 
@@ -235,7 +264,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": "dsp_switch 1x64x4096x1152 bf16 -> 8 chunks and its inverse 1x4096x64x1152 -> 8 "
-                        "chunks; 8-rank exchange+unpack of such shards; spatial attn B2 T16 S4096 H16 D72; "
+                        "chunks; 8-rank exchange+unpack of such shards; the shard as 1x64x64x64x1152 "
+                        "switched T->H (K=3); split along S / gather along T of 8 shards; spatial attn B2 T16 S4096 H16 D72; "
                         "temporal attn B2 S512 T128 H16 D72; ST block B1 T32 S1024 C1152 H16 F4608",
             "attn_frac_mfma_peak": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
             "switch_GBps": round(sw_gbps, 1),
@@ -245,6 +275,9 @@ def main():
             "exchange_unpack_GBps": round(ex_gbps, 1),
             "exchange_unpack_frac_hbm_peak": round(ex_gbps / HBM_PEAK_GBPS, 4),
             "temporal_unswitched_layout_GBps": round(tps_gbps, 1),
+            "switch_k3_GBps": round(k3_gbps, 1),
+            "split_GBps": round(split_gbps, 1),
+            "gather_GBps": round(gather_gbps, 1),
             "spatial_TFLOPs": round(sp_tflops, 2),
             "temporal_TFLOPs": round(tp_tflops, 2),
             "temporal_GBps": round(tp_gbps, 1),

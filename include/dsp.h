@@ -62,8 +62,9 @@ int dsp_version(void);
  * dsp_switch -- one GPU's share of DynamicSwitch(X, i, j)
  * (primitive table, row s_i -> s_j; Eq. 10; system overview figure).
  *
- * x:      [B, D1, D2, C] (ndim must be 4: two sequence dimensions), the local
- *         shard, currently sharded on `from_dim`.
+ * x:      [B, D1, D2, C] (ndim 4: K = 2 sequence dimensions) or
+ *         [B, D1, D2, D3, C] (ndim 5: K = 3, the multi-dimensional form of
+ *         Eq. 7), the local shard, currently sharded on `from_dim`.
  * y:      output, same number of elements as x, written as `n_chunks`
  *         contiguous per-destination chunks.  With from_dim=1, to_dim=2:
  *             y[n][b][j'][i][c] = x[b][i][n*D2/n_chunks + j'][c]
@@ -74,10 +75,14 @@ int dsp_version(void);
  *         For (B,T,S,C) with T sharded, from=1 (T), to=2 (S) and n_chunks=1
  *         this is the permute to (B,S,T,C).  Chunk n is what rank n receives
  *         in the all-to-all; the exchange itself is not part of this call.
+ *         For K = 3 the chunk keeps the other two sequence dimensions in
+ *         their order (the to-dim cut to D_to/n_chunks) and puts the from-dim
+ *         next to C, e.g. from=1, to=3:
+ *             y[n][b][j][k'][i][c] = x[b][i][j][n*D3/n_chunks + k'][c].
  * from_dim == to_dim is the "no primitive" row of the table: y = copy of x.
  * Errors: DSP_ERR_NULL (shape NULL, or x / y NULL for a non-empty tensor;
- *   an empty tensor may come with NULL pointers), DSP_ERR_DIM (ndim != 4 or a dim
- *   not in {1,2}), DSP_ERR_SHAPE (a size < 0, n_chunks < 1, the to-dim not
+ *   an empty tensor may come with NULL pointers), DSP_ERR_DIM (ndim not 4 or 5,
+ *   or a dim not in 1..K), DSP_ERR_SHAPE (a size < 0, n_chunks < 1, the to-dim not
  *   divisible by n_chunks, or more than 2^31 rows / 16-byte vectors),
  *   DSP_ERR_DTYPE, DSP_ERR_ARG (x and y overlap).  A tensor with a zero size
  *   is accepted and launches nothing.
@@ -88,9 +93,44 @@ int dsp_switch(const void* x, void* y, const int64_t* shape, int ndim, int from_
 
 /* Same as dsp_switch with an explicit kernel choice: 0 = automatic,
  * 1 = direct 128-bit row copy (requires 16-byte aligned pointers and rows),
- * 2 = LDS-staged tile transpose.  Any other value -> DSP_ERR_ARG. */
+ * 2 = LDS-staged tile transpose.  Any other value -> DSP_ERR_ARG.  K = 3
+ * tensors (ndim 5) have one kernel: only variant 0 is accepted. */
 int dsp_switch_variant(const void* x, void* y, const int64_t* shape, int ndim, int from_dim,
                        int to_dim, int n_chunks, int dtype, int variant, void* stream);
+
+/* ------------------------------------------------------------------------
+ * dsp_split -- the Split row of the primitive table (s^ -> s_i): a tensor
+ * replicated on every rank becomes sharded on sequence dimension `dim`, with
+ * no communication; rank `rank` keeps its slice.
+ *
+ * x:      [B, S_1, .., S_K, C] (ndim = K + 2, K = 2 or 3), replicated.
+ * y:      [B, .., S_dim / n_chunks, .., C], dense:
+ *             y[b][..][i'][..][c] = x[b][..][rank * S_dim/n_chunks + i'][..][c].
+ * Errors: DSP_ERR_NULL, DSP_ERR_DIM (ndim not 4 or 5, dim not in 1..K),
+ *   DSP_ERR_SHAPE (a negative size, n_chunks < 1, S_dim not divisible),
+ *   DSP_ERR_DTYPE, DSP_ERR_ARG (rank not in [0, n_chunks), x and y overlap).
+ * A bit copy; an empty result launches nothing.
+ * ------------------------------------------------------------------------ */
+int dsp_split(const void* x, void* y, const int64_t* shape, int ndim, int dim, int n_chunks,
+              int rank, int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * dsp_gather -- the Gather row of the primitive table (s_i -> s^, an
+ * all-gather): the receiver's concatenation of every rank's shard, run on
+ * one GPU with one buffer per rank.
+ *
+ * shards:      host array of n_shards device pointers, each a dense
+ *              [B, S_1, .., S_K, C] shard with the size shard_shape
+ *              (ndim = K + 2, K = 2 or 3); they may alias each other.
+ * y:           [B, .., n_shards * S_dim, .., C], dense:
+ *                  y[b][..][m * S_dim + i][..][c] = shards[m][b][..][i][..][c].
+ * n_shards:    1..64.
+ * Errors: DSP_ERR_NULL, DSP_ERR_DIM, DSP_ERR_SHAPE (a negative size, n_shards
+ *   out of range), DSP_ERR_DTYPE, DSP_ERR_ARG (y overlaps a shard).
+ * A bit copy; an empty result launches nothing.
+ * ------------------------------------------------------------------------ */
+int dsp_gather(const void* const* shards, void* y, const int64_t* shard_shape, int ndim, int dim,
+               int n_shards, int dtype, void* stream);
 
 /* ------------------------------------------------------------------------
  * dsp_exchange_unpack -- the exchange of DynamicSwitch among N ranks (the
@@ -99,7 +139,9 @@ int dsp_switch_variant(const void* x, void* y, const int64_t* shape, int ndim, i
  *
  * packed: host array of N device pointers; packed[m] is rank m's dsp_switch
  *         output, shape [N][B][P][F][C] (P = D_to / N, F = rank m's length of
- *         the from-dimension).  Read only; the N buffers may alias each other.
+ *         the from-dimension; for K = 3, P is the product of the two other
+ *         sequence dimensions of a chunk).  Read only; the N buffers may alias
+ *         each other.
  * out:    host array of N device pointers; out[n] receives rank n's result,
  *         shape [B][P][N*F][C]:
  *             out[n][b][p][m*F + f][c] = packed[m][n][b][p][f][c]

@@ -9,8 +9,8 @@ status.  There is no fallback: if the library is missing, importing the
 binding's functions raises.
 
 Entry points (see ``include/dsp.h`` for the exact contracts):
-``dsp_switch``, ``dsp_exchange_unpack``, ``dsp_spatial_attn``, ``dsp_temporal_attn``,
-``dsp_attn_strided``,
+``dsp_switch``, ``dsp_exchange_unpack``, ``dsp_split``, ``dsp_gather``,
+``dsp_spatial_attn``, ``dsp_temporal_attn``, ``dsp_attn_strided``,
 ``dsp_layernorm``, ``dsp_linear``, ``dsp_st_block_forward``.
 """
 from __future__ import annotations
@@ -53,6 +53,8 @@ _SIGNATURES = {
     "dsp_switch": (_I, [_P, _P, _c.POINTER(_I64), _I, _I, _I, _I, _I, _P]),
     "dsp_switch_variant": (_I, [_P, _P, _c.POINTER(_I64), _I, _I, _I, _I, _I, _I, _P]),
     "dsp_exchange_unpack": (_I, [_c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_I64), _I, _P]),
+    "dsp_split": (_I, [_P, _P, _c.POINTER(_I64), _I, _I, _I, _I, _I, _P]),
+    "dsp_gather": (_I, [_c.POINTER(_P), _P, _c.POINTER(_I64), _I, _I, _I, _I, _P]),
     "dsp_spatial_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
     "dsp_temporal_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
     "dsp_attn_strided": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _c.POINTER(_I64),
@@ -125,26 +127,78 @@ def _require_device(*ts):
 
 def dsp_switch(x, from_dim: int, to_dim: int, n_chunks: int, out=None, variant: int = 0,
                stream=None):
-    """Permute + pack of a [B, D1, D2, C] shard (see dsp.h).  Returns ``out`` as a
-    tensor of shape [n_chunks, B, D_to/n_chunks, D_from, C] (or x's shape when
+    """Permute + pack of a [B, S_1, .., S_K, C] shard, K = 2 or 3 (see dsp.h).
+    Returns ``out`` as a tensor of shape [n_chunks, B, (the other sequence dims,
+    the to-dim cut to D_to/n_chunks), D_from, C] (or x's shape when
     from_dim == to_dim)."""
     torch = _torch()
     _require_device(x)
-    if x.dim() != 4:
-        raise ValueError("x must be [B, D1, D2, C]")
+    if x.dim() not in (4, 5):
+        raise ValueError("x must be [B, S_1, .., S_K, C] with K = 2 or 3")
     x = x.contiguous()
-    B, D1, D2, C = x.shape
-    if from_dim == to_dim:
+    nd = x.dim()
+    dims = list(x.shape)
+    if from_dim == to_dim or not (1 <= from_dim <= nd - 2 and 1 <= to_dim <= nd - 2):
         oshape = tuple(x.shape)
     else:
-        d_to, d_from = (D2, D1) if to_dim == 2 else (D1, D2)
-        oshape = (n_chunks, B, d_to // max(n_chunks, 1), d_from, C)
+        others = [k for k in range(1, nd - 1) if k != from_dim]
+        mid = [dims[k] // max(n_chunks, 1) if k == to_dim else dims[k] for k in others]
+        oshape = (n_chunks, dims[0], *mid, dims[from_dim], dims[-1])
     if out is None:
         out = torch.empty(oshape, dtype=x.dtype, device=x.device)
-    shape = (ctypes.c_int64 * 4)(B, D1, D2, C)
-    st = lib().dsp_switch_variant(_ptr(x), _ptr(out), shape, 4, from_dim, to_dim, n_chunks,
+    shape = (ctypes.c_int64 * nd)(*dims)
+    st = lib().dsp_switch_variant(_ptr(x), _ptr(out), shape, nd, from_dim, to_dim, n_chunks,
                                   _dtype_code(x), variant, _stream(stream))
     _check(st, "dsp_switch")
+    return out
+
+
+def dsp_split(x, dim: int, n_chunks: int, rank: int, out=None, stream=None):
+    """Split (primitive table, s^ -> s_i): rank ``rank``'s slice of the replicated
+    tensor x [B, S_1, .., S_K, C] along sequence dimension ``dim`` (see dsp.h)."""
+    torch = _torch()
+    _require_device(x, out)
+    if x.dim() not in (4, 5):
+        raise ValueError("x must be [B, S_1, .., S_K, C] with K = 2 or 3")
+    x = x.contiguous()
+    dims = list(x.shape)
+    if out is None:
+        oshape = list(dims)
+        if 1 <= dim < x.dim() - 1 and n_chunks >= 1:
+            oshape[dim] //= n_chunks
+        out = torch.empty(oshape, dtype=x.dtype, device=x.device)
+    shape = (ctypes.c_int64 * x.dim())(*dims)
+    st = lib().dsp_split(_ptr(x), _ptr(out), shape, x.dim(), dim, n_chunks, rank, _dtype_code(x),
+                         _stream(stream))
+    _check(st, "dsp_split")
+    return out
+
+
+def dsp_gather(shards, dim: int, out=None, stream=None):
+    """Gather (primitive table, s_i -> s^): the concatenation along sequence
+    dimension ``dim`` of N equal shards [B, S_1, .., S_K, C], in rank order; the
+    receiving side of the all-gather, with every rank's shard on one GPU."""
+    torch = _torch()
+    shards = [s.contiguous() for s in shards]
+    _require_device(*shards, out)
+    if not shards:
+        raise ValueError("at least one shard")
+    x0 = shards[0]
+    if any(s.shape != x0.shape or s.dtype != x0.dtype for s in shards):
+        raise ValueError("shards must share shape and dtype")
+    if x0.dim() not in (4, 5):
+        raise ValueError("shards must be [B, S_1, .., S_K, C] with K = 2 or 3")
+    dims = list(x0.shape)
+    if out is None:
+        oshape = list(dims)
+        if 1 <= dim < x0.dim() - 1:
+            oshape[dim] *= len(shards)
+        out = torch.empty(oshape, dtype=x0.dtype, device=x0.device)
+    ptrs = (ctypes.c_void_p * len(shards))(*[_ptr(s) for s in shards])
+    shape = (ctypes.c_int64 * x0.dim())(*dims)
+    st = lib().dsp_gather(ptrs, _ptr(out), shape, x0.dim(), dim, len(shards), _dtype_code(x0),
+                          _stream(stream))
+    _check(st, "dsp_gather")
     return out
 
 

@@ -32,13 +32,78 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
   return true;
 }
 
+// Sequence tensors [B, S_1, .., S_K, C] with K = 2 or 3: checks ndim and the
+// sizes, and returns the element count (via *elems) and the row strides of
+// dims 0..K (row = C elements).
+int seq_shape(const int64_t* shape, int ndim, int64_t* elems, int64_t* row_st) {
+  if (!shape) return DSP_ERR_NULL;
+  if (ndim != 4 && ndim != 5) return DSP_ERR_DIM;
+  for (int k = 0; k < ndim; ++k)
+    if (shape[k] < 0) return DSP_ERR_SHAPE;
+  const int K = ndim - 2;
+  int64_t rows = 1;
+  row_st[K] = 1;
+  for (int k = K; k >= 0; --k) {
+    if (!mul_ok(rows, shape[k], &rows)) return DSP_ERR_SHAPE;
+    if (k > 0) row_st[k - 1] = rows;
+  }
+  if (!mul_ok(rows, shape[K + 1], elems)) return DSP_ERR_SHAPE;
+  return DSP_OK;
+}
+
+// Fills d with dense destination strides for its sizes.
+void dense_dst(RowCopyDesc* d) {
+  d->dst_stride[d->nd - 1] = 1;
+  for (int i = d->nd - 2; i >= 0; --i) d->dst_stride[i] = d->dst_stride[i + 1] * d->size[i + 1];
+}
+
+// One GPU's Switch for K = 3 as a row copy: output rows enumerated
+// (n, b, the other sequence dims in order with the to-dim sliced, from-dim).
+int switch_k3(const void* x, void* y, const int64_t* shape, const int64_t* row_st, int from, int to,
+              int64_t n_chunks, int64_t es, hipStream_t s) {
+  const int K = 3;
+  RowCopyDesc d = {};
+  if (from == to) {
+    d.nd = 1;
+    d.size[0] = row_st[0] * shape[0];
+    d.src_stride[0] = 1;
+  } else {
+    const int64_t per = shape[to] / n_chunks;
+    d.size[d.nd] = n_chunks;  d.src_stride[d.nd++] = per * row_st[to];
+    d.size[d.nd] = shape[0];  d.src_stride[d.nd++] = row_st[0];
+    for (int k = 1; k <= K; ++k) {
+      if (k == from) continue;
+      d.size[d.nd] = k == to ? per : shape[k];
+      d.src_stride[d.nd++] = row_st[k];
+    }
+    d.size[d.nd] = shape[from];
+    d.src_stride[d.nd++] = row_st[from];
+  }
+  dense_dst(&d);
+  d.row_bytes = shape[K + 1] * es;
+  return launch_rowcopy(&x, &y, 1, d, s);
+}
+
 int switch_impl(const void* x, void* y, const int64_t* shape, int ndim, int from_dim, int to_dim,
                 int n_chunks, int dtype, int variant, void* stream) {
   if (!shape) return DSP_ERR_NULL;
-  if (ndim != 4) return DSP_ERR_DIM;
-  if (from_dim < 1 || from_dim > 2 || to_dim < 1 || to_dim > 2) return DSP_ERR_DIM;
+  if (ndim != 4 && ndim != 5) return DSP_ERR_DIM;
+  if (from_dim < 1 || from_dim > ndim - 2 || to_dim < 1 || to_dim > ndim - 2) return DSP_ERR_DIM;
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
-  if (variant < 0 || variant > 2) return DSP_ERR_ARG;
+  if (variant < 0 || variant > 2 || (ndim == 5 && variant != 0)) return DSP_ERR_ARG;
+  if (ndim == 5) {
+    int64_t elems, row_st[4];
+    int st = seq_shape(shape, ndim, &elems, row_st);
+    if (st != DSP_OK) return st;
+    if (n_chunks < 1 || (from_dim != to_dim && shape[to_dim] % n_chunks)) return DSP_ERR_SHAPE;
+    if (elems > INT64_MAX / 4) return DSP_ERR_SHAPE;
+    const int64_t bytes = elems * elem_size(dtype);
+    if (bytes == 0) return DSP_OK;
+    if (!x || !y) return DSP_ERR_NULL;
+    if (overlap(x, (size_t)bytes, y, (size_t)bytes)) return DSP_ERR_ARG;
+    return switch_k3(x, y, shape, row_st, from_dim, to_dim, n_chunks, elem_size(dtype),
+                     as_stream(stream));
+  }
   const int64_t B = shape[0], D1 = shape[1], D2 = shape[2], C = shape[3];
   if (B < 0 || D1 < 0 || D2 < 0 || C < 0 || n_chunks < 1) return DSP_ERR_SHAPE;
   const int64_t d_to = to_dim == 2 ? D2 : D1;
@@ -249,6 +314,70 @@ int dsp_exchange_unpack(const void* const* packed, void* const* out, const int64
     }
   }
   return launch_exchange_unpack(packed, out, N, B, P, run_bytes, static_cast<hipStream_t>(stream));
+}
+
+int dsp_split(const void* x, void* y, const int64_t* shape, int ndim, int dim, int n_chunks,
+              int rank, int dtype, void* stream) {
+  int64_t elems, row_st[4];
+  if (!shape) return DSP_ERR_NULL;
+  int st = seq_shape(shape, ndim, &elems, row_st);
+  if (st != DSP_OK) return st;
+  if (dim < 1 || dim > ndim - 2) return DSP_ERR_DIM;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (n_chunks < 1 || shape[dim] % n_chunks) return DSP_ERR_SHAPE;
+  if (rank < 0 || rank >= n_chunks) return DSP_ERR_ARG;
+  if (elems > INT64_MAX / 4) return DSP_ERR_SHAPE;
+  const int64_t es = elem_size(dtype), in_bytes = elems * es, out_bytes = in_bytes / n_chunks;
+  if (out_bytes == 0) return DSP_OK;
+  if (!x || !y) return DSP_ERR_NULL;
+  if (overlap(x, (size_t)in_bytes, y, (size_t)out_bytes)) return DSP_ERR_ARG;
+  const int K = ndim - 2;
+  const int64_t per = shape[dim] / n_chunks;
+  RowCopyDesc d = {};
+  for (int k = 0; k <= K; ++k) {
+    d.size[d.nd] = k == dim ? per : shape[k];
+    d.src_stride[d.nd++] = row_st[k];
+  }
+  dense_dst(&d);
+  d.row_bytes = shape[K + 1] * es;
+  const void* src = static_cast<const char*>(x) + rank * per * row_st[dim] * d.row_bytes;
+  return launch_rowcopy(&src, &y, 1, d, as_stream(stream));
+}
+
+int dsp_gather(const void* const* shards, void* y, const int64_t* shard_shape, int ndim, int dim,
+               int n_shards, int dtype, void* stream) {
+  int64_t elems, row_st[4];
+  if (!shard_shape) return DSP_ERR_NULL;
+  int st = seq_shape(shard_shape, ndim, &elems, row_st);
+  if (st != DSP_OK) return st;
+  if (dim < 1 || dim > ndim - 2) return DSP_ERR_DIM;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (n_shards < 1 || n_shards > kMaxCopyPairs) return DSP_ERR_SHAPE;
+  int64_t out_elems;
+  if (!mul_ok(elems, n_shards, &out_elems) || out_elems > INT64_MAX / 4) return DSP_ERR_SHAPE;
+  const int64_t es = elem_size(dtype), shard_bytes = elems * es, out_bytes = out_elems * es;
+  if (out_bytes == 0) return DSP_OK;
+  if (!shards || !y) return DSP_ERR_NULL;
+  for (int m = 0; m < n_shards; ++m) {
+    if (!shards[m]) return DSP_ERR_NULL;
+    if (overlap(shards[m], (size_t)shard_bytes, y, (size_t)out_bytes)) return DSP_ERR_ARG;
+  }
+  // destination row strides: the shard's with dim grown n_shards times
+  const int K = ndim - 2;
+  int64_t out_st[4];
+  out_st[K] = 1;
+  for (int k = K - 1; k >= 0; --k) out_st[k] = out_st[k + 1] * shard_shape[k + 1] * (k + 1 == dim ? n_shards : 1);
+  RowCopyDesc d = {};
+  for (int k = 0; k <= K; ++k) {
+    d.size[d.nd] = shard_shape[k];
+    d.src_stride[d.nd] = row_st[k];
+    d.dst_stride[d.nd++] = out_st[k];
+  }
+  d.row_bytes = shard_shape[K + 1] * es;
+  void* dst[kMaxCopyPairs];
+  for (int m = 0; m < n_shards; ++m)
+    dst[m] = static_cast<char*>(y) + m * shard_shape[dim] * out_st[dim] * d.row_bytes;
+  return launch_rowcopy(shards, dst, n_shards, d, as_stream(stream));
 }
 
 int dsp_spatial_attn(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t T,

@@ -14,6 +14,20 @@ namespace dsp {
 constexpr int kMaxExchangeRanks = 64;
 int launch_exchange_unpack(const void* const* packed, void* const* out, int64_t N, int64_t B,
                            int64_t P, int64_t run_bytes, hipStream_t s);
+// Strided row copy (rowcopy.hip): rows of row_bytes bytes; the row at
+// multi-index (i_0, .., i_{nd-1}) moves from row sum(i_d * src_stride[d]) of
+// src[p] to row sum(i_d * dst_stride[d]) of dst[p], for each pair p.
+constexpr int kMaxCopyDims = 6;
+constexpr int kMaxCopyPairs = 64;
+struct RowCopyDesc {
+  int nd;
+  int64_t size[kMaxCopyDims];
+  int64_t src_stride[kMaxCopyDims];
+  int64_t dst_stride[kMaxCopyDims];
+  int64_t row_bytes;
+};
+int launch_rowcopy(const void* const* src, void* const* dst, int n_pairs, const RowCopyDesc& desc,
+                   hipStream_t s);
 int launch_switch_rows(const void* x, void* y, int64_t B, int64_t D1, int64_t D2, int64_t row_bytes,
                        int from_dim, int to_dim, int64_t n_chunks, hipStream_t s);
 int launch_switch_tiles(const void* x, void* y, int64_t B, int64_t D1, int64_t D2, int64_t C,

@@ -83,6 +83,48 @@ def test_switch_validation(lib):
     assert sw(FAKE, FAKE2, _shape(1, 4, 6, 0), 4, 1, 2, 2, 1) == dsp.DSP_OK
 
 
+def test_switch_k3_split_gather_validation(lib):
+    sw = lambda x, y, shape, ndim, f, t, n, dt, var=0: lib.dsp_switch_variant(
+        x, y, shape, ndim, f, t, n, dt, var, None)
+    s5 = _shape(1, 4, 2, 6, 8)
+    assert sw(FAKE, FAKE2, s5, 5, 1, 4, 2, 1) == dsp.DSP_ERR_DIM        # 4 is C when K = 3
+    assert sw(FAKE, FAKE2, _shape(1, 2, 2, 2, 2, 2), 6, 1, 2, 1, 1) == dsp.DSP_ERR_DIM
+    assert sw(FAKE, FAKE2, s5, 5, 1, 3, 4, 1) == dsp.DSP_ERR_SHAPE      # 6 % 4
+    assert sw(FAKE, FAKE2, s5, 5, 1, 3, 2, 1, 1) == dsp.DSP_ERR_ARG     # one kernel for K = 3
+    assert sw(FAKE, FAKE + 16, s5, 5, 1, 3, 2, 1) == dsp.DSP_ERR_ARG    # overlapping buffers
+    assert sw(None, FAKE2, s5, 5, 1, 3, 2, 1) == dsp.DSP_ERR_NULL
+    assert sw(FAKE, FAKE2, _shape(1, 4, 0, 6, 8), 5, 1, 3, 2, 1) == dsp.DSP_OK
+    split = lambda x=FAKE, y=FAKE2, s=s5, nd=5, dim=3, n=2, r=0, dt=1: lib.dsp_split(
+        x, y, s, nd, dim, n, r, dt, None)
+    assert split(x=None) == dsp.DSP_ERR_NULL
+    assert split(s=None) == dsp.DSP_ERR_NULL
+    assert split(nd=3) == dsp.DSP_ERR_DIM
+    assert split(dim=4) == dsp.DSP_ERR_DIM
+    assert split(dim=0) == dsp.DSP_ERR_DIM
+    assert split(n=4) == dsp.DSP_ERR_SHAPE                 # 6 % 4
+    assert split(n=0) == dsp.DSP_ERR_SHAPE
+    assert split(r=2) == dsp.DSP_ERR_ARG
+    assert split(r=-1) == dsp.DSP_ERR_ARG
+    assert split(dt=5) == dsp.DSP_ERR_DTYPE
+    assert split(y=FAKE + 16) == dsp.DSP_ERR_ARG           # overlaps x
+    assert split(s=_shape(0, 4, 2, 6, 8)) == dsp.DSP_OK
+    P = ctypes.c_void_p
+    def gather(ptrs=(FAKE, FAKE + 0x1000), y=FAKE2, s=s5, nd=5, dim=1, n=None, dt=1):
+        arr = (P * len(ptrs))(*ptrs) if ptrs is not None else None
+        return lib.dsp_gather(arr, y, s, nd, dim, len(ptrs or ()) if n is None else n, dt, None)
+    assert gather(ptrs=None, n=2) == dsp.DSP_ERR_NULL
+    assert gather(ptrs=(FAKE, None)) == dsp.DSP_ERR_NULL
+    assert gather(y=None) == dsp.DSP_ERR_NULL
+    assert gather(s=None) == dsp.DSP_ERR_NULL
+    assert gather(dim=4) == dsp.DSP_ERR_DIM
+    assert gather(nd=6) == dsp.DSP_ERR_DIM
+    assert gather(n=0) == dsp.DSP_ERR_SHAPE
+    assert gather(ptrs=(FAKE,) * 65) == dsp.DSP_ERR_SHAPE
+    assert gather(dt=3) == dsp.DSP_ERR_DTYPE
+    assert gather(y=FAKE + 0x1000 + 64) == dsp.DSP_ERR_ARG  # y overlaps a shard
+    assert gather(s=_shape(1, 4, 2, 0, 8)) == dsp.DSP_OK
+
+
 def test_exchange_validation(lib):
     P = ctypes.c_void_p
     def call(srcs, dsts, shape, dt=1):
