@@ -18,6 +18,8 @@ float64 NumPy (library matmul and erf as the only primitives):
   (Eq. 1-2) along one sequence dimension of a multi-dimensional sequence
   (Eq. 7-8): ``spatial_attention`` over S within each frame and
   ``temporal_attention`` over T at each location.
+* ``attention_bwd`` / ``attention_lse`` -- the backward of attention (the
+  chain rule through the softmax) and the row logsumexp it uses.
 * ``layernorm``, ``linear``, ``gelu`` and the composites ``st_block`` (the
   full spatial-temporal block) and ``tiny_chain``.
 
@@ -28,10 +30,13 @@ of each module for what pins it.
 from .switch import switch, unswitch, exchange_unpack, switch_index_map, split, gather
 from .attention import attention, attention_rows, spatial_attention, temporal_attention, \
     temporal_attention_strided
+from .backward import attention_bwd, attention_bwd_units, attention_lse, attention_lse_units, \
+    attention_delta_units
 from .block import layernorm, linear, gelu, relu, st_block, tiny_chain, BLOCK_NO_MLP_LN, BLOCK_POST_LN, \
     BLOCK_RELU
 
 __all__ = ["switch", "unswitch", "exchange_unpack", "switch_index_map", "split", "gather", "attention",
            "attention_rows", "spatial_attention", "temporal_attention",
            "temporal_attention_strided", "layernorm", "linear", "gelu", "st_block", "tiny_chain",
-           "BLOCK_NO_MLP_LN", "BLOCK_POST_LN", "BLOCK_RELU", "relu"]
+           "BLOCK_NO_MLP_LN", "BLOCK_POST_LN", "BLOCK_RELU", "relu", "attention_bwd",
+           "attention_bwd_units", "attention_lse", "attention_lse_units", "attention_delta_units"]

@@ -300,6 +300,82 @@ def pin_spatial_temporal_units(spatial, temporal, temporal_strided, switch):
         assert np.allclose(ot[b, s, :, cs], want, rtol=1e-12, atol=1e-13)
 
 
+# ----------------------------------------------------------------------------- attention backward
+def _fd_grad(f, x, h=1e-6):
+    """Central finite differences of the scalar f at x (float64)."""
+    g = np.zeros_like(x)
+    for idx in np.ndindex(x.shape):
+        xp = x.copy(); xp[idx] += h
+        xm = x.copy(); xm[idx] -= h
+        g[idx] = (f(xp) - f(xm)) / (2 * h)
+    return g
+
+
+def pin_attention_bwd_fd(attention, attention_bwd):
+    """<dO, attention(q, k, v)> differentiated numerically in each input."""
+    rng = np.random.default_rng(30)
+    for U, Lq, L, d, scale in [(2, 3, 4, 4, None), (1, 5, 5, 3, 0.7)]:
+        q, k, v, do = (rng.standard_normal(sh) for sh in [(U, Lq, d), (U, L, d), (U, L, d), (U, Lq, d)])
+        dq, dk, dv = attention_bwd(q, k, v, do, scale)
+        loss = lambda qq, kk, vv: float((do * attention(qq, kk, vv, scale)).sum())
+        assert np.allclose(dq, _fd_grad(lambda a: loss(a, k, v), q), atol=1e-8, rtol=1e-7)
+        assert np.allclose(dk, _fd_grad(lambda a: loss(q, a, v), k), atol=1e-8, rtol=1e-7)
+        assert np.allclose(dv, _fd_grad(lambda a: loss(q, k, a), v), atol=1e-8, rtol=1e-7)
+
+
+def pin_attention_bwd_invariants(attention_bwd):
+    rng = np.random.default_rng(31)
+    q, k, v, do = (rng.standard_normal((3, 6, 5)) for _ in range(4))
+    _, dk, _ = attention_bwd(q, k, v, do)
+    # softmax is invariant to a common shift of a row's scores, so the key
+    # gradients of a unit sum to zero
+    assert np.allclose(dk.sum(axis=-2), 0.0, atol=1e-12)
+    # one key: the output is v whatever q and k are
+    dq, dk, dv = attention_bwd(q[:, :, :], k[:, :1], v[:, :1], do)
+    assert np.allclose(dq, 0.0, atol=1e-14) and np.allclose(dk, 0.0, atol=1e-14)
+    assert np.allclose(dv[:, 0], do.sum(axis=1))
+    # identical keys: P is uniform, so dq = 0 and dv = the column sums of dO / L
+    kk = np.repeat(k[:, :1], 6, axis=1)
+    dq, _, dv = attention_bwd(q, kk, v, do)
+    assert np.allclose(dq, 0.0, atol=1e-12)
+    assert np.allclose(dv, np.repeat(do.sum(axis=1, keepdims=True) / 6, 6, axis=1))
+
+
+def pin_attention_lse(attention_lse):
+    from scipy.special import logsumexp
+    rng = np.random.default_rng(32)
+    q, k = rng.standard_normal((2, 4, 8)) * 3, rng.standard_normal((2, 7, 8)) * 3
+    z = np.einsum("uid,ujd->uij", q, k) / math.sqrt(8)
+    lse = attention_lse(q, k)
+    assert np.allclose(lse, logsumexp(z, axis=-1))
+    assert (lse >= z.max(axis=-1)).all()
+    assert np.allclose(np.exp(z - lse[..., None]).sum(axis=-1), 1.0)
+    assert np.allclose(attention_lse(q, k, 0.25), logsumexp(z * math.sqrt(8) * 0.25, axis=-1))
+
+
+def pin_attention_bwd_units(attention_bwd, attention_bwd_units, attention_lse_units,
+                            attention_lse, attention_delta_units, attention):
+    """The (B, X, L, C) wrappers run each (b, x, head) unit on its own columns."""
+    rng = np.random.default_rng(33)
+    B, X, L, H, d = 2, 3, 5, 2, 4
+    q, k, v, do = (rng.standard_normal((B, X, L, H * d)) for _ in range(4))
+    dq, dk, dv = attention_bwd_units(q, k, v, do, H)
+    lse = attention_lse_units(q, k, H)
+    o = np.zeros_like(q)
+    for b, x, h in itertools.product(range(B), range(X), range(H)):
+        cs = slice(h * d, (h + 1) * d)
+        g = attention_bwd(q[b, x, :, cs], k[b, x, :, cs], v[b, x, :, cs], do[b, x, :, cs])
+        assert np.allclose(dq[b, x, :, cs], g[0]) and np.allclose(dk[b, x, :, cs], g[1])
+        assert np.allclose(dv[b, x, :, cs], g[2])
+        u = (b * X + x) * H + h
+        assert np.allclose(lse[u], attention_lse(q[b, x, :, cs], k[b, x, :, cs]))
+        o[b, x, :, cs] = attention(q[b, x, :, cs], k[b, x, :, cs], v[b, x, :, cs])
+    delta = attention_delta_units(o, do, H)
+    for b, x, h in itertools.product(range(B), range(X), range(H)):
+        cs = slice(h * d, (h + 1) * d)
+        assert np.allclose(delta[(b * X + x) * H + h], (o[b, x, :, cs] * do[b, x, :, cs]).sum(-1))
+
+
 # ----------------------------------------------------------------------------- LN / linear / GELU
 def pin_layernorm(layernorm):
     x = np.array([[1.0, 2.0, 3.0, 4.0]])

@@ -15,6 +15,7 @@ from tests import oracle_pins as P
 SW = sys.modules["oracle.switch"]
 AT = sys.modules["oracle.attention"]
 BL = sys.modules["oracle.block"]
+BW = sys.modules["oracle.backward"]
 
 
 def _impl():
@@ -23,7 +24,9 @@ def _impl():
         index_map=SW.switch_index_map, split=SW.split, gather=SW.gather, attention=AT.attention, spatial=AT.spatial_attention,
         temporal=AT.temporal_attention, strided=AT.temporal_attention_strided,
         layernorm=BL.layernorm, linear=BL.linear, gelu=BL.gelu, relu=BL.relu, st_block=BL.st_block,
-        tiny_chain=BL.tiny_chain)
+        tiny_chain=BL.tiny_chain, attention_bwd=BW.attention_bwd,
+        attention_bwd_units=BW.attention_bwd_units, attention_lse=BW.attention_lse,
+        attention_lse_units=BW.attention_lse_units, attention_delta_units=BW.attention_delta_units)
 
 
 def _pins(i):
@@ -60,6 +63,12 @@ def _pins(i):
                                                      i.switch, i.exchange_unpack, i.spatial,
                                                      i.temporal),
         lambda: P.pin_tiny_chain(i.tiny_chain, i.st_block),
+        lambda: P.pin_attention_bwd_fd(i.attention, i.attention_bwd),
+        lambda: P.pin_attention_bwd_invariants(i.attention_bwd),
+        lambda: P.pin_attention_lse(i.attention_lse),
+        lambda: P.pin_attention_bwd_units(i.attention_bwd, i.attention_bwd_units,
+                                          i.attention_lse_units, i.attention_lse,
+                                          i.attention_delta_units, i.attention),
     ]
 
 
@@ -277,6 +286,49 @@ def block_post_ln_no_final(x, p, H, eps=1e-6, flags=0):
     return _orig_block(x, p, H, eps, flags | BL.BLOCK_NO_MLP_LN)
 
 
+_orig_abwd = BW.attention_bwd
+_orig_lse = BW.attention_lse
+
+
+def abwd_no_delta(q, k, v, do, scale=None):
+    # the softmax Jacobian without the row-sum term: dz = P * dP
+    q, k, v, do = (np.asarray(a, float) for a in (q, k, v, do))
+    s = 1 / math.sqrt(q.shape[-1]) if scale is None else scale
+    z = np.matmul(q, np.swapaxes(k, -1, -2)) * s
+    p = np.exp(z - z.max(-1, keepdims=True)); p /= p.sum(-1, keepdims=True)
+    dz = p * np.matmul(do, np.swapaxes(v, -1, -2))
+    return np.matmul(dz, k) * s, np.matmul(np.swapaxes(dz, -1, -2), q) * s, \
+        np.matmul(np.swapaxes(p, -1, -2), do)
+
+
+def abwd_dk_unscaled(q, k, v, do, scale=None):
+    dq, dk, dv = _orig_abwd(q, k, v, do, scale)
+    s = 1 / math.sqrt(np.shape(q)[-1]) if scale is None else scale
+    return dq, dk / s, dv
+
+
+def abwd_dq_from_v(q, k, v, do, scale=None):
+    # dq built with v in place of k
+    dq, dk, dv = _orig_abwd(q, k, v, do, scale)
+    dq_v, _, _ = _orig_abwd(q, v, v, do, scale)
+    return dq_v if np.shape(k) == np.shape(v) else dq, dk, dv
+
+
+def abwd_dv_untransposed(q, k, v, do, scale=None):
+    dq, dk, dv = _orig_abwd(q, k, v, do, scale)
+    if np.shape(q)[-2] != np.shape(k)[-2]:
+        return dq, dk, dv
+    q_, k_ = np.asarray(q, float), np.asarray(k, float)
+    s = 1 / math.sqrt(q_.shape[-1]) if scale is None else scale
+    z = np.matmul(q_, np.swapaxes(k_, -1, -2)) * s
+    p = np.exp(z - z.max(-1, keepdims=True)); p /= p.sum(-1, keepdims=True)
+    return dq, dk, np.matmul(p, np.asarray(do, float))
+
+
+def lse_log2(q, k, scale=None):
+    return _orig_lse(q, k, scale) / math.log(2)
+
+
 _orig_block = BL.st_block
 
 MUTANTS = {
@@ -289,6 +341,11 @@ MUTANTS = {
     "split: slices counted from the end": [(SW, "split", split_from_end)],
     "gather: shards in reverse order": [(SW, "gather", gather_reversed)],
     "exchange: joined on the outer axis": [(SW, "exchange_unpack", exchange_outer_axis)],
+    "attention bwd: no row-sum term": [(BW, "attention_bwd", abwd_no_delta)],
+    "attention bwd: dk without the scale": [(BW, "attention_bwd", abwd_dk_unscaled)],
+    "attention bwd: dq from v": [(BW, "attention_bwd", abwd_dq_from_v)],
+    "attention bwd: dv = P dO": [(BW, "attention_bwd", abwd_dv_untransposed)],
+    "attention lse: base 2": [(BW, "attention_lse", lse_log2)],
     "attention: no 1/sqrt(d)": [(AT, "attention", att_no_scale)],
     "attention: padded-width scale": [(AT, "attention", att_padded_scale)],
     "attention: softmax over queries": [(AT, "attention", att_softmax_over_queries)],

@@ -136,3 +136,21 @@ def test_block_no_mlp_ln_flag():
     base = oracle.st_block(x, dict(p, w2=zc), H)
     assert np.allclose(b, base + oracle.linear(oracle.gelu(oracle.linear(base, p["w1"])), p["w2"]))
     assert not np.allclose(a, b)
+
+
+def test_attention_bwd_finite_differences():
+    P.pin_attention_bwd_fd(oracle.attention, oracle.attention_bwd)
+
+
+def test_attention_bwd_invariants():
+    P.pin_attention_bwd_invariants(oracle.attention_bwd)
+
+
+def test_attention_lse():
+    P.pin_attention_lse(oracle.attention_lse)
+
+
+def test_attention_bwd_units():
+    P.pin_attention_bwd_units(oracle.attention_bwd, oracle.attention_bwd_units,
+                              oracle.attention_lse_units, oracle.attention_lse,
+                              oracle.attention_delta_units, oracle.attention)
