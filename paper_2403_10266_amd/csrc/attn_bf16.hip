@@ -45,6 +45,7 @@
 
 #include <algorithm>
 
+#include "attn_bf16_common.h"
 #include "dsp_internal.h"
 
 // Compile-time tiling of the long-sequence (spatial) and short-sequence
@@ -79,6 +80,10 @@
 #ifndef DSP_ATTN_PV_SLAB
 #define DSP_ATTN_PV_SLAB 1
 #endif
+// Units of L <= 128 go to the persistent single-tile kernel (attn_short.hip).
+#ifndef DSP_ATTN_SHORT_PERSISTENT
+#define DSP_ATTN_SHORT_PERSISTENT 1
+#endif
 // Fold the running maximum into the Q K^T contraction when D allows it.
 #ifndef DSP_ATTN_BIAS_COLUMN
 #define DSP_ATTN_BIAS_COLUMN 1
@@ -87,39 +92,7 @@
 namespace dsp {
 namespace {
 
-typedef __bf16 bf16;
-typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
-typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
-typedef __attribute__((__vector_size__(8 * sizeof(short)))) short shortx8;
-typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
-typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4;
-typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
 constexpr float kLazyRescale = 8.0f;       // log2 headroom before the reference moves
-constexpr int kRsrcWord3 = 0x00020000;     // buffer resource flags, gfx9 family
-
-__device__ __forceinline__ float swap_halves(float v) {
-  // value held by lane (l ^ 32)
-  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(threadIdx.x & 32 ? r[0] : r[1]);
-}
-
-// Buffer resource over [base, base + bytes): all inputs are wave-uniform, and are
-// passed through readfirstlane so the descriptor is built in scalar registers.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  const uint64_t a = reinterpret_cast<uint64_t>(base);
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-  const uint32_t n = __builtin_amdgcn_readfirstlane(bytes);
-  void* p = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
-  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)n, kRsrcWord3);
-}
-
-__device__ __forceinline__ shortx4 lds_read_tr(const bf16* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) shortx4*)(p));
-}
 
 template <int D, int KB>
 struct Geo {
@@ -608,6 +581,9 @@ bool attn_bf16_supports(int D) {
 }
 
 int launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
+#if DSP_ATTN_SHORT_PERSISTENT
+  if (attn_bf16_short_fits(a)) return launch_attn_bf16_short(a, s);
+#endif
   switch (a.D) {
     case 16: return launch_d<16>(a, s);
     case 32: return launch_d<32>(a, s);

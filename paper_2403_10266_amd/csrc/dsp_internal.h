@@ -51,6 +51,11 @@ struct AttnArgs {
 int launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 int launch_attn_f32(const AttnArgs& a, hipStream_t s);
 bool attn_bf16_supports(int D);
+// Persistent kernel for short units, L <= kShortAttnMaxL (attn_short.hip);
+// attn_bf16_short_fits() tells whether the shape is in its 32-bit range.
+constexpr int kShortAttnMaxL = 128;
+bool attn_bf16_short_fits(const AttnArgs& a);
+int launch_attn_bf16_short(const AttnArgs& a, hipStream_t s);
 
 int launch_layernorm(const void* x, int x_bf16, void* y, int y_bf16, int64_t rows, int C, float eps,
                      hipStream_t s);

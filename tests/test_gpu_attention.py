@@ -85,9 +85,20 @@ def test_l1_returns_v_exactly(torch):
     (1, 64, 128, 2, 64),    # D a multiple of 32: VALU row sums
     (1, 40, 77, 2, 16),
     (1, 40, 127, 2, 96),
+    (1, 300, 32, 4, 72),    # 32-key variant: 1200 units, one wave per work-group
+    (2, 150, 20, 3, 72),    # 32-key variant, ragged L
+    (1, 260, 64, 2, 72),    # 64-key variant: 520 units
+    (3, 50, 45, 2, 80),     # 64-key variant, ragged L, VALU-free row sums from a 32-row tile
+    (1, 70, 33, 2, 32),
+    (1, 300, 32, 8, 72),    # 32 keys, 4-head groups: 600 groups
+    (2, 100, 64, 4, 72),    # 64 keys, 4-head groups
+    (1, 64, 50, 8, 80),     # 64 keys, 4-head groups, ragged L
+    (1, 64, 128, 4, 96),    # 128 keys, 2-head groups at the LDS limit (160 KB)
+    (1, 90, 111, 6, 72),    # 128 keys, 2-head groups, ragged L
 ])
 def test_temporal_stream_many_units(torch, B, X, L, H, D):
-    """64 < L <= 128 runs the persistent streaming kernel: many units per work-group."""
+    """L <= 128 runs the persistent single-tile kernel: many units per work-group,
+    unit counts that are and are not multiples of the XCD count."""
     import paper_2403_10266_amd as dsp
     C = H * D
     q, k, v = _inputs((B, X, L, C), "bf16", seed=B * 77 + X + L * 3 + D)
@@ -141,7 +152,7 @@ def test_deterministic(torch):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("B,T,S,H,D", [(1, 40, 12, 2, 72), (2, 130, 6, 3, 72), (1, 17, 9, 2, 64),
-                                       (1, 300, 4, 1, 72)])
+                                       (1, 300, 4, 1, 72), (1, 100, 6, 4, 72), (2, 24, 5, 8, 72)])
 def test_temporal_attention_on_unswitched_layout(torch, dtype, B, T, S, H, D):
     """dsp_attn_strided reads (B, T, S, C) directly (no switch): equal to the
     oracle's strided temporal attention, output also written in (B, T, S, C)."""
