@@ -209,6 +209,55 @@ int dsp_attn_strided(const void* q, const void* k, const void* v, void* o, int64
                      float scale, int dtype, void* stream);
 
 /* ------------------------------------------------------------------------
+ * dsp_attn_fwd_lse -- dsp_attn_strided that also saves, for every query, the
+ * natural-log log-sum-exp of its scaled scores,
+ *     lse[u][i] = log sum_j exp(scale * q_i . k_j),
+ * the row statistic of the softmax in Eq. 3 that the backward pass needs to
+ * recompute the probabilities.  Used for training, which the paper's models
+ * undergo (its weak-scaling runs are a training stage, with ZeRO-2).
+ * lse: DEVICE fp32 [B * X * H][L], unit u = (b * X + x) * H + h, caller-owned,
+ *   4-byte aligned (DSP_ERR_ALIGN), required unless the input is empty
+ *   (DSP_ERR_NULL).  The bf16 kernels compute it from the same bf16-rounded
+ *   scores and probabilities that produce o.
+ * Everything else, including errors, as for dsp_attn_strided.
+ * ------------------------------------------------------------------------ */
+int dsp_attn_fwd_lse(const void* q, const void* k, const void* v, void* o, float* lse, int64_t B,
+                     int64_t X, int64_t L, int H, int D, const int64_t* in_strides,
+                     const int64_t* out_strides, float scale, int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * dsp_attn_bwd -- gradient of attention along one sequence dimension (Eq. 3
+ * per head, Eq. 1-2; any layout as in dsp_attn_strided) by the chain rule
+ * through the softmax.  With z = scale * q.k, P = softmax(z) per row and
+ * Delta_i = sum_d dout[i][d] * o[i][d]:
+ *     dv = P^T dout,  dz = P * (dout v^T - Delta),
+ *     dq = scale * dz k,  dk = scale * dz^T q.
+ * q, k, v: the forward's inputs; o, lse: its outputs (dsp_attn_fwd_lse);
+ *   dout: the gradient of the loss with respect to o.
+ * dq, dk, dv: outputs, same shapes and strides as q, k, v (qkv_strides), so
+ *   gradients of a packed [Q|K|V] buffer land in a packed buffer.
+ * o, dout: element (b, x, l, h*D + d) at b*o_strides[0] + x*o_strides[1] +
+ *   l*o_strides[2] + h*D + d.
+ * delta: DEVICE fp32 workspace [B * X * H][L]; on return it holds Delta.
+ * All pointers are DEVICE pointers owned by the caller; dq, dk, dv must not
+ *   overlap each other or any input, and delta must not overlap lse
+ *   (checked: DSP_ERR_ARG).
+ * dtype DSP_BF16: bf16 tensors, fp32 accumulation on the matrix cores; D in
+ *   {16, 32, 64, 72, 80, 96}; 16-byte aligned tensors and strides that are
+ *   multiples of 8 (DSP_ERR_ALIGN); 64 * qkv_strides[2] * 2 and
+ *   64 * o_strides[2] * 2 below 2^31 (DSP_ERR_SHAPE).  Deterministic: no
+ *   atomics, so repeated calls give identical bits.
+ * dtype DSP_F32: fp32 FMA throughout; 1 <= D <= 256.
+ * scale <= 0 selects 1/sqrt(D).  An empty input launches nothing.
+ * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE, DSP_ERR_DTYPE, DSP_ERR_ALIGN,
+ *   DSP_ERR_ARG (scale not finite, overlapping gradient rows), DSP_ERR_HIP.
+ * ------------------------------------------------------------------------ */
+int dsp_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                 const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
+                 int64_t L, int H, int D, const int64_t* qkv_strides, const int64_t* o_strides,
+                 float scale, int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
  * dsp_layernorm -- per-row normalisation over C (Eq. 4, 6):
  *   y = (x - mean) / sqrt(var + eps), biased variance, no affine part,
  *   statistics in fp32.

@@ -11,6 +11,7 @@ binding's functions raises.
 Entry points (see ``include/dsp.h`` for the exact contracts):
 ``dsp_switch``, ``dsp_exchange_unpack``, ``dsp_split``, ``dsp_gather``,
 ``dsp_spatial_attn``, ``dsp_temporal_attn``, ``dsp_attn_strided``,
+``dsp_attn_fwd_lse``, ``dsp_attn_bwd``,
 ``dsp_layernorm``, ``dsp_linear``, ``dsp_st_block_forward``.
 """
 from __future__ import annotations
@@ -59,6 +60,10 @@ _SIGNATURES = {
     "dsp_temporal_attn": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _I64, _I64, _F, _I, _P]),
     "dsp_attn_strided": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _c.POINTER(_I64),
                               _c.POINTER(_I64), _F, _I, _P]),
+    "dsp_attn_fwd_lse": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _I, _c.POINTER(_I64),
+                              _c.POINTER(_I64), _F, _I, _P]),
+    "dsp_attn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _I,
+                          _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
     "dsp_layernorm": (_I, [_P, _I, _P, _I, _I64, _I, _F, _P]),
     "dsp_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
     "dsp_st_block_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
@@ -292,6 +297,80 @@ def dsp_attn_strided(q, k, v, H: int, out=None, scale: float = 0.0, stream=None)
     _check(lib().dsp_attn_strided(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, X, L, H, C // H, ins, outs,
                                   float(scale), _dtype_code(q), _stream(stream)), "dsp_attn_strided")
     return out
+
+
+def _qkv_views(where, q, k, v, H):
+    _require_device(q, k, v)
+    if q.dim() != 4 or q.shape != k.shape or q.shape != v.shape:
+        raise ValueError(f"{where}: q, k, v must be 4-D views of one shape [B, X, L, C]")
+    if q.stride() != k.stride() or q.stride() != v.stride() or q.stride(3) != 1:
+        raise ValueError(f"{where}: q, k, v must share strides, with a unit last stride")
+    B, X, L, C = q.shape
+    if C % H:
+        raise ValueError(f"{where}: C must be a multiple of H")
+    return B, X, L, C
+
+
+def _like_view(where, t, shape, name):
+    if t.shape != shape or t.stride(3) != 1:
+        raise ValueError(f"{where}: {name} must be a view of shape {tuple(shape)} with a unit last stride")
+
+
+def dsp_attn_fwd_lse(q, k, v, H: int, out=None, lse=None, scale: float = 0.0, stream=None):
+    """dsp_attn_strided that also returns the row log-sum-exp: (out, lse) with
+    lse a float32 tensor [B, X, H, L]."""
+    torch = _torch()
+    B, X, L, C = _qkv_views("dsp_attn_fwd_lse", q, k, v, H)
+    _require_device(out, lse)
+    if out is None:
+        out = torch.empty((B, X, L, C), dtype=q.dtype, device=q.device)
+    _like_view("dsp_attn_fwd_lse", out, q.shape, "out")
+    if lse is None:
+        lse = torch.empty((B, X, H, L), dtype=torch.float32, device=q.device)
+    if lse.dtype != torch.float32 or lse.numel() != B * X * H * L or not lse.is_contiguous():
+        raise ValueError("dsp_attn_fwd_lse: lse must be a contiguous float32 tensor of B*X*H*L elements")
+    ins = (ctypes.c_int64 * 3)(*q.stride()[:3])
+    outs = (ctypes.c_int64 * 3)(*out.stride()[:3])
+    _check(lib().dsp_attn_fwd_lse(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, X, L, H, C // H,
+                                  ins, outs, float(scale), _dtype_code(q), _stream(stream)),
+           "dsp_attn_fwd_lse")
+    return out, lse
+
+
+def dsp_attn_bwd(q, k, v, o, dout, lse, H: int, dq=None, dk=None, dv=None, delta=None,
+                 scale: float = 0.0, stream=None):
+    """Gradients (dq, dk, dv) of attention over dim 2 of the 4-D views q, k, v
+    (as dsp_attn_strided), given its output o, the row log-sum-exp ``lse``
+    from dsp_attn_fwd_lse and the output gradient ``dout`` (o and dout share
+    one layout).  New contiguous gradients unless dq/dk/dv (views with the
+    strides of q) are given.  ``delta``: optional float32 workspace of
+    B*X*H*L elements (holds rowsum(dout * o) on return)."""
+    torch = _torch()
+    B, X, L, C = _qkv_views("dsp_attn_bwd", q, k, v, H)
+    _require_device(o, dout, lse, dq, dk, dv, delta)
+    _like_view("dsp_attn_bwd", o, q.shape, "o")
+    if dout.shape != o.shape or dout.stride() != o.stride():
+        raise ValueError("dsp_attn_bwd: dout must have the shape and strides of o")
+    if lse.dtype != torch.float32 or lse.numel() != B * X * H * L or not lse.is_contiguous():
+        raise ValueError("dsp_attn_bwd: lse must be a contiguous float32 tensor of B*X*H*L elements")
+    if dq is None or dk is None or dv is None:
+        if not q.is_contiguous():
+            raise ValueError("dsp_attn_bwd: for a non-contiguous q pass dq, dk, dv views with its strides")
+        dq, dk, dv = (torch.empty_like(q) if g is None else g for g in (dq, dk, dv))
+    for g, name in ((dq, "dq"), (dk, "dk"), (dv, "dv")):
+        _like_view("dsp_attn_bwd", g, q.shape, name)
+        if tuple(g.stride()) != tuple(q.stride()):
+            raise ValueError(f"dsp_attn_bwd: {name} must have the strides of q, k, v")
+    if delta is None:
+        delta = torch.empty(B * X * H * L, dtype=torch.float32, device=q.device)
+    if delta.dtype != torch.float32 or delta.numel() != B * X * H * L or not delta.is_contiguous():
+        raise ValueError("dsp_attn_bwd: delta must be a contiguous float32 tensor of B*X*H*L elements")
+    qs = (ctypes.c_int64 * 3)(*q.stride()[:3])
+    os_ = (ctypes.c_int64 * 3)(*o.stride()[:3])
+    _check(lib().dsp_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
+                              _ptr(dk), _ptr(dv), _ptr(delta), B, X, L, H, C // H, qs, os_,
+                              float(scale), _dtype_code(q), _stream(stream)), "dsp_attn_bwd")
+    return dq, dk, dv
 
 
 def dsp_layernorm(x, eps: float = 1e-6, out=None, out_dtype=None, stream=None):

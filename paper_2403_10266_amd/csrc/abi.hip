@@ -144,7 +144,7 @@ bool rows_disjoint(int64_t B, int64_t X, int64_t L, const int64_t* st, int64_t w
 
 int attn_impl_strided(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X,
                       int64_t L, int H, int D, const int64_t* in_st, const int64_t* out_st,
-                      float scale, int dtype, void* stream) {
+                      float scale, int dtype, void* stream, float* lse = nullptr) {
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
   if (!in_st || !out_st) return DSP_ERR_NULL;
   if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
@@ -182,8 +182,67 @@ int attn_impl_strided(const void* q, const void* k, const void* v, void* o, int6
   a.x_stride_out = out_st[1];
   a.r_stride_out = out_st[2];
   a.scale = scale > 0.0f ? scale : (float)(1.0 / sqrt((double)D));
+  a.lse = lse;
   hipStream_t s = as_stream(stream);
   return dtype == DSP_BF16 ? launch_attn_bf16(a, s) : launch_attn_f32(a, s);
+}
+
+// The largest element offset of a (B, X, L) grid of rows with strides st is
+// addressable (each term well inside int64).
+bool offsets_ok(int64_t B, int64_t X, int64_t L, const int64_t* st) {
+  int64_t tb, tx, tl;
+  return mul_ok(B - 1, st[0], &tb) && mul_ok(X - 1, st[1], &tx) && mul_ok(L - 1, st[2], &tl) &&
+         tb <= INT64_MAX / 4 && tx <= INT64_MAX / 4 && tl <= INT64_MAX / 4;
+}
+
+int attn_bwd_impl(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                  const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
+                  int64_t L, int H, int D, const int64_t* qkv_st, const int64_t* o_st, float scale,
+                  int dtype, void* stream) {
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (!qkv_st || !o_st) return DSP_ERR_NULL;
+  if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
+  const bool empty = B == 0 || X == 0 || L == 0;
+  if (!empty && (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv || !delta))
+    return DSP_ERR_NULL;
+  for (int i = 0; i < 3; ++i)
+    if (qkv_st[i] < 0 || o_st[i] < 0) return DSP_ERR_SHAPE;
+  if (isnan(scale) || isinf(scale)) return DSP_ERR_ARG;
+  int64_t width, units, stat_elems;
+  if (!mul_ok(H, D, &width) || !mul_ok(B, X, &units) || !mul_ok(units, H, &units) ||
+      !mul_ok(units, L, &stat_elems))
+    return DSP_ERR_SHAPE;
+  if (dtype == DSP_BF16) {
+    if (!attn_bf16_supports(D) || D % 32 > 16) return DSP_ERR_SHAPE;
+    for (const void* ptr : {q, k, v, o, dout, (const void*)dq, (const void*)dk, (const void*)dv})
+      if (!aligned(ptr, 16)) return DSP_ERR_ALIGN;
+    for (int i = 0; i < 3; ++i)
+      if (qkv_st[i] % 8 || o_st[i] % 8) return DSP_ERR_ALIGN;
+  } else if (D > 256) {
+    return DSP_ERR_SHAPE;
+  }
+  if (!aligned(lse, 4) || !aligned(delta, 4)) return DSP_ERR_ALIGN;
+  if (empty) return DSP_OK;
+  // every gradient row is written by exactly one (unit, position)
+  if (!rows_disjoint(B, X, L, qkv_st, width)) return DSP_ERR_ARG;
+  if (!offsets_ok(B, X, L, qkv_st) || !offsets_ok(B, X, L, o_st)) return DSP_ERR_SHAPE;
+  if (stat_elems > INT64_MAX / 8) return DSP_ERR_SHAPE;
+  if (overlap(delta, (size_t)stat_elems * 4, lse, (size_t)stat_elems * 4)) return DSP_ERR_ARG;
+  AttnBwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lse = lse;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.delta = delta;
+  a.B = B; a.X = X; a.L = L; a.H = H; a.D = D;
+  for (int i = 0; i < 3; ++i) {
+    a.qkv_strides[i] = qkv_st[i];
+    a.o_strides[i] = o_st[i];
+  }
+  a.scale = scale > 0.0f ? scale : (float)(1.0 / sqrt((double)D));
+  hipStream_t s = as_stream(stream);
+  if (dtype == DSP_BF16) {
+    if (!attn_bwd_bf16_fits(a)) return DSP_ERR_SHAPE;
+    return launch_attn_bwd_bf16(a, s);
+  }
+  return launch_attn_bwd_f32(a, s);
 }
 
 // Spatial (B,T,S,*): unit (b, t), positions s.  Temporal (B,S,T,*): unit
@@ -396,6 +455,23 @@ int dsp_attn_strided(const void* q, const void* k, const void* v, void* o, int64
                      int64_t L, int H, int D, const int64_t* in_strides, const int64_t* out_strides,
                      float scale, int dtype, void* stream) {
   return attn_impl_strided(q, k, v, o, B, X, L, H, D, in_strides, out_strides, scale, dtype, stream);
+}
+
+int dsp_attn_fwd_lse(const void* q, const void* k, const void* v, void* o, float* lse, int64_t B,
+                     int64_t X, int64_t L, int H, int D, const int64_t* in_strides,
+                     const int64_t* out_strides, float scale, int dtype, void* stream) {
+  if (B > 0 && X > 0 && L > 0 && !lse) return DSP_ERR_NULL;
+  if (lse && !aligned(lse, 4)) return DSP_ERR_ALIGN;
+  return attn_impl_strided(q, k, v, o, B, X, L, H, D, in_strides, out_strides, scale, dtype, stream,
+                           lse);
+}
+
+int dsp_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                 const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
+                 int64_t L, int H, int D, const int64_t* qkv_strides, const int64_t* o_strides,
+                 float scale, int dtype, void* stream) {
+  return attn_bwd_impl(q, k, v, o, dout, lse, dq, dk, dv, delta, B, X, L, H, D, qkv_strides, o_strides,
+                       scale, dtype, stream);
 }
 
 int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows, int C, float eps,

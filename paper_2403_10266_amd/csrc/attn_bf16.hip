@@ -80,6 +80,10 @@
 #ifndef DSP_ATTN_PV_SLAB
 #define DSP_ATTN_PV_SLAB 1
 #endif
+// Q K^T with the d step outer and the next step's K fragments read ahead.
+#ifndef DSP_ATTN_QK_PIPELINE
+#define DSP_ATTN_QK_PIPELINE 1
+#endif
 // Units of L <= 128 go to the persistent single-tile kernel (attn_short.hip).
 #ifndef DSP_ATTN_SHORT_PERSISTENT
 #define DSP_ATTN_SHORT_PERSISTENT 1
@@ -112,6 +116,7 @@ struct Params {
   const bf16* k;
   const bf16* v;
   bf16* o;
+  float* lse;  // optional row log-sum-exp output
   int64_t b_in, x_in, r_in, b_out, x_out, r_out;
   uint32_t X, H, L, n_units, n_qb, n_blocks;
   float c;  // scale * log2(e)
@@ -119,7 +124,7 @@ struct Params {
 
 // Work-group -> unit and query block (XCD-aware), and the unit's base offsets.
 struct UnitMap {
-  uint32_t qb;
+  uint32_t unit, qb;
   int64_t in_base, out_base;
 };
 
@@ -129,6 +134,7 @@ __device__ __forceinline__ UnitMap map_unit(const Params& p, int D) {
   if ((p.n_blocks & 7u) == 0) bid = (bid & 7u) * (p.n_blocks >> 3) + (bid >> 3);
   const uint32_t unit = bid / p.n_qb;
   UnitMap m;
+  m.unit = unit;
   m.qb = bid - unit * p.n_qb;
   const uint32_t h = unit % p.H;
   const uint32_t bx = unit / p.H;
@@ -292,11 +298,35 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
     // ---- S'^T = K Q'^T (exp2-domain scores, minus the reference with BIAS)
     floatx16 s[NKT][QT];
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int j = 0; j < QT; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[kt][j][r] = 0.0f;
+#if DSP_ATTN_QK_PIPELINE
+    // d step outer: the K fragments of step st + 1 are read from LDS while the
+    // NKT * QT independent MFMAs of step st run
+    auto k_frag = [&](int kt, int st) {
+      return *reinterpret_cast<const bf16x8*>(k_lds + (32 * kt + l32) * G::KP + 16 * st + 8 * g);
+    };
+    bf16x8 ka[2][NKT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) ka[0][kt] = k_frag(kt, 0);
+#pragma unroll
+    for (int st = 0; st < G::NDK; ++st) {
+      if (st + 1 < G::NDK) {
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) ka[(st + 1) & 1][kt] = k_frag(kt, st + 1);
+      }
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int j = 0; j < QT; ++j)
+          s[kt][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st & 1][kt], qf[j][st], s[kt][j], 0, 0, 0);
+    }
+#else
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int st = 0; st < G::NDK; ++st) {
         const bf16x8 a =
@@ -305,7 +335,7 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
         for (int j = 0; j < QT; ++j)
           s[kt][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[j][st], s[kt][j], 0, 0, 0);
       }
-    }
+#endif
     if (kb + KB > L) {  // keys past L: score -inf (only the last tile can hold any)
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
@@ -475,6 +505,12 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
       l = l_run[j] + swap_halves(l_run[j]);
     }
     const float inv = 1.0f / l;
+    if (p.lse && g == 0) {
+      // natural-log row log-sum-exp: the scores were exp2(s' - m_ref) with s'
+      // the log2-domain score, summing to l
+      const uint32_t q = q_wave + 32 * j + l32;
+      if (q < L) p.lse[(int64_t)um.unit * L + q] = 0.6931471805599453f * (m_ref[j] + log2f(l));
+    }
     if constexpr (SLAB) {
       // slab rows d < D: lanes 0-31 hold d = 32 NT32 + 4 (lane / 16) + r for
       // query 16 h + lane % 16; their row sum is that query's
@@ -523,6 +559,7 @@ int64_t make_params(const AttnArgs& a, int QB, int KB, Params& p) {
   p.k = static_cast<const bf16*>(a.k);
   p.v = static_cast<const bf16*>(a.v);
   p.o = static_cast<bf16*>(a.o);
+  p.lse = a.lse;
   p.b_in = a.b_stride_in;
   p.x_in = a.x_stride_in;
   p.r_in = a.r_stride_in;

@@ -1,0 +1,715 @@
+// Backward of attention along one sequence dimension: the gradient of
+// softmax(Q K^T * scale) V (Eq. 3, per head as in Eq. 1-2) by the chain rule
+// through the softmax.  With z = scale * q.k, P = softmax(z) row by row and
+// Delta_i = sum_d dO[i][d] O[i][d] (= sum_j dP[i][j] P[i][j]):
+//   dV = P^T dO,  dP = dO V^T,  dZ = P * (dP - Delta),
+//   dQ = scale * dZ K,  dK = scale * dZ^T Q.
+// P is recomputed from the forward's row log-sum-exp, so nothing of size
+// L x L is ever stored.
+//
+// bf16 path, on v_mfma_f32_32x32x16_bf16 like the forward:
+//  * Two deterministic kernels, no atomics: the first owns a block of queries
+//    and loops over key tiles (dQ, and Delta for its queries); the second owns
+//    a block of keys and loops over query tiles (dK and dV).  Each recomputes
+//    the scores it needs.
+//  * The head width is padded to a multiple of 16 with two spare columns.
+//    They carry the per-row statistics into the score products, as a bf16 hi/lo
+//    pair (|x - hi - lo| <= 2^-16 |x|): the query side holds -lse and the
+//    key side 1.0, so the MFMA yields z' - lse directly and P = exp2 of the
+//    accumulator.  In the same way the dO side holds -Delta and the V side 1.0,
+//    so the dP product yields dP - Delta.
+//  * Scores use Q' = Q * scale * log2(e), rounded to bf16 exactly as in the
+//    forward, so P matches the probabilities whose log-sum-exp was saved.
+//  * The d-row products (dQ^T = K^T dZ^T, dV^T = dO^T P, dK^T = Q'^T dZ) take
+//    their A operand transposed from row-major LDS tiles (ds_read_b64_tr_b16)
+//    and their B operand straight from the score accumulators converted to
+//    bf16, with the same permuted row order on both sides.  The last 16 rows
+//    of a head width that is not a multiple of 32 run on 16x16x32 MFMAs.
+//
+// fp32 path: plain FMA loops, one thread per (unit, row, 32-column slice).
+#include <math.h>
+
+#include <algorithm>
+
+#include "attn_bf16_common.h"
+#include "dsp_internal.h"
+
+namespace dsp {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <int D>
+struct BGeo {
+  static constexpr int NDK = (D + 2 + 15) / 16;  // 16-wide d steps of the score products
+  static constexpr int NT32 = D / 32;            // 32-row tiles of the d-row products
+  static constexpr bool SLAB = (D % 32) != 0;    // rows 32 NT32 .. + 15 on 16x16x32
+  static constexpr int P = NDK * 16 + 24;        // LDS row pitch (elements): an odd multiple of 16 B
+  static constexpr int CH = D / 8;               // 16-byte chunks of a row
+  static constexpr int SB = D / 16;              // d step holding the bias columns D, D + 1
+  static constexpr int GB = (D % 16) / 8;        // ... in lanes with g == GB, elements 0 and 1
+  static_assert(D % 8 == 0 && D % 32 <= 16, "head width");
+};
+
+struct BwdParams {
+  const bf16* q;
+  const bf16* k;
+  const bf16* v;
+  const bf16* o;
+  const bf16* dout;
+  const float* lse;
+  bf16* dq;
+  bf16* dk;
+  bf16* dv;
+  float* delta;
+  int64_t b_in, x_in, r_in;  // q, k, v and dq, dk, dv
+  int64_t b_o, x_o, r_o;     // o and dout
+  uint32_t X, H, L, n_blk, n_blocks;
+  float c;      // scale * log2(e)
+  float scale;
+};
+
+struct BwdMap {
+  uint32_t unit, blk;
+  int64_t in_base, o_base;
+};
+
+__device__ __forceinline__ BwdMap bwd_map(const BwdParams& p, int D) {
+  uint32_t bid = blockIdx.x;
+  // hardware places block i on XCD i % 8; give each XCD a contiguous range
+  if ((p.n_blocks & 7u) == 0) bid = (bid & 7u) * (p.n_blocks >> 3) + (bid >> 3);
+  BwdMap m;
+  m.unit = bid / p.n_blk;
+  m.blk = bid - m.unit * p.n_blk;
+  const uint32_t h = m.unit % p.H, bx = m.unit / p.H, xx = bx % p.X, bb = bx / p.X;
+  m.in_base = (int64_t)bb * p.b_in + (int64_t)xx * p.x_in + (int64_t)h * D;
+  m.o_base = (int64_t)bb * p.b_o + (int64_t)xx * p.x_o + (int64_t)h * D;
+  return m;
+}
+
+// A operand of a 32x32x16 MFMA read transposed from a row-major LDS tile:
+// lane (m + 32g) gets column col0 + m at rows row0 + 4g + {0..3, 8..11}, the
+// row order of the registers 8kk .. 8kk + 7 of a 32x32 accumulator.
+__device__ __forceinline__ bf16x8 tr_frag32(const bf16* t, int pitch, int row0, int col0, int lane) {
+  const int j16 = lane & 15, g = lane >> 5, mbase = 16 * ((lane >> 4) & 1);
+  const int row = row0 + 4 * g + (j16 >> 2);
+  const int col = col0 + mbase + 4 * (j16 & 3);
+  const shortx4 lo = lds_read_tr(t + row * pitch + col);
+  const shortx4 hi = lds_read_tr(t + (row + 8) * pitch + col);
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// A operand of the 16x16x32 slab (16 columns col0 .. col0 + 15, 32 rows of a
+// 32x32 tile starting at row0), in the row order that one permlane16 swap
+// gives the B operand (see slab_b).
+__device__ __forceinline__ bf16x8 tr_slab(const bf16* t, int pitch, int row0, int col0, int lane) {
+  const int j16 = lane & 15, c = lane >> 4;
+  const int kbase = ((c & 1) ? 16 : 0) + ((c & 2) ? 4 : 0);
+  const int row = row0 + kbase + (j16 >> 2);
+  const int col = col0 + 4 * (j16 & 3);
+  const shortx4 lo = lds_read_tr(t + row * pitch + col);
+  const shortx4 hi = lds_read_tr(t + (row + 8) * pitch + col);
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// B operands of the slab from the two bf16 halves (registers 0-7, 8-15) of a
+// 32x32 accumulator: b0 for its columns 0-15, b1 for 16-31.
+__device__ __forceinline__ void slab_b(const bf16x8& x8, const bf16x8& y8, bf16x8& b0, bf16x8& b1) {
+  const u32x4 x = __builtin_bit_cast(u32x4, x8), y = __builtin_bit_cast(u32x4, y8);
+  u32x4 r0, r1;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
+    r0[w] = r[0];
+    r1[w] = r[1];
+  }
+  b0 = __builtin_bit_cast(bf16x8, r0);
+  b1 = __builtin_bit_cast(bf16x8, r1);
+}
+
+// Row fragment (B operand of a score product) of one row of a bf16 tensor:
+// lane (n + 32g) gets elements 16s + 8g .. + 7 for every d step s; columns
+// >= D are 0.  `row` may be null (rows past L): all zero.
+template <int D>
+__device__ __forceinline__ void row_frags(const bf16* row, int g, bf16x8 (&f)[BGeo<D>::NDK]) {
+#pragma unroll
+  for (int s = 0; s < BGeo<D>::NDK; ++s) {
+    const int d = 16 * s + 8 * g;
+    if (row && d < D) {
+      f[s] = *reinterpret_cast<const bf16x8*>(row + d);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[s][e] = (bf16)0.0f;
+    }
+  }
+}
+
+// Stores the 32x32 accumulator tiles (and slab) of a d-row product: lane
+// (n + 32g) owns row `row` of the output, t-th tile holding d = 32t + 8(r/4) +
+// 4g + r%4; slab h (16x16) holds d = 32 NT32 + 4 (lane / 16) + r of output
+// row 16h + lane % 16 of the wave's 32.
+template <int D>
+__device__ __forceinline__ void store_rows(bf16* base, int64_t r_st, uint32_t row0, uint32_t L, int lane,
+                                           const floatx16 (&t32)[BGeo<D>::NT32 > 0 ? BGeo<D>::NT32 : 1],
+                                           const floatx4 (&sl)[2], float mul) {
+  using G = BGeo<D>;
+  const int l32 = lane & 31, g = lane >> 5;
+  const uint32_t row = row0 + l32;
+  if (row < L) {
+    bf16* orow = base + (int64_t)row * r_st;
+#pragma unroll
+    for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int d0 = 32 * t + 8 * r4 + 4 * g;
+        bf16x2 lo = {(bf16)(t32[t][4 * r4 + 0] * mul), (bf16)(t32[t][4 * r4 + 1] * mul)};
+        bf16x2 hi = {(bf16)(t32[t][4 * r4 + 2] * mul), (bf16)(t32[t][4 * r4 + 3] * mul)};
+        uint2 w;
+        w.x = __builtin_bit_cast(uint32_t, lo);
+        w.y = __builtin_bit_cast(uint32_t, hi);
+        *reinterpret_cast<uint2*>(orow + d0) = w;
+      }
+  }
+  if constexpr (G::SLAB) {
+    const int d0 = 32 * G::NT32 + 4 * (lane >> 4);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t rs = row0 + 16 * h + (lane & 15);
+      if (d0 < D && rs < L) {
+        bf16x2 lo = {(bf16)(sl[h][0] * mul), (bf16)(sl[h][1] * mul)};
+        bf16x2 hi = {(bf16)(sl[h][2] * mul), (bf16)(sl[h][3] * mul)};
+        uint2 w;
+        w.x = __builtin_bit_cast(uint32_t, lo);
+        w.y = __builtin_bit_cast(uint32_t, hi);
+        *reinterpret_cast<uint2*>(base + (int64_t)rs * r_st + d0) = w;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ (and Delta): a work-group owns 32 NW queries of one unit and loops over
+// the unit's keys in LDS tiles of 64 (K and V, double-buffered, the next tile
+// prefetched into registers).  Per wave and 32-key step:
+//   S^T = K Q'^T - lse2   (bias columns)     -> P^T = exp2(S^T)
+//   dP^T = V dO^T - Delta (bias columns)     -> dZ^T = P^T * dP^T
+//   dQ^T += K^T dZ^T
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
+  using G = BGeo<D>;
+  constexpr int KB = 64, NKT = KB / 32, NT = NW * 64, FT = NT / 2;
+  constexpr int TCH = KB * G::CH;
+  constexpr int NLOAD = (TCH + FT - 1) / FT;
+  constexpr int TILE = 2 * KB * G::P;  // K then V
+  static_assert(NW % 2 == 0, "K/V fetch split needs an even wave count");
+  __shared__ __attribute__((aligned(16))) bf16 lds[2 * TILE];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l32 = lane & 31, g = lane >> 5;
+  const BwdMap um = bwd_map(p, D);
+  const uint32_t L = p.L;
+
+  // padding columns of both buffers: D and D + 1 are 1.0 (they multiply the
+  // bias columns of the query side), the rest 0
+  for (int e = threadIdx.x; e < 4 * KB; e += NT) {
+    bf16* row = lds + (e / (2 * KB)) * TILE + (e % (2 * KB)) * G::P;
+    for (int c = D; c < G::P; ++c) row[c] = (bf16)(c < D + 2 ? 1.0f : 0.0f);
+  }
+
+  // this wave's 32 queries: Q' and dO row fragments with the bias columns,
+  // and Delta = rowsum(dO * O)
+  const uint32_t q = um.blk * 32 * NW + 32 * wave + l32;
+  const bool qv = q < L;
+  bf16x8 qf[G::NDK], df[G::NDK], of[G::NDK];
+  row_frags<D>(qv ? p.q + um.in_base + (int64_t)q * p.r_in : nullptr, g, qf);
+  row_frags<D>(qv ? p.dout + um.o_base + (int64_t)q * p.r_o : nullptr, g, df);
+  row_frags<D>(qv ? p.o + um.o_base + (int64_t)q * p.r_o : nullptr, g, of);
+  float dl = 0.0f;
+#pragma unroll
+  for (int s = 0; s < G::NDK; ++s)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      dl += (float)df[s][e] * (float)of[s][e];
+      qf[s][e] = (bf16)((float)qf[s][e] * p.c);
+    }
+  const float delta = dl + swap_halves(dl);
+  const float lse2 = qv ? p.lse[(int64_t)um.unit * L + q] * kLog2e : 0.0f;
+  if (qv && g == 0) p.delta[(int64_t)um.unit * L + q] = delta;
+  if (g == G::GB) {
+    const bf16 lh = (bf16)lse2, dh = (bf16)delta;
+    qf[G::SB][0] = (bf16)(-(float)lh);
+    qf[G::SB][1] = (bf16)(-(lse2 - (float)lh));
+    df[G::SB][0] = (bf16)(-(float)dh);
+    df[G::SB][1] = (bf16)(-(delta - (float)dh));
+  }
+
+  // tile fetch: waves [0, NW/2) K, the others V; rows past L read as zero
+  const bool fetch_v = wave >= NW / 2;
+  const int ft = threadIdx.x % FT;
+  const uint32_t row_bytes = (uint32_t)p.r_in * 2u;
+  uint32_t voff[NLOAD];
+  int lofs[NLOAD];
+#pragma unroll
+  for (int i = 0; i < NLOAD; ++i) {
+    const int c = ft + i * FT;
+    const int row = c / G::CH, col = c - row * G::CH;
+    voff[i] = (uint32_t)row * row_bytes + (uint32_t)col * 16u;
+    lofs[i] = (fetch_v ? KB * G::P : 0) + row * G::P + col * 8;
+  }
+  u32x4 pre[NLOAD];
+  auto fetch = [&](uint32_t kb) {
+    const uint32_t rows = kb < L ? min(L - kb, (uint32_t)KB) : 0u;
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc((fetch_v ? p.v : p.k) + um.in_base + (int64_t)kb * p.r_in, rows * row_bytes);
+#pragma unroll
+    for (int i = 0; i < NLOAD; ++i)
+      if (ft + i * FT < TCH) pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NLOAD; ++i)
+      if (ft + i * FT < TCH) *reinterpret_cast<u32x4*>(lds + buf * TILE + lofs[i]) = pre[i];
+  };
+
+  floatx16 dqt[G::NT32 > 0 ? G::NT32 : 1];
+  floatx4 dqs[2];
+#pragma unroll
+  for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dqt[t][r] = 0.0f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dqs[h][r] = 0.0f;
+
+  const uint32_t n_kb = (L + KB - 1) / KB;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (uint32_t it = 0; it < n_kb; ++it) {
+    const uint32_t kb = it * KB;
+    const bool more = it + 1 < n_kb;
+    if (more) fetch(kb + KB);
+    const bf16* k_lds = lds + (it & 1) * TILE;
+    const bf16* v_lds = k_lds + KB * G::P;
+
+    floatx16 s[NKT], dp[NKT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kt][r] = dp[kt][r] = 0.0f;
+#pragma unroll
+    for (int st = 0; st < G::NDK; ++st)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(k_lds + (32 * kt + l32) * G::P + 16 * st + 8 * g);
+        const bf16x8 va = *reinterpret_cast<const bf16x8*>(v_lds + (32 * kt + l32) * G::P + 16 * st + 8 * g);
+        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s[kt], 0, 0, 0);
+        dp[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, df[st], dp[kt], 0, 0, 0);
+      }
+    // lane (n + 32g) holds keys kb + 32kt + 8(r/4) + 4g + r%4 of query n
+    const bool tail = kb + KB > L;
+    bf16x8 zb[NKT][2];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float pr = __builtin_amdgcn_exp2f(s[kt][r]);
+        if (tail && kb + 32 * kt + (r / 4) * 8 + 4 * g + (r % 4) >= L) pr = 0.0f;
+        zb[kt][r / 8][r % 8] = (bf16)(pr * dp[kt][r]);
+      }
+    // dQ^T += K^T dZ^T
+#pragma unroll
+    for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+          dqt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              tr_frag32(k_lds, G::P, 32 * kt + 16 * kk, 32 * t, lane), zb[kt][kk], dqt[t], 0, 0, 0);
+    if constexpr (G::SLAB) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        const bf16x8 a = tr_slab(k_lds, G::P, 32 * kt, 32 * G::NT32, lane);
+        bf16x8 b0, b1;
+        slab_b(zb[kt][0], zb[kt][1], b0, b1);
+        dqs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, dqs[0], 0, 0, 0);
+        dqs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, dqs[1], 0, 0, 0);
+      }
+    }
+    if (more) stash((it + 1) & 1);
+    __syncthreads();
+  }
+  store_rows<D>(p.dq + um.in_base, p.r_in, um.blk * 32 * NW + 32 * wave, L, lane, dqt, dqs, p.scale);
+}
+
+// ---------------------------------------------------------------------------
+// dK and dV: a work-group owns 32 NW keys of one unit and loops over the
+// unit's queries in LDS tiles of 64 (Q' and dO, with their bias columns,
+// double-buffered, the next tile prefetched into registers).  Per wave and
+// 32-query step:
+//   S = Q' K^T - lse2  -> P = exp2(S);   dP = dO V^T - Delta -> dZ = P * dP
+//   dV^T += dO^T P;    dK^T += Q'^T dZ
+// Query rows past L are zero with zero bias, so they contribute nothing.
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
+  using G = BGeo<D>;
+  constexpr int QB = 64, NT = NW * 64, FT = NT / 2;
+  constexpr int TCH = QB * G::CH;
+  constexpr int NLOAD = (TCH + FT - 1) / FT;
+  constexpr int TILE = 2 * QB * G::P;  // Q' then dO
+  static_assert(NW % 2 == 0 && FT >= QB, "fetch split");
+  __shared__ __attribute__((aligned(16))) bf16 lds[2 * TILE];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l32 = lane & 31, g = lane >> 5;
+  const BwdMap um = bwd_map(p, D);
+  const uint32_t L = p.L;
+
+  // padding columns past the bias pair: 0 (the bias columns are rewritten per tile)
+  for (int e = threadIdx.x; e < 4 * QB; e += NT) {
+    bf16* row = lds + (e / (2 * QB)) * TILE + (e % (2 * QB)) * G::P;
+    for (int c = D + 2; c < G::P; ++c) row[c] = (bf16)0.0f;
+  }
+
+  // this wave's 32 keys: K and V row fragments, bias columns 1.0
+  const uint32_t key0 = um.blk * 32 * NW + 32 * wave;
+  const uint32_t key = key0 + l32;
+  const bool kv = key < L;
+  bf16x8 kf[G::NDK], vf[G::NDK];
+  row_frags<D>(kv ? p.k + um.in_base + (int64_t)key * p.r_in : nullptr, g, kf);
+  row_frags<D>(kv ? p.v + um.in_base + (int64_t)key * p.r_in : nullptr, g, vf);
+  if (g == G::GB) {
+    kf[G::SB][0] = kf[G::SB][1] = vf[G::SB][0] = vf[G::SB][1] = (bf16)1.0f;
+  }
+
+  // tile fetch: waves [0, NW/2) Q (scaled to Q' when stashed), the others dO;
+  // threads ft < QB of each half also fetch the row's lse or Delta
+  const bool fetch_do = wave >= NW / 2;
+  const int ft = threadIdx.x % FT;
+  const uint32_t qrow_bytes = (uint32_t)p.r_in * 2u, orow_bytes = (uint32_t)p.r_o * 2u;
+  const uint32_t row_bytes = fetch_do ? orow_bytes : qrow_bytes;
+  uint32_t voff[NLOAD];
+  int lofs[NLOAD];
+#pragma unroll
+  for (int i = 0; i < NLOAD; ++i) {
+    const int c = ft + i * FT;
+    const int row = c / G::CH, col = c - row * G::CH;
+    voff[i] = (uint32_t)row * row_bytes + (uint32_t)col * 16u;
+    lofs[i] = (fetch_do ? QB * G::P : 0) + row * G::P + col * 8;
+  }
+  const float* stat = fetch_do ? p.delta : p.lse;
+  u32x4 pre[NLOAD];
+  float pstat = 0.0f;
+  auto fetch = [&](uint32_t qb) {
+    const uint32_t rows = qb < L ? min(L - qb, (uint32_t)QB) : 0u;
+    const bf16* base = fetch_do ? p.dout + um.o_base + (int64_t)qb * p.r_o
+                                : p.q + um.in_base + (int64_t)qb * p.r_in;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(base, rows * row_bytes);
+#pragma unroll
+    for (int i = 0; i < NLOAD; ++i)
+      if (ft + i * FT < TCH) pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
+    pstat = (ft < QB && qb + ft < L) ? stat[(int64_t)um.unit * L + qb + ft] : 0.0f;
+  };
+  auto stash = [&](int buf) {
+    bf16* t = lds + buf * TILE;
+#pragma unroll
+    for (int i = 0; i < NLOAD; ++i)
+      if (ft + i * FT < TCH) {
+        u32x4 v = pre[i];
+        if (!fetch_do) {  // Q' = Q * scale * log2(e), rounded as in the forward
+          bf16x8 x = __builtin_bit_cast(bf16x8, v);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] = (bf16)((float)x[e] * p.c);
+          v = __builtin_bit_cast(u32x4, x);
+        }
+        *reinterpret_cast<u32x4*>(t + lofs[i]) = v;
+      }
+    if (ft < QB) {  // bias pair of row ft: -(lse * log2 e) for Q', -Delta for dO
+      const float x = fetch_do ? pstat : pstat * kLog2e;
+      const bf16 hi = (bf16)x;
+      bf16* row = t + (fetch_do ? QB * G::P : 0) + ft * G::P;
+      row[D] = (bf16)(-(float)hi);
+      row[D + 1] = (bf16)(-(x - (float)hi));
+    }
+  };
+
+  floatx16 dvt[G::NT32 > 0 ? G::NT32 : 1], dkt[G::NT32 > 0 ? G::NT32 : 1];
+  floatx4 dvs[2], dks[2];
+#pragma unroll
+  for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dvt[t][r] = dkt[t][r] = 0.0f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dvs[h][r] = dks[h][r] = 0.0f;
+
+  const uint32_t n_qt = (L + QB - 1) / QB;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (uint32_t it = 0; it < n_qt; ++it) {
+    const bool more = it + 1 < n_qt;
+    if (more) fetch((it + 1) * QB);
+    const bf16* q_lds = lds + (it & 1) * TILE;
+    const bf16* o_lds = q_lds + QB * G::P;
+    if (key0 < L) {  // wave-uniform: waves whose keys are all past L only fetch
+#pragma unroll
+      for (int sub = 0; sub < QB / 32; ++sub) {
+        const int q0 = 32 * sub;
+        floatx16 s, dp;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[r] = dp[r] = 0.0f;
+#pragma unroll
+        for (int st = 0; st < G::NDK; ++st) {
+          const bf16x8 qa = *reinterpret_cast<const bf16x8*>(q_lds + (q0 + l32) * G::P + 16 * st + 8 * g);
+          const bf16x8 da = *reinterpret_cast<const bf16x8*>(o_lds + (q0 + l32) * G::P + 16 * st + 8 * g);
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[st], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[st], dp, 0, 0, 0);
+        }
+        // lane (n + 32g) holds queries q0 + 8(r/4) + 4g + r%4 of key n
+        bf16x8 pb[2], zb[2];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float pr = __builtin_amdgcn_exp2f(s[r]);
+          pb[r / 8][r % 8] = (bf16)pr;
+          zb[r / 8][r % 8] = (bf16)(pr * dp[r]);
+        }
+#pragma unroll
+        for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            dvt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                tr_frag32(o_lds, G::P, q0 + 16 * kk, 32 * t, lane), pb[kk], dvt[t], 0, 0, 0);
+            dkt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                tr_frag32(q_lds, G::P, q0 + 16 * kk, 32 * t, lane), zb[kk], dkt[t], 0, 0, 0);
+          }
+        if constexpr (G::SLAB) {
+          bf16x8 b0, b1;
+          const bf16x8 ao = tr_slab(o_lds, G::P, q0, 32 * G::NT32, lane);
+          slab_b(pb[0], pb[1], b0, b1);
+          dvs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b0, dvs[0], 0, 0, 0);
+          dvs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b1, dvs[1], 0, 0, 0);
+          const bf16x8 aq = tr_slab(q_lds, G::P, q0, 32 * G::NT32, lane);
+          slab_b(zb[0], zb[1], b0, b1);
+          dks[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b0, dks[0], 0, 0, 0);
+          dks[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b1, dks[1], 0, 0, 0);
+        }
+      }
+    }
+    if (more) stash((it + 1) & 1);
+    __syncthreads();
+  }
+  // dK = scale * dZ^T Q = ln 2 * dZ^T Q'
+  store_rows<D>(p.dv + um.in_base, p.r_in, key0, L, lane, dvt, dvs, 1.0f);
+  store_rows<D>(p.dk + um.in_base, p.r_in, key0, L, lane, dkt, dks, kLn2);
+}
+
+// ---------------------------------------------------------------------------
+// fp32 path: plain FMA loops.  One thread per (unit, row, 32-column slice).
+constexpr int DC = 32;
+
+struct BwdParamsF {
+  const float* q;
+  const float* k;
+  const float* v;
+  const float* o;
+  const float* dout;
+  const float* lse;
+  float* dq;
+  float* dk;
+  float* dv;
+  float* delta;
+  int64_t b_in, x_in, r_in, b_o, x_o, r_o;
+  int64_t X, H, L, D, n_dc, total;
+  float scale;
+};
+
+struct RowRef {
+  int64_t unit, row, c0, nc, in_base, o_base;
+};
+
+__device__ __forceinline__ RowRef row_ref(const BwdParamsF& p, int64_t tid) {
+  RowRef r;
+  const int64_t dc = tid % p.n_dc;
+  const int64_t ur = tid / p.n_dc;
+  r.row = ur % p.L;
+  r.unit = ur / p.L;
+  const int64_t h = r.unit % p.H, bx = r.unit / p.H, xx = bx % p.X, bb = bx / p.X;
+  r.in_base = bb * p.b_in + xx * p.x_in + h * p.D;
+  r.o_base = bb * p.b_o + xx * p.x_o + h * p.D;
+  r.c0 = dc * DC;
+  r.nc = min((int64_t)DC, p.D - r.c0);
+  return r;
+}
+
+__device__ __forceinline__ float dotf(const float* a, const float* b, int64_t n) {
+  float s = 0.0f;
+  for (int64_t d = 0; d < n; ++d) s = fmaf(a[d], b[d], s);
+  return s;
+}
+
+__global__ __launch_bounds__(256) void attn_bwd_f32_dq_kernel(BwdParamsF p) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= p.total) return;
+  const RowRef r = row_ref(p, tid);
+  const float* qrow = p.q + r.in_base + r.row * p.r_in;
+  const float* drow = p.dout + r.o_base + r.row * p.r_o;
+  const float delta = dotf(drow, p.o + r.o_base + r.row * p.r_o, p.D);
+  const float lse = p.lse[r.unit * p.L + r.row];
+  if (r.c0 == 0) p.delta[r.unit * p.L + r.row] = delta;
+  float acc[DC];
+#pragma unroll
+  for (int c = 0; c < DC; ++c) acc[c] = 0.0f;
+  for (int64_t j = 0; j < p.L; ++j) {
+    const float* krow = p.k + r.in_base + j * p.r_in;
+    const float pr = expf(dotf(qrow, krow, p.D) * p.scale - lse);
+    const float dz = pr * (dotf(drow, p.v + r.in_base + j * p.r_in, p.D) - delta);
+#pragma unroll
+    for (int c = 0; c < DC; ++c)
+      if (c < r.nc) acc[c] = fmaf(dz, krow[r.c0 + c], acc[c]);
+  }
+  float* out = p.dq + r.in_base + r.row * p.r_in + r.c0;
+#pragma unroll
+  for (int c = 0; c < DC; ++c)
+    if (c < r.nc) out[c] = acc[c] * p.scale;
+}
+
+__global__ __launch_bounds__(256) void attn_bwd_f32_dkv_kernel(BwdParamsF p) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= p.total) return;
+  const RowRef r = row_ref(p, tid);
+  const float* krow = p.k + r.in_base + r.row * p.r_in;
+  const float* vrow = p.v + r.in_base + r.row * p.r_in;
+  float ak[DC], av[DC];
+#pragma unroll
+  for (int c = 0; c < DC; ++c) ak[c] = av[c] = 0.0f;
+  for (int64_t i = 0; i < p.L; ++i) {
+    const float* qrow = p.q + r.in_base + i * p.r_in;
+    const float* drow = p.dout + r.o_base + i * p.r_o;
+    const float pr = expf(dotf(qrow, krow, p.D) * p.scale - p.lse[r.unit * p.L + i]);
+    const float dz = pr * (dotf(drow, vrow, p.D) - p.delta[r.unit * p.L + i]);
+#pragma unroll
+    for (int c = 0; c < DC; ++c)
+      if (c < r.nc) {
+        ak[c] = fmaf(dz, qrow[r.c0 + c], ak[c]);
+        av[c] = fmaf(pr, drow[r.c0 + c], av[c]);
+      }
+  }
+  float* ok = p.dk + r.in_base + r.row * p.r_in + r.c0;
+  float* ov = p.dv + r.in_base + r.row * p.r_in + r.c0;
+#pragma unroll
+  for (int c = 0; c < DC; ++c)
+    if (c < r.nc) {
+      ok[c] = ak[c] * p.scale;
+      ov[c] = av[c];
+    }
+}
+
+template <int D, int NW>
+int launch_bwd_nw(const AttnBwdArgs& a, hipStream_t s) {
+  BwdParams p;
+  p.q = static_cast<const bf16*>(a.q);
+  p.k = static_cast<const bf16*>(a.k);
+  p.v = static_cast<const bf16*>(a.v);
+  p.o = static_cast<const bf16*>(a.o);
+  p.dout = static_cast<const bf16*>(a.dout);
+  p.lse = a.lse;
+  p.dq = static_cast<bf16*>(a.dq);
+  p.dk = static_cast<bf16*>(a.dk);
+  p.dv = static_cast<bf16*>(a.dv);
+  p.delta = a.delta;
+  p.b_in = a.qkv_strides[0];
+  p.x_in = a.qkv_strides[1];
+  p.r_in = a.qkv_strides[2];
+  p.b_o = a.o_strides[0];
+  p.x_o = a.o_strides[1];
+  p.r_o = a.o_strides[2];
+  p.X = (uint32_t)a.X;
+  p.H = (uint32_t)a.H;
+  p.L = (uint32_t)a.L;
+  p.c = a.scale * kLog2e;
+  p.scale = a.scale;
+  const int64_t units = a.B * a.X * a.H;
+  const int64_t n_blk = (a.L + 32 * NW - 1) / (32 * NW);
+  const int64_t blocks = units * n_blk;
+  if (blocks == 0) return DSP_OK;
+  p.n_blk = (uint32_t)n_blk;
+  p.n_blocks = (uint32_t)blocks;
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW>), dim3((uint32_t)blocks), dim3(NW * 64), 0, s, p);
+  int st = last_launch_status();
+  if (st != DSP_OK) return st;
+  hipLaunchKernelGGL((attn_bwd_dkv_kernel<D, NW>), dim3((uint32_t)blocks), dim3(NW * 64), 0, s, p);
+  return last_launch_status();
+}
+
+template <int D>
+int launch_bwd_d(const AttnBwdArgs& a, hipStream_t s) {
+  if (a.L <= 64) return launch_bwd_nw<D, 2>(a, s);
+  if (a.L <= 128) return launch_bwd_nw<D, 4>(a, s);
+  return launch_bwd_nw<D, 8>(a, s);
+}
+
+}  // namespace
+
+bool attn_bwd_bf16_fits(const AttnBwdArgs& a) {
+  // block indices, and the byte ranges of a 64-row tile, are 32-bit
+  const int64_t units = a.B * a.X * a.H;
+  const int64_t blocks = units * ((a.L + 63) / 64);
+  return blocks < (int64_t(1) << 31) && a.L < (int64_t(1) << 31) &&
+         64 * a.qkv_strides[2] * 2 < (int64_t(1) << 31) && 64 * a.o_strides[2] * 2 < (int64_t(1) << 31);
+}
+
+int launch_attn_bwd_bf16(const AttnBwdArgs& a, hipStream_t s) {
+  if (!attn_bwd_bf16_fits(a)) return DSP_ERR_SHAPE;
+  switch (a.D) {
+    case 16: return launch_bwd_d<16>(a, s);
+    case 32: return launch_bwd_d<32>(a, s);
+    case 64: return launch_bwd_d<64>(a, s);
+    case 72: return launch_bwd_d<72>(a, s);
+    case 80: return launch_bwd_d<80>(a, s);
+    case 96: return launch_bwd_d<96>(a, s);
+    default: return DSP_ERR_SHAPE;
+  }
+}
+
+int launch_attn_bwd_f32(const AttnBwdArgs& a, hipStream_t s) {
+  BwdParamsF p;
+  p.q = static_cast<const float*>(a.q);
+  p.k = static_cast<const float*>(a.k);
+  p.v = static_cast<const float*>(a.v);
+  p.o = static_cast<const float*>(a.o);
+  p.dout = static_cast<const float*>(a.dout);
+  p.lse = a.lse;
+  p.dq = static_cast<float*>(a.dq);
+  p.dk = static_cast<float*>(a.dk);
+  p.dv = static_cast<float*>(a.dv);
+  p.delta = a.delta;
+  p.b_in = a.qkv_strides[0];
+  p.x_in = a.qkv_strides[1];
+  p.r_in = a.qkv_strides[2];
+  p.b_o = a.o_strides[0];
+  p.x_o = a.o_strides[1];
+  p.r_o = a.o_strides[2];
+  p.X = a.X;
+  p.H = a.H;
+  p.L = a.L;
+  p.D = a.D;
+  p.n_dc = (a.D + DC - 1) / DC;
+  p.total = a.B * a.X * a.H * a.L * p.n_dc;
+  p.scale = a.scale;
+  if (p.total == 0) return DSP_OK;
+  const int64_t blocks = (p.total + 255) / 256;
+  if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
+  hipLaunchKernelGGL(attn_bwd_f32_dq_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p);
+  int st = last_launch_status();
+  if (st != DSP_OK) return st;
+  hipLaunchKernelGGL(attn_bwd_f32_dkv_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p);
+  return last_launch_status();
+}
+
+}  // namespace dsp

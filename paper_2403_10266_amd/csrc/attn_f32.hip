@@ -19,6 +19,7 @@ struct ParamsF {
   const float* k;
   const float* v;
   float* o;
+  float* lse;  // optional row log-sum-exp output
   int64_t b_in, x_in, r_in, b_out, x_out, r_out;
   int64_t X, H, L, D, n_dc, total;
   float scale;
@@ -66,6 +67,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(ParamsF p) {
   }
   float* orow = p.o + bb * p.b_out + xx * p.x_out + h * p.D + qi * p.r_out + c0;
   const float inv = 1.0f / l;
+  if (p.lse && dc == 0) p.lse[unit * p.L + qi] = m + logf(l);
 #pragma unroll
   for (int c = 0; c < DC; ++c)
     if (c < nc) orow[c] = acc[c] * inv;
@@ -79,6 +81,7 @@ int launch_attn_f32(const AttnArgs& a, hipStream_t s) {
   p.k = static_cast<const float*>(a.k);
   p.v = static_cast<const float*>(a.v);
   p.o = static_cast<float*>(a.o);
+  p.lse = a.lse;
   p.b_in = a.b_stride_in;
   p.x_in = a.x_stride_in;
   p.r_in = a.r_stride_in;

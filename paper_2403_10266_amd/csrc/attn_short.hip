@@ -52,6 +52,7 @@ struct ShortParams {
   const bf16* k;
   const bf16* v;
   bf16* o;
+  float* lse;  // optional row log-sum-exp output
   int64_t b_in, x_in, r_in, b_out, x_out, r_out;
   uint32_t X, H, L, n_units;
   float c;  // scale * log2(e)
@@ -305,6 +306,11 @@ __global__ __launch_bounds__(HG * KB / 32 * 64, 2) void attn_short_kernel(ShortP
       l = ls + swap_halves(ls);
     }
     const float inv = 1.0f / l;
+    if (p.lse && g == 0 && q_row < L) {
+      // natural-log row log-sum-exp (exact maximum m, row sum l of exp2(s' - m))
+      const uint32_t unit = (u / n_groups) * p.H + (u % n_groups) * HG + hw;
+      p.lse[(int64_t)unit * L + q_row] = 0.6931471805599453f * (m + log2f(l));
+    }
     // stage this wave's 32 output rows in its own Q rows of LDS (only this
     // wave reads them), then store whole 16-byte chunks, CH lanes per row
     if constexpr (G::SLAB) {
@@ -361,6 +367,7 @@ int launch_short_kb(const AttnArgs& a, hipStream_t s) {
   p.k = static_cast<const bf16*>(a.k);
   p.v = static_cast<const bf16*>(a.v);
   p.o = static_cast<bf16*>(a.o);
+  p.lse = a.lse;
   p.b_in = a.b_stride_in;
   p.x_in = a.x_stride_in;
   p.r_in = a.r_stride_in;

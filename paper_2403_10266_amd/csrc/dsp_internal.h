@@ -47,8 +47,34 @@ struct AttnArgs {
   int64_t b_stride_in, x_stride_in, r_stride_in;
   int64_t b_stride_out, x_stride_out, r_stride_out;
   float scale;
+  // optional (may be null): fp32 [B * X * H][L], the natural-log row
+  // log-sum-exp of the scaled scores of each query (the backward's statistic)
+  float* lse;
 };
 int launch_attn_bf16(const AttnArgs& a, hipStream_t s);
+
+// Backward of attention (attn_bwd.hip).  Units and positions as in AttnArgs;
+// q, k, v, dq, dk, dv use qkv_strides, o and dout use o_strides; lse and
+// delta are fp32 [B * X * H][L] (delta is written by the first kernel).
+struct AttnBwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* dout;
+  const float* lse;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* delta;
+  int64_t B, X, L;
+  int H, D;
+  int64_t qkv_strides[3], o_strides[3];
+  float scale;
+};
+bool attn_bwd_bf16_fits(const AttnBwdArgs& a);
+int launch_attn_bwd_bf16(const AttnBwdArgs& a, hipStream_t s);
+int launch_attn_bwd_f32(const AttnBwdArgs& a, hipStream_t s);
 int launch_attn_f32(const AttnArgs& a, hipStream_t s);
 bool attn_bf16_supports(int D);
 // Persistent kernel for short units, L <= kShortAttnMaxL (attn_short.hip);

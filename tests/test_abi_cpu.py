@@ -184,6 +184,50 @@ def test_attn_strided_validation(lib):
     assert call(B=0) == dsp.DSP_OK
 
 
+def test_attn_fwd_lse_validation(lib):
+    ok_in, ok_out = _shape(8 * 1152 * 5, 1152, 8 * 1152), _shape(3 * 5 * 1152, 5 * 1152, 1152)
+    call = lambda q=FAKE, o=FAKE2, lse=FAKE2 + 2 ** 24, B=2, X=3, L=5, H=16, D=72, dt=1: \
+        lib.dsp_attn_fwd_lse(q, q, q, o, lse, B, X, L, H, D, ok_in, ok_out, 0.0, dt, None)
+    assert call(lse=None) == dsp.DSP_ERR_NULL
+    assert call(lse=FAKE2 + 2 ** 24 + 2) == dsp.DSP_ERR_ALIGN
+    assert call(q=None) == dsp.DSP_ERR_NULL
+    assert call(dt=4) == dsp.DSP_ERR_DTYPE
+    assert call(D=70) == dsp.DSP_ERR_SHAPE
+    assert call(B=0, lse=None) == dsp.DSP_OK
+
+
+def test_attn_bwd_validation(lib):
+    st_qkv = _shape(3 * 5 * 3456, 5 * 3456, 3456)     # a packed [Q|K|V] layout
+    st_o = _shape(3 * 5 * 1152, 5 * 1152, 1152)
+    A, BUF = 2 ** 24, 2 ** 26
+
+    def call(q=FAKE, o=FAKE + BUF, lse=FAKE + 2 * BUF, dq=FAKE + 3 * BUF, delta=FAKE + 4 * BUF, B=2, X=3,
+             L=5, H=16, D=72, sq=st_qkv, so=st_o, sc=0.0, dt=1):
+        return lib.dsp_attn_bwd(q, q, q, o, o, lse, dq, dq, dq, delta, B, X, L, H, D, sq, so, sc, dt, None)
+    assert call(sq=None) == dsp.DSP_ERR_NULL
+    assert call(so=None) == dsp.DSP_ERR_NULL
+    assert call(lse=None) == dsp.DSP_ERR_NULL
+    assert call(delta=None) == dsp.DSP_ERR_NULL
+    assert call(dq=None) == dsp.DSP_ERR_NULL
+    assert call(dt=3) == dsp.DSP_ERR_DTYPE
+    assert call(H=0) == dsp.DSP_ERR_SHAPE
+    assert call(L=-1) == dsp.DSP_ERR_SHAPE
+    assert call(D=70) == dsp.DSP_ERR_SHAPE                   # unsupported bf16 head width
+    assert call(D=48, H=24) == dsp.DSP_ERR_SHAPE             # 48 % 32 > 16: no 16-row slab
+    assert call(dt=0, D=300, H=1) == dsp.DSP_ERR_SHAPE
+    assert call(q=MIS) == dsp.DSP_ERR_ALIGN
+    assert call(dq=FAKE + 3 * BUF + 8) == dsp.DSP_ERR_ALIGN
+    assert call(sq=_shape(3 * 5 * 3456, 5 * 3456, 3460)) == dsp.DSP_ERR_ALIGN
+    assert call(lse=FAKE + 2 * BUF + 2) == dsp.DSP_ERR_ALIGN
+    assert call(sc=float("inf")) == dsp.DSP_ERR_ARG
+    assert call(sq=_shape(0, 0, 3456)) == dsp.DSP_ERR_ARG   # gradient rows of different units coincide
+    assert call(sq=_shape(3 * 5 * 3456, 5 * 3456, 576)) == dsp.DSP_ERR_ARG   # rows narrower than H*D
+    assert call(delta=FAKE + 2 * BUF + 4) == dsp.DSP_ERR_ARG   # delta overlaps lse
+    assert call(B=1, sq=_shape(0, 2 ** 33, 2 ** 26)) == dsp.DSP_ERR_SHAPE   # 64 rows exceed a 2^31-byte range
+    assert call(B=0, q=None, o=None, lse=None, dq=None, delta=None) == dsp.DSP_OK
+    assert call(L=0) == dsp.DSP_OK
+
+
 def test_layernorm_validation(lib):
     f = lambda x=FAKE, xd=1, y=FAKE2, yd=1, rows=4, C=8, eps=1e-6: lib.dsp_layernorm(
         x, xd, y, yd, rows, C, eps, None)
