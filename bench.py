@@ -21,6 +21,10 @@ and, timed separately after the steps (not part of a step):
             1 x 64 x 64 x 64 x 1152 (T x H x W), T -> H into 8 chunks
   split     dsp_split of that shard along S into 8, one rank's slice
   gather    dsp_gather of 8 shards 1 x 512 x 64 x 1152 along T (604 MB out)
+  attn_bwd_spatial / attn_bwd_temporal  dsp_attn_bwd (dq, dk, dv) of the
+            spatial and temporal workloads, given o and the row log-sum-exp
+            from dsp_attn_fwd_lse; counted as 10 L^2 D flops per unit (the
+            five L x L x D products of the gradient)
 
 The headline value is the combined attention throughput
 (F_spatial + F_temporal) / (t_spatial + t_temporal) in TFLOP/s with
@@ -65,7 +69,8 @@ def parse():
                          "spatial kernel; used only while the kernel source is unchanged")
     ap.add_argument("--only", default=None,
                     choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange",
-                             "temporal_strided", "switch_k3", "split", "gather", "copy"],
+                             "temporal_strided", "switch_k3", "split", "gather", "copy",
+                             "attn_bwd_spatial", "attn_bwd_temporal"],
                     help="run a single part (for profiling); prints per-kernel times only. "
                          "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
                          "plain 604 MB copy used to calibrate traffic counters")
@@ -94,7 +99,12 @@ def main():
     ws, wsp, wtp, wbl = (W["switch_bf16_T64_S4096"], W["spatial_bf16_B2_T16_S4096"],
                          W["temporal_bf16_B2_S512_T128"], W["block_bf16_B1_T32_S1024"])
     wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block", "exchange",
-                                            "temporal_strided", "switch_k3", "split", "gather"}
+                                            "temporal_strided", "switch_k3", "split", "gather",
+                                            "attn_bwd_spatial", "attn_bwd_temporal"}
+    if "attn_bwd_spatial" in wanted:
+        wanted.add("spatial")
+    if "attn_bwd_temporal" in wanted:
+        wanted.add("temporal")
     if wanted & {"copy", "switch_inv", "exchange", "switch_k3", "split", "gather"}:
         wanted.add("switch")
     if "temporal_strided" in wanted:
@@ -138,6 +148,16 @@ def main():
         # the same tensors left in the unswitched (B, T, S, C) layout
         t["tq_tsc"] = [a.permute(0, 2, 1, 3).contiguous() for a in (t["q_tp"], t["k_tp"], t["v_tp"])]
         t["to_tsc"] = torch.empty_like(t["tq_tsc"][0])
+    for kind in ("spatial", "temporal"):
+        if f"attn_bwd_{kind}" in wanted:
+            sfx = "sp" if kind == "spatial" else "tp"
+            w = wsp if kind == "spatial" else wtp
+            q = t[f"q_{sfx}"]
+            gen = torch.Generator(device=dev).manual_seed(w.seed + 100)
+            t[f"do_{sfx}"] = torch.randn(q.shape, generator=gen, device=dev).to(torch.bfloat16)
+            t[f"of_{sfx}"], t[f"lse_{sfx}"] = dsp.dsp_attn_fwd_lse(q, t[f"k_{sfx}"], t[f"v_{sfx}"], w.H)
+            t[f"g_{sfx}"] = [torch.empty_like(q) for _ in range(3)]
+            t[f"dl_{sfx}"] = torch.empty(q.numel() // w.D, dtype=torch.float32, device=dev)
     if "block" in wanted:
         x_bl_np, p_bl = synth.block_inputs(wbl)
         t["x_bl"] = to_dev(x_bl_np, "f32")
@@ -179,6 +199,16 @@ def main():
     def run_block():
         dsp.dsp_st_block_forward(t["x_bl"], t["w_bl"], wbl.H, out=t["y_bl"], workspace=t["ws_bl"])
 
+    def run_bwd(sfx, w):
+        dsp.dsp_attn_bwd(t[f"q_{sfx}"], t[f"k_{sfx}"], t[f"v_{sfx}"], t[f"of_{sfx}"], t[f"do_{sfx}"],
+                         t[f"lse_{sfx}"], w.H, *t[f"g_{sfx}"], delta=t[f"dl_{sfx}"])
+
+    def run_attn_bwd_spatial():
+        run_bwd("sp", wsp)
+
+    def run_attn_bwd_temporal():
+        run_bwd("tp", wtp)
+
     def run_copy():
         dsp.dsp_switch(t["x_sw"], 1, 1, 1, out=t["y_sw"].view(t["x_sw"].shape))
 
@@ -186,7 +216,8 @@ def main():
              ("temporal", run_temporal), ("block", run_block)]
     # timed on its own after the steps: not a step of the single-GPU hot path
     extras = [("exchange", run_exchange), ("temporal_strided", run_temporal_strided),
-              ("switch_k3", run_switch_k3), ("split", run_split), ("gather", run_gather)]
+              ("switch_k3", run_switch_k3), ("split", run_split), ("gather", run_gather),
+              ("attn_bwd_spatial", run_attn_bwd_spatial), ("attn_bwd_temporal", run_attn_bwd_temporal)]
     if args.only:
         every = dict(parts + extras)
         parts, extras = [(args.only, run_copy if args.only == "copy" else every[args.only])], []
@@ -266,7 +297,8 @@ def main():
             "workload": "dsp_switch 1x64x4096x1152 bf16 -> 8 chunks and its inverse 1x4096x64x1152 -> 8 "
                         "chunks; 8-rank exchange+unpack of such shards; the shard as 1x64x64x64x1152 "
                         "switched T->H (K=3); split along S / gather along T of 8 shards; spatial attn B2 T16 S4096 H16 D72; "
-                        "temporal attn B2 S512 T128 H16 D72; ST block B1 T32 S1024 C1152 H16 F4608",
+                        "temporal attn B2 S512 T128 H16 D72; ST block B1 T32 S1024 C1152 H16 F4608; "
+                        "attention backward of the spatial and temporal workloads",
             "attn_frac_mfma_peak": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
             "switch_GBps": round(sw_gbps, 1),
             "switch_frac_hbm_peak": round(sw_gbps / HBM_PEAK_GBPS, 4),
@@ -283,6 +315,8 @@ def main():
             "temporal_GBps": round(tp_gbps, 1),
             "temporal_frac_hbm_peak": round(tp_gbps / HBM_PEAK_GBPS, 4),
             "block_TFLOPs": round(F_bl / (ms["block"] * 1e-3) / 1e12, 2),
+            "attn_bwd_spatial_TFLOPs": round(2.5 * F_sp / (ms["attn_bwd_spatial"] * 1e-3) / 1e12, 2),
+            "attn_bwd_temporal_TFLOPs": round(2.5 * F_tp / (ms["attn_bwd_temporal"] * 1e-3) / 1e12, 2),
             "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
         },
         "roofline": {
@@ -348,7 +382,7 @@ def cpu_baseline(budget_s: float) -> dict:
     t_sp = f_sp = 0.0
     n_sp = 0
     q, k, v = unit_set(wsp, wsp.S, 1)
-    while t_sp < budget_s / 2 and n_sp < 64:
+    while t_sp < budget_s / 2 and n_sp < 512:
         t0 = time.perf_counter()
         oracle.attention(q[0], k[0], v[0])
         t_sp += time.perf_counter() - t0
