@@ -22,6 +22,8 @@ float64 NumPy (library matmul and erf as the only primitives):
   chain rule through the softmax) and the row logsumexp it uses.
 * ``layernorm``, ``linear``, ``gelu`` and the composites ``st_block`` (the
   full spatial-temporal block) and ``tiny_chain``.
+* ``linear_bwd``, ``layernorm_bwd``, ``gelu_bwd``, ``relu_bwd`` and
+  ``st_block_bwd`` -- the chain rule through the block, in reverse order.
 
 Pins: every function is checked in ``tests/test_oracle_pins.py`` against
 closed forms, invariants, hand-worked fixtures and brute force; see the header
@@ -32,6 +34,7 @@ from .attention import attention, attention_rows, spatial_attention, temporal_at
     temporal_attention_strided
 from .backward import attention_bwd, attention_bwd_units, attention_lse, attention_lse_units, \
     attention_delta_units
+from .block_bwd import linear_bwd, layernorm_bwd, gelu_bwd, relu_bwd, st_block_bwd
 from .block import layernorm, linear, gelu, relu, st_block, tiny_chain, BLOCK_NO_MLP_LN, BLOCK_POST_LN, \
     BLOCK_RELU
 
@@ -39,4 +42,5 @@ __all__ = ["switch", "unswitch", "exchange_unpack", "switch_index_map", "split",
            "attention_rows", "spatial_attention", "temporal_attention",
            "temporal_attention_strided", "layernorm", "linear", "gelu", "st_block", "tiny_chain",
            "BLOCK_NO_MLP_LN", "BLOCK_POST_LN", "BLOCK_RELU", "relu", "attention_bwd",
-           "attention_bwd_units", "attention_lse", "attention_lse_units", "attention_delta_units"]
+           "attention_bwd_units", "attention_lse", "attention_lse_units", "attention_delta_units",
+           "linear_bwd", "layernorm_bwd", "gelu_bwd", "relu_bwd", "st_block_bwd"]

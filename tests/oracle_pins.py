@@ -565,3 +565,129 @@ def pin_tiny_chain(tiny_chain, st_block):
     y = np.ascontiguousarray(y.transpose(0, 2, 1, 3))
     y = attn_all(y @ p["wqkv_t"], T, False) @ p["wo_t"]
     assert np.allclose(got, y, rtol=1e-12, atol=1e-13)
+
+
+# ----------------------------------------------------------------------------- block backward
+def pin_linear_bwd(linear, linear_bwd):
+    """<dy, x W + b> differentiated numerically in x, W and b."""
+    rng = np.random.default_rng(40)
+    x, w, b, dy = rng.standard_normal((2, 3, 4)), rng.standard_normal((4, 5)), \
+        rng.standard_normal(5), rng.standard_normal((2, 3, 5))
+    dx, dw, db = linear_bwd(x, w, dy)
+    loss = lambda xx, ww, bb: float((dy * linear(xx, ww, bb)).sum())
+    assert np.allclose(dx, _fd_grad(lambda a: loss(a, w, b), x), atol=1e-8)
+    assert np.allclose(dw, _fd_grad(lambda a: loss(x, a, b), w), atol=1e-8)
+    assert np.allclose(db, _fd_grad(lambda a: loss(x, w, a), b), atol=1e-8)
+
+
+def pin_layernorm_bwd(layernorm, layernorm_bwd):
+    rng = np.random.default_rng(41)
+    for eps in (1e-6, 0.3):
+        x, dy = rng.standard_normal((3, 7)) * 2 + 1, rng.standard_normal((3, 7))
+        dx = layernorm_bwd(x, dy, eps)
+        assert np.allclose(dx, _fd_grad(lambda a: float((dy * layernorm(a, eps)).sum()), x), atol=1e-7)
+        # the output is invariant to adding a constant to a row (and, for eps = 0,
+        # to scaling it), so the gradient has no component along the ones vector
+        assert np.allclose(dx.sum(axis=-1), 0.0, atol=1e-12)
+    x, dy = rng.standard_normal((4, 9)), rng.standard_normal((4, 9))
+    y = layernorm(x, 0.0)
+    assert np.allclose((layernorm_bwd(x, dy, 0.0) * (x - x.mean(-1, keepdims=True))).sum(-1), 0.0,
+                       atol=1e-11)
+    # a gradient along the output itself or along ones gives zero
+    assert np.allclose(layernorm_bwd(x, y, 0.0), 0.0, atol=1e-12)
+    assert np.allclose(layernorm_bwd(x, np.ones_like(x), 0.0), 0.0, atol=1e-12)
+
+
+def pin_gelu_bwd(gelu, gelu_bwd, relu, relu_bwd):
+    rng = np.random.default_rng(42)
+    u, dy = rng.standard_normal(50) * 3, rng.standard_normal(50)
+    assert np.allclose(gelu_bwd(u, dy), _fd_grad(lambda a: float((dy * gelu(a)).sum()), u), atol=1e-8)
+    # GELU(u) - GELU(-u) = u, so GELU'(u) + GELU'(-u) = 1
+    one = np.ones_like(u)
+    assert np.allclose(gelu_bwd(u, one) + gelu_bwd(-u, one), 1.0)
+    assert gelu_bwd(np.array([0.0]), np.array([1.0]))[0] == 0.5
+    v = u[np.abs(u) > 1e-3]
+    assert np.allclose(relu_bwd(v, dy[:v.size]), np.where(v > 0, dy[:v.size], 0.0))
+
+
+def _block_case(seed, B=1, T=3, S=4, C=8, H=2, F=12, bias=False):
+    rng = np.random.default_rng(seed)
+    p = {"wqkv_s": rng.standard_normal((C, 3 * C)) * 0.3, "wo_s": rng.standard_normal((C, C)) * 0.3,
+         "wqkv_t": rng.standard_normal((C, 3 * C)) * 0.3, "wo_t": rng.standard_normal((C, C)) * 0.3,
+         "w1": rng.standard_normal((C, F)) * 0.3, "w2": rng.standard_normal((F, C)) * 0.3}
+    if bias:
+        for n, k in (("bqkv_s", 3 * C), ("bo_s", C), ("bqkv_t", 3 * C), ("bo_t", C), ("b1", F), ("b2", C)):
+            p[n] = rng.standard_normal(k) * 0.2
+    x = rng.standard_normal((B, T, S, C))
+    dy = rng.standard_normal((B, S, T, C))
+    return x, p, dy, H
+
+
+def pin_block_bwd_fd(st_block, st_block_bwd, flag_sets):
+    """Finite differences of <dy, st_block(x)> in x and in sampled entries of
+    every weight and bias, for each flag combination."""
+    for i, flags in enumerate(flag_sets):
+        x, p, dy, H = _block_case(50 + i, bias=True)
+        dx, g = st_block_bwd(x, p, H, dy, flags=flags)
+        f = lambda xx, pp: float((dy * st_block(xx, pp, H, flags=flags)).sum())
+        assert np.allclose(dx, _fd_grad(lambda a: f(a, p), x, h=1e-5), atol=1e-6, rtol=1e-5), flags
+        rng = np.random.default_rng(60 + i)
+        for name, w in p.items():
+            assert g[name].shape == w.shape, name
+            for _ in range(3):
+                idx = tuple(rng.integers(s) for s in w.shape)
+                def fw(val):
+                    q = dict(p)
+                    q[name] = w.copy()
+                    q[name][idx] = val
+                    return f(x, q)
+                num = (fw(w[idx] + 1e-5) - fw(w[idx] - 1e-5)) / 2e-5
+                assert abs(g[name][idx] - num) <= 1e-6 + 1e-5 * abs(num), (flags, name, idx)
+
+
+def pin_block_bwd_autograd(st_block_bwd, flag_sets):
+    """The same gradients from torch autograd in float64 on the CPU: an
+    independent differentiation of the block written with torch operations."""
+    import torch
+    for i, flags in enumerate(flag_sets):
+        x, p, dy, H = _block_case(70 + i, B=2, T=3, S=5, C=12, H=3, F=20, bias=(i % 2 == 0))
+        dx, g = st_block_bwd(x, p, H, dy, flags=flags)
+        tx = torch.tensor(x, requires_grad=True)
+        tp = {n: torch.tensor(v, requires_grad=True) for n, v in p.items()}
+        C = x.shape[-1]
+
+        def ln(v):
+            mu = v.mean(-1, keepdim=True)
+            return (v - mu) / torch.sqrt(((v - mu) ** 2).mean(-1, keepdim=True) + 1e-6)
+
+        def lin(v, w, b):
+            return v @ tp[w] + (tp[b] if b in tp else 0.0)
+
+        def attn(q, k, v, dim):
+            # attention over sequence axis `dim` (1 = T, 2 = S) of (B, T, S, C), per head
+            qs, ks, vs = (t.movedim(dim, 2) for t in (q, k, v))          # (B, X, L, C)
+            Bq, X, L, _ = qs.shape
+            sh = lambda t: t.reshape(Bq, X, L, H, C // H).permute(0, 1, 3, 2, 4)
+            qh, kh, vh = sh(qs), sh(ks), sh(vs)
+            z = qh @ kh.transpose(-1, -2) / math.sqrt(C // H)
+            o = torch.softmax(z, dim=-1) @ vh
+            return o.permute(0, 1, 3, 2, 4).reshape(Bq, X, L, C).movedim(2, dim)
+
+        post, relu_ = bool(flags & 4), bool(flags & 8)
+        act = torch.relu if relu_ else (lambda u: 0.5 * u * (1 + torch.erf(u / math.sqrt(2.0))))
+
+        def sub_attn(v, tag, dim):
+            qkv = lin(v, "wqkv_" + tag, "bqkv_" + tag)
+            return lin(attn(qkv[..., :C], qkv[..., C:2 * C], qkv[..., 2 * C:], dim), "wo_" + tag, "bo_" + tag)
+        x1 = ln(tx + sub_attn(tx, "s", 2)) if post else tx + sub_attn(ln(tx), "s", 2)
+        y0 = x1                                                   # kept in (B, T, S, C): temporal attends over dim 1
+        y1 = ln(y0 + sub_attn(y0, "t", 1)) if post else y0 + sub_attn(ln(y0), "t", 1)
+        ffn = lambda v: lin(act(lin(v, "w1", "b1")), "w2", "b2")
+        if flags & 1:
+            out = y1 + ffn(y1)
+        else:
+            out = ln(y1 + ffn(y1)) if post else y1 + ffn(ln(y1))
+        (out.transpose(1, 2) * torch.tensor(dy)).sum().backward()
+        assert np.allclose(dx, tx.grad.numpy(), atol=1e-10, rtol=1e-8), flags
+        for n in p:
+            assert np.allclose(g[n], tp[n].grad.numpy(), atol=1e-10, rtol=1e-8), (flags, n)

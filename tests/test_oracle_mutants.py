@@ -8,6 +8,7 @@ import types
 
 import numpy as np
 import pytest
+from scipy.special import erf as SCIPY_ERF
 
 import oracle  # noqa: F401  (loads the submodules)
 from tests import oracle_pins as P
@@ -16,6 +17,9 @@ SW = sys.modules["oracle.switch"]
 AT = sys.modules["oracle.attention"]
 BL = sys.modules["oracle.block"]
 BW = sys.modules["oracle.backward"]
+OB = sys.modules["oracle.block_bwd"]
+BWD_FLAGS = [0, BL.BLOCK_NO_MLP_LN, BL.BLOCK_POST_LN, BL.BLOCK_POST_LN | BL.BLOCK_RELU,
+             BL.BLOCK_RELU | BL.BLOCK_NO_MLP_LN]
 
 
 def _impl():
@@ -26,7 +30,9 @@ def _impl():
         layernorm=BL.layernorm, linear=BL.linear, gelu=BL.gelu, relu=BL.relu, st_block=BL.st_block,
         tiny_chain=BL.tiny_chain, attention_bwd=BW.attention_bwd,
         attention_bwd_units=BW.attention_bwd_units, attention_lse=BW.attention_lse,
-        attention_lse_units=BW.attention_lse_units, attention_delta_units=BW.attention_delta_units)
+        attention_lse_units=BW.attention_lse_units, attention_delta_units=BW.attention_delta_units,
+        linear_bwd=OB.linear_bwd, layernorm_bwd=OB.layernorm_bwd, gelu_bwd=OB.gelu_bwd,
+        relu_bwd=OB.relu_bwd, st_block_bwd=OB.st_block_bwd)
 
 
 def _pins(i):
@@ -69,16 +75,24 @@ def _pins(i):
         lambda: P.pin_attention_bwd_units(i.attention_bwd, i.attention_bwd_units,
                                           i.attention_lse_units, i.attention_lse,
                                           i.attention_delta_units, i.attention),
+        # the block backward pins last: they are the slowest
+        lambda: P.pin_linear_bwd(i.linear, i.linear_bwd),
+        lambda: P.pin_layernorm_bwd(i.layernorm, i.layernorm_bwd),
+        lambda: P.pin_gelu_bwd(i.gelu, i.gelu_bwd, i.relu, i.relu_bwd),
+        lambda: P.pin_block_bwd_fd(i.st_block, i.st_block_bwd, BWD_FLAGS),
+        lambda: P.pin_block_bwd_autograd(i.st_block_bwd, BWD_FLAGS),
     ]
 
 
-def _n_failed():
+def _n_failed(stop_at_first: bool = False):
     failed = 0
     for pin in _pins(_impl()):
         try:
             pin()
         except Exception:
             failed += 1
+            if stop_at_first:
+                break
     return failed
 
 
@@ -330,6 +344,35 @@ def lse_log2(q, k, scale=None):
 
 
 _orig_block = BL.st_block
+_orig_ln_bwd = OB.layernorm_bwd
+_orig_lin_bwd = OB.linear_bwd
+_orig_sub_bwd = OB._attn_sublayer_bwd
+
+
+def lnb_no_projection(x, dy, eps=1e-6):
+    # drops the term along the normalised row: (dy - mean(dy)) / sigma
+    x = np.asarray(x, float)
+    mu = x.mean(-1, keepdims=True)
+    sigma = np.sqrt(((x - mu) ** 2).mean(-1, keepdims=True) + eps)
+    dy = np.asarray(dy, float)
+    return (dy - dy.mean(-1, keepdims=True)) / sigma
+
+
+def gelub_cdf_only(u, dy):
+    # d/du (u Phi(u)) taken as Phi(u): the u phi(u) term dropped
+    u = np.asarray(u, float)
+    return np.asarray(dy, float) * 0.5 * (1 + SCIPY_ERF(u / math.sqrt(2)))
+
+
+def linb_db_mean(x, w, dy):
+    dx, dw, db = _orig_lin_bwd(x, w, dy)
+    return dx, dw, db / max(1, np.asarray(dy).reshape(-1, np.shape(dy)[-1]).shape[0])
+
+
+def subb_wo_transposed(saved, p, tag, H, d_out, grads):
+    dh = _orig_sub_bwd(saved, p, tag, H, d_out, grads)
+    grads["wo_" + tag] = grads["wo_" + tag].T
+    return dh
 
 MUTANTS = {
     "switch: interleaved chunks": [(SW, "switch", sw_interleaved_chunks), (BL, "switch", sw_interleaved_chunks)],
@@ -346,6 +389,11 @@ MUTANTS = {
     "attention bwd: dq from v": [(BW, "attention_bwd", abwd_dq_from_v)],
     "attention bwd: dv = P dO": [(BW, "attention_bwd", abwd_dv_untransposed)],
     "attention lse: base 2": [(BW, "attention_lse", lse_log2)],
+    "layernorm bwd: no projection on the output": [(OB, "layernorm_bwd", lnb_no_projection)],
+    "gelu bwd: Phi only": [(OB, "gelu_bwd", gelub_cdf_only)],
+    "linear bwd: bias gradient averaged": [(OB, "linear_bwd", linb_db_mean)],
+    "block bwd: switch adjoint without the transpose": [(OB, "switch", sw_no_transpose)],
+    "block bwd: out-projection weight gradient transposed": [(OB, "_attn_sublayer_bwd", subb_wo_transposed)],
     "attention: no 1/sqrt(d)": [(AT, "attention", att_no_scale)],
     "attention: padded-width scale": [(AT, "attention", att_padded_scale)],
     "attention: softmax over queries": [(AT, "attention", att_softmax_over_queries)],
@@ -376,4 +424,4 @@ def test_unmutated_oracle_passes_every_pin():
 def test_mutant_is_caught(name, monkeypatch):
     for mod, attr, fn in MUTANTS[name]:
         monkeypatch.setattr(mod, attr, fn)
-    assert _n_failed() >= 1, f"no pin catches the planted mistake: {name}"
+    assert _n_failed(stop_at_first=True) >= 1, f"no pin catches the planted mistake: {name}"

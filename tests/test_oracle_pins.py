@@ -154,3 +154,30 @@ def test_attention_bwd_units():
     P.pin_attention_bwd_units(oracle.attention_bwd, oracle.attention_bwd_units,
                               oracle.attention_lse_units, oracle.attention_lse,
                               oracle.attention_delta_units, oracle.attention)
+
+
+# ---- block backward
+from oracle import block_bwd as OB  # noqa: E402
+
+BWD_FLAGS = [0, oracle.BLOCK_NO_MLP_LN, oracle.BLOCK_POST_LN, oracle.BLOCK_POST_LN | oracle.BLOCK_RELU,
+             oracle.BLOCK_RELU | oracle.BLOCK_NO_MLP_LN]
+
+
+def test_linear_bwd():
+    P.pin_linear_bwd(oracle.linear, OB.linear_bwd)
+
+
+def test_layernorm_bwd():
+    P.pin_layernorm_bwd(oracle.layernorm, OB.layernorm_bwd)
+
+
+def test_gelu_relu_bwd():
+    P.pin_gelu_bwd(oracle.gelu, OB.gelu_bwd, oracle.relu, OB.relu_bwd)
+
+
+def test_block_bwd_finite_differences():
+    P.pin_block_bwd_fd(oracle.st_block, OB.st_block_bwd, BWD_FLAGS)
+
+
+def test_block_bwd_matches_autograd():
+    P.pin_block_bwd_autograd(OB.st_block_bwd, BWD_FLAGS)
