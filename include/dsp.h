@@ -269,6 +269,21 @@ int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows
                   void* stream);
 
 /* ------------------------------------------------------------------------
+ * dsp_layernorm_bwd -- gradient of dsp_layernorm with respect to its input
+ * (Eq. 4, 6; used to train the block):
+ *   dx = dres + (dy - mean(dy) - y * mean(dy * y)) / sqrt(var + eps),
+ *   y = (x - mean) / sqrt(var + eps), statistics of x recomputed in fp32.
+ * x: [rows, C] of x_dtype (the forward's input); dy: [rows, C] of dy_dtype;
+ * dres: [rows, C] fp32 gradient already flowing into x (e.g. through a
+ *   residual connection), or NULL; may equal dx (accumulate in place);
+ * dx: [rows, C] fp32.  DEVICE pointers owned by the caller.
+ * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE, DSP_ERR_DTYPE, DSP_ERR_ARG (eps < 0
+ *   or not finite; dx overlapping x, dy, or dres other than in place).
+ * ------------------------------------------------------------------------ */
+int dsp_layernorm_bwd(const void* x, int x_dtype, const void* dy, int dy_dtype, const float* dres, float* dx,
+                      int64_t rows, int C, float eps, void* stream);
+
+/* ------------------------------------------------------------------------
  * dsp_linear -- out = epilogue(a * W + bias)  (Eq. 1 W^O, Eq. 5 W_1/W_2)
  *
  * a:        [M, K] of dtype.
@@ -289,6 +304,44 @@ int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows
 enum { DSP_EPI_NONE = 0, DSP_EPI_GELU = 1, DSP_EPI_RESID = 2, DSP_EPI_F32 = 3, DSP_EPI_RELU = 4 };
 int dsp_linear(const void* a, const void* w, const void* bias, const float* residual, void* out,
                int64_t M, int N, int K, int epilogue, int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Gradients of dsp_linear, y = a * W + bias (W stored [N][K] = [out][in]),
+ * for training the block (the paper trains its models; weak scaling is a
+ * training stage with ZeRO-2).  Chain rule: da = dy * W^T-stored = dy W,
+ * dW = dy^T a, dbias = the column sums of dy.
+ *
+ * dsp_linear_bwd_data -- dx[M][K] = epilogue(dy[M][N] * W[N][K]).
+ *   dy: [M, N] of dtype;  w: [N, K] of dtype (the forward's weight);
+ *   u:  [M, K] of dtype, the saved pre-activation for DSP_GRAD_EPI_GELU_BWD
+ *       (dx = (dy W) * GELU'(u), GELU'(u) = Phi(u) + u phi(u): the backward
+ *       through the MLP's activation, Eq. 5) and DSP_GRAD_EPI_RELU_BWD
+ *       (dx = (dy W) where u > 0, else 0); NULL otherwise;
+ *   dx: [M, K], fp32 for DSP_GRAD_EPI_F32, dtype otherwise.
+ * dsp_linear_bwd_weight -- dw[N][K] = dy^T[N][M] * x[M][K] (fp32) and, when
+ *   db is not NULL, db[N] = sum over m of dy[m][n] (fp32).
+ *   dy: [M, N] of dtype; x: [M, K] of dtype (the forward's input).
+ *   workspace: device memory of at least
+ *   dsp_linear_bwd_weight_workspace_bytes(M, N, K, dtype) bytes (may be NULL
+ *   when that is 0).  The reduction over M is split across work-groups, and
+ *   their fp32 partial sums are added in a fixed order: the result is
+ *   deterministic.
+ * dtype DSP_BF16: bf16 operands on the matrix cores, fp32 accumulation;
+ *   N % 8 == 0 and K % 8 == 0 and 16-byte aligned tensors (DSP_ERR_ALIGN).
+ * dtype DSP_F32: fp32 FMA.
+ * All pointers are DEVICE pointers owned by the caller; outputs must not
+ * overlap inputs (DSP_ERR_ARG).  M == 0: dsp_linear_bwd_data launches
+ * nothing; dsp_linear_bwd_weight writes dw = 0 (and db = 0).
+ * Errors: DSP_ERR_NULL, DSP_ERR_SHAPE (M < 0, N < 1, K < 1, sizes past the
+ *   32-bit tile range), DSP_ERR_DTYPE, DSP_ERR_ALIGN, DSP_ERR_ARG (unknown
+ *   epilogue, overlap), DSP_ERR_WORKSPACE, DSP_ERR_HIP.
+ * ------------------------------------------------------------------------ */
+enum { DSP_GRAD_EPI_F32 = 0, DSP_GRAD_EPI_BF16 = 1, DSP_GRAD_EPI_GELU_BWD = 2, DSP_GRAD_EPI_RELU_BWD = 3 };
+int dsp_linear_bwd_data(const void* dy, const void* w, const void* u, void* dx, int64_t M, int N, int K,
+                        int epilogue, int dtype, void* stream);
+size_t dsp_linear_bwd_weight_workspace_bytes(int64_t M, int N, int K, int dtype);
+int dsp_linear_bwd_weight(const void* dy, const void* x, float* dw, float* db, void* workspace,
+                          size_t ws_bytes, int64_t M, int N, int K, int dtype, void* stream);
 
 /* ------------------------------------------------------------------------
  * The spatial-temporal block: one GPU's share of one layer of the 2D

@@ -11,7 +11,7 @@ binding's functions raises.
 Entry points (see ``include/dsp.h`` for the exact contracts):
 ``dsp_switch``, ``dsp_exchange_unpack``, ``dsp_split``, ``dsp_gather``,
 ``dsp_spatial_attn``, ``dsp_temporal_attn``, ``dsp_attn_strided``,
-``dsp_attn_fwd_lse``, ``dsp_attn_bwd``,
+``dsp_attn_fwd_lse``, ``dsp_attn_bwd``, ``dsp_layernorm_bwd``, ``dsp_linear_bwd_data``, ``dsp_linear_bwd_weight``,
 ``dsp_layernorm``, ``dsp_linear``, ``dsp_st_block_forward``.
 """
 from __future__ import annotations
@@ -29,6 +29,7 @@ DSP_OK, DSP_ERR_NULL, DSP_ERR_DIM, DSP_ERR_SHAPE, DSP_ERR_DTYPE, DSP_ERR_ALIGN, 
 DSP_F32, DSP_BF16 = 0, 1
 DSP_EPI_NONE, DSP_EPI_GELU, DSP_EPI_RESID, DSP_EPI_F32, DSP_EPI_RELU = 0, 1, 2, 3, 4
 DSP_BLOCK_NO_MLP_LN, DSP_BLOCK_ATTN_ONLY, DSP_BLOCK_POST_LN, DSP_BLOCK_RELU = 1, 2, 4, 8
+DSP_GRAD_EPI_F32, DSP_GRAD_EPI_BF16, DSP_GRAD_EPI_GELU_BWD, DSP_GRAD_EPI_RELU_BWD = 0, 1, 2, 3
 
 BLOCK_WEIGHT_FIELDS = ("wqkv_s", "bqkv_s", "wo_s", "bo_s", "wqkv_t", "bqkv_t", "wo_t", "bo_t",
                        "w1", "b1", "w2", "b2")
@@ -65,6 +66,10 @@ _SIGNATURES = {
     "dsp_attn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _I,
                           _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
     "dsp_layernorm": (_I, [_P, _I, _P, _I, _I64, _I, _F, _P]),
+    "dsp_layernorm_bwd": (_I, [_P, _I, _P, _I, _P, _P, _I64, _I, _F, _P]),
+    "dsp_linear_bwd_data": (_I, [_P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
+    "dsp_linear_bwd_weight_workspace_bytes": (_SZ, [_I64, _I, _I, _I]),
+    "dsp_linear_bwd_weight": (_I, [_P, _P, _P, _P, _P, _SZ, _I64, _I, _I, _I, _P]),
     "dsp_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
     "dsp_st_block_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
     "dsp_st_block_forward": (_I, [_P, _P, _c.POINTER(BlockWeights), _P, _SZ, _I64, _I64, _I64, _I,
@@ -387,6 +392,20 @@ def dsp_layernorm(x, eps: float = 1e-6, out=None, out_dtype=None, stream=None):
     return out
 
 
+def dsp_layernorm_bwd(x, dy, eps: float = 1e-6, dres=None, out=None, stream=None):
+    """dx (fp32) = dres + the LayerNorm backward of dy at x (rows of C)."""
+    torch = _torch()
+    _require_device(x, dy, dres, out)
+    x, dy = x.contiguous(), dy.contiguous()
+    C = x.shape[-1]
+    rows = x.numel() // C
+    if out is None:
+        out = torch.empty(x.shape, dtype=torch.float32, device=x.device)
+    _check(lib().dsp_layernorm_bwd(_ptr(x), _dtype_code(x), _ptr(dy), _dtype_code(dy), _ptr(dres), _ptr(out), rows,
+                                   C, float(eps), _stream(stream)), "dsp_layernorm_bwd")
+    return out
+
+
 def dsp_linear(a, w, bias=None, residual=None, epilogue: int = DSP_EPI_NONE, out=None,
                stream=None):
     """out = epilogue(a @ w.T + bias); w stored [N, K]."""
@@ -403,6 +422,42 @@ def dsp_linear(a, w, bias=None, residual=None, epilogue: int = DSP_EPI_NONE, out
                           epilogue, _dtype_code(a), _stream(stream))
     _check(st, "dsp_linear")
     return out
+
+
+def dsp_linear_bwd_data(dy, w, u=None, epilogue: int = DSP_GRAD_EPI_F32, out=None, stream=None):
+    """dx = epilogue(dy @ w) for y = x @ w.T (w stored [N, K]); u: the saved
+    pre-activation for the GELU/ReLU backward epilogues."""
+    torch = _torch()
+    _require_device(dy, w, u, out)
+    dy = dy.contiguous()
+    N, K = w.shape
+    M = dy.numel() // N
+    if out is None:
+        odt = torch.float32 if epilogue == DSP_GRAD_EPI_F32 else dy.dtype
+        out = torch.empty((*dy.shape[:-1], K), dtype=odt, device=dy.device)
+    _check(lib().dsp_linear_bwd_data(_ptr(dy), _ptr(w.contiguous()), _ptr(u), _ptr(out), M, N, K, epilogue,
+                                     _dtype_code(dy), _stream(stream)), "dsp_linear_bwd_data")
+    return out
+
+
+def dsp_linear_bwd_weight(dy, x, with_bias: bool = False, dw=None, db=None, workspace=None, stream=None):
+    """(dw [N, K] fp32, db [N] fp32 or None) for y = x @ w.T + b: dw = dy^T x."""
+    torch = _torch()
+    _require_device(dy, x, dw, db, workspace)
+    dy, x = dy.contiguous(), x.contiguous()
+    N, K = dy.shape[-1], x.shape[-1]
+    M = dy.numel() // N
+    if dw is None:
+        dw = torch.empty((N, K), dtype=torch.float32, device=dy.device)
+    if with_bias and db is None:
+        db = torch.empty(N, dtype=torch.float32, device=dy.device)
+    need = int(lib().dsp_linear_bwd_weight_workspace_bytes(M, N, K, _dtype_code(dy)))
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dy.device)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().dsp_linear_bwd_weight(_ptr(dy), _ptr(x), _ptr(dw), _ptr(db), _ptr(workspace), ws_bytes, M, N, K,
+                                       _dtype_code(dy), _stream(stream)), "dsp_linear_bwd_weight")
+    return dw, db
 
 
 def block_workspace_bytes(B, T, S, C, H, F, dtype_code) -> int:

@@ -474,6 +474,95 @@ int dsp_attn_bwd(const void* q, const void* k, const void* v, const void* o, con
                        scale, dtype, stream);
 }
 
+int dsp_linear_bwd_data(const void* dy, const void* w, const void* u, void* dx, int64_t M, int N, int K,
+                        int epilogue, int dtype, void* stream) {
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
+  if (epilogue < DSP_GRAD_EPI_F32 || epilogue > DSP_GRAD_EPI_RELU_BWD) return DSP_ERR_ARG;
+  const bool act = epilogue == DSP_GRAD_EPI_GELU_BWD || epilogue == DSP_GRAD_EPI_RELU_BWD;
+  if (!w) return DSP_ERR_NULL;
+  if (M == 0) return DSP_OK;
+  if (!dy || !dx || (act && !u)) return DSP_ERR_NULL;
+  int64_t mn, mk, nk;
+  if (!mul_ok(M, N, &mn) || !mul_ok(M, K, &mk) || !mul_ok(N, K, &nk)) return DSP_ERR_SHAPE;
+  const int es = elem_size(dtype);
+  const size_t out_bytes = (size_t)mk * (epilogue == DSP_GRAD_EPI_F32 ? 4 : es);
+  if (overlap(dx, out_bytes, dy, (size_t)mn * es) || overlap(dx, out_bytes, w, (size_t)nk * es) ||
+      (act && overlap(dx, out_bytes, u, (size_t)mk * es)))
+    return DSP_ERR_ARG;
+  hipStream_t s = as_stream(stream);
+  if (dtype == DSP_BF16) {
+    if (N % 8 || K % 8) return DSP_ERR_ALIGN;
+    for (const void* ptr : {dy, w, (const void*)dx, act ? u : w})
+      if (!aligned(ptr, 16)) return DSP_ERR_ALIGN;
+    if (!grad_gemm_fits(M, K, N, N, K)) return DSP_ERR_SHAPE;
+    // dx[m][k] = sum_n dy[m][n] W[n][k]: A = dy as stored, B(k, n) = W[n][k] transposed
+    return launch_gemm_grad(dy, 0, N, w, 1, K, act ? u : nullptr, dx, M, K, N, epilogue, 1, nullptr, s);
+  }
+  if (epilogue == DSP_GRAD_EPI_BF16) return DSP_ERR_ARG;  // fp32 path: fp32 output only
+  return launch_gemm_grad_f32(static_cast<const float*>(dy), 0, N, static_cast<const float*>(w), 1, K,
+                              static_cast<const float*>(act ? u : nullptr), static_cast<float*>(dx), M, K, N,
+                              epilogue, s);
+}
+
+size_t dsp_linear_bwd_weight_workspace_bytes(int64_t M, int N, int K, int dtype) {
+  if (dtype != DSP_BF16 || M <= 0 || N < 1 || K < 1) return 0;
+  const int splits = grad_splits(N, K, M);
+  return splits > 1 ? (size_t)splits * (size_t)N * (size_t)K * 4 : 0;
+}
+
+int dsp_linear_bwd_weight(const void* dy, const void* x, float* dw, float* db, void* workspace,
+                          size_t ws_bytes, int64_t M, int N, int K, int dtype, void* stream) {
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
+  if (!dw || (M > 0 && (!dy || !x))) return DSP_ERR_NULL;
+  int64_t mn, mk, nk;
+  if (!mul_ok(M, N, &mn) || !mul_ok(M, K, &mk) || !mul_ok(N, K, &nk)) return DSP_ERR_SHAPE;
+  const int es = elem_size(dtype);
+  if (overlap(dw, (size_t)nk * 4, dy, (size_t)mn * es) || overlap(dw, (size_t)nk * 4, x, (size_t)mk * es) ||
+      (db && (overlap(db, (size_t)N * 4, dy, (size_t)mn * es) || overlap(db, (size_t)N * 4, dw, (size_t)nk * 4))))
+    return DSP_ERR_ARG;
+  if (!aligned(dw, 16) || (db && !aligned(db, 16))) return DSP_ERR_ALIGN;
+  hipStream_t s = as_stream(stream);
+  if (dtype == DSP_BF16) {
+    if (N % 8 || K % 8) return DSP_ERR_ALIGN;
+    if ((M > 0 && (!aligned(dy, 16) || !aligned(x, 16)))) return DSP_ERR_ALIGN;
+    if (!grad_gemm_fits(N, K, M, N, K)) return DSP_ERR_SHAPE;
+    const size_t need = dsp_linear_bwd_weight_workspace_bytes(M, N, K, dtype);
+    if (need && (!workspace || ws_bytes < need || !aligned(workspace, 16))) return DSP_ERR_WORKSPACE;
+    if (need && (overlap(workspace, need, dw, (size_t)nk * 4) || overlap(workspace, need, dy, (size_t)mn * es) ||
+                 overlap(workspace, need, x, (size_t)mk * es)))
+      return DSP_ERR_ARG;
+    // dw[n][k] = sum_m dy[m][n] x[m][k]: A(n, m) = dy[m][n] and B(k, m) = x[m][k], both transposed
+    const int splits = need ? grad_splits(N, K, M) : 1;
+    int st = launch_gemm_grad(dy, 1, N, x, 1, K, nullptr, dw, N, K, M, DSP_GRAD_EPI_F32, splits,
+                              static_cast<float*>(workspace), s);
+    if (st != DSP_OK || !db) return st;
+    return launch_colsum_bf16(dy, db, M, N, s);
+  }
+  int st = launch_gemm_grad_f32(static_cast<const float*>(dy), 1, N, static_cast<const float*>(x), 1, K, nullptr,
+                                dw, N, K, M, DSP_GRAD_EPI_F32, s);
+  if (st != DSP_OK || !db) return st;
+  return launch_colsum_f32(static_cast<const float*>(dy), db, M, N, s);
+}
+
+int dsp_layernorm_bwd(const void* x, int x_dtype, const void* dy, int dy_dtype, const float* dres, float* dx,
+                      int64_t rows, int C, float eps, void* stream) {
+  if (!valid_dtype(x_dtype) || !valid_dtype(dy_dtype)) return DSP_ERR_DTYPE;
+  if (rows < 0 || C < 1) return DSP_ERR_SHAPE;
+  if (!(eps >= 0.0f) || isinf(eps)) return DSP_ERR_ARG;
+  if (rows == 0) return DSP_OK;
+  if (!x || !dy || !dx) return DSP_ERR_NULL;
+  int64_t n;
+  if (!mul_ok(rows, C, &n) || n > INT64_MAX / 8) return DSP_ERR_SHAPE;
+  const size_t out = (size_t)n * 4;
+  if (overlap(dx, out, x, (size_t)n * elem_size(x_dtype)) || overlap(dx, out, dy, (size_t)n * elem_size(dy_dtype)))
+    return DSP_ERR_ARG;
+  if (dres && dres != dx && overlap(dx, out, dres, out)) return DSP_ERR_ARG;
+  return launch_layernorm_bwd(x, x_dtype == DSP_BF16, dy, dy_dtype == DSP_BF16, dres, dx, rows, C, eps,
+                              as_stream(stream));
+}
+
 int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows, int C, float eps,
                   void* stream) {
   if (!valid_dtype(x_dtype) || !valid_dtype(y_dtype)) return DSP_ERR_DTYPE;

@@ -86,6 +86,23 @@ int launch_attn_bf16_short(const AttnArgs& a, hipStream_t s);
 int launch_layernorm(const void* x, int x_bf16, void* y, int y_bf16, int64_t rows, int C, float eps,
                      hipStream_t s);
 
+// Gradient GEMMs (gemm_grad.hip): out[m][n] = sum_k A(m, k) B(n, k) with
+// A(m, k) = a[m * lda + k] (ta = 0) or a[k * lda + m] (ta = 1), B likewise.
+// epi: DSP_GRAD_EPI_*.  splits > 1 (fp32 output only) uses ws, fp32
+// [splits][M][N].  bf16 needs M, N, K multiples of 8 (checked by the ABI).
+int grad_splits(int64_t M, int64_t N, int64_t K);
+bool grad_gemm_fits(int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb);
+int launch_gemm_grad(const void* a, int ta, int64_t lda, const void* b, int tb, int64_t ldb, const void* aux,
+                     void* out, int64_t M, int64_t N, int64_t K, int epi, int splits, float* ws, hipStream_t s);
+int launch_gemm_grad_f32(const float* a, int ta, int64_t lda, const float* b, int tb, int64_t ldb,
+                         const float* aux, float* out, int64_t M, int64_t N, int64_t K, int epi, hipStream_t s);
+int launch_colsum_bf16(const void* dy, float* db, int64_t M, int N, hipStream_t s);
+int launch_colsum_f32(const float* dy, float* db, int64_t M, int N, hipStream_t s);
+
+// dx = dres (if not null) + the LayerNorm backward of dy at x (layernorm.hip).
+int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16, const float* dres, float* dx,
+                         int64_t rows, int C, float eps, hipStream_t s);
+
 int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s);
 
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,

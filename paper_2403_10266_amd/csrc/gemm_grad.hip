@@ -1,0 +1,426 @@
+// Gradient GEMMs of the block's linear maps (the backward of Eq. 1's W^O, the
+// Q/K/V projections and Eq. 5's W_1, W_2).  With y = x W^T (W stored [out][in],
+// as in the forward), the gradients are
+//   dx = dy W          -- [tokens, in]  = [tokens, out] x [out, in]
+//   dW = dy^T x        -- [out, in]     = [out, tokens] x [tokens, in]
+// so one operand, or both, has its reduction index strided in memory.  This
+// kernel computes out[m][n] = sum_k A(m, k) B(n, k) for either storage of each
+// operand:  A(m, k) = a[m * lda + k] (TA = 0) or a[k * lda + m] (TA = 1), and
+// the same for B with TB.
+//
+// Design for gfx950, on v_mfma_f32_32x32x16_bf16 like the forward GEMM
+// (256 x 128 tiles, 4 waves of 128 x 64, 64-wide k slices through LDS, the next
+// slice prefetched into registers, B rows on the MFMA M side so a lane owns one
+// output row):
+//  * An operand stored with the reduction contiguous keeps the forward's LDS
+//    layout [rows][k] (144-byte rows).  One stored transposed is copied as it
+//    lies, [k][rows] (rows contiguous, 16-byte chunks), and its MFMA fragments
+//    are read with ds_read_b64_tr_b16, which gives each lane 8 k values of one
+//    row in the order {4g..4g+3, 8+4g..8+4g+3} of a 16-k step.  The natural
+//    operand is read in the same k order (two 8-byte reads), so the two sides
+//    of every MFMA agree.
+//  * Split-K: the reduction range is cut into `splits` parts, one per grid z;
+//    each writes fp32 partial sums to its own slab of a workspace and a second
+//    kernel adds the slabs in a fixed order (no atomics: deterministic).  The
+//    weight gradients reduce over all tokens (32768 at the block's size) onto
+//    few output tiles, which is what this is for.
+//  * Epilogues: fp32 output; bf16 output; the GELU / ReLU backward, out =
+//    acc * act'(u) with u the saved pre-activation (bf16), rounded to bf16.
+#include <math.h>
+
+#include "attn_bf16_common.h"
+#include "dsp_internal.h"
+
+namespace dsp {
+namespace {
+
+constexpr int GBM = 256, GBN = 128, GBK = 64;
+constexpr int GNTHR = 256;
+constexpr int NPITCH = GBK + 8;   // natural tiles: 144-byte rows
+
+template <int ROWS>
+struct TPitch {
+  static constexpr int P = ROWS + 8;  // transposed tiles: an odd multiple of 16 bytes
+};
+
+// erf by Abramowitz and Stegun 7.1.26 (|error| <= 1.5e-7)
+__device__ __forceinline__ float erf_as(float z) {
+  const float a = fabsf(z);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  poly *= t;
+  const float e = __builtin_amdgcn_exp2f(-a * a * 1.4426950408889634f);
+  return copysignf(1.0f - poly * e, z);
+}
+
+// d/du (u Phi(u)) = Phi(u) + u phi(u)
+__device__ __forceinline__ float gelu_grad(float u) {
+  const float cdf = 0.5f * (1.0f + erf_as(u * 0.70710678118654752f));
+  const float pdf = 0.3989422804014327f * __builtin_amdgcn_exp2f(-0.5f * u * u * 1.4426950408889634f);
+  return cdf + u * pdf;
+}
+
+struct GradArgs {
+  const bf16* a;
+  const bf16* b;
+  const bf16* aux;  // saved pre-activation for the activation backward epilogues
+  void* out;        // [M][N] (or, with splits > 1, the fp32 workspace [splits][M][N])
+  int64_t lda, ldb;
+  int M, N, K, n_ntiles, n_tiles, k_per_split;
+};
+
+// One operand's tile of one k slice: global -> registers -> LDS, and its MFMA
+// fragments.  ROWS = tile rows on the M or N side (256 or 128).
+template <int ROWS, bool TRANS>
+struct Operand {
+  static constexpr int CHUNKS = ROWS * GBK / 8;    // 16-byte chunks per slice
+  static constexpr int LOADS = CHUNKS / GNTHR;
+  static constexpr int ELEMS = TRANS ? GBK * TPitch<ROWS>::P : ROWS * NPITCH;
+  static_assert(CHUNKS % GNTHR == 0, "loader shape");
+
+  const bf16* base;
+  int64_t ld;
+  int r0, rows_valid, k_total;
+  u32x4 pre[LOADS];
+  uint32_t off[LOADS];
+  int lds_off[LOADS];
+  bool col_ok[LOADS];
+
+  __device__ void init(const bf16* p, int64_t ld_, int r0_, int rows_total, int k_total_) {
+    base = p;
+    ld = ld_;
+    r0 = r0_;
+    rows_valid = min(ROWS, rows_total - r0_);
+    k_total = k_total_;
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      if (!TRANS) {
+        // chunk (row t/8 + 32 i, k columns 8 (t % 8) .. + 7)
+        const int row = (t >> 3) + 32 * i, kc = t & 7;
+        off[i] = (uint32_t)row * (uint32_t)(ld * 2) + (uint32_t)kc * 16u;
+        lds_off[i] = row * NPITCH + kc * 8;
+        col_ok[i] = true;
+      } else {
+        // chunk (k row r, columns 8 c .. + 7), ROWS / 8 chunks per k row
+        constexpr int CPR = ROWS / 8;
+        const int c = t % CPR, r = t / CPR + (GNTHR / CPR) * i;
+        off[i] = (uint32_t)r * (uint32_t)(ld * 2) + (uint32_t)c * 16u;
+        lds_off[i] = r * TPitch<ROWS>::P + c * 8;
+        col_ok[i] = 8 * c < rows_valid;
+      }
+    }
+  }
+
+  // loads the slice starting at reduction index k0 (rows / k past the end read zero)
+  __device__ void load(int k0) {
+    if (!TRANS) {
+      const __amdgpu_buffer_rsrc_t rs =
+          make_rsrc(base + (int64_t)r0 * ld, (uint32_t)max(rows_valid, 0) * (uint32_t)(ld * 2));
+      const bool kin = k0 + 8 * (int)(threadIdx.x & 7) < k_total;
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i)
+        pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, kin ? off[i] + (uint32_t)k0 * 2u : 0xFFFFFFF0u, 0, 0);
+    } else {
+      const int krows = max(0, min(GBK, k_total - k0));
+      const __amdgpu_buffer_rsrc_t rs =
+          make_rsrc(base + (int64_t)k0 * ld + r0, (uint32_t)krows * (uint32_t)(ld * 2));
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i)
+        pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, col_ok[i] ? off[i] : 0xFFFFFFF0u, 0, 0);
+    }
+  }
+
+  __device__ void store(bf16* lds) const {
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) *reinterpret_cast<u32x4*>(lds + lds_off[i]) = pre[i];
+  }
+
+  // fragment of tile rows rbase .. rbase + 31 for 16-k step ks: lane
+  // (l32 + 32g) gets row rbase + l32 at k = 16 ks + {4g..4g+3, 8+4g..8+4g+3}
+  __device__ static bf16x8 frag(const bf16* lds, int rbase, int ks, int lane) {
+    const int l32 = lane & 31, g = lane >> 5;
+    if (!TRANS) {
+      const bf16* row = lds + (rbase + l32) * NPITCH + 16 * ks + 4 * g;
+      const shortx4 lo = *reinterpret_cast<const shortx4*>(row);
+      const shortx4 hi = *reinterpret_cast<const shortx4*>(row + 8);
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    } else {
+      constexpr int P = TPitch<ROWS>::P;
+      const int j16 = lane & 15, mbase = 16 * ((lane >> 4) & 1);
+      const int row = 16 * ks + 4 * g + (j16 >> 2);
+      const int col = rbase + mbase + 4 * (j16 & 3);
+      const shortx4 lo = lds_read_tr(lds + row * P + col);
+      const shortx4 hi = lds_read_tr(lds + (row + 8) * P + col);
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+  }
+};
+
+template <bool TA, bool TB, int EPI>
+__global__ __launch_bounds__(GNTHR, 2) void gemm_grad_kernel(GradArgs p) {
+  using OA = Operand<GBM, TA>;
+  using OB = Operand<GBN, TB>;
+  __shared__ __attribute__((aligned(16))) bf16 As[OA::ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16 Bs[OB::ELEMS];
+
+  // XCD-aware order (tiles m-major, n fastest; each XCD a contiguous range)
+  uint32_t bid = blockIdx.x;
+  if ((p.n_tiles & 7) == 0) bid = (bid & 7u) * ((uint32_t)p.n_tiles >> 3) + (bid >> 3);
+  const int mt = bid / p.n_ntiles;
+  const int nt = bid - mt * p.n_ntiles;
+  const int m0 = mt * GBM, n0 = nt * GBN;
+  const int kb = blockIdx.z * p.k_per_split;
+  const int ke = min(p.K, kb + p.k_per_split);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int l32 = lane & 31, g = lane >> 5;
+
+  OA a;
+  OB b;
+  a.init(p.a, p.lda, m0, p.M, ke);
+  b.init(p.b, p.ldb, n0, p.N, ke);
+
+  floatx16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = (ke - kb + GBK - 1) / GBK;
+  if (nk > 0) {
+    a.load(kb);
+    b.load(kb);
+    a.store(As);
+    b.store(Bs);
+  }
+  __syncthreads();
+  for (int it = 0; it < nk; ++it) {
+    const bool more = it + 1 < nk;
+    if (more) {
+      a.load(kb + (it + 1) * GBK);
+      b.load(kb + (it + 1) * GBK);
+    }
+#pragma unroll
+    for (int ks = 0; ks < GBK / 16; ++ks) {
+      bf16x8 af[4], bfr[2];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) af[j] = OA::frag(As, wm * 128 + 32 * j, ks, lane);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) bfr[i] = OB::frag(Bs, wn * 64 + 32 * i, ks, lane);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[i], af[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) {
+      __syncthreads();
+      a.store(As);
+      b.store(Bs);
+      __syncthreads();
+    }
+  }
+
+  // epilogue: lane owns row m = .. + l32 and columns n = .. + 8 r4 + 4g + {0..3}
+  const int64_t slab = (int64_t)blockIdx.z * p.M * p.N;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int m = m0 + wm * 128 + 32 * j + l32;
+    if (m >= p.M) continue;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int n = n0 + wn * 64 + 32 * i + 8 * r4 + 4 * g;
+        if (n >= p.N) continue;   // N % 4 == 0: the group of 4 is whole
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * r4 + e];
+        const int64_t off = (int64_t)m * p.N + n;
+        if (EPI == DSP_GRAD_EPI_F32) {
+          *reinterpret_cast<float4*>(static_cast<float*>(p.out) + slab + off) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          if (EPI == DSP_GRAD_EPI_GELU_BWD || EPI == DSP_GRAD_EPI_RELU_BWD) {
+            const uint2 uw = *reinterpret_cast<const uint2*>(p.aux + off);
+            const bf16x2 u01 = __builtin_bit_cast(bf16x2, uw.x), u23 = __builtin_bit_cast(bf16x2, uw.y);
+            const float u[4] = {(float)u01[0], (float)u01[1], (float)u23[0], (float)u23[1]};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              v[e] *= EPI == DSP_GRAD_EPI_GELU_BWD ? gelu_grad(u[e]) : (u[e] > 0.0f ? 1.0f : 0.0f);
+          }
+          bf16x2 lo = {(bf16)v[0], (bf16)v[1]};
+          bf16x2 hi = {(bf16)v[2], (bf16)v[3]};
+          uint2 w;
+          w.x = __builtin_bit_cast(uint32_t, lo);
+          w.y = __builtin_bit_cast(uint32_t, hi);
+          *reinterpret_cast<uint2*>(static_cast<bf16*>(p.out) + off) = w;
+        }
+      }
+  }
+}
+
+// out[i] = sum over z of ws[z][i], z in order (deterministic)
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float4* __restrict__ ws, float4* out,
+                                                            int64_t n4, int splits) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  float4 s = ws[i];
+  for (int z = 1; z < splits; ++z) {
+    const float4 v = ws[(int64_t)z * n4 + i];
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  out[i] = s;
+}
+
+// db[n] = sum over rows m of dy[m][n] (fp32), one thread per column group of 4,
+// rows in order (deterministic)
+__global__ __launch_bounds__(256) void colsum_bf16_kernel(const bf16* __restrict__ dy, float* db, int64_t M,
+                                                          int N) {
+  const int n4 = blockIdx.x * blockDim.x + threadIdx.x;
+  if (4 * n4 >= N) return;
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int64_t m = 0; m < M; ++m) {
+    const uint2 w = *reinterpret_cast<const uint2*>(dy + m * N + 4 * n4);
+    const bf16x2 a = __builtin_bit_cast(bf16x2, w.x), b = __builtin_bit_cast(bf16x2, w.y);
+    s[0] += (float)a[0];
+    s[1] += (float)a[1];
+    s[2] += (float)b[0];
+    s[3] += (float)b[1];
+  }
+  *reinterpret_cast<float4*>(db + 4 * n4) = make_float4(s[0], s[1], s[2], s[3]);
+}
+
+template <bool TA, bool TB, int EPI>
+int launch_grad(const GradArgs& p0, int splits, float* ws, hipStream_t s) {
+  GradArgs p = p0;
+  const int64_t n_mt = (p.M + GBM - 1) / GBM, n_nt = (p.N + GBN - 1) / GBN;
+  const int64_t tiles = n_mt * n_nt;
+  p.n_ntiles = (int)n_nt;
+  p.n_tiles = (int)tiles;
+  p.k_per_split = ((p.K + splits - 1) / splits + GBK - 1) / GBK * GBK;
+  void* final_out = p.out;
+  if (splits > 1) p.out = ws;
+  hipLaunchKernelGGL((gemm_grad_kernel<TA, TB, EPI>), dim3((uint32_t)tiles, 1, (uint32_t)splits), dim3(GNTHR),
+                     0, s, p);
+  int st = last_launch_status();
+  if (st != DSP_OK || splits == 1) return st;
+  const int64_t n4 = (int64_t)p.M * p.N / 4;
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((uint32_t)((n4 + 255) / 256)), dim3(256), 0, s,
+                     reinterpret_cast<const float4*>(ws), reinterpret_cast<float4*>(final_out), n4, splits);
+  return last_launch_status();
+}
+
+// fp32 path: out[m][n] = sum_k A(m, k) B(n, k) with the same storage choices,
+// plain FMA, one thread per output (small problems and checks)
+__global__ __launch_bounds__(256) void gemm_grad_f32_kernel(const float* a, int ta, int64_t lda, const float* b,
+                                                            int tb, int64_t ldb, const float* aux, float* out,
+                                                            int64_t M, int64_t N, int64_t K, int epi) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M * N) return;
+  const int64_t m = i / N, n = i % N;
+  float s = 0.0f;
+  for (int64_t k = 0; k < K; ++k) {
+    const float av = ta ? a[k * lda + m] : a[m * lda + k];
+    const float bv = tb ? b[k * ldb + n] : b[n * ldb + k];
+    s = fmaf(av, bv, s);
+  }
+  if (epi == DSP_GRAD_EPI_GELU_BWD) {
+    const float u = aux[i];
+    s *= 0.5f * (1.0f + erff(u * 0.70710678118654752f)) + u * 0.3989422804014327f * expf(-0.5f * u * u);
+  } else if (epi == DSP_GRAD_EPI_RELU_BWD) {
+    s = aux[i] > 0.0f ? s : 0.0f;
+  }
+  out[i] = s;
+}
+
+__global__ __launch_bounds__(256) void colsum_f32_kernel(const float* __restrict__ dy, float* db, int64_t M,
+                                                         int N) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  float s = 0.0f;
+  for (int64_t m = 0; m < M; ++m) s += dy[m * N + n];
+  db[n] = s;
+}
+
+}  // namespace
+
+int launch_gemm_grad_f32(const float* a, int ta, int64_t lda, const float* b, int tb, int64_t ldb,
+                         const float* aux, float* out, int64_t M, int64_t N, int64_t K, int epi, hipStream_t s) {
+  const int64_t total = M * N;
+  if (total == 0) return DSP_OK;
+  const int64_t blocks = (total + 255) / 256;
+  if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
+  hipLaunchKernelGGL(gemm_grad_f32_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, a, ta, lda, b, tb, ldb, aux,
+                     out, M, N, K, epi);
+  return last_launch_status();
+}
+
+int launch_colsum_f32(const float* dy, float* db, int64_t M, int N, hipStream_t s) {
+  if (N == 0) return DSP_OK;
+  hipLaunchKernelGGL(colsum_f32_kernel, dim3((uint32_t)((N + 255) / 256)), dim3(256), 0, s, dy, db, M, N);
+  return last_launch_status();
+}
+
+int grad_splits(int64_t M, int64_t N, int64_t K) {
+  // enough work-groups to fill 256 CUs twice, slices of at least 2048
+  const int64_t tiles = ((M + GBM - 1) / GBM) * ((N + GBN - 1) / GBN);
+  int64_t s = 1;
+  while (tiles * s < 512 && K / (2 * s) >= 2048 && s < 16) s *= 2;
+  return (int)s;
+}
+
+bool grad_gemm_fits(int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb) {
+  // 32-bit tile offsets: GBM (or GBK) rows of a row stride in bytes
+  return M < (int64_t(1) << 31) && N < (int64_t(1) << 31) && K < (int64_t(1) << 31) &&
+         (int64_t)GBM * lda * 2 < (int64_t(1) << 31) && (int64_t)GBM * ldb * 2 < (int64_t(1) << 31) &&
+         ((M + GBM - 1) / GBM) * ((N + GBN - 1) / GBN) < (int64_t(1) << 31);
+}
+
+int launch_gemm_grad(const void* a, int ta, int64_t lda, const void* b, int tb, int64_t ldb, const void* aux,
+                     void* out, int64_t M, int64_t N, int64_t K, int epi, int splits, float* ws, hipStream_t s) {
+  if (M == 0 || N == 0) return DSP_OK;
+  GradArgs p;
+  p.a = static_cast<const bf16*>(a);
+  p.b = static_cast<const bf16*>(b);
+  p.aux = static_cast<const bf16*>(aux);
+  p.out = out;
+  p.lda = lda;
+  p.ldb = ldb;
+  p.M = (int)M;
+  p.N = (int)N;
+  p.K = (int)K;
+#define DSP_GRAD_CASE(TA_, TB_)                                                                    \
+  if (ta == TA_ && tb == TB_) {                                                                   \
+    switch (epi) {                                                                                \
+      case DSP_GRAD_EPI_F32: return launch_grad<TA_, TB_, DSP_GRAD_EPI_F32>(p, splits, ws, s);    \
+      case DSP_GRAD_EPI_BF16: return launch_grad<TA_, TB_, DSP_GRAD_EPI_BF16>(p, 1, ws, s);       \
+      case DSP_GRAD_EPI_GELU_BWD: return launch_grad<TA_, TB_, DSP_GRAD_EPI_GELU_BWD>(p, 1, ws, s); \
+      case DSP_GRAD_EPI_RELU_BWD: return launch_grad<TA_, TB_, DSP_GRAD_EPI_RELU_BWD>(p, 1, ws, s); \
+      default: return DSP_ERR_ARG;                                                                \
+    }                                                                                             \
+  }
+  DSP_GRAD_CASE(0, 1)
+  DSP_GRAD_CASE(1, 1)
+  DSP_GRAD_CASE(0, 0)
+  DSP_GRAD_CASE(1, 0)
+#undef DSP_GRAD_CASE
+  return DSP_ERR_ARG;
+}
+
+int launch_colsum_bf16(const void* dy, float* db, int64_t M, int N, hipStream_t s) {
+  if (N == 0) return DSP_OK;
+  const int groups = (N + 3) / 4;
+  hipLaunchKernelGGL(colsum_bf16_kernel, dim3((uint32_t)((groups + 255) / 256)), dim3(256), 0, s,
+                     static_cast<const bf16*>(dy), db, M, N);
+  return last_launch_status();
+}
+
+}  // namespace dsp

@@ -90,6 +90,86 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_long_kernel(
   for (int c = lane; c < C; c += 64) store_elem(y, base + c, (load_elem(x, base + c, x_bf) - mean) * rstd, y_bf);
 }
 
+// Backward: with y = (x - mean) / sigma, dx = dres + (dy - mean(dy) - y mean(dy y)) / sigma.
+// One wave per row: x and dy held in registers, the statistics of x recomputed
+// in fp32 as in the forward, then two row means of the upstream gradient.
+template <int VPL>
+__global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_kernel(
+    const void* __restrict__ x, int x_bf, const void* __restrict__ dy, int dy_bf, const float* dres,
+    float* dx, int64_t rows, int C, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int64_t base = row * C;
+  float v[VPL], g[VPL];
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int c = lane + 64 * i;
+    v[i] = c < C ? load_elem(x, base + c, x_bf) : 0.0f;
+    g[i] = c < C ? load_elem(dy, base + c, dy_bf) : 0.0f;
+    s += v[i];
+  }
+  const float mean = wave_sum(s) / (float)C;
+  float ss = 0.0f;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int c = lane + 64 * i;
+    const float d = c < C ? v[i] - mean : 0.0f;
+    ss = fmaf(d, d, ss);
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(ss) / (float)C + eps);
+  float sg = 0.0f, sgy = 0.0f;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    v[i] = (v[i] - mean) * rstd;  // y (0 past C: g is 0 there too)
+    sg += g[i];
+    sgy = fmaf(g[i], v[i], sgy);
+  }
+  const float mg = wave_sum(sg) / (float)C, mgy = wave_sum(sgy) / (float)C;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int c = lane + 64 * i;
+    if (c < C) {
+      float d = (g[i] - mg - v[i] * mgy) * rstd;
+      if (dres) d += dres[base + c];
+      dx[base + c] = d;
+    }
+  }
+}
+
+// Rows longer than the register budget: passes over global memory.
+__global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_long_kernel(
+    const void* __restrict__ x, int x_bf, const void* __restrict__ dy, int dy_bf, const float* dres,
+    float* dx, int64_t rows, int C, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int64_t base = row * C;
+  float s = 0.0f;
+  for (int c = lane; c < C; c += 64) s += load_elem(x, base + c, x_bf);
+  const float mean = wave_sum(s) / (float)C;
+  float ss = 0.0f;
+  for (int c = lane; c < C; c += 64) {
+    const float d = load_elem(x, base + c, x_bf) - mean;
+    ss = fmaf(d, d, ss);
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(ss) / (float)C + eps);
+  float sg = 0.0f, sgy = 0.0f;
+  for (int c = lane; c < C; c += 64) {
+    const float gv = load_elem(dy, base + c, dy_bf);
+    sg += gv;
+    sgy = fmaf(gv, (load_elem(x, base + c, x_bf) - mean) * rstd, sgy);
+  }
+  const float mg = wave_sum(sg) / (float)C, mgy = wave_sum(sgy) / (float)C;
+  for (int c = lane; c < C; c += 64) {
+    const float yv = (load_elem(x, base + c, x_bf) - mean) * rstd;
+    float d = (load_elem(dy, base + c, dy_bf) - mg - yv * mgy) * rstd;
+    if (dres) d += dres[base + c];
+    dx[base + c] = d;
+  }
+}
+
 __global__ __launch_bounds__(256) void cast_kernel(const void* __restrict__ x, int x_bf,
                                                    void* __restrict__ y, int y_bf, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -98,6 +178,26 @@ __global__ __launch_bounds__(256) void cast_kernel(const void* __restrict__ x, i
 }
 
 }  // namespace
+
+int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16, const float* dres, float* dx,
+                         int64_t rows, int C, float eps, hipStream_t s) {
+  if (rows == 0) return DSP_OK;
+  const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
+  if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
+  const dim3 grid((uint32_t)blocks), block(64 * kRowsPerBlock);
+  const int vpl = (C + 63) / 64;
+  if (vpl <= 4) {
+    hipLaunchKernelGGL(layernorm_bwd_kernel<4>, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C, eps);
+  } else if (vpl <= 8) {
+    hipLaunchKernelGGL(layernorm_bwd_kernel<8>, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C, eps);
+  } else if (vpl <= 18) {
+    hipLaunchKernelGGL(layernorm_bwd_kernel<18>, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C, eps);
+  } else {
+    hipLaunchKernelGGL(layernorm_bwd_long_kernel, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C,
+                       eps);
+  }
+  return last_launch_status();
+}
 
 // Element-wise format conversion (fp32 <-> bf16, round to nearest even).
 int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s) {

@@ -228,6 +228,52 @@ def test_attn_bwd_validation(lib):
     assert call(L=0) == dsp.DSP_OK
 
 
+def test_linear_bwd_validation(lib):
+    A = 2 ** 24
+    data = lambda dy=FAKE, w=FAKE + A, u=None, dx=FAKE + 2 * A, M=64, N=72, K=136, epi=0, dt=1: \
+        lib.dsp_linear_bwd_data(dy, w, u, dx, M, N, K, epi, dt, None)
+    assert data(w=None) == dsp.DSP_ERR_NULL
+    assert data(dy=None) == dsp.DSP_ERR_NULL
+    assert data(epi=2) == dsp.DSP_ERR_NULL                      # GELU backward needs u
+    assert data(epi=7) == dsp.DSP_ERR_ARG
+    assert data(dt=0, epi=1) == dsp.DSP_ERR_ARG                  # fp32 path: fp32 output only
+    assert data(dt=5) == dsp.DSP_ERR_DTYPE
+    assert data(N=0) == dsp.DSP_ERR_SHAPE
+    assert data(M=-1) == dsp.DSP_ERR_SHAPE
+    assert data(N=70) == dsp.DSP_ERR_ALIGN
+    assert data(K=130) == dsp.DSP_ERR_ALIGN
+    assert data(dy=MIS) == dsp.DSP_ERR_ALIGN
+    assert data(dx=FAKE + 64) == dsp.DSP_ERR_ARG                 # dx overlaps dy
+    assert data(M=0, dy=None, dx=None) == dsp.DSP_OK
+    ws_need = lib.dsp_linear_bwd_weight_workspace_bytes(32768, 3456, 1152, 1)
+    assert ws_need > 0 and lib.dsp_linear_bwd_weight_workspace_bytes(32768, 3456, 1152, 0) == 0
+    wgt = lambda dy=FAKE, x=FAKE + A, dw=FAKE + 2 * A, db=None, ws=None, wsb=0, M=64, N=72, K=136, dt=1: \
+        lib.dsp_linear_bwd_weight(dy, x, dw, db, ws, wsb, M, N, K, dt, None)
+    assert wgt(dw=None) == dsp.DSP_ERR_NULL
+    assert wgt(x=None) == dsp.DSP_ERR_NULL
+    assert wgt(dt=4) == dsp.DSP_ERR_DTYPE
+    assert wgt(K=0) == dsp.DSP_ERR_SHAPE
+    assert wgt(N=12) == dsp.DSP_ERR_ALIGN
+    assert wgt(dw=FAKE + 2 * A + 4) == dsp.DSP_ERR_ALIGN
+    assert wgt(db=FAKE + 2 * A) == dsp.DSP_ERR_ARG                # db overlaps dw
+    big = dict(M=32768, N=3456, K=1152, dy=2 ** 36, x=2 ** 37, dw=2 ** 38)
+    assert wgt(**big) == dsp.DSP_ERR_WORKSPACE
+    assert wgt(ws=2 ** 39, wsb=ws_need - 16, **big) == dsp.DSP_ERR_WORKSPACE
+
+
+def test_layernorm_bwd_validation(lib):
+    f = lambda x=FAKE, xd=0, dy=FAKE2, dyd=1, dres=None, dx=FAKE2 + 2 ** 24, rows=4, C=8, eps=1e-6: \
+        lib.dsp_layernorm_bwd(x, xd, dy, dyd, dres, dx, rows, C, eps, None)
+    assert f(x=None) == dsp.DSP_ERR_NULL
+    assert f(dx=None) == dsp.DSP_ERR_NULL
+    assert f(dyd=2) == dsp.DSP_ERR_DTYPE
+    assert f(C=0) == dsp.DSP_ERR_SHAPE
+    assert f(eps=float("nan")) == dsp.DSP_ERR_ARG
+    assert f(dx=FAKE + 4) == dsp.DSP_ERR_ARG                      # dx overlaps x
+    assert f(dres=FAKE2 + 2 ** 24 + 4) == dsp.DSP_ERR_ARG          # dres partly overlaps dx
+    assert f(rows=0, x=None) == dsp.DSP_OK
+
+
 def test_layernorm_validation(lib):
     f = lambda x=FAKE, xd=1, y=FAKE2, yd=1, rows=4, C=8, eps=1e-6: lib.dsp_layernorm(
         x, xd, y, yd, rows, C, eps, None)
