@@ -25,6 +25,10 @@ and, timed separately after the steps (not part of a step):
             spatial and temporal workloads, given o and the row log-sum-exp
             from dsp_attn_fwd_lse; counted as 10 L^2 D flops per unit (the
             five L x L x D products of the gradient)
+  block_train_fwd / block_bwd  dsp_st_block_forward_train (the block keeping
+            its activations) and dsp_st_block_backward (dx and every weight
+            gradient) on the block workload; the backward counted as twice
+            the forward's GEMM flops (dx and dW) plus 10 L^2 D per attention unit
 
 The headline value is the combined attention throughput
 (F_spatial + F_temporal) / (t_spatial + t_temporal) in TFLOP/s with
@@ -70,7 +74,7 @@ def parse():
     ap.add_argument("--only", default=None,
                     choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange",
                              "temporal_strided", "switch_k3", "split", "gather", "copy",
-                             "attn_bwd_spatial", "attn_bwd_temporal"],
+                             "attn_bwd_spatial", "attn_bwd_temporal", "block_train_fwd", "block_bwd"],
                     help="run a single part (for profiling); prints per-kernel times only. "
                          "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
                          "plain 604 MB copy used to calibrate traffic counters")
@@ -100,7 +104,10 @@ def main():
                          W["temporal_bf16_B2_S512_T128"], W["block_bf16_B1_T32_S1024"])
     wanted = {args.only} if args.only else {"switch", "spatial", "temporal", "block", "exchange",
                                             "temporal_strided", "switch_k3", "split", "gather",
-                                            "attn_bwd_spatial", "attn_bwd_temporal"}
+                                            "attn_bwd_spatial", "attn_bwd_temporal", "block_train_fwd",
+                                            "block_bwd"}
+    if wanted & {"block_train_fwd", "block_bwd"}:
+        wanted.add("block")
     if "attn_bwd_spatial" in wanted:
         wanted.add("spatial")
     if "attn_bwd_temporal" in wanted:
@@ -166,6 +173,13 @@ def main():
         ws_bytes = dsp.block_workspace_bytes(wbl.B, wbl.T, wbl.S, wbl.C, wbl.H, wbl.F, dsp.DSP_BF16)
         t["ws_bl"] = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
         del x_bl_np, p_bl
+    if wanted & {"block_train_fwd", "block_bwd"}:
+        gen = torch.Generator(device=dev).manual_seed(wbl.seed + 100)
+        t["dy_bl"] = torch.randn((wbl.B, wbl.S, wbl.T, wbl.C), generator=gen, device=dev)
+        t["y_tr"], t["sv_bl"] = dsp.dsp_st_block_forward_train(t["x_bl"], t["w_bl"], wbl.H)
+        t["dx_bl"], t["g_bl"] = dsp.dsp_st_block_backward(t["x_bl"], t["dy_bl"], t["w_bl"], t["sv_bl"], wbl.H)
+        t["bws_bl"] = torch.empty(int(dsp.lib().dsp_st_block_backward_workspace_bytes(
+            wbl.B, wbl.T, wbl.S, wbl.C, wbl.H, wbl.F, dsp.DSP_BF16)), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
 
     def run_switch():
@@ -209,6 +223,13 @@ def main():
     def run_attn_bwd_temporal():
         run_bwd("tp", wtp)
 
+    def run_block_train_fwd():
+        dsp.dsp_st_block_forward_train(t["x_bl"], t["w_bl"], wbl.H, out=t["y_tr"], saved=t["sv_bl"])
+
+    def run_block_bwd():
+        dsp.dsp_st_block_backward(t["x_bl"], t["dy_bl"], t["w_bl"], t["sv_bl"], wbl.H, dx=t["dx_bl"],
+                                  grads=t["g_bl"], workspace=t["bws_bl"])
+
     def run_copy():
         dsp.dsp_switch(t["x_sw"], 1, 1, 1, out=t["y_sw"].view(t["x_sw"].shape))
 
@@ -217,7 +238,8 @@ def main():
     # timed on its own after the steps: not a step of the single-GPU hot path
     extras = [("exchange", run_exchange), ("temporal_strided", run_temporal_strided),
               ("switch_k3", run_switch_k3), ("split", run_split), ("gather", run_gather),
-              ("attn_bwd_spatial", run_attn_bwd_spatial), ("attn_bwd_temporal", run_attn_bwd_temporal)]
+              ("attn_bwd_spatial", run_attn_bwd_spatial), ("attn_bwd_temporal", run_attn_bwd_temporal),
+              ("block_train_fwd", run_block_train_fwd), ("block_bwd", run_block_bwd)]
     if args.only:
         every = dict(parts + extras)
         parts, extras = [(args.only, run_copy if args.only == "copy" else every[args.only])], []
@@ -263,8 +285,10 @@ def main():
     tp_bytes_all = tp_bytes
     tok = wbl.B * wbl.T * wbl.S
     C, F = wbl.C, wbl.F
-    F_bl = (2.0 * tok * C * (3 * C) * 2 + 2.0 * tok * C * C * 2 + 2.0 * tok * C * F * 2
-            + attn_flops(wbl.B * wbl.T * wbl.H, wbl.S, wbl.D) + attn_flops(wbl.B * wbl.S * wbl.H, wbl.T, wbl.D))
+    F_gemm = 2.0 * tok * C * (3 * C) * 2 + 2.0 * tok * C * C * 2 + 2.0 * tok * C * F * 2
+    F_att = attn_flops(wbl.B * wbl.T * wbl.H, wbl.S, wbl.D) + attn_flops(wbl.B * wbl.S * wbl.H, wbl.T, wbl.D)
+    F_bl = F_gemm + F_att
+    F_bl_bwd = 2.0 * F_gemm + 2.5 * F_att
 
     sp_tflops = F_sp / (ms["spatial"] * 1e-3) / 1e12
     tp_tflops = F_tp / (ms["temporal"] * 1e-3) / 1e12
@@ -298,7 +322,8 @@ def main():
                         "chunks; 8-rank exchange+unpack of such shards; the shard as 1x64x64x64x1152 "
                         "switched T->H (K=3); split along S / gather along T of 8 shards; spatial attn B2 T16 S4096 H16 D72; "
                         "temporal attn B2 S512 T128 H16 D72; ST block B1 T32 S1024 C1152 H16 F4608; "
-                        "attention backward of the spatial and temporal workloads",
+                        "attention backward of the spatial and temporal workloads; training forward and "
+                        "backward of the ST block",
             "attn_frac_mfma_peak": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
             "switch_GBps": round(sw_gbps, 1),
             "switch_frac_hbm_peak": round(sw_gbps / HBM_PEAK_GBPS, 4),
@@ -317,6 +342,8 @@ def main():
             "block_TFLOPs": round(F_bl / (ms["block"] * 1e-3) / 1e12, 2),
             "attn_bwd_spatial_TFLOPs": round(2.5 * F_sp / (ms["attn_bwd_spatial"] * 1e-3) / 1e12, 2),
             "attn_bwd_temporal_TFLOPs": round(2.5 * F_tp / (ms["attn_bwd_temporal"] * 1e-3) / 1e12, 2),
+            "block_train_fwd_TFLOPs": round(F_bl / (ms["block_train_fwd"] * 1e-3) / 1e12, 2),
+            "block_bwd_TFLOPs": round(F_bl_bwd / (ms["block_bwd"] * 1e-3) / 1e12, 2),
             "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
         },
         "roofline": {

@@ -385,6 +385,47 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
                          void* workspace, size_t ws_bytes, int64_t B, int64_t T, int64_t S, int C,
                          int H, int F, float ln_eps, int flags, int dtype, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Training the block: a forward that keeps its activations, and the backward.
+ * The paper trains its models (weak scaling as a training stage, ZeRO-2), so
+ * every step of the block has a gradient: the chain rule through LayerNorm,
+ * the linear maps and the MLP activation, attention along each sequence
+ * dimension (Eq. 3 per head), and the Switch, whose adjoint is the switch
+ * back (S -> T).
+ *
+ * dsp_st_block_forward_train -- dsp_st_block_forward (same x, y, w, sizes,
+ *   eps and dtype) that writes the activations the backward needs into
+ *   `saved`: DEVICE memory of at least dsp_st_block_train_saved_bytes(...)
+ *   bytes, 256-byte aligned, owned by the caller (1.7 GB at B1 T32 S1024
+ *   C1152 F4608 in bf16).  Flags: 0, DSP_BLOCK_NO_MLP_LN, DSP_BLOCK_RELU (the
+ *   pre-LN blocks); post-LN and the projection-only chain give DSP_ERR_ARG.
+ * dsp_st_block_backward -- given the forward's x (B,T,S,C), its saved
+ *   activations, and dy (B,S,T,C) = dL/dy, writes dx = dL/dx (B,T,S,C, fp32)
+ *   and the weight gradients into `grads`: fp32 arrays shaped like the weights
+ *   (stored [out][in]), required for the six weights; bias gradients are
+ *   written where the pointer is not NULL (whether or not the forward used a
+ *   bias).  workspace: DEVICE scratch of at least
+ *   dsp_st_block_backward_workspace_bytes(...) bytes, 256-byte aligned.
+ *   Gradients are deterministic (no atomics).  bf16: the operands of every
+ *   product are bf16 (gradients rounded to bf16 where they enter a product),
+ *   accumulation and the residual-stream gradient are fp32.
+ * Errors: as dsp_st_block_forward, plus DSP_ERR_WORKSPACE (saved or
+ *   workspace missing or too small) and DSP_ERR_ARG (unsupported flags,
+ *   overlapping buffers).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  float *wqkv_s, *bqkv_s, *wo_s, *bo_s, *wqkv_t, *bqkv_t, *wo_t, *bo_t, *w1, *b1, *w2, *b2;
+} dsp_block_grads_t;
+size_t dsp_st_block_train_saved_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype);
+size_t dsp_st_block_backward_workspace_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype);
+int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_block_weights_t* w, void* saved,
+                               size_t saved_bytes, int64_t B, int64_t T, int64_t S, int C, int H, int F,
+                               float ln_eps, int flags, int dtype, void* stream);
+int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_block_weights_t* w,
+                          const void* saved, size_t saved_bytes, void* workspace, size_t ws_bytes, float* dx_BTSC,
+                          const dsp_block_grads_t* grads, int64_t B, int64_t T, int64_t S, int C, int H, int F,
+                          float ln_eps, int flags, int dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

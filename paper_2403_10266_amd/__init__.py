@@ -45,6 +45,10 @@ class BlockWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_WEIGHT_FIELDS]
 
 
+class BlockGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_WEIGHT_FIELDS]
+
+
 _lib = None
 
 _c = ctypes
@@ -72,6 +76,12 @@ _SIGNATURES = {
     "dsp_linear_bwd_weight": (_I, [_P, _P, _P, _P, _P, _SZ, _I64, _I, _I, _I, _P]),
     "dsp_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
     "dsp_st_block_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
+    "dsp_st_block_train_saved_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
+    "dsp_st_block_backward_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
+    "dsp_st_block_forward_train": (_I, [_P, _P, _c.POINTER(BlockWeights), _P, _SZ, _I64, _I64, _I64, _I, _I,
+                                        _I, _F, _I, _I, _P]),
+    "dsp_st_block_backward": (_I, [_P, _P, _c.POINTER(BlockWeights), _P, _SZ, _P, _SZ, _P,
+                                   _c.POINTER(BlockGrads), _I64, _I64, _I64, _I, _I, _I, _F, _I, _I, _P]),
     "dsp_st_block_forward": (_I, [_P, _P, _c.POINTER(BlockWeights), _P, _SZ, _I64, _I64, _I64, _I,
                                   _I, _I, _F, _I, _I, _P]),
 }
@@ -488,6 +498,61 @@ def dsp_st_block_forward(x, weights: dict, H: int, eps: float = 1e-6, flags: int
     return out
 
 
+def _block_sizes(x, weights, dtype):
+    torch = _torch()
+    B, T, S, C = x.shape
+    code = DSP_BF16 if (dtype or weights["wqkv_s"].dtype) == torch.bfloat16 else DSP_F32
+    return B, T, S, C, weights["w1"].shape[0], code
+
+
+def dsp_st_block_forward_train(x, weights: dict, H: int, eps: float = 1e-6, flags: int = 0, out=None,
+                               saved=None, dtype=None, stream=None):
+    """dsp_st_block_forward that also keeps the activations the backward needs:
+    returns (y (B, S, T, C) fp32, saved: a uint8 device tensor)."""
+    torch = _torch()
+    _require_device(x, out, saved, *weights.values())
+    B, T, S, C, F, code = _block_sizes(x, weights, dtype)
+    if out is None:
+        out = torch.empty((B, S, T, C), dtype=torch.float32, device=x.device)
+    need = int(lib().dsp_st_block_train_saved_bytes(B, T, S, C, H, F, code))
+    if saved is None:
+        saved = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    wt = BlockWeights(**{n: (weights[n].data_ptr() if weights.get(n) is not None else None)
+                         for n in BLOCK_WEIGHT_FIELDS})
+    _check(lib().dsp_st_block_forward_train(_ptr(x), _ptr(out), ctypes.byref(wt), _ptr(saved), saved.numel(), B, T,
+                                            S, C, H, F, float(eps), flags, code, _stream(stream)),
+           "dsp_st_block_forward_train")
+    return out, saved
+
+
+def dsp_st_block_backward(x, dy, weights: dict, saved, H: int, eps: float = 1e-6, flags: int = 0, dx=None,
+                          grads=None, with_bias: bool = False, workspace=None, dtype=None, stream=None):
+    """Backward of the block: returns (dx (B, T, S, C) fp32, grads: dict of fp32
+    tensors shaped like the weights, plus the biases when with_bias)."""
+    torch = _torch()
+    _require_device(x, dy, saved, dx, workspace, *weights.values())
+    B, T, S, C, F, code = _block_sizes(x, weights, dtype)
+    if dx is None:
+        dx = torch.empty((B, T, S, C), dtype=torch.float32, device=x.device)
+    if grads is None:
+        shapes = {"wqkv_s": (3 * C, C), "wo_s": (C, C), "wqkv_t": (3 * C, C), "wo_t": (C, C), "w1": (F, C),
+                  "w2": (C, F)}
+        if with_bias:
+            shapes.update({"bqkv_s": (3 * C,), "bo_s": (C,), "bqkv_t": (3 * C,), "bo_t": (C,), "b1": (F,),
+                           "b2": (C,)})
+        grads = {n: torch.empty(s, dtype=torch.float32, device=x.device) for n, s in shapes.items()}
+    need = int(lib().dsp_st_block_backward_workspace_bytes(B, T, S, C, H, F, code))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    wt = BlockWeights(**{n: (weights[n].data_ptr() if weights.get(n) is not None else None)
+                         for n in BLOCK_WEIGHT_FIELDS})
+    gt = BlockGrads(**{n: (grads[n].data_ptr() if grads.get(n) is not None else None) for n in BLOCK_WEIGHT_FIELDS})
+    _check(lib().dsp_st_block_backward(_ptr(x), _ptr(dy.contiguous()), ctypes.byref(wt), _ptr(saved), saved.numel(),
+                                       _ptr(workspace), workspace.numel(), _ptr(dx), ctypes.byref(gt), B, T, S, C,
+                                       H, F, float(eps), flags, code, _stream(stream)), "dsp_st_block_backward")
+    return dx, grads
+
+
 __all__ = ["lib", "status_str", "DspError", "BlockWeights", "dsp_switch", "dsp_spatial_attn",
            "dsp_temporal_attn", "dsp_layernorm", "dsp_linear", "dsp_st_block_forward",
-           "block_workspace_bytes", "LIB_PATH"]
+           "dsp_st_block_forward_train", "dsp_st_block_backward", "block_workspace_bytes", "LIB_PATH"]

@@ -318,6 +318,71 @@ bool block_ws_layout(int64_t B, int64_t T, int64_t S, int C, int F, int dtype, B
   return true;
 }
 
+// Activations a training forward keeps for the backward (offsets into the
+// caller's `saved` buffer, each 256-byte aligned).  Residual streams in fp32,
+// operands in the block dtype, log-sum-exps in fp32 ([units][L] = tokens * H).
+struct BlockSaved {
+  size_t y0, y1, h1, qkv1, a1, lse1, h2, qkv2, a2, lse2, h3, u, g, total;
+};
+
+bool block_saved_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype, BlockSaved* sv) {
+  int64_t tokens, tc, t3c, tf, th;
+  if (!mul_ok(B, T, &tokens) || !mul_ok(tokens, S, &tokens) || !mul_ok(tokens, C, &tc) ||
+      !mul_ok(tokens, 3 * (int64_t)C, &t3c) || !mul_ok(tokens, F, &tf) || !mul_ok(tokens, H, &th))
+    return false;
+  if (tc > INT64_MAX / 64 || tf > INT64_MAX / 64) return false;
+  const size_t es = elem_size(dtype);
+  auto up = [](size_t v) { return (v + 255) & ~size_t(255); };
+  size_t off = 0;
+  sv->y0 = off;   off += up((size_t)tc * 4);
+  sv->y1 = off;   off += up((size_t)tc * 4);
+  sv->h1 = off;   off += up((size_t)tc * es);
+  sv->qkv1 = off; off += up((size_t)t3c * es);
+  sv->a1 = off;   off += up((size_t)tc * es);
+  sv->lse1 = off; off += up((size_t)th * 4);
+  sv->h2 = off;   off += up((size_t)tc * es);
+  sv->qkv2 = off; off += up((size_t)t3c * es);
+  sv->a2 = off;   off += up((size_t)tc * es);
+  sv->lse2 = off; off += up((size_t)th * 4);
+  sv->h3 = off;   off += up((size_t)tc * es);
+  sv->u = off;    off += up((size_t)tf * es);
+  sv->g = off;    off += up((size_t)tf * es);
+  sv->total = off;
+  return true;
+}
+
+// Scratch of the block backward.
+struct BlockBwdWs {
+  size_t dyb, du, dh, dcur, dx1, da, dqkv, delta, wg, wg_bytes, total;
+};
+
+bool block_bwd_ws_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype, BlockBwdWs* ws) {
+  int64_t tokens, tc, t3c, tf, th;
+  if (!mul_ok(B, T, &tokens) || !mul_ok(tokens, S, &tokens) || !mul_ok(tokens, C, &tc) ||
+      !mul_ok(tokens, 3 * (int64_t)C, &t3c) || !mul_ok(tokens, F, &tf) || !mul_ok(tokens, H, &th))
+    return false;
+  if (tc > INT64_MAX / 64 || tf > INT64_MAX / 64) return false;
+  const size_t es = elem_size(dtype);
+  auto up = [](size_t v) { return (v + 255) & ~size_t(255); };
+  size_t wg = 0;
+  const int64_t shapes[4][2] = {{3 * (int64_t)C, C}, {C, C}, {F, C}, {C, F}};
+  for (const auto& nk : shapes)
+    wg = std::max(wg, dsp_linear_bwd_weight_workspace_bytes(tokens, (int)nk[0], (int)nk[1], dtype));
+  size_t off = 0;
+  ws->dyb = off;   off += up((size_t)tc * es);
+  ws->du = off;    off += up((size_t)tf * es);
+  ws->dh = off;    off += up((size_t)tc * 4);
+  ws->dcur = off;  off += up((size_t)tc * 4);
+  ws->dx1 = off;   off += up((size_t)tc * 4);
+  ws->da = off;    off += up((size_t)tc * es);
+  ws->dqkv = off;  off += up((size_t)t3c * es);
+  ws->delta = off; off += up((size_t)th * 4);
+  ws->wg = off;    off += up(wg);
+  ws->wg_bytes = wg;
+  ws->total = off;
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -706,6 +771,208 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
   }
   DSP_TRY(linear_impl(f, w->w2, w->b2, x1, x1, tokens, C, F, DSP_EPI_RESID, dtype, s));
   DSP_TRY(launch_layernorm(x1, 0, y_BSTC, 0, tokens, C, ln_eps, s));
+  return DSP_OK;
+#undef DSP_TRY
+}
+
+size_t dsp_st_block_train_saved_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype) {
+  if (!valid_dtype(dtype) || B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || F < 1 || C % H) return 0;
+  BlockSaved sv;
+  return block_saved_layout(B, T, S, C, H, F, dtype, &sv) ? sv.total : 0;
+}
+
+size_t dsp_st_block_backward_workspace_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype) {
+  if (!valid_dtype(dtype) || B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || F < 1 || C % H) return 0;
+  BlockBwdWs ws;
+  return block_bwd_ws_layout(B, T, S, C, H, F, dtype, &ws) ? ws.total : 0;
+}
+
+namespace {
+
+// Checks shared by the training forward and the backward.
+int block_train_check(const dsp_block_weights_t* w, int64_t B, int64_t T, int64_t S, int C, int H, int F,
+                      float ln_eps, int flags, int dtype) {
+  if (!w) return DSP_ERR_NULL;
+  if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
+  // training covers the pre-LN blocks (GELU or ReLU, with or without the MLP's LN)
+  if (flags & ~(DSP_BLOCK_NO_MLP_LN | DSP_BLOCK_RELU)) return DSP_ERR_ARG;
+  if (B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || C % H || F < 1) return DSP_ERR_SHAPE;
+  const int D = C / H;
+  if (dtype == DSP_BF16 && (!attn_bf16_supports(D) || D % 32 > 16 || C % 8 || F % 8)) return DSP_ERR_SHAPE;
+  if (!(ln_eps >= 0.0f) || isinf(ln_eps)) return DSP_ERR_ARG;
+  if (!w->wqkv_s || !w->wo_s || !w->wqkv_t || !w->wo_t || !w->w1 || !w->w2) return DSP_ERR_NULL;
+  if (dtype == DSP_BF16) {
+    const void* all[] = {w->wqkv_s, w->bqkv_s, w->wo_s, w->bo_s, w->wqkv_t, w->bqkv_t,
+                         w->wo_t, w->bo_t, w->w1, w->b1, w->w2, w->b2};
+    for (const void* p : all)
+      if (p && !aligned(p, 16)) return DSP_ERR_ALIGN;
+  }
+  return DSP_OK;
+}
+
+}  // namespace
+
+int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_block_weights_t* w, void* saved,
+                               size_t saved_bytes, int64_t B, int64_t T, int64_t S, int C, int H, int F,
+                               float ln_eps, int flags, int dtype, void* stream) {
+  int st = block_train_check(w, B, T, S, C, H, F, ln_eps, flags, dtype);
+  if (st != DSP_OK) return st;
+  if (!x_BTSC || !y_BSTC) return DSP_ERR_NULL;
+  BlockSaved sv;
+  if (!block_saved_layout(B, T, S, C, H, F, dtype, &sv)) return DSP_ERR_SHAPE;
+  if (!saved || saved_bytes < sv.total) return DSP_ERR_WORKSPACE;
+  if (!aligned(saved, 256)) return DSP_ERR_ALIGN;
+  if (!aligned(x_BTSC, 16) || !aligned(y_BSTC, 16)) return DSP_ERR_ALIGN;
+  const int64_t tokens = B * T * S;
+  const size_t act_bytes = (size_t)tokens * C * 4;
+  if (overlap(x_BTSC, act_bytes, y_BSTC, act_bytes) || overlap(x_BTSC, act_bytes, saved, saved_bytes) ||
+      overlap(y_BSTC, act_bytes, saved, saved_bytes))
+    return DSP_ERR_ARG;
+  if (tokens == 0) return DSP_OK;
+  hipStream_t s = as_stream(stream);
+  char* base = static_cast<char*>(saved);
+  float* y0 = reinterpret_cast<float*>(base + sv.y0);
+  float* y1 = reinterpret_cast<float*>(base + sv.y1);
+  char *h1 = base + sv.h1, *qkv1 = base + sv.qkv1, *a1 = base + sv.a1, *h2 = base + sv.h2, *qkv2 = base + sv.qkv2,
+       *a2 = base + sv.a2, *h3 = base + sv.h3, *u = base + sv.u, *g = base + sv.g;
+  float* lse1 = reinterpret_cast<float*>(base + sv.lse1);
+  float* lse2 = reinterpret_cast<float*>(base + sv.lse2);
+  const int bf = dtype == DSP_BF16;
+  const size_t es = elem_size(dtype);
+  const int D = C / H;
+  const int64_t shp[4] = {B, T, S, C};
+#define DSP_TRY(expr)            \
+  do {                           \
+    st = (expr);                 \
+    if (st != DSP_OK) return st; \
+  } while (0)
+  // an attention sublayer's projection and attention over L, positions of
+  // unit (b, x) at rows (b X + x) L + l, saving q/k/v, the output and lse
+  auto attn_sub = [&](const void* h, const void* wqkv, const void* bqkv, char* qkv, char* a, float* lse,
+                      int64_t X, int64_t L) {
+    int r = linear_impl(h, wqkv, bqkv, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s);
+    if (r != DSP_OK) return r;
+    const int64_t in_st[3] = {X * L * 3 * C, L * 3 * C, 3 * (int64_t)C}, out_st[3] = {X * L * C, L * C, C};
+    return attn_impl_strided(qkv, qkv + (size_t)C * es, qkv + (size_t)2 * C * es, a, B, X, L, H, D, in_st, out_st,
+                             0.0f, dtype, stream, lse);
+  };
+  // spatial half on (B, T, S, C); y1's slot holds the pre-switch stream x1
+  DSP_TRY(launch_layernorm(x_BTSC, 0, h1, bf, tokens, C, ln_eps, s));
+  DSP_TRY(attn_sub(h1, w->wqkv_s, w->bqkv_s, qkv1, a1, lse1, T, S));
+  DSP_TRY(linear_impl(a1, w->wo_s, w->bo_s, x_BTSC, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));
+  // the Switch T -> S
+  DSP_TRY(switch_impl(y1, y0, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+  // temporal half on (B, S, T, C)
+  DSP_TRY(launch_layernorm(y0, 0, h2, bf, tokens, C, ln_eps, s));
+  DSP_TRY(attn_sub(h2, w->wqkv_t, w->bqkv_t, qkv2, a2, lse2, S, T));
+  DSP_TRY(linear_impl(a2, w->wo_t, w->bo_t, y0, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));
+  // MLP: u = h3 W1 + b1 (kept), g = act(u) (kept), y = y1 + g W2 + b2
+  if (flags & DSP_BLOCK_NO_MLP_LN) {
+    DSP_TRY(launch_cast(y1, 0, h3, bf, tokens * C, s));
+  } else {
+    DSP_TRY(launch_layernorm(y1, 0, h3, bf, tokens, C, ln_eps, s));
+  }
+  DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, u, tokens, F, C, DSP_EPI_NONE, dtype, s));
+  DSP_TRY(launch_activation(u, g, tokens * F, bf, (flags & DSP_BLOCK_RELU) != 0, s));
+  DSP_TRY(linear_impl(g, w->w2, w->b2, y1, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
+  return DSP_OK;
+#undef DSP_TRY
+}
+
+int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_block_weights_t* w,
+                          const void* saved, size_t saved_bytes, void* workspace, size_t ws_bytes, float* dx_BTSC,
+                          const dsp_block_grads_t* grads, int64_t B, int64_t T, int64_t S, int C, int H, int F,
+                          float ln_eps, int flags, int dtype, void* stream) {
+  int st = block_train_check(w, B, T, S, C, H, F, ln_eps, flags, dtype);
+  if (st != DSP_OK) return st;
+  if (!x_BTSC || !dy_BSTC || !dx_BTSC || !grads) return DSP_ERR_NULL;
+  if (!grads->wqkv_s || !grads->wo_s || !grads->wqkv_t || !grads->wo_t || !grads->w1 || !grads->w2)
+    return DSP_ERR_NULL;
+  BlockSaved sv;
+  BlockBwdWs bw;
+  if (!block_saved_layout(B, T, S, C, H, F, dtype, &sv) || !block_bwd_ws_layout(B, T, S, C, H, F, dtype, &bw))
+    return DSP_ERR_SHAPE;
+  if (!saved || saved_bytes < sv.total || !workspace || ws_bytes < bw.total) return DSP_ERR_WORKSPACE;
+  if (!aligned(saved, 256) || !aligned(workspace, 256)) return DSP_ERR_ALIGN;
+  const float* gp[] = {grads->wqkv_s, grads->bqkv_s, grads->wo_s, grads->bo_s, grads->wqkv_t, grads->bqkv_t,
+                       grads->wo_t, grads->bo_t, grads->w1, grads->b1, grads->w2, grads->b2};
+  for (const float* p : gp)
+    if (p && !aligned(p, 16)) return DSP_ERR_ALIGN;
+  if (!aligned(x_BTSC, 16) || !aligned(dy_BSTC, 16) || !aligned(dx_BTSC, 16)) return DSP_ERR_ALIGN;
+  const int64_t tokens = B * T * S;
+  const size_t act_bytes = (size_t)tokens * C * 4;
+  if (overlap(dx_BTSC, act_bytes, x_BTSC, act_bytes) || overlap(dx_BTSC, act_bytes, dy_BSTC, act_bytes) ||
+      overlap(dx_BTSC, act_bytes, saved, saved_bytes) || overlap(dx_BTSC, act_bytes, workspace, ws_bytes) ||
+      overlap(workspace, ws_bytes, saved, saved_bytes))
+    return DSP_ERR_ARG;
+  if (tokens == 0) return DSP_OK;
+  hipStream_t s = as_stream(stream);
+  const char* sb = static_cast<const char*>(saved);
+  const float* y0 = reinterpret_cast<const float*>(sb + sv.y0);
+  const float* y1 = reinterpret_cast<const float*>(sb + sv.y1);
+  const char *h1 = sb + sv.h1, *qkv1 = sb + sv.qkv1, *a1 = sb + sv.a1, *h2 = sb + sv.h2, *qkv2 = sb + sv.qkv2,
+             *a2 = sb + sv.a2, *h3 = sb + sv.h3, *u = sb + sv.u, *g = sb + sv.g;
+  const float* lse1 = reinterpret_cast<const float*>(sb + sv.lse1);
+  const float* lse2 = reinterpret_cast<const float*>(sb + sv.lse2);
+  char* wb = static_cast<char*>(workspace);
+  char *dyb = wb + bw.dyb, *du = wb + bw.du, *da = wb + bw.da, *dqkv = wb + bw.dqkv;
+  float* dh = reinterpret_cast<float*>(wb + bw.dh);
+  float* dcur = reinterpret_cast<float*>(wb + bw.dcur);
+  float* dx1 = reinterpret_cast<float*>(wb + bw.dx1);
+  float* delta = reinterpret_cast<float*>(wb + bw.delta);
+  void* wg = bw.wg_bytes ? wb + bw.wg : nullptr;
+  const int bf = dtype == DSP_BF16;
+  const size_t es = elem_size(dtype);
+  const int D = C / H;
+  const int act_epi = bf ? DSP_GRAD_EPI_BF16 : DSP_GRAD_EPI_F32;   // gradients fed to bf16 / fp32 operands
+  const int act_bwd = (flags & DSP_BLOCK_RELU) ? DSP_GRAD_EPI_RELU_BWD : DSP_GRAD_EPI_GELU_BWD;
+  const int64_t shp_bstc[4] = {B, S, T, C};
+#define DSP_TRY(expr)            \
+  do {                           \
+    st = (expr);                 \
+    if (st != DSP_OK) return st; \
+  } while (0)
+  // the upstream fp32 gradient as an operand of the block dtype
+  auto operand = [&](const float* d) { return launch_cast(d, 0, dyb, bf, tokens * C, s); };
+  // backward of one attention sublayer: d_out (in dyb) -> dh (fp32), weight gradients
+  auto attn_sub_bwd = [&](const char* h, const char* qkv, const char* a, const float* lse, const void* wqkv,
+                          const void* wo, float* g_wqkv, float* g_bqkv, float* g_wo, float* g_bo, int64_t X,
+                          int64_t L) {
+    int r = dsp_linear_bwd_weight(dyb, a, g_wo, g_bo, wg, bw.wg_bytes, tokens, C, C, dtype, stream);
+    if (r != DSP_OK) return r;
+    r = dsp_linear_bwd_data(dyb, wo, nullptr, da, tokens, C, C, act_epi, dtype, stream);
+    if (r != DSP_OK) return r;
+    const int64_t q_st[3] = {X * L * 3 * C, L * 3 * C, 3 * (int64_t)C}, o_st[3] = {X * L * C, L * C, C};
+    r = attn_bwd_impl(qkv, qkv + (size_t)C * es, qkv + (size_t)2 * C * es, a, da, lse, dqkv, dqkv + (size_t)C * es,
+                      dqkv + (size_t)2 * C * es, delta, B, X, L, H, D, q_st, o_st, 0.0f, dtype, stream);
+    if (r != DSP_OK) return r;
+    r = dsp_linear_bwd_weight(dqkv, h, g_wqkv, g_bqkv, wg, bw.wg_bytes, tokens, 3 * C, C, dtype, stream);
+    if (r != DSP_OK) return r;
+    return dsp_linear_bwd_data(dqkv, wqkv, nullptr, dh, tokens, 3 * C, C, DSP_GRAD_EPI_F32, dtype, stream);
+  };
+  // ---- MLP: y = y1 + act(h3 W1 + b1) W2 + b2
+  DSP_TRY(operand(dy_BSTC));
+  DSP_TRY(dsp_linear_bwd_weight(dyb, g, grads->w2, grads->b2, wg, bw.wg_bytes, tokens, C, F, dtype, stream));
+  DSP_TRY(dsp_linear_bwd_data(dyb, w->w2, u, du, tokens, C, F, act_bwd, dtype, stream));
+  DSP_TRY(dsp_linear_bwd_weight(du, h3, grads->w1, grads->b1, wg, bw.wg_bytes, tokens, F, C, dtype, stream));
+  DSP_TRY(dsp_linear_bwd_data(du, w->w1, nullptr, dh, tokens, F, C, DSP_GRAD_EPI_F32, dtype, stream));
+  if (flags & DSP_BLOCK_NO_MLP_LN) {
+    DSP_TRY(launch_add_f32(dy_BSTC, dh, dcur, tokens * C, s));
+  } else {
+    DSP_TRY(launch_layernorm_bwd(y1, 0, dh, 0, dy_BSTC, dcur, tokens, C, ln_eps, s));
+  }
+  // ---- temporal half: y1 = y0 + Attn_T(LN(y0) Wqkv_t) Wo_t
+  DSP_TRY(operand(dcur));
+  DSP_TRY(attn_sub_bwd(h2, qkv2, a2, lse2, w->wqkv_t, w->wo_t, grads->wqkv_t, grads->bqkv_t, grads->wo_t,
+                       grads->bo_t, S, T));
+  DSP_TRY(launch_layernorm_bwd(y0, 0, dh, 0, dcur, dcur, tokens, C, ln_eps, s));
+  // ---- the Switch's adjoint: (B, S, T, C) -> (B, T, S, C)
+  DSP_TRY(switch_impl(dcur, dx1, shp_bstc, 4, 1, 2, 1, DSP_F32, 0, s));
+  // ---- spatial half: x1 = x + Attn_S(LN(x) Wqkv_s) Wo_s
+  DSP_TRY(operand(dx1));
+  DSP_TRY(attn_sub_bwd(h1, qkv1, a1, lse1, w->wqkv_s, w->wo_s, grads->wqkv_s, grads->bqkv_s, grads->wo_s,
+                       grads->bo_s, T, S));
+  DSP_TRY(launch_layernorm_bwd(x_BTSC, 0, dh, 0, dx1, dx_BTSC, tokens, C, ln_eps, s));
   return DSP_OK;
 #undef DSP_TRY
 }

@@ -96,6 +96,8 @@ int launch_gemm_grad(const void* a, int ta, int64_t lda, const void* b, int tb, 
                      void* out, int64_t M, int64_t N, int64_t K, int epi, int splits, float* ws, hipStream_t s);
 int launch_gemm_grad_f32(const float* a, int ta, int64_t lda, const float* b, int tb, int64_t ldb,
                          const float* aux, float* out, int64_t M, int64_t N, int64_t K, int epi, hipStream_t s);
+int launch_activation(const void* u, void* g, int64_t n, int bf16, int relu, hipStream_t s);
+int launch_add_f32(const float* a, const float* b, float* out, int64_t n, hipStream_t s);
 int launch_colsum_bf16(const void* dy, float* db, int64_t M, int N, hipStream_t s);
 int launch_colsum_f32(const float* dy, float* db, int64_t M, int N, hipStream_t s);
 

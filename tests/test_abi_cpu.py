@@ -274,6 +274,36 @@ def test_layernorm_bwd_validation(lib):
     assert f(rows=0, x=None) == dsp.DSP_OK
 
 
+def test_block_train_validation(lib):
+    import ctypes as c
+    W = dsp.BlockWeights(**{n: (FAKE + 2 ** 26 * i if n.startswith("w") else None)
+                            for i, n in enumerate(dsp.BLOCK_WEIGHT_FIELDS)})
+    G = dsp.BlockGrads(**{n: (2 ** 40 + 2 ** 26 * i if n.startswith("w") else None)
+                          for i, n in enumerate(dsp.BLOCK_WEIGHT_FIELDS)})
+    dims = (1, 4, 8, 144, 2, 576)
+    need = lib.dsp_st_block_train_saved_bytes(*dims, 1)
+    ws_need = lib.dsp_st_block_backward_workspace_bytes(*dims, 1)
+    assert need > 0 and ws_need > 0
+    assert lib.dsp_st_block_train_saved_bytes(1, 4, 8, 144, 5, 576, 1) == 0     # C % H
+    X, Y, SV, WS, DX = 2 ** 34, 2 ** 35, 2 ** 36, 2 ** 37, 2 ** 38
+    fwd = lambda flags=0, sv=SV, svb=need, dt=1, F=576: lib.dsp_st_block_forward_train(
+        X, Y, c.byref(W), sv, svb, 1, 4, 8, 144, 2, F, 1e-6, flags, dt, None)
+    assert fwd(flags=dsp.DSP_BLOCK_POST_LN) == dsp.DSP_ERR_ARG                  # post-LN: not for training
+    assert fwd(flags=dsp.DSP_BLOCK_ATTN_ONLY) == dsp.DSP_ERR_ARG
+    assert fwd(sv=None) == dsp.DSP_ERR_WORKSPACE
+    assert fwd(svb=need - 1) == dsp.DSP_ERR_WORKSPACE
+    assert fwd(sv=SV + 16) == dsp.DSP_ERR_ALIGN
+    assert fwd(dt=2) == dsp.DSP_ERR_DTYPE
+    assert fwd(F=0) == dsp.DSP_ERR_SHAPE
+    bwd = lambda grads=c.byref(G), ws=WS, wsb=ws_need, dx=DX, flags=0: lib.dsp_st_block_backward(
+        X, Y, c.byref(W), SV, need, ws, wsb, dx, grads, 1, 4, 8, 144, 2, 576, 1e-6, flags, 1, None)
+    assert bwd(grads=None) == dsp.DSP_ERR_NULL
+    assert bwd(dx=None) == dsp.DSP_ERR_NULL
+    assert bwd(wsb=ws_need - 1) == dsp.DSP_ERR_WORKSPACE
+    assert bwd(dx=X + 16) == dsp.DSP_ERR_ARG                                     # dx overlaps x
+    assert bwd(flags=dsp.DSP_BLOCK_POST_LN | dsp.DSP_BLOCK_RELU) == dsp.DSP_ERR_ARG
+
+
 def test_layernorm_validation(lib):
     f = lambda x=FAKE, xd=1, y=FAKE2, yd=1, rows=4, C=8, eps=1e-6: lib.dsp_layernorm(
         x, xd, y, yd, rows, C, eps, None)
