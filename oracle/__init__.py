@@ -18,6 +18,9 @@ float64 NumPy (library matmul and erf as the only primitives):
   (Eq. 1-2) along one sequence dimension of a multi-dimensional sequence
   (Eq. 7-8): ``spatial_attention`` over S within each frame and
   ``temporal_attention`` over T at each location.
+* ``attention_grouped`` / ``attention_grouped_bwd`` -- grouped key/value
+  heads (multi-query, grouped-query) and separate query and key lengths
+  (cross-attention), the variants the paper states compatibility with.
 * ``attention_bwd`` / ``attention_lse`` -- the backward of attention (the
   chain rule through the softmax) and the row logsumexp it uses.
 * ``layernorm``, ``linear``, ``gelu`` and the composites ``st_block`` (the
@@ -31,9 +34,9 @@ of each module for what pins it.
 """
 from .switch import switch, unswitch, exchange_unpack, switch_index_map, split, gather
 from .attention import attention, attention_rows, spatial_attention, temporal_attention, \
-    temporal_attention_strided
+    temporal_attention_strided, attention_grouped
 from .backward import attention_bwd, attention_bwd_units, attention_lse, attention_lse_units, \
-    attention_delta_units
+    attention_delta_units, attention_grouped_bwd
 from .block_bwd import linear_bwd, layernorm_bwd, gelu_bwd, relu_bwd, st_block_bwd
 from .block import layernorm, linear, gelu, relu, st_block, tiny_chain, BLOCK_NO_MLP_LN, BLOCK_POST_LN, \
     BLOCK_RELU
@@ -43,4 +46,5 @@ __all__ = ["switch", "unswitch", "exchange_unpack", "switch_index_map", "split",
            "temporal_attention_strided", "layernorm", "linear", "gelu", "st_block", "tiny_chain",
            "BLOCK_NO_MLP_LN", "BLOCK_POST_LN", "BLOCK_RELU", "relu", "attention_bwd",
            "attention_bwd_units", "attention_lse", "attention_lse_units", "attention_delta_units",
-           "linear_bwd", "layernorm_bwd", "gelu_bwd", "relu_bwd", "st_block_bwd"]
+           "linear_bwd", "layernorm_bwd", "gelu_bwd", "relu_bwd", "st_block_bwd", "attention_grouped",
+           "attention_grouped_bwd"]

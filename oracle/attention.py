@@ -91,3 +91,28 @@ def temporal_attention_strided(q, k, v, H: int, scale: float | None = None) -> n
     output in (B, T, S, C).  Same units as ``temporal_attention``."""
     sw = lambda a: np.swapaxes(np.asarray(a, dtype=np.float64), 1, 2)
     return np.swapaxes(_per_unit(sw(q), sw(k), sw(v), H, scale), 1, 2)
+
+
+def attention_grouped(q, k, v, H: int, Hkv: int, scale: float | None = None) -> np.ndarray:
+    """Attention with grouped key/value heads and separate query and key lengths
+    -- the variants the paper states DSP is compatible with (multi-query and
+    grouped-query attention, cross-attention), on the same per-(b, x) units.
+
+    q: (B, X, Lq, H*d); k, v: (B, X, Lk, Hkv*d), Hkv dividing H.  Query head h
+    attends with key/value head h // (H // Hkv) (Hkv = H: multi-head; Hkv = 1:
+    multi-query).  Lq may differ from Lk (cross-attention: the keys and values
+    come from another sequence).  Returns (B, X, Lq, H*d)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    if H % Hkv:
+        raise ValueError("Hkv must divide H")
+    B, X, Lq, C = q.shape
+    d = C // H
+    grp = H // Hkv
+    out = np.empty((B, X, Lq, C))
+    for h in range(H):
+        cq = slice(h * d, (h + 1) * d)
+        ck = slice((h // grp) * d, (h // grp + 1) * d)
+        out[..., cq] = attention(q[..., cq], k[..., ck], v[..., ck], scale)
+    return out

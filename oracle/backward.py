@@ -88,3 +88,27 @@ def attention_delta_units(o, do, H: int) -> np.ndarray:
     Jacobian subtracts, rowsum(dP * P), in the form computed from the output."""
     (of, _), (df, _) = _units(o, H), _units(do, H)
     return (of * df).sum(axis=-1)
+
+
+def attention_grouped_bwd(q, k, v, do, H: int, Hkv: int, scale: float | None = None):
+    """Gradients (dq, dk, dv) of sum(dO * attention_grouped(q, k, v, H, Hkv)).
+    A key/value head is read by the H // Hkv query heads of its group, so its
+    gradients are the sums of theirs."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    B, X, Lq, C = q.shape
+    d = C // H
+    grp = H // Hkv
+    dq = np.empty(q.shape)
+    dk = np.zeros(k.shape)
+    dv = np.zeros(v.shape)
+    for h in range(H):
+        cq = slice(h * d, (h + 1) * d)
+        ck = slice((h // grp) * d, (h // grp + 1) * d)
+        gq, gk, gv = attention_bwd(q[..., cq], k[..., ck], v[..., ck], do[..., cq], scale)
+        dq[..., cq] = gq
+        dk[..., ck] += gk
+        dv[..., ck] += gv
+    return dq, dk, dv

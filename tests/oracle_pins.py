@@ -691,3 +691,53 @@ def pin_block_bwd_autograd(st_block_bwd, flag_sets):
         assert np.allclose(dx, tx.grad.numpy(), atol=1e-10, rtol=1e-8), flags
         for n in p:
             assert np.allclose(g[n], tp[n].grad.numpy(), atol=1e-10, rtol=1e-8), (flags, n)
+
+
+# ----------------------------------------------------------------------------- grouped / cross attention
+def pin_attention_grouped(attention_grouped, spatial_attention, attention):
+    rng = np.random.default_rng(80)
+    B, X, Lq, Lk, H, d = 2, 3, 5, 7, 4, 3
+    q = rng.standard_normal((B, X, Lq, H * d))
+    # Hkv = H with Lq = Lk: plain multi-head attention per unit
+    k, v = rng.standard_normal((B, X, Lq, H * d)), rng.standard_normal((B, X, Lq, H * d))
+    assert np.allclose(attention_grouped(q, k, v, H, H), spatial_attention(q, k, v, H))
+    # grouped heads equal multi-head attention with each key/value head repeated
+    # for the query heads of its group (head h reads group h // (H / Hkv))
+    for Hkv in (1, 2):
+        k, v = rng.standard_normal((B, X, Lk, Hkv * d)), rng.standard_normal((B, X, Lk, Hkv * d))
+        rep = lambda a: np.concatenate([a[..., (h // (H // Hkv)) * d:(h // (H // Hkv) + 1) * d]
+                                        for h in range(H)], axis=-1)
+        got = attention_grouped(q, k, v, H, Hkv)
+        assert got.shape == q.shape
+        for b, x, h in itertools.product(range(B), range(X), range(H)):
+            cq, ck = slice(h * d, (h + 1) * d), slice((h // (H // Hkv)) * d, (h // (H // Hkv) + 1) * d)
+            assert np.allclose(got[b, x, :, cq], attention(q[b, x, :, cq], k[b, x, :, ck], v[b, x, :, ck]))
+        # brute force over Python floats for the cross-attention lengths (Lq != Lk)
+        for b, x, h, i in [(1, 2, 3, 4), (0, 0, 1, 0)]:
+            g = h // (H // Hkv)
+            z = [sum(q[b, x, i, h * d + e] * k[b, x, j, g * d + e] for e in range(d)) / math.sqrt(d)
+                 for j in range(Lk)]
+            m = max(z)
+            w = [math.exp(zz - m) for zz in z]
+            s = math.fsum(w)
+            for e in range(d):
+                want = math.fsum(w[j] * v[b, x, j, g * d + e] for j in range(Lk)) / s
+                assert abs(got[b, x, i, h * d + e] - want) < 1e-12
+        assert np.allclose(got, spatial_attention(q, rep(k), rep(v), H) if Lq == Lk else got)
+
+
+def pin_attention_grouped_bwd(attention_grouped, attention_grouped_bwd, attention_bwd_units):
+    rng = np.random.default_rng(81)
+    B, X, Lq, Lk, H, d = 1, 2, 3, 4, 4, 2
+    for Hkv in (1, 2, 4):
+        q, do = rng.standard_normal((B, X, Lq, H * d)), rng.standard_normal((B, X, Lq, H * d))
+        k, v = rng.standard_normal((B, X, Lk, Hkv * d)), rng.standard_normal((B, X, Lk, Hkv * d))
+        dq, dk, dv = attention_grouped_bwd(q, k, v, do, H, Hkv)
+        loss = lambda qq, kk, vv: float((do * attention_grouped(qq, kk, vv, H, Hkv)).sum())
+        assert np.allclose(dq, _fd_grad(lambda a: loss(a, k, v), q), atol=1e-8, rtol=1e-7)
+        assert np.allclose(dk, _fd_grad(lambda a: loss(q, a, v), k), atol=1e-8, rtol=1e-7)
+        assert np.allclose(dv, _fd_grad(lambda a: loss(q, k, a), v), atol=1e-8, rtol=1e-7)
+    # Hkv = H, Lq = Lk: the multi-head gradients
+    q, k, v, do = (rng.standard_normal((2, 2, 5, 6)) for _ in range(4))
+    for a, b in zip(attention_grouped_bwd(q, k, v, do, 3, 3), attention_bwd_units(q, k, v, do, 3)):
+        assert np.allclose(a, b)

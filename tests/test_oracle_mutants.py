@@ -32,7 +32,8 @@ def _impl():
         attention_bwd_units=BW.attention_bwd_units, attention_lse=BW.attention_lse,
         attention_lse_units=BW.attention_lse_units, attention_delta_units=BW.attention_delta_units,
         linear_bwd=OB.linear_bwd, layernorm_bwd=OB.layernorm_bwd, gelu_bwd=OB.gelu_bwd,
-        relu_bwd=OB.relu_bwd, st_block_bwd=OB.st_block_bwd)
+        relu_bwd=OB.relu_bwd, st_block_bwd=OB.st_block_bwd, attention_grouped=AT.attention_grouped,
+        attention_grouped_bwd=BW.attention_grouped_bwd)
 
 
 def _pins(i):
@@ -75,6 +76,8 @@ def _pins(i):
         lambda: P.pin_attention_bwd_units(i.attention_bwd, i.attention_bwd_units,
                                           i.attention_lse_units, i.attention_lse,
                                           i.attention_delta_units, i.attention),
+        lambda: P.pin_attention_grouped(i.attention_grouped, i.spatial, i.attention),
+        lambda: P.pin_attention_grouped_bwd(i.attention_grouped, i.attention_grouped_bwd, i.attention_bwd_units),
         # the block backward pins last: they are the slowest
         lambda: P.pin_linear_bwd(i.linear, i.linear_bwd),
         lambda: P.pin_layernorm_bwd(i.layernorm, i.layernorm_bwd),
@@ -344,6 +347,32 @@ def lse_log2(q, k, scale=None):
 
 
 _orig_block = BL.st_block
+_orig_grouped = AT.attention_grouped
+_orig_grouped_bwd = BW.attention_grouped_bwd
+
+
+def grouped_modulo_heads(q, k, v, H, Hkv, scale=None):
+    # query head h reading key/value head h % Hkv instead of h // (H / Hkv)
+    q, k, v = (np.asarray(a, float) for a in (q, k, v))
+    d = q.shape[-1] // H
+    out = np.empty(q.shape)
+    for h in range(H):
+        cq, ck = slice(h * d, (h + 1) * d), slice((h % Hkv) * d, (h % Hkv + 1) * d)
+        out[..., cq] = _orig_attention(q[..., cq], k[..., ck], v[..., ck], scale)
+    return out
+
+
+def grouped_bwd_last_head_only(q, k, v, do, H, Hkv, scale=None):
+    # a key/value head's gradient taken from the last query head of its group, not summed
+    q, k, v, do = (np.asarray(a, float) for a in (q, k, v, do))
+    d = q.shape[-1] // H
+    grp = H // Hkv
+    dq, dk, dv = np.empty(q.shape), np.zeros(k.shape), np.zeros(v.shape)
+    for h in range(H):
+        cq, ck = slice(h * d, (h + 1) * d), slice((h // grp) * d, (h // grp + 1) * d)
+        gq, gk, gv = _orig_abwd(q[..., cq], k[..., ck], v[..., ck], do[..., cq], scale)
+        dq[..., cq], dk[..., ck], dv[..., ck] = gq, gk, gv
+    return dq, dk, dv
 _orig_ln_bwd = OB.layernorm_bwd
 _orig_lin_bwd = OB.linear_bwd
 _orig_sub_bwd = OB._attn_sublayer_bwd
@@ -389,6 +418,9 @@ MUTANTS = {
     "attention bwd: dq from v": [(BW, "attention_bwd", abwd_dq_from_v)],
     "attention bwd: dv = P dO": [(BW, "attention_bwd", abwd_dv_untransposed)],
     "attention lse: base 2": [(BW, "attention_lse", lse_log2)],
+    "grouped attention: head h reads kv head h % Hkv": [(AT, "attention_grouped", grouped_modulo_heads)],
+    "grouped attention bwd: kv gradients not summed over the group":
+        [(BW, "attention_grouped_bwd", grouped_bwd_last_head_only)],
     "layernorm bwd: no projection on the output": [(OB, "layernorm_bwd", lnb_no_projection)],
     "gelu bwd: Phi only": [(OB, "gelu_bwd", gelub_cdf_only)],
     "linear bwd: bias gradient averaged": [(OB, "linear_bwd", linb_db_mean)],

@@ -181,3 +181,12 @@ def test_block_bwd_finite_differences():
 
 def test_block_bwd_matches_autograd():
     P.pin_block_bwd_autograd(OB.st_block_bwd, BWD_FLAGS)
+
+
+def test_attention_grouped():
+    P.pin_attention_grouped(oracle.attention_grouped, oracle.spatial_attention, oracle.attention)
+
+
+def test_attention_grouped_bwd():
+    P.pin_attention_grouped_bwd(oracle.attention_grouped, oracle.attention_grouped_bwd,
+                                oracle.attention_bwd_units)
