@@ -258,6 +258,37 @@ int dsp_attn_bwd(const void* q, const void* k, const void* v, const void* o, con
                  float scale, int dtype, void* stream);
 
 /* ------------------------------------------------------------------------
+ * dsp_attn_general / dsp_attn_general_bwd -- the attention variants the
+ * paper states DSP is compatible with: multi-query and grouped-query attention
+ * (Hkv key/value heads shared by H / Hkv query heads each) and cross-attention
+ * (keys and values from another sequence, of their own length), on the same
+ * per-(b, x) units as dsp_attn_strided.  For unit (b, x, h):
+ *   queries: Lq positions, element (b, x, l, h*D + d) of q at
+ *            b*q_strides[0] + x*q_strides[1] + l*q_strides[2] + h*D + d;
+ *   keys, values: Lk positions of head h / (H / Hkv), at
+ *            b*kv_strides[0] + x*kv_strides[1] + l*kv_strides[2] + (h/(H/Hkv))*D + d;
+ *   output (and dout): o_strides, H heads, Lq positions.
+ * Hkv == H, Lq == Lk and kv_strides == q_strides is dsp_attn_strided.  A
+ * kv stride of 0 broadcasts keys and values (e.g. one text sequence shared
+ * by every frame: kv_strides[1] = 0); the backward rejects it (its key and
+ * value gradients would have no single owner: DSP_ERR_ARG).
+ * lse (forward, optional: NULL skips it): fp32 [B * X * H][Lq].  The
+ * backward's contract (lse, delta [B*X*H][Lq], dq with q's strides, dk and dv
+ * with kv_strides -- the sums over each group's query heads) is otherwise
+ * dsp_attn_bwd's.  H % Hkv != 0, or Lk == 0 with Lq > 0: DSP_ERR_SHAPE.
+ * Everything else, including dtypes, alignment and errors, as for
+ * dsp_attn_strided / dsp_attn_bwd.
+ * ------------------------------------------------------------------------ */
+int dsp_attn_general(const void* q, const void* k, const void* v, void* o, float* lse, int64_t B, int64_t X,
+                     int64_t Lq, int64_t Lk, int H, int Hkv, int D, const int64_t* q_strides,
+                     const int64_t* kv_strides, const int64_t* o_strides, float scale, int dtype, void* stream);
+int dsp_attn_general_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                         const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
+                         int64_t Lq, int64_t Lk, int H, int Hkv, int D, const int64_t* q_strides,
+                         const int64_t* kv_strides, const int64_t* o_strides, float scale, int dtype,
+                         void* stream);
+
+/* ------------------------------------------------------------------------
  * dsp_layernorm -- per-row normalisation over C (Eq. 4, 6):
  *   y = (x - mean) / sqrt(var + eps), biased variance, no affine part,
  *   statistics in fp32.

@@ -11,7 +11,7 @@ binding's functions raises.
 Entry points (see ``include/dsp.h`` for the exact contracts):
 ``dsp_switch``, ``dsp_exchange_unpack``, ``dsp_split``, ``dsp_gather``,
 ``dsp_spatial_attn``, ``dsp_temporal_attn``, ``dsp_attn_strided``,
-``dsp_attn_fwd_lse``, ``dsp_attn_bwd``, ``dsp_layernorm_bwd``, ``dsp_linear_bwd_data``, ``dsp_linear_bwd_weight``,
+``dsp_attn_fwd_lse``, ``dsp_attn_bwd``, ``dsp_attn_general``, ``dsp_attn_general_bwd``, ``dsp_layernorm_bwd``, ``dsp_linear_bwd_data``, ``dsp_linear_bwd_weight``,
 ``dsp_layernorm``, ``dsp_linear``, ``dsp_st_block_forward``.
 """
 from __future__ import annotations
@@ -70,6 +70,10 @@ _SIGNATURES = {
     "dsp_attn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _I,
                           _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
     "dsp_layernorm": (_I, [_P, _I, _P, _I, _I64, _I, _F, _P]),
+    "dsp_attn_general": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I, _I, _I, _c.POINTER(_I64),
+                              _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
+    "dsp_attn_general_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I, _I, _I,
+                                  _c.POINTER(_I64), _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
     "dsp_layernorm_bwd": (_I, [_P, _I, _P, _I, _P, _P, _I64, _I, _F, _P]),
     "dsp_linear_bwd_data": (_I, [_P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
     "dsp_linear_bwd_weight_workspace_bytes": (_SZ, [_I64, _I, _I, _I]),
@@ -400,6 +404,61 @@ def dsp_layernorm(x, eps: float = 1e-6, out=None, out_dtype=None, stream=None):
                              float(eps), _stream(stream))
     _check(st, "dsp_layernorm")
     return out
+
+
+def _st3(t):
+    return (ctypes.c_int64 * 3)(*t.stride()[:3])
+
+
+def dsp_attn_general(q, k, v, H: int, Hkv: int, out=None, lse=None, with_lse: bool = False,
+                     scale: float = 0.0, stream=None):
+    """Grouped-query / multi-query / cross-attention over dim 2 of 4-D views:
+    q [B, X, Lq, H*D], k and v [B, X, Lk, Hkv*D] (same strides; a 0 stride
+    broadcasts).  Returns out [B, X, Lq, H*D] (and lse [B, X, H, Lq] fp32 when
+    with_lse or lse is given)."""
+    torch = _torch()
+    _require_device(q, k, v, out, lse)
+    if q.dim() != 4 or k.shape != v.shape or k.stride() != v.stride() or q.stride(3) != 1 or k.stride(3) != 1:
+        raise ValueError("dsp_attn_general: q [B, X, Lq, C] and k, v [B, X, Lk, Ckv] views of one layout")
+    B, X, Lq, C = q.shape
+    if C % H or tuple(k.shape[:2]) != (B, X):
+        raise ValueError("dsp_attn_general: shapes do not match")
+    D = C // H
+    Lk = k.shape[2]
+    if k.shape[3] != Hkv * D:
+        raise ValueError("dsp_attn_general: k and v must hold Hkv heads of the query head width")
+    if out is None:
+        out = torch.empty((B, X, Lq, C), dtype=q.dtype, device=q.device)
+    if (with_lse or lse is not None) and lse is None:
+        lse = torch.empty((B, X, H, Lq), dtype=torch.float32, device=q.device)
+    _check(lib().dsp_attn_general(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, X, Lq, Lk, H, Hkv, D,
+                                  _st3(q), _st3(k), _st3(out), float(scale), _dtype_code(q), _stream(stream)),
+           "dsp_attn_general")
+    return (out, lse) if lse is not None else out
+
+
+def dsp_attn_general_bwd(q, k, v, o, dout, lse, H: int, Hkv: int, dq=None, dk=None, dv=None, delta=None,
+                         scale: float = 0.0, stream=None):
+    """Gradients of dsp_attn_general: (dq like q, dk and dv like k and v)."""
+    torch = _torch()
+    _require_device(q, k, v, o, dout, lse, dq, dk, dv, delta)
+    B, X, Lq, C = q.shape
+    D = C // H
+    Lk = k.shape[2]
+    if dout.stride() != o.stride() or dout.shape != o.shape:
+        raise ValueError("dsp_attn_general_bwd: dout must have the shape and strides of o")
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    if dq.stride() != q.stride() or dk.stride() != k.stride() or dv.stride() != k.stride():
+        raise ValueError("dsp_attn_general_bwd: dq must have q's strides, dk and dv k's")
+    if delta is None:
+        delta = torch.empty(B * X * H * Lq, dtype=torch.float32, device=q.device)
+    _check(lib().dsp_attn_general_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
+                                      _ptr(dk), _ptr(dv), _ptr(delta), B, X, Lq, Lk, H, Hkv, D, _st3(q), _st3(k),
+                                      _st3(o), float(scale), _dtype_code(q), _stream(stream)),
+           "dsp_attn_general_bwd")
+    return dq, dk, dv
 
 
 def dsp_layernorm_bwd(x, dy, eps: float = 1e-6, dres=None, out=None, stream=None):

@@ -142,49 +142,67 @@ bool rows_disjoint(int64_t B, int64_t X, int64_t L, const int64_t* st, int64_t w
   return true;
 }
 
-int attn_impl_strided(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X,
-                      int64_t L, int H, int D, const int64_t* in_st, const int64_t* out_st,
-                      float scale, int dtype, void* stream, float* lse = nullptr) {
+// Attention over general layouts: queries (B, X, Lq) of H heads with q_st,
+// keys/values (B, X, Lk) of Hkv heads with kv_st, output with o_st.
+int attn_general_impl(const void* q, const void* k, const void* v, void* o, float* lse, int64_t B,
+                      int64_t X, int64_t Lq, int64_t Lk, int H, int Hkv, int D, const int64_t* q_st,
+                      const int64_t* kv_st, const int64_t* o_st, float scale, int dtype, void* stream) {
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
-  if (!in_st || !out_st) return DSP_ERR_NULL;
-  if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
-  if ((!q || !k || !v || !o) && B != 0 && X != 0 && L != 0) return DSP_ERR_NULL;
+  if (!q_st || !kv_st || !o_st) return DSP_ERR_NULL;
+  if (B < 0 || X < 0 || Lq < 0 || Lk < 0 || H < 1 || D < 1 || Hkv < 1 || H % Hkv) return DSP_ERR_SHAPE;
+  const bool empty = B == 0 || X == 0 || Lq == 0;
+  if (!empty && Lk == 0) return DSP_ERR_SHAPE;  // a softmax over no keys
+  if ((!q || !k || !v || !o) && !empty) return DSP_ERR_NULL;
   for (int i = 0; i < 3; ++i)
-    if (in_st[i] < 0 || out_st[i] < 0) return DSP_ERR_SHAPE;
+    if (q_st[i] < 0 || kv_st[i] < 0 || o_st[i] < 0) return DSP_ERR_SHAPE;
   if (isnan(scale) || isinf(scale)) return DSP_ERR_ARG;
+  if (lse && !aligned(lse, 4)) return DSP_ERR_ALIGN;
   int64_t width;
   if (!mul_ok(H, D, &width)) return DSP_ERR_SHAPE;
   if (dtype == DSP_BF16) {
     if (!attn_bf16_supports(D)) return DSP_ERR_SHAPE;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return DSP_ERR_ALIGN;
     for (int i = 0; i < 3; ++i)
-      if (in_st[i] % 8 || out_st[i] % 8) return DSP_ERR_ALIGN;
+      if (q_st[i] % 8 || kv_st[i] % 8 || o_st[i] % 8) return DSP_ERR_ALIGN;
   } else if (D > 256) {
     return DSP_ERR_SHAPE;
   }
-  if (B == 0 || X == 0 || L == 0) return DSP_OK;
+  if (empty) return DSP_OK;
   // every output row is written by exactly one unit
-  if (!rows_disjoint(B, X, L, out_st, width)) return DSP_ERR_ARG;
-  // the largest element offset of either side must be addressable
-  for (const int64_t* st : {in_st, out_st}) {
+  if (!rows_disjoint(B, X, Lq, o_st, width)) return DSP_ERR_ARG;
+  // the largest element offset of each side must be addressable
+  const int64_t* sts[3] = {q_st, kv_st, o_st};
+  const int64_t lens[3] = {Lq, Lk, Lq};
+  for (int i = 0; i < 3; ++i) {
     int64_t tb, tx, tl;
-    if (!mul_ok(B - 1, st[0], &tb) || !mul_ok(X - 1, st[1], &tx) || !mul_ok(L - 1, st[2], &tl) ||
+    if (!mul_ok(B - 1, sts[i][0], &tb) || !mul_ok(X - 1, sts[i][1], &tx) || !mul_ok(lens[i] - 1, sts[i][2], &tl) ||
         tb > INT64_MAX / 4 || tx > INT64_MAX / 4 || tl > INT64_MAX / 4)
       return DSP_ERR_SHAPE;
   }
   AttnArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o;
-  a.B = B; a.X = X; a.L = L; a.H = H; a.D = D;
-  a.b_stride_in = in_st[0];
-  a.x_stride_in = in_st[1];
-  a.r_stride_in = in_st[2];
-  a.b_stride_out = out_st[0];
-  a.x_stride_out = out_st[1];
-  a.r_stride_out = out_st[2];
+  a.B = B; a.X = X; a.L = Lq; a.H = H; a.D = D;
+  a.b_stride_in = q_st[0];
+  a.x_stride_in = q_st[1];
+  a.r_stride_in = q_st[2];
+  a.b_stride_out = o_st[0];
+  a.x_stride_out = o_st[1];
+  a.r_stride_out = o_st[2];
+  a.Lk = Lk;
+  a.Hkv = Hkv;
+  a.b_stride_kv = kv_st[0];
+  a.x_stride_kv = kv_st[1];
+  a.r_stride_kv = kv_st[2];
   a.scale = scale > 0.0f ? scale : (float)(1.0 / sqrt((double)D));
   a.lse = lse;
   hipStream_t s = as_stream(stream);
   return dtype == DSP_BF16 ? launch_attn_bf16(a, s) : launch_attn_f32(a, s);
+}
+
+int attn_impl_strided(const void* q, const void* k, const void* v, void* o, int64_t B, int64_t X,
+                      int64_t L, int H, int D, const int64_t* in_st, const int64_t* out_st,
+                      float scale, int dtype, void* stream, float* lse = nullptr) {
+  return attn_general_impl(q, k, v, o, lse, B, X, L, L, H, H, D, in_st, in_st, out_st, scale, dtype, stream);
 }
 
 // The largest element offset of a (B, X, L) grid of rows with strides st is
@@ -195,45 +213,49 @@ bool offsets_ok(int64_t B, int64_t X, int64_t L, const int64_t* st) {
          tb <= INT64_MAX / 4 && tx <= INT64_MAX / 4 && tl <= INT64_MAX / 4;
 }
 
-int attn_bwd_impl(const void* q, const void* k, const void* v, const void* o, const void* dout,
-                  const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
-                  int64_t L, int H, int D, const int64_t* qkv_st, const int64_t* o_st, float scale,
-                  int dtype, void* stream) {
+int attn_bwd_general_impl(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                          const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
+                          int64_t Lq, int64_t Lk, int H, int Hkv, int D, const int64_t* q_st,
+                          const int64_t* kv_st, const int64_t* o_st, float scale, int dtype, void* stream) {
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
-  if (!qkv_st || !o_st) return DSP_ERR_NULL;
-  if (B < 0 || X < 0 || L < 0 || H < 1 || D < 1) return DSP_ERR_SHAPE;
-  const bool empty = B == 0 || X == 0 || L == 0;
+  if (!q_st || !kv_st || !o_st) return DSP_ERR_NULL;
+  if (B < 0 || X < 0 || Lq < 0 || Lk < 0 || H < 1 || D < 1 || Hkv < 1 || H % Hkv) return DSP_ERR_SHAPE;
+  const bool empty = B == 0 || X == 0 || (Lq == 0 && Lk == 0);
+  if (!empty && (Lq == 0) != (Lk == 0)) return DSP_ERR_SHAPE;  // queries without keys, or keys without queries
   if (!empty && (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv || !delta))
     return DSP_ERR_NULL;
   for (int i = 0; i < 3; ++i)
-    if (qkv_st[i] < 0 || o_st[i] < 0) return DSP_ERR_SHAPE;
+    if (q_st[i] < 0 || kv_st[i] < 0 || o_st[i] < 0) return DSP_ERR_SHAPE;
   if (isnan(scale) || isinf(scale)) return DSP_ERR_ARG;
-  int64_t width, units, stat_elems;
-  if (!mul_ok(H, D, &width) || !mul_ok(B, X, &units) || !mul_ok(units, H, &units) ||
-      !mul_ok(units, L, &stat_elems))
+  int64_t width, kv_width, units, stat_elems;
+  if (!mul_ok(H, D, &width) || !mul_ok(Hkv, D, &kv_width) || !mul_ok(B, X, &units) || !mul_ok(units, H, &units) ||
+      !mul_ok(units, Lq, &stat_elems))
     return DSP_ERR_SHAPE;
   if (dtype == DSP_BF16) {
     if (!attn_bf16_supports(D) || D % 32 > 16) return DSP_ERR_SHAPE;
     for (const void* ptr : {q, k, v, o, dout, (const void*)dq, (const void*)dk, (const void*)dv})
       if (!aligned(ptr, 16)) return DSP_ERR_ALIGN;
     for (int i = 0; i < 3; ++i)
-      if (qkv_st[i] % 8 || o_st[i] % 8) return DSP_ERR_ALIGN;
+      if (q_st[i] % 8 || kv_st[i] % 8 || o_st[i] % 8) return DSP_ERR_ALIGN;
   } else if (D > 256) {
     return DSP_ERR_SHAPE;
   }
   if (!aligned(lse, 4) || !aligned(delta, 4)) return DSP_ERR_ALIGN;
   if (empty) return DSP_OK;
-  // every gradient row is written by exactly one (unit, position)
-  if (!rows_disjoint(B, X, L, qkv_st, width)) return DSP_ERR_ARG;
-  if (!offsets_ok(B, X, L, qkv_st) || !offsets_ok(B, X, L, o_st)) return DSP_ERR_SHAPE;
+  // every gradient row is written by exactly one (unit, position): key/value
+  // rows shared by several units (a broadcast layout) have no single owner
+  if (!rows_disjoint(B, X, Lq, q_st, width) || !rows_disjoint(B, X, Lk, kv_st, kv_width)) return DSP_ERR_ARG;
+  if (!offsets_ok(B, X, Lq, q_st) || !offsets_ok(B, X, Lk, kv_st) || !offsets_ok(B, X, Lq, o_st))
+    return DSP_ERR_SHAPE;
   if (stat_elems > INT64_MAX / 8) return DSP_ERR_SHAPE;
   if (overlap(delta, (size_t)stat_elems * 4, lse, (size_t)stat_elems * 4)) return DSP_ERR_ARG;
   AttnBwdArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lse = lse;
   a.dq = dq; a.dk = dk; a.dv = dv; a.delta = delta;
-  a.B = B; a.X = X; a.L = L; a.H = H; a.D = D;
+  a.B = B; a.X = X; a.L = Lq; a.Lk = Lk; a.H = H; a.Hkv = Hkv; a.D = D;
   for (int i = 0; i < 3; ++i) {
-    a.qkv_strides[i] = qkv_st[i];
+    a.q_strides[i] = q_st[i];
+    a.kv_strides[i] = kv_st[i];
     a.o_strides[i] = o_st[i];
   }
   a.scale = scale > 0.0f ? scale : (float)(1.0 / sqrt((double)D));
@@ -243,6 +265,14 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* o, co
     return launch_attn_bwd_bf16(a, s);
   }
   return launch_attn_bwd_f32(a, s);
+}
+
+int attn_bwd_impl(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                  const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
+                  int64_t L, int H, int D, const int64_t* qkv_st, const int64_t* o_st, float scale,
+                  int dtype, void* stream) {
+  return attn_bwd_general_impl(q, k, v, o, dout, lse, dq, dk, dv, delta, B, X, L, L, H, H, D, qkv_st, qkv_st, o_st,
+                               scale, dtype, stream);
 }
 
 // Spatial (B,T,S,*): unit (b, t), positions s.  Temporal (B,S,T,*): unit
@@ -537,6 +567,22 @@ int dsp_attn_bwd(const void* q, const void* k, const void* v, const void* o, con
                  float scale, int dtype, void* stream) {
   return attn_bwd_impl(q, k, v, o, dout, lse, dq, dk, dv, delta, B, X, L, H, D, qkv_strides, o_strides,
                        scale, dtype, stream);
+}
+
+int dsp_attn_general(const void* q, const void* k, const void* v, void* o, float* lse, int64_t B, int64_t X,
+                     int64_t Lq, int64_t Lk, int H, int Hkv, int D, const int64_t* q_strides,
+                     const int64_t* kv_strides, const int64_t* o_strides, float scale, int dtype, void* stream) {
+  return attn_general_impl(q, k, v, o, lse, B, X, Lq, Lk, H, Hkv, D, q_strides, kv_strides, o_strides, scale, dtype,
+                           stream);
+}
+
+int dsp_attn_general_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                         const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
+                         int64_t Lq, int64_t Lk, int H, int Hkv, int D, const int64_t* q_strides,
+                         const int64_t* kv_strides, const int64_t* o_strides, float scale, int dtype,
+                         void* stream) {
+  return attn_bwd_general_impl(q, k, v, o, dout, lse, dq, dk, dv, delta, B, X, Lq, Lk, H, Hkv, D, q_strides,
+                               kv_strides, o_strides, scale, dtype, stream);
 }
 
 int dsp_linear_bwd_data(const void* dy, const void* w, const void* u, void* dx, int64_t M, int N, int K,

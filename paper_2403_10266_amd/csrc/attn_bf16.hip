@@ -118,14 +118,16 @@ struct Params {
   bf16* o;
   float* lse;  // optional row log-sum-exp output
   int64_t b_in, x_in, r_in, b_out, x_out, r_out;
+  int64_t b_kv, x_kv, r_kv;  // k and v
   uint32_t X, H, L, n_units, n_qb, n_blocks;
+  uint32_t Lk, grp;          // keys per unit; query heads per key/value head
   float c;  // scale * log2(e)
 };
 
 // Work-group -> unit and query block (XCD-aware), and the unit's base offsets.
 struct UnitMap {
   uint32_t unit, qb;
-  int64_t in_base, out_base;
+  int64_t in_base, out_base, kv_base;
 };
 
 __device__ __forceinline__ UnitMap map_unit(const Params& p, int D) {
@@ -142,6 +144,7 @@ __device__ __forceinline__ UnitMap map_unit(const Params& p, int D) {
   const uint32_t bb = bx / p.X;
   m.in_base = (int64_t)bb * p.b_in + (int64_t)xx * p.x_in + (int64_t)h * D;
   m.out_base = (int64_t)bb * p.b_out + (int64_t)xx * p.x_out + (int64_t)h * D;
+  m.kv_base = (int64_t)bb * p.b_kv + (int64_t)xx * p.x_kv + (int64_t)(h / p.grp) * D;
   return m;
 }
 
@@ -166,7 +169,8 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   const int l32 = lane & 31;
   const int g = lane >> 5;
   const UnitMap um = map_unit(p, D);
-  const uint32_t L = p.L;
+  const uint32_t L = p.L;     // queries of the unit
+  const uint32_t Lk = p.Lk;   // keys and values of the unit
 
   // ---- padding columns of the LDS buffers.  K: column D is 1.0 when it
   // carries the bias, the rest 0.  V: column D is 1.0 (row sum), the rest 0.
@@ -209,7 +213,7 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   // fetch K and the others V; a single wave fetches both.
   const bool fetch_v = SPLIT && wave >= NW / 2;
   const int ft = SPLIT ? threadIdx.x % FT : threadIdx.x;
-  const uint32_t row_bytes = (uint32_t)p.r_in * 2u;
+  const uint32_t row_bytes = (uint32_t)p.r_kv * 2u;
   uint32_t voff[NLOAD];
   int lofs[NLOAD];
 #pragma unroll
@@ -223,8 +227,8 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   // the range covers the tile's own rows only, so that widely strided rows
   // (a row stride of many megabytes) still fit a 32-bit byte range
   auto rsrc = [&](const bf16* tensor, uint32_t kb) {
-    const uint32_t rows_left = kb < L ? min(L - kb, (uint32_t)KB) : 0u;
-    return make_rsrc(tensor + um.in_base + (int64_t)kb * p.r_in, rows_left * row_bytes);
+    const uint32_t rows_left = kb < Lk ? min(Lk - kb, (uint32_t)KB) : 0u;
+    return make_rsrc(tensor + um.kv_base + (int64_t)kb * p.r_kv, rows_left * row_bytes);
   };
   u32x4 pre[SPLIT ? NLOAD : 1];
   auto fetch = [&](uint32_t kb) {  // SPLIT: one tensor into registers
@@ -280,7 +284,7 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
 #pragma unroll
   for (int j = 0; j < QT; ++j) { m_ref[j] = -INFINITY; l_run[j] = 0.0f; }
 
-  const uint32_t n_kb = (L + KB - 1) / KB;
+  const uint32_t n_kb = (Lk + KB - 1) / KB;
   if (SPLIT) {
     fetch(0);
     stash(0);
@@ -336,13 +340,13 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
           s[kt][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[j][st], s[kt][j], 0, 0, 0);
       }
 #endif
-    if (kb + KB > L) {  // keys past L: score -inf (only the last tile can hold any)
+    if (kb + KB > Lk) {  // keys past Lk: score -inf (only the last tile can hold any)
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const uint32_t key = kb + 32 * kt + (r / 4) * 8 + 4 * g + (r % 4);
-          if (key >= L) {
+          if (key >= Lk) {
 #pragma unroll
             for (int j = 0; j < QT; ++j) s[kt][j][r] = -INFINITY;
           }
@@ -563,6 +567,11 @@ int64_t make_params(const AttnArgs& a, int QB, int KB, Params& p) {
   p.b_in = a.b_stride_in;
   p.x_in = a.x_stride_in;
   p.r_in = a.r_stride_in;
+  p.b_kv = a.b_stride_kv;
+  p.x_kv = a.x_stride_kv;
+  p.r_kv = a.r_stride_kv;
+  p.Lk = (uint32_t)a.Lk;
+  p.grp = (uint32_t)(a.H / a.Hkv);
   p.b_out = a.b_stride_out;
   p.x_out = a.x_stride_out;
   p.r_out = a.r_stride_out;
@@ -574,7 +583,7 @@ int64_t make_params(const AttnArgs& a, int QB, int KB, Params& p) {
   const int64_t blocks = units * n_qb;
   if (blocks == 0) return 0;
   // a tile's buffer resource addresses its rows with 32-bit byte offsets
-  if (blocks >= (int64_t(1) << 31) || std::min<int64_t>(a.L, KB) * a.r_stride_in * 2 >= (int64_t(1) << 31))
+  if (blocks >= (int64_t(1) << 31) || std::min<int64_t>(a.Lk, KB) * a.r_stride_kv * 2 >= (int64_t(1) << 31))
     return -1;
   p.n_units = (uint32_t)units;
   p.n_qb = (uint32_t)n_qb;
@@ -585,7 +594,7 @@ int64_t make_params(const AttnArgs& a, int QB, int KB, Params& p) {
 
 template <int D, int NW, int QT, int KB, int MINW, int NBUF = 2>
 int launch_cfg(const AttnArgs& a, hipStream_t s) {
-  if (NBUF == 1 && a.L > KB) return DSP_ERR_SHAPE;
+  if (NBUF == 1 && a.Lk > KB) return DSP_ERR_SHAPE;
   Params p;
   const int64_t blocks = make_params(a, NW * 32 * QT, KB, p);
   if (blocks <= 0) return blocks == 0 ? DSP_OK : DSP_ERR_SHAPE;
@@ -596,10 +605,11 @@ int launch_cfg(const AttnArgs& a, hipStream_t s) {
 
 template <int D>
 int launch_d(const AttnArgs& a, hipStream_t s) {
-  // short sequences: the whole unit is one tile, fetched at once
-  if (a.L <= 32) return launch_cfg<D, 1, 1, 32, 1, 1>(a, s);
-  if (a.L <= 64) return launch_cfg<D, 2, 1, 64, 2, 1>(a, s);
-  if (a.L <= 128) {
+  // few keys: all of a unit's keys are one tile, fetched at once (the tiling
+  // is chosen by the key count; any number of queries runs in query blocks)
+  if (a.Lk <= 32) return launch_cfg<D, 1, 1, 32, 1, 1>(a, s);
+  if (a.Lk <= 64) return launch_cfg<D, 2, 1, 64, 2, 1>(a, s);
+  if (a.Lk <= 128) {
     if constexpr (DSP_TATTN_KB >= 128)
       return launch_cfg<D, DSP_TATTN_NW, DSP_TATTN_QT, 128, DSP_TATTN_MINW, 1>(a, s);
     else

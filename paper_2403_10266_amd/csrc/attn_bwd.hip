@@ -63,29 +63,34 @@ struct BwdParams {
   bf16* dk;
   bf16* dv;
   float* delta;
-  int64_t b_in, x_in, r_in;  // q, k, v and dq, dk, dv
+  int64_t b_q, x_q, r_q;     // q and dq
+  int64_t b_kv, x_kv, r_kv;  // k, v and dk, dv
   int64_t b_o, x_o, r_o;     // o and dout
-  uint32_t X, H, L, n_blk, n_blocks;
+  uint32_t X, H, L, Lk, grp, n_blk, n_blocks;  // L queries, Lk keys; grp query heads per kv head
   float c;      // scale * log2(e)
   float scale;
 };
 
+// Work-group -> (unit, block) with an XCD-aware order; units are (b, x, head)
+// over `heads` heads per (b, x).  Also the (b, x) index for the bases.
 struct BwdMap {
-  uint32_t unit, blk;
-  int64_t in_base, o_base;
+  uint32_t unit, blk, bx, head;
 };
 
-__device__ __forceinline__ BwdMap bwd_map(const BwdParams& p, int D) {
+__device__ __forceinline__ BwdMap bwd_map(const BwdParams& p, uint32_t heads) {
   uint32_t bid = blockIdx.x;
   // hardware places block i on XCD i % 8; give each XCD a contiguous range
   if ((p.n_blocks & 7u) == 0) bid = (bid & 7u) * (p.n_blocks >> 3) + (bid >> 3);
   BwdMap m;
   m.unit = bid / p.n_blk;
   m.blk = bid - m.unit * p.n_blk;
-  const uint32_t h = m.unit % p.H, bx = m.unit / p.H, xx = bx % p.X, bb = bx / p.X;
-  m.in_base = (int64_t)bb * p.b_in + (int64_t)xx * p.x_in + (int64_t)h * D;
-  m.o_base = (int64_t)bb * p.b_o + (int64_t)xx * p.x_o + (int64_t)h * D;
+  m.head = m.unit % heads;
+  m.bx = m.unit / heads;
   return m;
+}
+
+__device__ __forceinline__ int64_t bx_base(const BwdParams& p, uint32_t bx, int64_t bs, int64_t xs) {
+  return (int64_t)(bx / p.X) * bs + (int64_t)(bx % p.X) * xs;
 }
 
 // A operand of a 32x32x16 MFMA read transposed from a row-major LDS tile:
@@ -208,8 +213,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, g = lane >> 5;
-  const BwdMap um = bwd_map(p, D);
-  const uint32_t L = p.L;
+  const BwdMap um = bwd_map(p, p.H);  // unit = a query head's (b, x, h)
+  const uint32_t L = p.L, Lk = p.Lk;
+  const int64_t q_base = bx_base(p, um.bx, p.b_q, p.x_q) + (int64_t)um.head * D;
+  const int64_t o_base = bx_base(p, um.bx, p.b_o, p.x_o) + (int64_t)um.head * D;
+  const int64_t kv_base = bx_base(p, um.bx, p.b_kv, p.x_kv) + (int64_t)(um.head / p.grp) * D;
 
   // padding columns of both buffers: D and D + 1 are 1.0 (they multiply the
   // bias columns of the query side), the rest 0
@@ -223,9 +231,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
   const uint32_t q = um.blk * 32 * NW + 32 * wave + l32;
   const bool qv = q < L;
   bf16x8 qf[G::NDK], df[G::NDK], of[G::NDK];
-  row_frags<D>(qv ? p.q + um.in_base + (int64_t)q * p.r_in : nullptr, g, qf);
-  row_frags<D>(qv ? p.dout + um.o_base + (int64_t)q * p.r_o : nullptr, g, df);
-  row_frags<D>(qv ? p.o + um.o_base + (int64_t)q * p.r_o : nullptr, g, of);
+  row_frags<D>(qv ? p.q + q_base + (int64_t)q * p.r_q : nullptr, g, qf);
+  row_frags<D>(qv ? p.dout + o_base + (int64_t)q * p.r_o : nullptr, g, df);
+  row_frags<D>(qv ? p.o + o_base + (int64_t)q * p.r_o : nullptr, g, of);
   float dl = 0.0f;
 #pragma unroll
   for (int s = 0; s < G::NDK; ++s)
@@ -248,7 +256,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
   // tile fetch: waves [0, NW/2) K, the others V; rows past L read as zero
   const bool fetch_v = wave >= NW / 2;
   const int ft = threadIdx.x % FT;
-  const uint32_t row_bytes = (uint32_t)p.r_in * 2u;
+  const uint32_t row_bytes = (uint32_t)p.r_kv * 2u;
   uint32_t voff[NLOAD];
   int lofs[NLOAD];
 #pragma unroll
@@ -260,9 +268,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
   }
   u32x4 pre[NLOAD];
   auto fetch = [&](uint32_t kb) {
-    const uint32_t rows = kb < L ? min(L - kb, (uint32_t)KB) : 0u;
+    const uint32_t rows = kb < Lk ? min(Lk - kb, (uint32_t)KB) : 0u;
     const __amdgpu_buffer_rsrc_t rs =
-        make_rsrc((fetch_v ? p.v : p.k) + um.in_base + (int64_t)kb * p.r_in, rows * row_bytes);
+        make_rsrc((fetch_v ? p.v : p.k) + kv_base + (int64_t)kb * p.r_kv, rows * row_bytes);
 #pragma unroll
     for (int i = 0; i < NLOAD; ++i)
       if (ft + i * FT < TCH) pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
@@ -284,7 +292,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) dqs[h][r] = 0.0f;
 
-  const uint32_t n_kb = (L + KB - 1) / KB;
+  const uint32_t n_kb = (Lk + KB - 1) / KB;
   fetch(0);
   stash(0);
   __syncthreads();
@@ -310,14 +318,14 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
         dp[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, df[st], dp[kt], 0, 0, 0);
       }
     // lane (n + 32g) holds keys kb + 32kt + 8(r/4) + 4g + r%4 of query n
-    const bool tail = kb + KB > L;
+    const bool tail = kb + KB > Lk;
     bf16x8 zb[NKT][2];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float pr = __builtin_amdgcn_exp2f(s[kt][r]);
-        if (tail && kb + 32 * kt + (r / 4) * 8 + 4 * g + (r % 4) >= L) pr = 0.0f;
+        if (tail && kb + 32 * kt + (r / 4) * 8 + 4 * g + (r % 4) >= Lk) pr = 0.0f;
         zb[kt][r / 8][r % 8] = (bf16)(pr * dp[kt][r]);
       }
     // dQ^T += K^T dZ^T
@@ -342,7 +350,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
     if (more) stash((it + 1) & 1);
     __syncthreads();
   }
-  store_rows<D>(p.dq + um.in_base, p.r_in, um.blk * 32 * NW + 32 * wave, L, lane, dqt, dqs, p.scale);
+  store_rows<D>(p.dq + q_base, p.r_q, um.blk * 32 * NW + 32 * wave, L, lane, dqt, dqs, p.scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -352,6 +360,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
 // 32-query step:
 //   S = Q' K^T - lse2  -> P = exp2(S);   dP = dO V^T - Delta -> dZ = P * dP
 //   dV^T += dO^T P;    dK^T += Q'^T dZ
+// With grouped key/value heads the keys belong to a key/value head, and the
+// query tiles of every query head of its group are visited in turn, so dK and
+// dV are the sums over the group (in a fixed order).
 // Query rows past L are zero with zero bias, so they contribute nothing.
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
@@ -366,8 +377,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, g = lane >> 5;
-  const BwdMap um = bwd_map(p, D);
-  const uint32_t L = p.L;
+  const BwdMap um = bwd_map(p, p.H / p.grp);  // unit = a key/value head's (b, x, h_kv)
+  const uint32_t L = p.L, Lk = p.Lk;
+  const int64_t kv_base = bx_base(p, um.bx, p.b_kv, p.x_kv) + (int64_t)um.head * D;
+  const int64_t q_bx = bx_base(p, um.bx, p.b_q, p.x_q), o_bx = bx_base(p, um.bx, p.b_o, p.x_o);
+  const uint32_t hq0 = um.head * p.grp;                 // first query head of the group
 
   // padding columns past the bias pair: 0 (the bias columns are rewritten per tile)
   for (int e = threadIdx.x; e < 4 * QB; e += NT) {
@@ -378,10 +392,10 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
   // this wave's 32 keys: K and V row fragments, bias columns 1.0
   const uint32_t key0 = um.blk * 32 * NW + 32 * wave;
   const uint32_t key = key0 + l32;
-  const bool kv = key < L;
+  const bool kv = key < Lk;
   bf16x8 kf[G::NDK], vf[G::NDK];
-  row_frags<D>(kv ? p.k + um.in_base + (int64_t)key * p.r_in : nullptr, g, kf);
-  row_frags<D>(kv ? p.v + um.in_base + (int64_t)key * p.r_in : nullptr, g, vf);
+  row_frags<D>(kv ? p.k + kv_base + (int64_t)key * p.r_kv : nullptr, g, kf);
+  row_frags<D>(kv ? p.v + kv_base + (int64_t)key * p.r_kv : nullptr, g, vf);
   if (g == G::GB) {
     kf[G::SB][0] = kf[G::SB][1] = vf[G::SB][0] = vf[G::SB][1] = (bf16)1.0f;
   }
@@ -390,7 +404,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
   // threads ft < QB of each half also fetch the row's lse or Delta
   const bool fetch_do = wave >= NW / 2;
   const int ft = threadIdx.x % FT;
-  const uint32_t qrow_bytes = (uint32_t)p.r_in * 2u, orow_bytes = (uint32_t)p.r_o * 2u;
+  const uint32_t qrow_bytes = (uint32_t)p.r_q * 2u, orow_bytes = (uint32_t)p.r_o * 2u;
   const uint32_t row_bytes = fetch_do ? orow_bytes : qrow_bytes;
   uint32_t voff[NLOAD];
   int lofs[NLOAD];
@@ -404,15 +418,19 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
   const float* stat = fetch_do ? p.delta : p.lse;
   u32x4 pre[NLOAD];
   float pstat = 0.0f;
-  auto fetch = [&](uint32_t qb) {
+  // tile `it` of the group's query heads: head hq0 + it / n_qt, queries from (it % n_qt) QB
+  const uint32_t n_qt = (L + QB - 1) / QB;
+  auto fetch = [&](uint32_t it) {
+    const uint32_t hq = hq0 + it / n_qt, qb = (it % n_qt) * QB;
     const uint32_t rows = qb < L ? min(L - qb, (uint32_t)QB) : 0u;
-    const bf16* base = fetch_do ? p.dout + um.o_base + (int64_t)qb * p.r_o
-                                : p.q + um.in_base + (int64_t)qb * p.r_in;
+    const bf16* base = fetch_do ? p.dout + o_bx + (int64_t)hq * D + (int64_t)qb * p.r_o
+                                : p.q + q_bx + (int64_t)hq * D + (int64_t)qb * p.r_q;
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(base, rows * row_bytes);
 #pragma unroll
     for (int i = 0; i < NLOAD; ++i)
       if (ft + i * FT < TCH) pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
-    pstat = (ft < QB && qb + ft < L) ? stat[(int64_t)um.unit * L + qb + ft] : 0.0f;
+    const uint32_t unit_q = um.bx * p.H + hq;
+    pstat = (ft < QB && qb + ft < L) ? stat[(int64_t)unit_q * L + qb + ft] : 0.0f;
   };
   auto stash = [&](int buf) {
     bf16* t = lds + buf * TILE;
@@ -448,16 +466,16 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) dvs[h][r] = dks[h][r] = 0.0f;
 
-  const uint32_t n_qt = (L + QB - 1) / QB;
+  const uint32_t n_it = n_qt * p.grp;
   fetch(0);
   stash(0);
   __syncthreads();
-  for (uint32_t it = 0; it < n_qt; ++it) {
-    const bool more = it + 1 < n_qt;
-    if (more) fetch((it + 1) * QB);
+  for (uint32_t it = 0; it < n_it; ++it) {
+    const bool more = it + 1 < n_it;
+    if (more) fetch(it + 1);
     const bf16* q_lds = lds + (it & 1) * TILE;
     const bf16* o_lds = q_lds + QB * G::P;
-    if (key0 < L) {  // wave-uniform: waves whose keys are all past L only fetch
+    if (key0 < Lk) {  // wave-uniform: waves whose keys are all past Lk only fetch
 #pragma unroll
       for (int sub = 0; sub < QB / 32; ++sub) {
         const int q0 = 32 * sub;
@@ -505,12 +523,14 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
     __syncthreads();
   }
   // dK = scale * dZ^T Q = ln 2 * dZ^T Q'
-  store_rows<D>(p.dv + um.in_base, p.r_in, key0, L, lane, dvt, dvs, 1.0f);
-  store_rows<D>(p.dk + um.in_base, p.r_in, key0, L, lane, dkt, dks, kLn2);
+  store_rows<D>(p.dv + kv_base, p.r_kv, key0, Lk, lane, dvt, dvs, 1.0f);
+  store_rows<D>(p.dk + kv_base, p.r_kv, key0, Lk, lane, dkt, dks, kLn2);
 }
 
 // ---------------------------------------------------------------------------
-// fp32 path: plain FMA loops.  One thread per (unit, row, 32-column slice).
+// fp32 path: plain FMA loops.  One thread per (unit, row, 32-column slice):
+// the dQ kernel's units are query heads (rows: queries), the dK/dV kernel's
+// key/value heads (rows: keys; it visits every query head of the group).
 constexpr int DC = 32;
 
 struct BwdParamsF {
@@ -524,28 +544,10 @@ struct BwdParamsF {
   float* dk;
   float* dv;
   float* delta;
-  int64_t b_in, x_in, r_in, b_o, x_o, r_o;
-  int64_t X, H, L, D, n_dc, total;
+  int64_t b_q, x_q, r_q, b_kv, x_kv, r_kv, b_o, x_o, r_o;
+  int64_t X, H, L, Lk, grp, D, n_dc;
   float scale;
 };
-
-struct RowRef {
-  int64_t unit, row, c0, nc, in_base, o_base;
-};
-
-__device__ __forceinline__ RowRef row_ref(const BwdParamsF& p, int64_t tid) {
-  RowRef r;
-  const int64_t dc = tid % p.n_dc;
-  const int64_t ur = tid / p.n_dc;
-  r.row = ur % p.L;
-  r.unit = ur / p.L;
-  const int64_t h = r.unit % p.H, bx = r.unit / p.H, xx = bx % p.X, bb = bx / p.X;
-  r.in_base = bb * p.b_in + xx * p.x_in + h * p.D;
-  r.o_base = bb * p.b_o + xx * p.x_o + h * p.D;
-  r.c0 = dc * DC;
-  r.nc = min((int64_t)DC, p.D - r.c0);
-  return r;
-}
 
 __device__ __forceinline__ float dotf(const float* a, const float* b, int64_t n) {
   float s = 0.0f;
@@ -553,61 +555,89 @@ __device__ __forceinline__ float dotf(const float* a, const float* b, int64_t n)
   return s;
 }
 
-__global__ __launch_bounds__(256) void attn_bwd_f32_dq_kernel(BwdParamsF p) {
+__global__ __launch_bounds__(256) void attn_bwd_f32_dq_kernel(BwdParamsF p, int64_t total) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid >= p.total) return;
-  const RowRef r = row_ref(p, tid);
-  const float* qrow = p.q + r.in_base + r.row * p.r_in;
-  const float* drow = p.dout + r.o_base + r.row * p.r_o;
-  const float delta = dotf(drow, p.o + r.o_base + r.row * p.r_o, p.D);
-  const float lse = p.lse[r.unit * p.L + r.row];
-  if (r.c0 == 0) p.delta[r.unit * p.L + r.row] = delta;
+  if (tid >= total) return;
+  const int64_t c0 = (tid % p.n_dc) * DC, ur = tid / p.n_dc;
+  const int64_t nc = min((int64_t)DC, p.D - c0);
+  const int64_t row = ur % p.L, unit = ur / p.L;
+  const int64_t h = unit % p.H, bx = unit / p.H, xx = bx % p.X, bb = bx / p.X;
+  const float* qrow = p.q + bb * p.b_q + xx * p.x_q + h * p.D + row * p.r_q;
+  const int64_t ob = bb * p.b_o + xx * p.x_o + h * p.D + row * p.r_o;
+  const int64_t kvb = bb * p.b_kv + xx * p.x_kv + (h / p.grp) * p.D;
+  const float* drow = p.dout + ob;
+  const float delta = dotf(drow, p.o + ob, p.D);
+  const float lse = p.lse[unit * p.L + row];
+  if (c0 == 0) p.delta[unit * p.L + row] = delta;
   float acc[DC];
 #pragma unroll
   for (int c = 0; c < DC; ++c) acc[c] = 0.0f;
-  for (int64_t j = 0; j < p.L; ++j) {
-    const float* krow = p.k + r.in_base + j * p.r_in;
+  for (int64_t j = 0; j < p.Lk; ++j) {
+    const float* krow = p.k + kvb + j * p.r_kv;
     const float pr = expf(dotf(qrow, krow, p.D) * p.scale - lse);
-    const float dz = pr * (dotf(drow, p.v + r.in_base + j * p.r_in, p.D) - delta);
+    const float dz = pr * (dotf(drow, p.v + kvb + j * p.r_kv, p.D) - delta);
 #pragma unroll
     for (int c = 0; c < DC; ++c)
-      if (c < r.nc) acc[c] = fmaf(dz, krow[r.c0 + c], acc[c]);
+      if (c < nc) acc[c] = fmaf(dz, krow[c0 + c], acc[c]);
   }
-  float* out = p.dq + r.in_base + r.row * p.r_in + r.c0;
+  float* out = p.dq + bb * p.b_q + xx * p.x_q + h * p.D + row * p.r_q + c0;
 #pragma unroll
   for (int c = 0; c < DC; ++c)
-    if (c < r.nc) out[c] = acc[c] * p.scale;
+    if (c < nc) out[c] = acc[c] * p.scale;
 }
 
-__global__ __launch_bounds__(256) void attn_bwd_f32_dkv_kernel(BwdParamsF p) {
+__global__ __launch_bounds__(256) void attn_bwd_f32_dkv_kernel(BwdParamsF p, int64_t total) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid >= p.total) return;
-  const RowRef r = row_ref(p, tid);
-  const float* krow = p.k + r.in_base + r.row * p.r_in;
-  const float* vrow = p.v + r.in_base + r.row * p.r_in;
+  if (tid >= total) return;
+  const int64_t Hkv = p.H / p.grp;
+  const int64_t c0 = (tid % p.n_dc) * DC, ur = tid / p.n_dc;
+  const int64_t nc = min((int64_t)DC, p.D - c0);
+  const int64_t key = ur % p.Lk, unit = ur / p.Lk;
+  const int64_t hk = unit % Hkv, bx = unit / Hkv, xx = bx % p.X, bb = bx / p.X;
+  const int64_t kvb = bb * p.b_kv + xx * p.x_kv + hk * p.D + key * p.r_kv;
+  const float* krow = p.k + kvb;
+  const float* vrow = p.v + kvb;
   float ak[DC], av[DC];
 #pragma unroll
   for (int c = 0; c < DC; ++c) ak[c] = av[c] = 0.0f;
-  for (int64_t i = 0; i < p.L; ++i) {
-    const float* qrow = p.q + r.in_base + i * p.r_in;
-    const float* drow = p.dout + r.o_base + i * p.r_o;
-    const float pr = expf(dotf(qrow, krow, p.D) * p.scale - p.lse[r.unit * p.L + i]);
-    const float dz = pr * (dotf(drow, vrow, p.D) - p.delta[r.unit * p.L + i]);
+  for (int64_t hq = hk * p.grp; hq < (hk + 1) * p.grp; ++hq) {
+    const int64_t uq = bx * p.H + hq;
+    for (int64_t i = 0; i < p.L; ++i) {
+      const float* qrow = p.q + bb * p.b_q + xx * p.x_q + hq * p.D + i * p.r_q;
+      const float* drow = p.dout + bb * p.b_o + xx * p.x_o + hq * p.D + i * p.r_o;
+      const float pr = expf(dotf(qrow, krow, p.D) * p.scale - p.lse[uq * p.L + i]);
+      const float dz = pr * (dotf(drow, vrow, p.D) - p.delta[uq * p.L + i]);
 #pragma unroll
-    for (int c = 0; c < DC; ++c)
-      if (c < r.nc) {
-        ak[c] = fmaf(dz, qrow[r.c0 + c], ak[c]);
-        av[c] = fmaf(pr, drow[r.c0 + c], av[c]);
-      }
+      for (int c = 0; c < DC; ++c)
+        if (c < nc) {
+          ak[c] = fmaf(dz, qrow[c0 + c], ak[c]);
+          av[c] = fmaf(pr, drow[c0 + c], av[c]);
+        }
+    }
   }
-  float* ok = p.dk + r.in_base + r.row * p.r_in + r.c0;
-  float* ov = p.dv + r.in_base + r.row * p.r_in + r.c0;
+  float* ok = p.dk + kvb + c0;
+  float* ov = p.dv + kvb + c0;
 #pragma unroll
   for (int c = 0; c < DC; ++c)
-    if (c < r.nc) {
+    if (c < nc) {
       ok[c] = ak[c] * p.scale;
       ov[c] = av[c];
     }
+}
+
+template <typename P>
+void fill_common(P& p, const AttnBwdArgs& a) {
+  p.b_q = a.q_strides[0];
+  p.x_q = a.q_strides[1];
+  p.r_q = a.q_strides[2];
+  p.b_kv = a.kv_strides[0];
+  p.x_kv = a.kv_strides[1];
+  p.r_kv = a.kv_strides[2];
+  p.b_o = a.o_strides[0];
+  p.x_o = a.o_strides[1];
+  p.r_o = a.o_strides[2];
+  p.lse = a.lse;
+  p.delta = a.delta;
 }
 
 template <int D, int NW>
@@ -618,39 +648,41 @@ int launch_bwd_nw(const AttnBwdArgs& a, hipStream_t s) {
   p.v = static_cast<const bf16*>(a.v);
   p.o = static_cast<const bf16*>(a.o);
   p.dout = static_cast<const bf16*>(a.dout);
-  p.lse = a.lse;
   p.dq = static_cast<bf16*>(a.dq);
   p.dk = static_cast<bf16*>(a.dk);
   p.dv = static_cast<bf16*>(a.dv);
-  p.delta = a.delta;
-  p.b_in = a.qkv_strides[0];
-  p.x_in = a.qkv_strides[1];
-  p.r_in = a.qkv_strides[2];
-  p.b_o = a.o_strides[0];
-  p.x_o = a.o_strides[1];
-  p.r_o = a.o_strides[2];
+  fill_common(p, a);
   p.X = (uint32_t)a.X;
   p.H = (uint32_t)a.H;
   p.L = (uint32_t)a.L;
+  p.Lk = (uint32_t)a.Lk;
+  p.grp = (uint32_t)(a.H / a.Hkv);
   p.c = a.scale * kLog2e;
   p.scale = a.scale;
-  const int64_t units = a.B * a.X * a.H;
-  const int64_t n_blk = (a.L + 32 * NW - 1) / (32 * NW);
-  const int64_t blocks = units * n_blk;
-  if (blocks == 0) return DSP_OK;
-  p.n_blk = (uint32_t)n_blk;
-  p.n_blocks = (uint32_t)blocks;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW>), dim3((uint32_t)blocks), dim3(NW * 64), 0, s, p);
+  // dQ: query heads x blocks of 32 NW queries
+  const int64_t nq = (a.L + 32 * NW - 1) / (32 * NW);
+  const int64_t bq = a.B * a.X * a.H * nq;
+  if (bq == 0) return DSP_OK;
+  p.n_blk = (uint32_t)nq;
+  p.n_blocks = (uint32_t)bq;
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW>), dim3((uint32_t)bq), dim3(NW * 64), 0, s, p);
   int st = last_launch_status();
   if (st != DSP_OK) return st;
-  hipLaunchKernelGGL((attn_bwd_dkv_kernel<D, NW>), dim3((uint32_t)blocks), dim3(NW * 64), 0, s, p);
+  // dK, dV: key/value heads x blocks of 32 NW keys
+  const int64_t nk = (a.Lk + 32 * NW - 1) / (32 * NW);
+  const int64_t bk = a.B * a.X * a.Hkv * nk;
+  if (bk == 0) return DSP_OK;
+  p.n_blk = (uint32_t)nk;
+  p.n_blocks = (uint32_t)bk;
+  hipLaunchKernelGGL((attn_bwd_dkv_kernel<D, NW>), dim3((uint32_t)bk), dim3(NW * 64), 0, s, p);
   return last_launch_status();
 }
 
 template <int D>
 int launch_bwd_d(const AttnBwdArgs& a, hipStream_t s) {
-  if (a.L <= 64) return launch_bwd_nw<D, 2>(a, s);
-  if (a.L <= 128) return launch_bwd_nw<D, 4>(a, s);
+  const int64_t L = std::max(a.L, a.Lk);
+  if (L <= 64) return launch_bwd_nw<D, 2>(a, s);
+  if (L <= 128) return launch_bwd_nw<D, 4>(a, s);
   return launch_bwd_nw<D, 8>(a, s);
 }
 
@@ -658,10 +690,11 @@ int launch_bwd_d(const AttnBwdArgs& a, hipStream_t s) {
 
 bool attn_bwd_bf16_fits(const AttnBwdArgs& a) {
   // block indices, and the byte ranges of a 64-row tile, are 32-bit
-  const int64_t units = a.B * a.X * a.H;
-  const int64_t blocks = units * ((a.L + 63) / 64);
-  return blocks < (int64_t(1) << 31) && a.L < (int64_t(1) << 31) &&
-         64 * a.qkv_strides[2] * 2 < (int64_t(1) << 31) && 64 * a.o_strides[2] * 2 < (int64_t(1) << 31);
+  const int64_t L = std::max(a.L, a.Lk);
+  const int64_t blocks = a.B * a.X * a.H * ((L + 63) / 64);
+  return blocks < (int64_t(1) << 31) && L < (int64_t(1) << 31) &&
+         64 * a.q_strides[2] * 2 < (int64_t(1) << 31) && 64 * a.kv_strides[2] * 2 < (int64_t(1) << 31) &&
+         64 * a.o_strides[2] * 2 < (int64_t(1) << 31) && (int64_t)(a.H / a.Hkv) * ((a.L + 63) / 64) < (int64_t(1) << 31);
 }
 
 int launch_attn_bwd_bf16(const AttnBwdArgs& a, hipStream_t s) {
@@ -684,31 +717,25 @@ int launch_attn_bwd_f32(const AttnBwdArgs& a, hipStream_t s) {
   p.v = static_cast<const float*>(a.v);
   p.o = static_cast<const float*>(a.o);
   p.dout = static_cast<const float*>(a.dout);
-  p.lse = a.lse;
   p.dq = static_cast<float*>(a.dq);
   p.dk = static_cast<float*>(a.dk);
   p.dv = static_cast<float*>(a.dv);
-  p.delta = a.delta;
-  p.b_in = a.qkv_strides[0];
-  p.x_in = a.qkv_strides[1];
-  p.r_in = a.qkv_strides[2];
-  p.b_o = a.o_strides[0];
-  p.x_o = a.o_strides[1];
-  p.r_o = a.o_strides[2];
+  fill_common(p, a);
   p.X = a.X;
   p.H = a.H;
   p.L = a.L;
+  p.Lk = a.Lk;
+  p.grp = a.H / a.Hkv;
   p.D = a.D;
   p.n_dc = (a.D + DC - 1) / DC;
-  p.total = a.B * a.X * a.H * a.L * p.n_dc;
   p.scale = a.scale;
-  if (p.total == 0) return DSP_OK;
-  const int64_t blocks = (p.total + 255) / 256;
-  if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
-  hipLaunchKernelGGL(attn_bwd_f32_dq_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p);
+  const int64_t tq = a.B * a.X * a.H * a.L * p.n_dc, tk = a.B * a.X * a.Hkv * a.Lk * p.n_dc;
+  if (tq == 0) return DSP_OK;
+  if ((tq + 255) / 256 >= (int64_t(1) << 31) || (tk + 255) / 256 >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
+  hipLaunchKernelGGL(attn_bwd_f32_dq_kernel, dim3((uint32_t)((tq + 255) / 256)), dim3(256), 0, s, p, tq);
   int st = last_launch_status();
-  if (st != DSP_OK) return st;
-  hipLaunchKernelGGL(attn_bwd_f32_dkv_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p);
+  if (st != DSP_OK || tk == 0) return st;
+  hipLaunchKernelGGL(attn_bwd_f32_dkv_kernel, dim3((uint32_t)((tk + 255) / 256)), dim3(256), 0, s, p, tk);
   return last_launch_status();
 }
 

@@ -1,4 +1,5 @@
-// fp32 attention along one sequence dimension (Eq. 3 per head), the exact
+// fp32 attention along one sequence dimension (Eq. 3 per head; also grouped
+// key/value heads and a key length of its own for cross-attention), the exact
 // path: fp32 storage, fp32 FMA arithmetic, no reduced-precision operand
 // anywhere.  One thread owns one (unit, query, 32-column slice of the output):
 // a first pass over the keys finds the row maximum of the scaled scores, a
@@ -21,6 +22,7 @@ struct ParamsF {
   float* o;
   float* lse;  // optional row log-sum-exp output
   int64_t b_in, x_in, r_in, b_out, x_out, r_out;
+  int64_t b_kv, x_kv, r_kv, Lk, grp;  // keys/values: layout, count, query heads per kv head
   int64_t X, H, L, D, n_dc, total;
   float scale;
 };
@@ -39,11 +41,12 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(ParamsF p) {
   const int64_t bb = bx / p.X;
   const int64_t in_base = bb * p.b_in + xx * p.x_in + h * p.D;
   const float* qrow = p.q + in_base + qi * p.r_in;
-  const float* kb = p.k + in_base;
-  const float* vb = p.v + in_base;
+  const int64_t kv_base = bb * p.b_kv + xx * p.x_kv + (h / p.grp) * p.D;
+  const float* kb = p.k + kv_base;
+  const float* vb = p.v + kv_base;
   float m = -INFINITY;
-  for (int64_t j = 0; j < p.L; ++j) {
-    const float* krow = kb + j * p.r_in;
+  for (int64_t j = 0; j < p.Lk; ++j) {
+    const float* krow = kb + j * p.r_kv;
     float s = 0.0f;
     for (int64_t d = 0; d < p.D; ++d) s = fmaf(qrow[d], krow[d], s);
     m = fmaxf(m, s * p.scale);
@@ -54,13 +57,13 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(ParamsF p) {
 #pragma unroll
   for (int c = 0; c < DC; ++c) acc[c] = 0.0f;
   float l = 0.0f;
-  for (int64_t j = 0; j < p.L; ++j) {
-    const float* krow = kb + j * p.r_in;
+  for (int64_t j = 0; j < p.Lk; ++j) {
+    const float* krow = kb + j * p.r_kv;
     float s = 0.0f;
     for (int64_t d = 0; d < p.D; ++d) s = fmaf(qrow[d], krow[d], s);
     const float e = expf(s * p.scale - m);
     l += e;
-    const float* vrow = vb + j * p.r_in + c0;
+    const float* vrow = vb + j * p.r_kv + c0;
 #pragma unroll
     for (int c = 0; c < DC; ++c)
       if (c < nc) acc[c] = fmaf(e, vrow[c], acc[c]);
@@ -88,6 +91,11 @@ int launch_attn_f32(const AttnArgs& a, hipStream_t s) {
   p.b_out = a.b_stride_out;
   p.x_out = a.x_stride_out;
   p.r_out = a.r_stride_out;
+  p.b_kv = a.b_stride_kv;
+  p.x_kv = a.x_stride_kv;
+  p.r_kv = a.r_stride_kv;
+  p.Lk = a.Lk;
+  p.grp = a.H / a.Hkv;
   p.X = a.X;
   p.H = a.H;
   p.L = a.L;

@@ -421,8 +421,12 @@ int launch_short_d(const AttnArgs& a, hipStream_t s) {
 }  // namespace
 
 bool attn_bf16_short_fits(const AttnArgs& a) {
+  // self-attention only (queries, keys and values of one layout and length);
   // unit indices and the byte offsets of a unit's rows (up to the padded
   // tile of 128) are 32-bit in the kernel
+  if (a.Lk != a.L || a.Hkv != a.H || a.b_stride_kv != a.b_stride_in || a.x_stride_kv != a.x_stride_in ||
+      a.r_stride_kv != a.r_stride_in)
+    return false;
   return a.L >= 1 && a.L <= kShortAttnMaxL && a.B * a.X * a.H < (int64_t(1) << 32) &&
          (int64_t)kShortAttnMaxL * a.r_stride_in * 2 < (int64_t(1) << 31);
 }

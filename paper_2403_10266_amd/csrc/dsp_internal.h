@@ -37,6 +37,10 @@ int launch_switch_tiles(const void* x, void* y, int64_t B, int64_t D1, int64_t D
 // as u = (b * X + x) * H + h; position r of unit (b, x, h) sits at element
 //   b * b_stride + x * x_stride + r * r_stride + h * D
 // of q/k/v (strides *_in) and of o (strides *_out).
+// Cross-attention and grouped key/value heads: the unit's keys and values are
+// Lk positions of key/value head h / (H / Hkv), at b * b_stride_kv + x *
+// x_stride_kv + r * r_stride_kv + (h / (H / Hkv)) * D of k and v (self-attention:
+// Lk = L, Hkv = H and the kv strides equal the in strides).
 struct AttnArgs {
   const void* q;
   const void* k;
@@ -46,6 +50,9 @@ struct AttnArgs {
   int H, D;
   int64_t b_stride_in, x_stride_in, r_stride_in;
   int64_t b_stride_out, x_stride_out, r_stride_out;
+  int64_t Lk;
+  int Hkv;
+  int64_t b_stride_kv, x_stride_kv, r_stride_kv;
   float scale;
   // optional (may be null): fp32 [B * X * H][L], the natural-log row
   // log-sum-exp of the scaled scores of each query (the backward's statistic)
@@ -53,9 +60,10 @@ struct AttnArgs {
 };
 int launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 
-// Backward of attention (attn_bwd.hip).  Units and positions as in AttnArgs;
-// q, k, v, dq, dk, dv use qkv_strides, o and dout use o_strides; lse and
-// delta are fp32 [B * X * H][L] (delta is written by the first kernel).
+// Backward of attention (attn_bwd.hip).  Units and positions as in AttnArgs
+// (L queries, Lk keys, Hkv key/value heads): q and dq use q_strides, k, v, dk
+// and dv kv_strides, o and dout o_strides; lse and delta are fp32
+// [B * X * H][L] (delta is written by the first kernel).
 struct AttnBwdArgs {
   const void* q;
   const void* k;
@@ -67,9 +75,9 @@ struct AttnBwdArgs {
   void* dk;
   void* dv;
   float* delta;
-  int64_t B, X, L;
-  int H, D;
-  int64_t qkv_strides[3], o_strides[3];
+  int64_t B, X, L, Lk;
+  int H, Hkv, D;
+  int64_t q_strides[3], kv_strides[3], o_strides[3];
   float scale;
 };
 bool attn_bwd_bf16_fits(const AttnBwdArgs& a);

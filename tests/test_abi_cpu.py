@@ -304,6 +304,30 @@ def test_block_train_validation(lib):
     assert bwd(flags=dsp.DSP_BLOCK_POST_LN | dsp.DSP_BLOCK_RELU) == dsp.DSP_ERR_ARG
 
 
+def test_attn_general_validation(lib):
+    qs, kvs, os_ = _shape(3 * 5 * 1152, 5 * 1152, 1152), _shape(3 * 7 * 288, 7 * 288, 288), \
+        _shape(3 * 5 * 1152, 5 * 1152, 1152)
+    A = 2 ** 26
+    fwd = lambda Lq=5, Lk=7, H=16, Hkv=4, D=72, k=FAKE + A, kst=kvs, dt=1, lse=None: lib.dsp_attn_general(
+        FAKE, k, k, FAKE + 2 * A, lse, 2, 3, Lq, Lk, H, Hkv, D, qs, kst, os_, 0.0, dt, None)
+    assert fwd(Hkv=5) == dsp.DSP_ERR_SHAPE          # Hkv must divide H
+    assert fwd(Hkv=0) == dsp.DSP_ERR_SHAPE
+    assert fwd(Lk=0) == dsp.DSP_ERR_SHAPE           # queries without keys
+    assert fwd(Lk=-1) == dsp.DSP_ERR_SHAPE
+    assert fwd(k=None) == dsp.DSP_ERR_NULL
+    assert fwd(kst=None) == dsp.DSP_ERR_NULL
+    assert fwd(kst=_shape(3 * 7 * 288, 7 * 288, 290)) == dsp.DSP_ERR_ALIGN
+    assert fwd(lse=FAKE + 3 * A + 2) == dsp.DSP_ERR_ALIGN
+    assert fwd(dt=7) == dsp.DSP_ERR_DTYPE
+    assert fwd(Lq=0, Lk=0) == dsp.DSP_OK
+    bwd = lambda kst=kvs, Lk=7, Hkv=4: lib.dsp_attn_general_bwd(
+        FAKE, FAKE + A, FAKE + A, FAKE + 2 * A, FAKE + 2 * A, FAKE + 3 * A, FAKE + 4 * A, FAKE + 5 * A,
+        FAKE + 6 * A, FAKE + 7 * A, 2, 3, 5, Lk, 16, Hkv, 72, qs, kst, os_, 0.0, 1, None)
+    assert bwd(kst=_shape(0, 0, 288)) == dsp.DSP_ERR_ARG      # broadcast k/v: no single owner of dk rows
+    assert bwd(Hkv=3) == dsp.DSP_ERR_SHAPE
+    assert bwd(Lk=0) == dsp.DSP_ERR_SHAPE
+
+
 def test_layernorm_validation(lib):
     f = lambda x=FAKE, xd=1, y=FAKE2, yd=1, rows=4, C=8, eps=1e-6: lib.dsp_layernorm(
         x, xd, y, yd, rows, C, eps, None)
