@@ -427,9 +427,14 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
  * dsp_st_block_forward_train -- dsp_st_block_forward (same x, y, w, sizes,
  *   eps and dtype) that writes the activations the backward needs into
  *   `saved`: DEVICE memory of at least dsp_st_block_train_saved_bytes(...)
- *   bytes, 256-byte aligned, owned by the caller (1.7 GB at B1 T32 S1024
- *   C1152 F4608 in bf16).  Flags: 0, DSP_BLOCK_NO_MLP_LN, DSP_BLOCK_RELU (the
- *   pre-LN blocks); post-LN and the projection-only chain give DSP_ERR_ARG.
+ *   bytes for the same sizes, flags and dtype, 256-byte aligned, owned by the
+ *   caller (1.7 GB at B1 T32 S1024 C1152 F4608 in bf16, pre-LN; post-LN with
+ *   the MLP's LayerNorm keeps one more fp32 stream).  Flags: any combination
+ *   of DSP_BLOCK_NO_MLP_LN, DSP_BLOCK_POST_LN (Eq. 4, 6: LN after each
+ *   residual add) and DSP_BLOCK_RELU; the projection-only chain
+ *   (DSP_BLOCK_ATTN_ONLY) gives DSP_ERR_ARG.  y has the bits
+ *   dsp_st_block_forward writes for the same arguments (the MLP's first GEMM
+ *   stores its pre-activation beside the activation from the same fp32 sum).
  * dsp_st_block_backward -- given the forward's x (B,T,S,C), its saved
  *   activations, and dy (B,S,T,C) = dL/dy, writes dx = dL/dx (B,T,S,C, fp32)
  *   and the weight gradients into `grads`: fp32 arrays shaped like the weights
@@ -447,7 +452,8 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
 typedef struct {
   float *wqkv_s, *bqkv_s, *wo_s, *bo_s, *wqkv_t, *bqkv_t, *wo_t, *bo_t, *w1, *b1, *w2, *b2;
 } dsp_block_grads_t;
-size_t dsp_st_block_train_saved_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype);
+size_t dsp_st_block_train_saved_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int flags,
+                                      int dtype);
 size_t dsp_st_block_backward_workspace_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype);
 int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_block_weights_t* w, void* saved,
                                size_t saved_bytes, int64_t B, int64_t T, int64_t S, int C, int H, int F,

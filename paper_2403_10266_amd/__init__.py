@@ -80,7 +80,7 @@ _SIGNATURES = {
     "dsp_linear_bwd_weight": (_I, [_P, _P, _P, _P, _P, _SZ, _I64, _I, _I, _I, _P]),
     "dsp_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
     "dsp_st_block_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
-    "dsp_st_block_train_saved_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
+    "dsp_st_block_train_saved_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I, _I]),
     "dsp_st_block_backward_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
     "dsp_st_block_forward_train": (_I, [_P, _P, _c.POINTER(BlockWeights), _P, _SZ, _I64, _I64, _I64, _I, _I,
                                         _I, _F, _I, _I, _P]),
@@ -573,7 +573,7 @@ def dsp_st_block_forward_train(x, weights: dict, H: int, eps: float = 1e-6, flag
     B, T, S, C, F, code = _block_sizes(x, weights, dtype)
     if out is None:
         out = torch.empty((B, S, T, C), dtype=torch.float32, device=x.device)
-    need = int(lib().dsp_st_block_train_saved_bytes(B, T, S, C, H, F, code))
+    need = int(lib().dsp_st_block_train_saved_bytes(B, T, S, C, H, F, flags, code))
     if saved is None:
         saved = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     wt = BlockWeights(**{n: (weights[n].data_ptr() if weights.get(n) is not None else None)

@@ -293,8 +293,9 @@ int attn_impl(const void* q, const void* k, const void* v, void* o, int64_t B, i
   return attn_impl_strided(q, k, v, o, B, X, L, H, D, in_st, out_st, scale, dtype, stream);
 }
 
+// pre (GELU/ReLU epilogue, may be null): also receives the pre-activation.
 int linear_impl(const void* a, const void* w, const void* bias, const float* residual, void* out,
-                int64_t M, int N, int K, int epilogue, int dtype, hipStream_t s) {
+                int64_t M, int N, int K, int epilogue, int dtype, hipStream_t s, void* pre = nullptr) {
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
   if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
   if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_RELU) return DSP_ERR_ARG;
@@ -313,16 +314,20 @@ int linear_impl(const void* a, const void* w, const void* bias, const float* res
   if (residual && epilogue == DSP_EPI_RESID && residual != out &&
       overlap(out, out_bytes, residual, (size_t)mn * 4))
     return DSP_ERR_ARG;
+  if (pre && ((epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) || overlap(pre, out_bytes, out, out_bytes) ||
+              overlap(pre, out_bytes, a, (size_t)mk * es)))
+    return DSP_ERR_ARG;
   if (dtype == DSP_BF16) {
     if (K % 8 || !aligned(a, 16) || !aligned(w, 16) || !aligned(out, 16)) return DSP_ERR_ALIGN;
     if (epilogue == DSP_EPI_RESID && !aligned(residual, 16)) return DSP_ERR_ALIGN;
+    if (pre && !aligned(pre, 16)) return DSP_ERR_ALIGN;
     return launch_linear_bf16(a, w, bias, epilogue == DSP_EPI_RESID ? residual : nullptr, out, M, N,
-                              K, epilogue, s);
+                              K, epilogue, s, pre);
   }
   return launch_linear_f32(static_cast<const float*>(a), static_cast<const float*>(w),
                            static_cast<const float*>(bias),
                            epilogue == DSP_EPI_RESID ? residual : nullptr,
-                           static_cast<float*>(out), M, N, K, epilogue, s);
+                           static_cast<float*>(out), M, N, K, epilogue, s, static_cast<float*>(pre));
 }
 
 // Workspace regions of the block (each 256-byte aligned).
@@ -351,11 +356,16 @@ bool block_ws_layout(int64_t B, int64_t T, int64_t S, int C, int F, int dtype, B
 // Activations a training forward keeps for the backward (offsets into the
 // caller's `saved` buffer, each 256-byte aligned).  Residual streams in fp32,
 // operands in the block dtype, log-sum-exps in fp32 ([units][L] = tokens * H).
+// Pre-LN: y0 and y1 hold the streams entering the temporal half and the MLP
+// (the inputs of their LayerNorms).  Post-LN: y0 and y1 hold the sums r1
+// (switched to (B, S, T, C)) and r2 that the first two LayerNorms normalise,
+// and r3, the sum the MLP's LayerNorm normalises, gets a slot of its own.
 struct BlockSaved {
-  size_t y0, y1, h1, qkv1, a1, lse1, h2, qkv2, a2, lse2, h3, u, g, total;
+  size_t y0, y1, h1, qkv1, a1, lse1, h2, qkv2, a2, lse2, h3, u, g, r3, total;
 };
 
-bool block_saved_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype, BlockSaved* sv) {
+bool block_saved_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, int flags, int dtype,
+                        BlockSaved* sv) {
   int64_t tokens, tc, t3c, tf, th;
   if (!mul_ok(B, T, &tokens) || !mul_ok(tokens, S, &tokens) || !mul_ok(tokens, C, &tc) ||
       !mul_ok(tokens, 3 * (int64_t)C, &t3c) || !mul_ok(tokens, F, &tf) || !mul_ok(tokens, H, &th))
@@ -377,6 +387,8 @@ bool block_saved_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, in
   sv->h3 = off;   off += up((size_t)tc * es);
   sv->u = off;    off += up((size_t)tf * es);
   sv->g = off;    off += up((size_t)tf * es);
+  sv->r3 = off;
+  if ((flags & DSP_BLOCK_POST_LN) && !(flags & DSP_BLOCK_NO_MLP_LN)) off += up((size_t)tc * 4);
   sv->total = off;
   return true;
 }
@@ -821,10 +833,11 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
 #undef DSP_TRY
 }
 
-size_t dsp_st_block_train_saved_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype) {
+size_t dsp_st_block_train_saved_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int flags,
+                                      int dtype) {
   if (!valid_dtype(dtype) || B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || F < 1 || C % H) return 0;
   BlockSaved sv;
-  return block_saved_layout(B, T, S, C, H, F, dtype, &sv) ? sv.total : 0;
+  return block_saved_layout(B, T, S, C, H, F, flags, dtype, &sv) ? sv.total : 0;
 }
 
 size_t dsp_st_block_backward_workspace_bytes(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype) {
@@ -840,8 +853,9 @@ int block_train_check(const dsp_block_weights_t* w, int64_t B, int64_t T, int64_
                       float ln_eps, int flags, int dtype) {
   if (!w) return DSP_ERR_NULL;
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
-  // training covers the pre-LN blocks (GELU or ReLU, with or without the MLP's LN)
-  if (flags & ~(DSP_BLOCK_NO_MLP_LN | DSP_BLOCK_RELU)) return DSP_ERR_ARG;
+  // training covers the pre- and post-LN blocks (GELU or ReLU, with or
+  // without the MLP's LN); the projection-only chain has no training path
+  if (flags & ~(DSP_BLOCK_NO_MLP_LN | DSP_BLOCK_POST_LN | DSP_BLOCK_RELU)) return DSP_ERR_ARG;
   if (B < 0 || T < 0 || S < 0 || C < 1 || H < 1 || C % H || F < 1) return DSP_ERR_SHAPE;
   const int D = C / H;
   if (dtype == DSP_BF16 && (!attn_bf16_supports(D) || D % 32 > 16 || C % 8 || F % 8)) return DSP_ERR_SHAPE;
@@ -865,7 +879,7 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
   if (st != DSP_OK) return st;
   if (!x_BTSC || !y_BSTC) return DSP_ERR_NULL;
   BlockSaved sv;
-  if (!block_saved_layout(B, T, S, C, H, F, dtype, &sv)) return DSP_ERR_SHAPE;
+  if (!block_saved_layout(B, T, S, C, H, F, flags, dtype, &sv)) return DSP_ERR_SHAPE;
   if (!saved || saved_bytes < sv.total) return DSP_ERR_WORKSPACE;
   if (!aligned(saved, 256)) return DSP_ERR_ALIGN;
   if (!aligned(x_BTSC, 16) || !aligned(y_BSTC, 16)) return DSP_ERR_ALIGN;
@@ -886,6 +900,7 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
   const int bf = dtype == DSP_BF16;
   const size_t es = elem_size(dtype);
   const int D = C / H;
+  const int act = (flags & DSP_BLOCK_RELU) ? DSP_EPI_RELU : DSP_EPI_GELU;
   const int64_t shp[4] = {B, T, S, C};
 #define DSP_TRY(expr)            \
   do {                           \
@@ -902,6 +917,30 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
     return attn_impl_strided(qkv, qkv + (size_t)C * es, qkv + (size_t)2 * C * es, a, B, X, L, H, D, in_st, out_st,
                              0.0f, dtype, stream, lse);
   };
+  if (flags & DSP_BLOCK_POST_LN) {
+    // post-LN (Eq. 4, 6): each sublayer reads the stream itself and LN follows
+    // the residual add.  y_BSTC holds the fp32 streams y0 and y1 until the
+    // output is written; the ops are those of dsp_st_block_forward, in its order.
+    float* r3 = reinterpret_cast<float*>(base + sv.r3);
+    DSP_TRY(launch_cast(x_BTSC, 0, h1, bf, tokens * C, s));
+    DSP_TRY(attn_sub(h1, w->wqkv_s, w->bqkv_s, qkv1, a1, lse1, T, S));
+    DSP_TRY(linear_impl(a1, w->wo_s, w->bo_s, x_BTSC, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));
+    DSP_TRY(switch_impl(y1, y0, shp, 4, 1, 2, 1, DSP_F32, 0, s));                 // y0 slot: r1 (B,S,T,C)
+    DSP_TRY(launch_layernorm(y0, 0, y_BSTC, 0, tokens, C, ln_eps, s));           // stream y0 = LN(r1)
+    DSP_TRY(launch_cast(y_BSTC, 0, h2, bf, tokens * C, s));
+    DSP_TRY(attn_sub(h2, w->wqkv_t, w->bqkv_t, qkv2, a2, lse2, S, T));
+    DSP_TRY(linear_impl(a2, w->wo_t, w->bo_t, y_BSTC, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));  // r2
+    DSP_TRY(launch_layernorm(y1, 0, y_BSTC, 0, tokens, C, ln_eps, s));           // stream y1 = LN(r2)
+    DSP_TRY(launch_cast(y_BSTC, 0, h3, bf, tokens * C, s));
+    DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, g, tokens, F, C, act, dtype, s, u));
+    if (flags & DSP_BLOCK_NO_MLP_LN) {
+      DSP_TRY(linear_impl(g, w->w2, w->b2, y_BSTC, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
+    } else {
+      DSP_TRY(linear_impl(g, w->w2, w->b2, y_BSTC, r3, tokens, C, F, DSP_EPI_RESID, dtype, s));
+      DSP_TRY(launch_layernorm(r3, 0, y_BSTC, 0, tokens, C, ln_eps, s));
+    }
+    return DSP_OK;
+  }
   // spatial half on (B, T, S, C); y1's slot holds the pre-switch stream x1
   DSP_TRY(launch_layernorm(x_BTSC, 0, h1, bf, tokens, C, ln_eps, s));
   DSP_TRY(attn_sub(h1, w->wqkv_s, w->bqkv_s, qkv1, a1, lse1, T, S));
@@ -912,14 +951,14 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
   DSP_TRY(launch_layernorm(y0, 0, h2, bf, tokens, C, ln_eps, s));
   DSP_TRY(attn_sub(h2, w->wqkv_t, w->bqkv_t, qkv2, a2, lse2, S, T));
   DSP_TRY(linear_impl(a2, w->wo_t, w->bo_t, y0, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));
-  // MLP: u = h3 W1 + b1 (kept), g = act(u) (kept), y = y1 + g W2 + b2
+  // MLP: u = h3 W1 + b1 and g = act(u) from one GEMM (both kept; g from the
+  // fp32 sum, as in the forward), y = y1 + g W2 + b2
   if (flags & DSP_BLOCK_NO_MLP_LN) {
     DSP_TRY(launch_cast(y1, 0, h3, bf, tokens * C, s));
   } else {
     DSP_TRY(launch_layernorm(y1, 0, h3, bf, tokens, C, ln_eps, s));
   }
-  DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, u, tokens, F, C, DSP_EPI_NONE, dtype, s));
-  DSP_TRY(launch_activation(u, g, tokens * F, bf, (flags & DSP_BLOCK_RELU) != 0, s));
+  DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, g, tokens, F, C, act, dtype, s, u));
   DSP_TRY(linear_impl(g, w->w2, w->b2, y1, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
   return DSP_OK;
 #undef DSP_TRY
@@ -936,7 +975,8 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
     return DSP_ERR_NULL;
   BlockSaved sv;
   BlockBwdWs bw;
-  if (!block_saved_layout(B, T, S, C, H, F, dtype, &sv) || !block_bwd_ws_layout(B, T, S, C, H, F, dtype, &bw))
+  if (!block_saved_layout(B, T, S, C, H, F, flags, dtype, &sv) ||
+      !block_bwd_ws_layout(B, T, S, C, H, F, dtype, &bw))
     return DSP_ERR_SHAPE;
   if (!saved || saved_bytes < sv.total || !workspace || ws_bytes < bw.total) return DSP_ERR_WORKSPACE;
   if (!aligned(saved, 256) || !aligned(workspace, 256)) return DSP_ERR_ALIGN;
@@ -996,6 +1036,38 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
     if (r != DSP_OK) return r;
     return dsp_linear_bwd_data(dqkv, wqkv, nullptr, dh, tokens, 3 * C, C, DSP_GRAD_EPI_F32, dtype, stream);
   };
+  if (flags & DSP_BLOCK_POST_LN) {
+    // post-LN: the gradient passes each LayerNorm before its sublayer, and the
+    // sublayer's input gradient adds to the stream's (the residual branch).
+    const float* r1 = y0;   // (B, S, T, C)
+    const float* r2 = y1;
+    const float* dr3 = dy_BSTC;
+    if (!(flags & DSP_BLOCK_NO_MLP_LN)) {
+      DSP_TRY(launch_layernorm_bwd(sb + sv.r3, 0, dy_BSTC, 0, nullptr, dcur, tokens, C, ln_eps, s));
+      dr3 = dcur;
+    }
+    // ---- MLP: r3 = y1 + act(y1 W1 + b1) W2 + b2
+    DSP_TRY(operand(dr3));
+    DSP_TRY(dsp_linear_bwd_weight(dyb, g, grads->w2, grads->b2, wg, bw.wg_bytes, tokens, C, F, dtype, stream));
+    DSP_TRY(dsp_linear_bwd_data(dyb, w->w2, u, du, tokens, C, F, act_bwd, dtype, stream));
+    DSP_TRY(dsp_linear_bwd_weight(du, h3, grads->w1, grads->b1, wg, bw.wg_bytes, tokens, F, C, dtype, stream));
+    DSP_TRY(dsp_linear_bwd_data(du, w->w1, nullptr, dh, tokens, F, C, DSP_GRAD_EPI_F32, dtype, stream));
+    DSP_TRY(launch_add_f32(dr3, dh, dcur, tokens * C, s));                           // dy1
+    // ---- temporal half: r2 = y0 + Attn_T(y0 Wqkv_t) Wo_t, y1 = LN(r2)
+    DSP_TRY(launch_layernorm_bwd(r2, 0, dcur, 0, nullptr, dx1, tokens, C, ln_eps, s));  // dr2
+    DSP_TRY(operand(dx1));
+    DSP_TRY(attn_sub_bwd(h2, qkv2, a2, lse2, w->wqkv_t, w->wo_t, grads->wqkv_t, grads->bqkv_t, grads->wo_t,
+                         grads->bo_t, S, T));
+    DSP_TRY(launch_add_f32(dx1, dh, dcur, tokens * C, s));                           // dy0
+    // ---- spatial half: r1 = x + Attn_S(x Wqkv_s) Wo_s, y0 = LN(Switch(r1))
+    DSP_TRY(launch_layernorm_bwd(r1, 0, dcur, 0, nullptr, dx1, tokens, C, ln_eps, s));  // dr1 (B,S,T,C)
+    DSP_TRY(switch_impl(dx1, dcur, shp_bstc, 4, 1, 2, 1, DSP_F32, 0, s));               // dr1 (B,T,S,C)
+    DSP_TRY(operand(dcur));
+    DSP_TRY(attn_sub_bwd(h1, qkv1, a1, lse1, w->wqkv_s, w->wo_s, grads->wqkv_s, grads->bqkv_s, grads->wo_s,
+                         grads->bo_s, T, S));
+    DSP_TRY(launch_add_f32(dcur, dh, dx_BTSC, tokens * C, s));
+    return DSP_OK;
+  }
   // ---- MLP: y = y1 + act(h3 W1 + b1) W2 + b2
   DSP_TRY(operand(dy_BSTC));
   DSP_TRY(dsp_linear_bwd_weight(dyb, g, grads->w2, grads->b2, wg, bw.wg_bytes, tokens, C, F, dtype, stream));

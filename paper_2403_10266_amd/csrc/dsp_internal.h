@@ -104,7 +104,6 @@ int launch_gemm_grad(const void* a, int ta, int64_t lda, const void* b, int tb, 
                      void* out, int64_t M, int64_t N, int64_t K, int epi, int splits, float* ws, hipStream_t s);
 int launch_gemm_grad_f32(const float* a, int ta, int64_t lda, const float* b, int tb, int64_t ldb,
                          const float* aux, float* out, int64_t M, int64_t N, int64_t K, int epi, hipStream_t s);
-int launch_activation(const void* u, void* g, int64_t n, int bf16, int relu, hipStream_t s);
 int launch_add_f32(const float* a, const float* b, float* out, int64_t n, hipStream_t s);
 int launch_colsum_bf16(const void* dy, float* db, int64_t M, int N, hipStream_t s);
 int launch_colsum_f32(const float* dy, float* db, int64_t M, int N, hipStream_t s);
@@ -115,10 +114,12 @@ int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16,
 
 int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s);
 
+// out = epilogue(a W^T + bias) (gemm.hip).  pre (GELU or ReLU epilogue only,
+// else null): also receives the pre-activation, in the output's dtype.
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
-                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s);
+                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre = nullptr);
 int launch_linear_f32(const float* a, const float* w, const float* bias, const float* residual,
-                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s);
+                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre = nullptr);
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? DSP_OK : DSP_ERR_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }

@@ -73,10 +73,14 @@ __device__ __forceinline__ float gelu_bf16out(float v) {
   return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f));
 }
 
-template <int EPI>
+// KEEP (GELU/ReLU only): also store the pre-activation a W + bias, rounded to
+// bf16, into `keep_out` at the output's offsets -- what a training forward keeps
+// for the activation's backward.  The activation itself still reads the fp32
+// sum, so `out` has the bits of the plain epilogue.
+template <int EPI, bool KEEP>
 __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
     const bf16* __restrict__ A, const bf16* __restrict__ W, const bf16* __restrict__ bias,
-    const float* resid, void* out, int M, int N, int K, int n_ntiles, int n_tiles) {
+    const float* resid, void* out, bf16* keep_out, int M, int N, int K, int n_ntiles, int n_tiles) {
   __shared__ __attribute__((aligned(16))) bf16 As[BM * PITCH];
   __shared__ __attribute__((aligned(16))) bf16 Ws[BN * PITCH];
 
@@ -183,6 +187,20 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
           for (int i = 0; i < 4; ++i)
             if (n + i < N) v[i] += bf2f(bias[n + i]);
         }
+        const int64_t off = (int64_t)m * N + n;
+        if (KEEP) {
+          if (full) {
+            bf16x2 lo = {(bf16)v[0], (bf16)v[1]};
+            bf16x2 hi = {(bf16)v[2], (bf16)v[3]};
+            uint2 w;
+            w.x = __builtin_bit_cast(uint32_t, lo);
+            w.y = __builtin_bit_cast(uint32_t, hi);
+            *reinterpret_cast<uint2*>(keep_out + off) = w;
+          } else {
+            for (int i = 0; i < 4; ++i)
+              if (n + i < N) keep_out[off + i] = (bf16)v[i];
+          }
+        }
         if (EPI == DSP_EPI_GELU) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
@@ -191,7 +209,6 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
 #pragma unroll
           for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
         }
-        const int64_t off = (int64_t)m * N + n;
         if (EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32) {
           float* o = static_cast<float*>(out);
           if (EPI == DSP_EPI_RESID) {
@@ -230,12 +247,13 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
 // ---------------------------------------------------------------- fp32 path
 constexpr int FT = 64, FK = 16;
 
+// `pre` (GELU/ReLU, may be null): also store the pre-activation there.
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A,
                                                         const float* __restrict__ W,
                                                         const float* __restrict__ bias,
-                                                        const float* resid, float* out, int M,
-                                                        int N, int K) {
+                                                        const float* resid, float* out, float* pre,
+                                                        int M, int N, int K) {
   __shared__ float As[FK][FT + 1];
   __shared__ float Bs[FK][FT + 1];
   const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
@@ -273,9 +291,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
       if (n >= N) continue;
       float v = acc[i][j];
       if (bias) v += bias[n];
+      const int64_t off = (int64_t)m * N + n;
+      if ((EPI == DSP_EPI_GELU || EPI == DSP_EPI_RELU) && pre) pre[off] = v;
       if (EPI == DSP_EPI_GELU) v = 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
       if (EPI == DSP_EPI_RELU) v = fmaxf(v, 0.0f);
-      const int64_t off = (int64_t)m * N + n;
       if (EPI == DSP_EPI_RESID) v += resid[off];
       out[off] = v;
     }
@@ -285,74 +304,59 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 }  // namespace
 
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
-                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s) {
+                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre) {
   if (M == 0) return DSP_OK;
   const int64_t n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN;
   const int64_t tiles = n_mt * n_nt;
   // a tile's buffer resources address BM rows of K bf16 with 32-bit offsets
   if (tiles >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) || (int64_t)BM * K * 2 >= (int64_t(1) << 31))
     return DSP_ERR_SHAPE;
+  const bool keep = pre != nullptr;
+  if (keep && epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) return DSP_ERR_ARG;
   const dim3 grid((uint32_t)tiles), block(NTHR);
   const bf16* A = static_cast<const bf16*>(a);
   const bf16* Wt = static_cast<const bf16*>(w);
   const bf16* bs = static_cast<const bf16*>(bias);
+  bf16* pb = static_cast<bf16*>(pre);
+#define DSP_GEMM_LAUNCH(E, KP)                                                                         \
+  hipLaunchKernelGGL((gemm_bf16_kernel<E, KP>), grid, block, 0, s, A, Wt, bs, residual, out, pb, (int)M, N, \
+                     K, (int)n_nt, (int)tiles)
   switch (epilogue) {
-    case DSP_EPI_NONE:
-      hipLaunchKernelGGL(gemm_bf16_kernel<DSP_EPI_NONE>, grid, block, 0, s, A, Wt, bs, residual,
-                         out, (int)M, N, K, (int)n_nt, (int)tiles);
-      break;
+    case DSP_EPI_NONE: DSP_GEMM_LAUNCH(DSP_EPI_NONE, false); break;
+    case DSP_EPI_RESID: DSP_GEMM_LAUNCH(DSP_EPI_RESID, false); break;
+    case DSP_EPI_F32: DSP_GEMM_LAUNCH(DSP_EPI_F32, false); break;
     case DSP_EPI_GELU:
-      hipLaunchKernelGGL(gemm_bf16_kernel<DSP_EPI_GELU>, grid, block, 0, s, A, Wt, bs, residual,
-                         out, (int)M, N, K, (int)n_nt, (int)tiles);
-      break;
-    case DSP_EPI_RESID:
-      hipLaunchKernelGGL(gemm_bf16_kernel<DSP_EPI_RESID>, grid, block, 0, s, A, Wt, bs, residual,
-                         out, (int)M, N, K, (int)n_nt, (int)tiles);
-      break;
-    case DSP_EPI_F32:
-      hipLaunchKernelGGL(gemm_bf16_kernel<DSP_EPI_F32>, grid, block, 0, s, A, Wt, bs, residual,
-                         out, (int)M, N, K, (int)n_nt, (int)tiles);
+      if (keep) DSP_GEMM_LAUNCH(DSP_EPI_GELU, true); else DSP_GEMM_LAUNCH(DSP_EPI_GELU, false);
       break;
     case DSP_EPI_RELU:
-      hipLaunchKernelGGL(gemm_bf16_kernel<DSP_EPI_RELU>, grid, block, 0, s, A, Wt, bs, residual,
-                         out, (int)M, N, K, (int)n_nt, (int)tiles);
+      if (keep) DSP_GEMM_LAUNCH(DSP_EPI_RELU, true); else DSP_GEMM_LAUNCH(DSP_EPI_RELU, false);
       break;
     default:
       return DSP_ERR_ARG;
   }
+#undef DSP_GEMM_LAUNCH
   return last_launch_status();
 }
 
 int launch_linear_f32(const float* a, const float* w, const float* bias, const float* residual,
-                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s) {
+                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre) {
   if (M == 0) return DSP_OK;
   const int64_t gy = (M + FT - 1) / FT;
   if (gy >= 65536 * 1024) return DSP_ERR_SHAPE;
+  if (pre && epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) return DSP_ERR_ARG;
   const dim3 grid((uint32_t)((N + FT - 1) / FT), (uint32_t)gy), block(256);
+#define DSP_GEMM_LAUNCH(E) \
+  hipLaunchKernelGGL(gemm_f32_kernel<E>, grid, block, 0, s, a, w, bias, residual, out, pre, (int)M, N, K)
   switch (epilogue) {
-    case DSP_EPI_NONE:
-      hipLaunchKernelGGL(gemm_f32_kernel<DSP_EPI_NONE>, grid, block, 0, s, a, w, bias, residual, out,
-                         (int)M, N, K);
-      break;
-    case DSP_EPI_GELU:
-      hipLaunchKernelGGL(gemm_f32_kernel<DSP_EPI_GELU>, grid, block, 0, s, a, w, bias, residual, out,
-                         (int)M, N, K);
-      break;
-    case DSP_EPI_RESID:
-      hipLaunchKernelGGL(gemm_f32_kernel<DSP_EPI_RESID>, grid, block, 0, s, a, w, bias, residual, out,
-                         (int)M, N, K);
-      break;
-    case DSP_EPI_F32:
-      hipLaunchKernelGGL(gemm_f32_kernel<DSP_EPI_NONE>, grid, block, 0, s, a, w, bias, residual, out,
-                         (int)M, N, K);
-      break;
-    case DSP_EPI_RELU:
-      hipLaunchKernelGGL(gemm_f32_kernel<DSP_EPI_RELU>, grid, block, 0, s, a, w, bias, residual, out,
-                         (int)M, N, K);
-      break;
+    case DSP_EPI_NONE: DSP_GEMM_LAUNCH(DSP_EPI_NONE); break;
+    case DSP_EPI_GELU: DSP_GEMM_LAUNCH(DSP_EPI_GELU); break;
+    case DSP_EPI_RESID: DSP_GEMM_LAUNCH(DSP_EPI_RESID); break;
+    case DSP_EPI_F32: DSP_GEMM_LAUNCH(DSP_EPI_NONE); break;
+    case DSP_EPI_RELU: DSP_GEMM_LAUNCH(DSP_EPI_RELU); break;
     default:
       return DSP_ERR_ARG;
   }
+#undef DSP_GEMM_LAUNCH
   return last_launch_status();
 }
 

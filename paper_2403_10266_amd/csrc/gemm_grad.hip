@@ -352,29 +352,6 @@ __global__ __launch_bounds__(256) void colsum_f32_kernel(const float* __restrict
   db[n] = s;
 }
 
-// g = act(u) element-wise (GELU x Phi(x) with erf by A&S 7.1.26 as in the
-// forward GEMM epilogue, or ReLU), bf16 or fp32
-__global__ __launch_bounds__(256) void activation_kernel(const void* __restrict__ u, void* __restrict__ g,
-                                                         int64_t n, int bf, int relu) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-    const float v = bf ? (float)static_cast<const bf16*>(u)[i] : static_cast<const float*>(u)[i];
-    float r;
-    if (relu) {
-      r = fmaxf(v, 0.0f);
-    } else if (bf) {
-      r = 0.5f * v * (1.0f + erf_as(v * 0.70710678118654752f));
-    } else {
-      r = 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
-    }
-    if (bf) {
-      static_cast<bf16*>(g)[i] = (bf16)r;
-    } else {
-      static_cast<float*>(g)[i] = r;
-    }
-  }
-}
-
 // out = a + b (fp32); out may alias a or b
 __global__ __launch_bounds__(256) void add_f32_kernel(const float* a, const float* b, float* out, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -382,13 +359,6 @@ __global__ __launch_bounds__(256) void add_f32_kernel(const float* a, const floa
 }
 
 }  // namespace
-
-int launch_activation(const void* u, void* g, int64_t n, int bf16, int relu, hipStream_t s) {
-  if (n == 0) return DSP_OK;
-  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
-  hipLaunchKernelGGL(activation_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, u, g, n, bf16, relu);
-  return last_launch_status();
-}
 
 int launch_add_f32(const float* a, const float* b, float* out, int64_t n, hipStream_t s) {
   if (n == 0) return DSP_OK;

@@ -281,15 +281,21 @@ def test_block_train_validation(lib):
     G = dsp.BlockGrads(**{n: (2 ** 40 + 2 ** 26 * i if n.startswith("w") else None)
                           for i, n in enumerate(dsp.BLOCK_WEIGHT_FIELDS)})
     dims = (1, 4, 8, 144, 2, 576)
-    need = lib.dsp_st_block_train_saved_bytes(*dims, 1)
+    need = lib.dsp_st_block_train_saved_bytes(*dims, 0, 1)
     ws_need = lib.dsp_st_block_backward_workspace_bytes(*dims, 1)
     assert need > 0 and ws_need > 0
-    assert lib.dsp_st_block_train_saved_bytes(1, 4, 8, 144, 5, 576, 1) == 0     # C % H
+    assert lib.dsp_st_block_train_saved_bytes(1, 4, 8, 144, 5, 576, 0, 1) == 0     # C % H
+    # post-LN with the MLP's LayerNorm keeps one more fp32 stream (tokens x C), else the same
+    post = dsp.DSP_BLOCK_POST_LN
+    assert lib.dsp_st_block_train_saved_bytes(*dims, post, 1) == need + 32 * 144 * 4
+    assert lib.dsp_st_block_train_saved_bytes(*dims, post | dsp.DSP_BLOCK_NO_MLP_LN, 1) == need
+    assert lib.dsp_st_block_train_saved_bytes(*dims, dsp.DSP_BLOCK_RELU, 1) == need
     X, Y, SV, WS, DX = 2 ** 34, 2 ** 35, 2 ** 36, 2 ** 37, 2 ** 38
     fwd = lambda flags=0, sv=SV, svb=need, dt=1, F=576: lib.dsp_st_block_forward_train(
         X, Y, c.byref(W), sv, svb, 1, 4, 8, 144, 2, F, 1e-6, flags, dt, None)
-    assert fwd(flags=dsp.DSP_BLOCK_POST_LN) == dsp.DSP_ERR_ARG                  # post-LN: not for training
-    assert fwd(flags=dsp.DSP_BLOCK_ATTN_ONLY) == dsp.DSP_ERR_ARG
+    assert fwd(flags=dsp.DSP_BLOCK_ATTN_ONLY) == dsp.DSP_ERR_ARG               # no training path
+    assert fwd(flags=16) == dsp.DSP_ERR_ARG                                     # unknown flag
+    assert fwd(flags=post) == dsp.DSP_ERR_WORKSPACE                             # post-LN needs the r3 slot
     assert fwd(sv=None) == dsp.DSP_ERR_WORKSPACE
     assert fwd(svb=need - 1) == dsp.DSP_ERR_WORKSPACE
     assert fwd(sv=SV + 16) == dsp.DSP_ERR_ALIGN
@@ -301,7 +307,8 @@ def test_block_train_validation(lib):
     assert bwd(dx=None) == dsp.DSP_ERR_NULL
     assert bwd(wsb=ws_need - 1) == dsp.DSP_ERR_WORKSPACE
     assert bwd(dx=X + 16) == dsp.DSP_ERR_ARG                                     # dx overlaps x
-    assert bwd(flags=dsp.DSP_BLOCK_POST_LN | dsp.DSP_BLOCK_RELU) == dsp.DSP_ERR_ARG
+    assert bwd(flags=dsp.DSP_BLOCK_POST_LN | dsp.DSP_BLOCK_RELU) == dsp.DSP_ERR_WORKSPACE
+    assert bwd(flags=dsp.DSP_BLOCK_ATTN_ONLY) == dsp.DSP_ERR_ARG
 
 
 def test_attn_general_validation(lib):

@@ -74,22 +74,40 @@ def _train_case(torch, w, with_bias, flags):
 
 
 @pytest.mark.parametrize("with_bias", [False, True])
-@pytest.mark.parametrize("flags", [0, 1, 8, 9])
+@pytest.mark.parametrize("flags", [0, 1, 8, 9, 4, 5, 12, 13])
 def test_block_train_bf16(torch, with_bias, flags):
+    """Pre-LN (flags 0, 1, 8, 9) and the paper's post-LN block (4, 5, 12, 13:
+    LN after each residual add), GELU or ReLU, with or without the MLP's LN."""
     w = synth.Workload("block_small", "block", "bf16", B=2, T=5, S=24, C=144, H=2, F=576, seed=21)
     _train_case(torch, w, with_bias, flags)
 
 
-@pytest.mark.parametrize("flags", [0, 9])
+@pytest.mark.parametrize("flags", [0, 9, 4, 13])
 def test_block_train_f32(torch, flags):
     w = synth.Workload("block_small_f32", "block", "f32", B=1, T=4, S=9, C=64, H=4, F=128, seed=22)
     _train_case(torch, w, True, flags)
 
 
-def test_block_train_full_width_bf16(torch):
+@pytest.mark.parametrize("flags", [0, 4])
+def test_block_train_full_width_bf16(torch, flags):
     """The 720M model's widths (C = 1152, 16 heads of 72, MLP 4608) on 2048 tokens."""
     w = synth.Workload("block_wide", "block", "bf16", B=1, T=8, S=256, C=1152, H=16, F=4608, seed=23)
-    _train_case(torch, w, False, 0)
+    _train_case(torch, w, False, flags)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("flags", [0, 1, 4, 5, 12, 13])
+def test_forward_train_output_matches_forward(torch, dtype, flags):
+    """The training forward writes the bits dsp_st_block_forward writes."""
+    import paper_2403_10266_amd as dsp
+    w = synth.Workload("block_bits", "block", dtype, B=1, T=6, S=40, C=144, H=2, F=576, seed=24)
+    x, p = synth.block_inputs(w, with_bias=True)
+    wd = {n: (None if v is None else dev(v, dtype)) for n, v in p.items()}
+    xd = dev(x, "f32")
+    y_train, _ = dsp.dsp_st_block_forward_train(xd, wd, w.H, flags=flags)
+    y = dsp.dsp_st_block_forward(xd, wd, w.H, flags=flags)
+    torch.cuda.synchronize()
+    assert torch.equal(y_train, y), flags
 
 
 def test_block_backward_deterministic_and_finite_full_size(torch):
