@@ -19,7 +19,14 @@
 // fp32 path: LDS-tiled FMA kernel, 64 x 64 tile, 4 x 4 outputs per thread.
 #include <math.h>
 
+#include <type_traits>
+
 #include "dsp_internal.h"
+
+// Large-tile kernel for problems of at least one full round of 256 x 192/256 tiles.
+#ifndef DSP_GEMM_BIG
+#define DSP_GEMM_BIG 1
+#endif
 
 namespace dsp {
 namespace {
@@ -73,10 +80,75 @@ __device__ __forceinline__ float gelu_bf16out(float v) {
   return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f));
 }
 
+__device__ __forceinline__ uint2 pack_bf16x4(const float v[4]) {
+  bf16x2 lo = {(bf16)v[0], (bf16)v[1]};
+  bf16x2 hi = {(bf16)v[2], (bf16)v[3]};
+  uint2 w;
+  w.x = __builtin_bit_cast(uint32_t, lo);
+  w.y = __builtin_bit_cast(uint32_t, hi);
+  return w;
+}
+
+// Epilogue of four consecutive outputs (row m, columns n .. n+3, n < N) held by
+// one lane: bias, optional pre-activation copy, activation or residual, store.
 // KEEP (GELU/ReLU only): also store the pre-activation a W + bias, rounded to
 // bf16, into `keep_out` at the output's offsets -- what a training forward keeps
 // for the activation's backward.  The activation itself still reads the fp32
 // sum, so `out` has the bits of the plain epilogue.
+template <int EPI, bool KEEP>
+__device__ __forceinline__ void epilogue4(float v[4], int m, int n, int N, const bf16* __restrict__ bias,
+                                          const float* resid, void* out, bf16* keep_out) {
+  const bool full = (n + 3 < N) && ((N & 3) == 0);
+  if (bias) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (n + i < N) v[i] += bf2f(bias[n + i]);
+  }
+  const int64_t off = (int64_t)m * N + n;
+  if (KEEP) {
+    if (full) {
+      *reinterpret_cast<uint2*>(keep_out + off) = pack_bf16x4(v);
+    } else {
+      for (int i = 0; i < 4; ++i)
+        if (n + i < N) keep_out[off + i] = (bf16)v[i];
+    }
+  }
+  if (EPI == DSP_EPI_GELU) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
+  }
+  if (EPI == DSP_EPI_RELU) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
+  }
+  if (EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32) {
+    float* o = static_cast<float*>(out);
+    if (EPI == DSP_EPI_RESID) {
+      if (full) {
+        const float4 rv = *reinterpret_cast<const float4*>(resid + off);
+        v[0] += rv.x; v[1] += rv.y; v[2] += rv.z; v[3] += rv.w;
+      } else {
+        for (int i = 0; i < 4; ++i)
+          if (n + i < N) v[i] += resid[off + i];
+      }
+    }
+    if (full) {
+      *reinterpret_cast<float4*>(o + off) = make_float4(v[0], v[1], v[2], v[3]);
+    } else {
+      for (int i = 0; i < 4; ++i)
+        if (n + i < N) o[off + i] = v[i];
+    }
+  } else {
+    bf16* o = static_cast<bf16*>(out);
+    if (full) {
+      *reinterpret_cast<uint2*>(o + off) = pack_bf16x4(v);
+    } else {
+      for (int i = 0; i < 4; ++i)
+        if (n + i < N) o[off + i] = (bf16)v[i];
+    }
+  }
+}
+
 template <int EPI, bool KEEP>
 __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
     const bf16* __restrict__ A, const bf16* __restrict__ W, const bf16* __restrict__ bias,
@@ -181,65 +253,161 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
         float v[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[i] = acc[a][b][4 * r4 + i];
-        const bool full = (n + 3 < N) && ((N & 3) == 0);
-        if (bias) {
+        epilogue4<EPI, KEEP>(v, m, n, N, bias, resid, out, keep_out);
+      }
+  }
+}
+
+// Large-tile variant for problems with many tiles: 256 x (64 TN) output tile,
+// 4 waves of 128 x (32 TN), one work-group per CU (one wave per SIMD) with the
+// accumulators in AGPRs.  Two LDS buffers, so one barrier per 64-wide K slice;
+// the next slice's global loads and LDS stores are spread between the MFMAs of
+// the current slice, and each 16-wide K step's fragments are read from LDS
+// during the previous step's MFMAs.  The MFMAs and their k order are those of
+// gemm_bf16_kernel, so both kernels give the same bits.
+constexpr int BIG_BM = 256, BIG_GROUP = 8;
+
+template <int EPI, bool KEEP, int TN>
+__global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
+    const bf16* __restrict__ A, const bf16* __restrict__ W, const bf16* __restrict__ bias,
+    const float* resid, void* out, bf16* keep_out, int M, int N, int K, int n_ntiles, int n_tiles) {
+  constexpr int TM = 4;
+  constexpr int BNB = 2 * TN * 32;
+  constexpr int STAGE = (BIG_BM + BNB) * PITCH;
+  __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
+
+  // tile order: contiguous ranges per XCD, then groups of BIG_GROUP m-tiles
+  // with m fastest, so that the A and W slices of the tiles running together
+  // on one XCD fit its L2
+  uint32_t bid = blockIdx.x;
+  if ((n_tiles & 7) == 0) bid = (bid & 7u) * ((uint32_t)n_tiles >> 3) + (bid >> 3);
+  const int n_mt = n_tiles / n_ntiles;
+  const int per_group = BIG_GROUP * n_ntiles;
+  const int grp = (int)bid / per_group;
+  const int first_m = grp * BIG_GROUP;
+  const int gm = min(BIG_GROUP, n_mt - first_m);
+  const int rem = (int)bid - grp * per_group;
+  const int m0 = (first_m + rem % gm) * BIG_BM, n0 = (rem / gm) * BNB;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int l32 = lane & 31, g = lane >> 5;
+
+  // loader: thread t moves 16-byte chunk (row t/8 + 32 i, column 8 (t % 8))
+  constexpr int A_LOADS = BIG_BM / 32, W_LOADS = BNB / 32, NL = A_LOADS + W_LOADS;
+  const int lrow = threadIdx.x >> 3, lcol = threadIdx.x & 7;
+  const uint32_t row_bytes = (uint32_t)K * 2u;
+  const uint32_t a_rows = (uint32_t)min(BIG_BM, M - m0), w_rows = (uint32_t)min(BNB, N - n0);
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + (int64_t)m0 * K, a_rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(W + (int64_t)n0 * K, w_rows * row_bytes);
+  const uint32_t off0 = (uint32_t)lrow * row_bytes + (uint32_t)lcol * 16u;
+  const uint32_t step32 = 32u * row_bytes;
+  u32x4 pre[NL];
+  auto gload = [&](int i, int k0) {
+    // columns past K: an offset past every range reads zero
+    const bool kin = k0 + 8 * lcol < K;
+    const uint32_t off = off0 + (uint32_t)k0 * 2u;
+    if (i < A_LOADS)
+      pre[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, kin ? off + i * step32 : 0xFFFFFFF0u, 0, 0);
+    else
+      pre[i] = __builtin_amdgcn_raw_buffer_load_b128(rw, kin ? off + (i - A_LOADS) * step32 : 0xFFFFFFF0u, 0, 0);
+  };
+  auto lstore = [&](int i, int buf) {
+    bf16* As = lds + buf * STAGE;
+    bf16* Ws = As + BIG_BM * PITCH;
+    if (i < A_LOADS)
+      *reinterpret_cast<u32x4*>(As + (lrow + 32 * i) * PITCH + lcol * 8) = pre[i];
+    else
+      *reinterpret_cast<u32x4*>(Ws + (lrow + 32 * (i - A_LOADS)) * PITCH + lcol * 8) = pre[i];
+  };
+
+  floatx16 acc[TN][TM];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (n + i < N) v[i] += bf2f(bias[n + i]);
-        }
-        const int64_t off = (int64_t)m * N + n;
-        if (KEEP) {
-          if (full) {
-            bf16x2 lo = {(bf16)v[0], (bf16)v[1]};
-            bf16x2 hi = {(bf16)v[2], (bf16)v[3]};
-            uint2 w;
-            w.x = __builtin_bit_cast(uint32_t, lo);
-            w.y = __builtin_bit_cast(uint32_t, hi);
-            *reinterpret_cast<uint2*>(keep_out + off) = w;
-          } else {
-            for (int i = 0; i < 4; ++i)
-              if (n + i < N) keep_out[off + i] = (bf16)v[i];
-          }
-        }
-        if (EPI == DSP_EPI_GELU) {
+  for (int a = 0; a < TN; ++a)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
-        }
-        if (EPI == DSP_EPI_RELU) {
+    for (int b = 0; b < TM; ++b)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+  bf16x8 af[2][TM], wf[2][TN];
+  auto fread = [&](int slot, int buf, int ks) {
+    const bf16* As = lds + buf * STAGE;
+    const bf16* Ws = As + BIG_BM * PITCH;
+#pragma unroll
+    for (int b = 0; b < TM; ++b)
+      af[slot][b] = *reinterpret_cast<const bf16x8*>(As + (wm * TM * 32 + 32 * b + l32) * PITCH + 16 * ks + 8 * g);
+#pragma unroll
+    for (int a = 0; a < TN; ++a)
+      wf[slot][a] = *reinterpret_cast<const bf16x8*>(Ws + (wn * TN * 32 + 32 * a + l32) * PITCH + 16 * ks + 8 * g);
+  };
+
+  // One K slice from LDS buffer kt & 1.  ST: store the prefetched slice kt + 1
+  // into the other buffer (during step 0); LD: load slice kt + 2 from global
+  // memory into the prefetch registers (during step 1).
+  auto slice = [&](int kt, auto st_c, auto ld_c) {
+    constexpr bool ST = decltype(st_c)::value, LD = decltype(ld_c)::value;
+    constexpr int NMF = TM * TN;
+    const int b = kt & 1;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < BK / 16) fread(cur ^ 1, b, ks + 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < NMF; ++j) {
+        const int a = j / TM, bb = j % TM;
+        acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][a], af[cur][bb], acc[a][bb], 0, 0, 0);
+        if (ks == 0 && ST) {
+#pragma unroll
+          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) lstore(i, b ^ 1);
         }
-        if (EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32) {
-          float* o = static_cast<float*>(out);
-          if (EPI == DSP_EPI_RESID) {
-            if (full) {
-              const float4 rv = *reinterpret_cast<const float4*>(resid + off);
-              v[0] += rv.x; v[1] += rv.y; v[2] += rv.z; v[3] += rv.w;
-            } else {
-              for (int i = 0; i < 4; ++i)
-                if (n + i < N) v[i] += resid[off + i];
-            }
-          }
-          if (full) {
-            *reinterpret_cast<float4*>(o + off) = make_float4(v[0], v[1], v[2], v[3]);
-          } else {
-            for (int i = 0; i < 4; ++i)
-              if (n + i < N) o[off + i] = v[i];
-          }
-        } else {
-          bf16* o = static_cast<bf16*>(out);
-          if (full) {
-            bf16x2 lo = {(bf16)v[0], (bf16)v[1]};
-            bf16x2 hi = {(bf16)v[2], (bf16)v[3]};
-            uint2 w;
-            w.x = __builtin_bit_cast(uint32_t, lo);
-            w.y = __builtin_bit_cast(uint32_t, hi);
-            *reinterpret_cast<uint2*>(o + off) = w;
-          } else {
-            for (int i = 0; i < 4; ++i)
-              if (n + i < N) o[off + i] = (bf16)v[i];
-          }
+        if (ks == 1 && LD) {
+#pragma unroll
+          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) gload(i, (kt + 2) * BK);
         }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    __syncthreads();
+    if (ST) fread(0, b ^ 1, 0);
+  };
+
+  const int nk = (K + BK - 1) / BK;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) gload(i, 0);
+#pragma unroll
+  for (int i = 0; i < NL; ++i) lstore(i, 0);
+  if (nk > 1) {
+#pragma unroll
+    for (int i = 0; i < NL; ++i) gload(i, BK);
+  }
+  __syncthreads();
+  fread(0, 0, 0);
+  using yes = std::true_type;
+  using no = std::false_type;
+  int kt = 0;
+  for (; kt + 2 < nk; ++kt) slice(kt, yes{}, yes{});
+  if (kt + 1 < nk) {
+    slice(kt, yes{}, no{});
+    ++kt;
+  }
+  slice(kt, no{}, no{});
+
+  // epilogue: lane owns row m = .. + l32 and columns n = .. + 8*r4 + 4g + {0..3}
+#pragma unroll
+  for (int bb = 0; bb < TM; ++bb) {
+    const int m = m0 + wm * TM * 32 + 32 * bb + l32;
+    if (m >= M) continue;
+#pragma unroll
+    for (int a = 0; a < TN; ++a)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int n = n0 + wn * TN * 32 + 32 * a + 8 * r4 + 4 * g;
+        if (n >= N) continue;
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = acc[a][bb][4 * r4 + i];
+        epilogue4<EPI, KEEP>(v, m, n, N, bias, resid, out, keep_out);
       }
   }
 }
@@ -313,14 +481,29 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
     return DSP_ERR_SHAPE;
   const bool keep = pre != nullptr;
   if (keep && epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) return DSP_ERR_ARG;
-  const dim3 grid((uint32_t)tiles), block(NTHR);
   const bf16* A = static_cast<const bf16*>(a);
   const bf16* Wt = static_cast<const bf16*>(w);
   const bf16* bs = static_cast<const bf16*>(bias);
   bf16* pb = static_cast<bf16*>(pre);
-#define DSP_GEMM_LAUNCH(E, KP)                                                                         \
-  hipLaunchKernelGGL((gemm_bf16_kernel<E, KP>), grid, block, 0, s, A, Wt, bs, residual, out, pb, (int)M, N, \
-                     K, (int)n_nt, (int)tiles)
+  // Large tiles when they still fill every CU at least once: 256 x 256 for
+  // wide outputs, 256 x 192 otherwise (N = 1152 is six of them).
+  const int big_bn = N >= 2048 ? 256 : 192;
+  const int64_t big_nt = (N + big_bn - 1) / big_bn;
+  const int64_t big_tiles = ((M + BIG_BM - 1) / BIG_BM) * big_nt;
+  const bool big = DSP_GEMM_BIG && big_tiles >= 256;
+#define DSP_GEMM_LAUNCH(E, KP)                                                                                  \
+  do {                                                                                                        \
+    if (!big) {                                                                                               \
+      hipLaunchKernelGGL((gemm_bf16_kernel<E, KP>), dim3((uint32_t)tiles), dim3(NTHR), 0, s, A, Wt, bs, residual, \
+                         out, pb, (int)M, N, K, (int)n_nt, (int)tiles);                                        \
+    } else if (big_bn == 256) {                                                                               \
+      hipLaunchKernelGGL((gemm_bf16_big_kernel<E, KP, 4>), dim3((uint32_t)big_tiles), dim3(NTHR), 0, s, A, Wt,  \
+                         bs, residual, out, pb, (int)M, N, K, (int)big_nt, (int)big_tiles);                    \
+    } else {                                                                                                  \
+      hipLaunchKernelGGL((gemm_bf16_big_kernel<E, KP, 3>), dim3((uint32_t)big_tiles), dim3(NTHR), 0, s, A, Wt,  \
+                         bs, residual, out, pb, (int)M, N, K, (int)big_nt, (int)big_tiles);                    \
+    }                                                                                                         \
+  } while (0)
   switch (epilogue) {
     case DSP_EPI_NONE: DSP_GEMM_LAUNCH(DSP_EPI_NONE, false); break;
     case DSP_EPI_RESID: DSP_GEMM_LAUNCH(DSP_EPI_RESID, false); break;

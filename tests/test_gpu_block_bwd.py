@@ -88,10 +88,12 @@ def test_block_train_f32(torch, flags):
     _train_case(torch, w, True, flags)
 
 
-@pytest.mark.parametrize("flags", [0, 4])
-def test_block_train_full_width_bf16(torch, flags):
-    """The 720M model's widths (C = 1152, 16 heads of 72, MLP 4608) on 2048 tokens."""
-    w = synth.Workload("block_wide", "block", "bf16", B=1, T=8, S=256, C=1152, H=16, F=4608, seed=23)
+@pytest.mark.parametrize("flags,T", [(0, 16), (4, 8)])
+def test_block_train_full_width_bf16(torch, flags, T):
+    """The 720M model's widths (C = 1152, 16 heads of 72, MLP 4608) on 4096 and
+    2048 tokens; at 4096 the MLP's first GEMM (with the pre-activation kept)
+    runs on the large-tile kernel."""
+    w = synth.Workload("block_wide", "block", "bf16", B=1, T=T, S=256, C=1152, H=16, F=4608, seed=23)
     _train_case(torch, w, False, flags)
 
 
@@ -108,6 +110,22 @@ def test_forward_train_output_matches_forward(torch, dtype, flags):
     y = dsp.dsp_st_block_forward(xd, wd, w.H, flags=flags)
     torch.cuda.synchronize()
     assert torch.equal(y_train, y), flags
+
+
+@pytest.mark.parametrize("flags", [0, 5])
+def test_forward_train_matches_forward_full_size(torch, flags):
+    """The bench workload (B1 T32 S1024, 32768 tokens: every GEMM on the
+    large-tile kernel): the training forward writes the inference forward's bits."""
+    import paper_2403_10266_amd as dsp
+    w = synth.WORKLOADS["block_bf16_B1_T32_S1024"]
+    x, p = synth.block_inputs(w)
+    wd = {n: (None if v is None else dev(v, "bf16")) for n, v in p.items()}
+    xd = dev(x, "f32")
+    y_train, saved = dsp.dsp_st_block_forward_train(xd, wd, w.H, flags=flags)
+    del saved
+    y = dsp.dsp_st_block_forward(xd, wd, w.H, flags=flags)
+    torch.cuda.synchronize()
+    assert torch.equal(y_train, y)
 
 
 def test_block_backward_deterministic_and_finite_full_size(torch):

@@ -28,8 +28,7 @@ def test_layernorm(torch, rows, C, out):
     assert_close(host(y), oracle.layernorm(x, 1e-6), out, "layernorm")
 
 
-# (M >= 256 and N >= 192 run the 256 x 192 pipelined kernel: ragged M, N and K
-# tails, a single partial K slice, and the block's own N = 3C)
+# ragged M, N and K tails, a single partial K slice, and the block's own N = 3C
 @pytest.mark.parametrize("M,N,K", [(1, 8, 8), (300, 200, 72), (513, 1152, 1152), (64, 4608, 1152),
                                    (257, 136, 4608), (256, 192, 8), (777, 385, 104),
                                    (512, 3456, 1152)])
@@ -55,6 +54,40 @@ def test_linear_bf16(torch, M, N, K, epi, bias):
         want = want + r
     # bf16 outputs carry a bf16 rounding; fp32 outputs only accumulation error
     assert_close(host(out), want, "bf16", f"linear epi={epi}")
+
+
+# Problems of at least 256 output tiles of 256 x 192 (N < 2048) or 256 x 256
+# run the large-tile kernel: ragged M, N and K (a partial last 64-wide slice).
+LARGE = [(16421, 1000, 1176), (8292, 2056, 136)]
+
+
+@pytest.mark.parametrize("M,N,K", LARGE)
+@pytest.mark.parametrize("epi", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("bias", [False, True])
+def test_linear_bf16_large_tiles(torch, M, N, K, epi, bias):
+    test_linear_bf16(torch, M, N, K, epi, bias)
+
+
+@pytest.mark.parametrize("M,N,K", LARGE + [(32768, 1152, 4608), (32768, 3456, 1152)])
+@pytest.mark.parametrize("epi", [0, 1, 2, 3, 4])
+def test_linear_large_tiles_match_small(torch, M, N, K, epi):
+    """Rows are independent, so rows computed by a call too small for the
+    large-tile kernel must have the bits of the same rows of the large call
+    (both kernels accumulate in the same k order)."""
+    import paper_2403_10266_amd as dsp
+    gen = torch.Generator(device="cuda").manual_seed(M + N + K + epi)
+    a = torch.randn((M, K), device="cuda", generator=gen).to(torch.bfloat16)
+    w = (torch.randn((N, K), device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    b = (torch.randn((N,), device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    r = torch.randn((M, N), device="cuda", generator=gen) if epi == 2 else None
+    say(f"linear large vs small tiles M={M} N={N} K={K} epi={epi}")
+    full = dsp.dsp_linear(a, w, b, r, epi)
+    for r0 in (0, 4096, M - 200):
+        rows = slice(r0, r0 + 200)
+        part = dsp.dsp_linear(a[rows].contiguous(), w, b, r[rows].contiguous() if r is not None else None, epi)
+        torch.cuda.synchronize()
+        assert torch.equal(part.view(torch.int16) if part.dtype == torch.bfloat16 else part,
+                           full[rows].view(torch.int16) if full.dtype == torch.bfloat16 else full[rows]), r0
 
 
 @pytest.mark.parametrize("M,N,K", [(130, 96, 64), (300, 200, 72)])
