@@ -51,6 +51,7 @@ import numpy as np
 
 HBM_PEAK_GBPS = 8000.0           # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PROBE_ITERS = 5000               # MFMA probe: 8 * 5000 MFMAs per wave, about 7 ms per launch
 
 METRIC = "spatial+temporal attn TFLOP/s (% MFMA peak); dsp_switch GB/s (% HBM peak)"
 
@@ -74,7 +75,8 @@ def parse():
     ap.add_argument("--only", default=None,
                     choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange",
                              "temporal_strided", "switch_k3", "split", "gather", "copy",
-                             "attn_bwd_spatial", "attn_bwd_temporal", "block_train_fwd", "block_bwd"],
+                             "attn_bwd_spatial", "attn_bwd_temporal", "block_train_fwd", "block_bwd",
+                             "mfma_probe"],
                     help="run a single part (for profiling); prints per-kernel times only. "
                          "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
                          "plain 604 MB copy used to calibrate traffic counters")
@@ -233,13 +235,19 @@ def main():
     def run_copy():
         dsp.dsp_switch(t["x_sw"], 1, 1, 1, out=t["y_sw"].view(t["x_sw"].shape))
 
+    probe_ws = torch.empty(dsp.probe_mfma_workspace_bytes(), dtype=torch.uint8, device=dev)
+
+    def run_mfma_probe():
+        dsp.dsp_probe_mfma(PROBE_ITERS, probe_ws)
+
     parts = [("switch", run_switch), ("switch_inv", run_switch_inv), ("spatial", run_spatial),
              ("temporal", run_temporal), ("block", run_block)]
     # timed on its own after the steps: not a step of the single-GPU hot path
     extras = [("exchange", run_exchange), ("temporal_strided", run_temporal_strided),
               ("switch_k3", run_switch_k3), ("split", run_split), ("gather", run_gather),
               ("attn_bwd_spatial", run_attn_bwd_spatial), ("attn_bwd_temporal", run_attn_bwd_temporal),
-              ("block_train_fwd", run_block_train_fwd), ("block_bwd", run_block_bwd)]
+              ("block_train_fwd", run_block_train_fwd), ("block_bwd", run_block_bwd),
+              ("mfma_probe", run_mfma_probe)]
     if args.only:
         every = dict(parts + extras)
         parts, extras = [(args.only, run_copy if args.only == "copy" else every[args.only])], []
@@ -303,6 +311,7 @@ def main():
     gather_gbps = sw_bytes / (ms["gather"] * 1e-3) / 1e9
 
     traffic = measured_traffic(args.traffic)
+    mfma_sustained = dsp.probe_mfma_flops(PROBE_ITERS) / (ms["mfma_probe"] * 1e-3) / 1e12
 
     out = {
         "metric": METRIC,
@@ -355,6 +364,16 @@ def main():
             "frac": round(sp_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
             "traffic": traffic,
         },
+    }
+    # context for roofline.frac: the bf16 MFMA rate this GPU sustains with every
+    # CU busy (independent MFMA chains only), measured in this run
+    out["mfma_sustained"] = {
+        "value": round(mfma_sustained, 1),
+        "unit": "TFLOP/s",
+        "frac_of_peak": round(mfma_sustained / MFMA_BF16_PEAK_TFLOPS, 4),
+        "spatial_frac_of_sustained": round(sp_tflops / mfma_sustained, 4),
+        "how": "dsp_probe_mfma: 8 independent v_mfma_f32_32x32x16_bf16 chains per wave, 2 waves per SIMD, "
+               "all CUs, operand bits changing every iteration; HIP events over %d launches" % K,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_budget)

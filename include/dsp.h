@@ -463,6 +463,26 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
                           const dsp_block_grads_t* grads, int64_t B, int64_t T, int64_t S, int C, int H, int F,
                           float ln_eps, int flags, int dtype, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Measurement aid (not a step of the method): the bf16 MFMA rate the chip
+ * sustains with every CU busy.  The published dense bf16 figure assumes the
+ * peak engine clock; under a long all-CU MFMA load the clock settles lower.
+ * A benchmark reports a kernel's fraction of the published peak, and this
+ * rate beside it, measured in the same process and conditions.
+ *
+ * dsp_probe_mfma -- launches 2048 work-groups of 4 waves (two per SIMD), each
+ *   wave issuing 8 * iters independent v_mfma_f32_32x32x16_bf16 on operands
+ *   whose bits change every iteration; nothing else runs in its loop.  The
+ *   caller times it (events on `stream`) and divides
+ *   dsp_probe_mfma_flops(iters) by the time.  workspace: DEVICE memory of at
+ *   least dsp_probe_mfma_workspace_bytes() bytes, 16-byte aligned (receives
+ *   one float per thread, meaningless).  Errors: DSP_ERR_ARG (iters < 1),
+ *   DSP_ERR_NULL, DSP_ERR_WORKSPACE, DSP_ERR_ALIGN.
+ * ------------------------------------------------------------------------ */
+size_t dsp_probe_mfma_workspace_bytes(void);
+double dsp_probe_mfma_flops(int iters);
+int dsp_probe_mfma(void* workspace, size_t ws_bytes, int iters, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -81,6 +81,9 @@ _SIGNATURES = {
     "dsp_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _P]),
     "dsp_st_block_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
     "dsp_st_block_train_saved_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I, _I]),
+    "dsp_probe_mfma_workspace_bytes": (_SZ, []),
+    "dsp_probe_mfma_flops": (_c.c_double, [_I]),
+    "dsp_probe_mfma": (_I, [_P, _SZ, _I, _P]),
     "dsp_st_block_backward_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I, _I, _I, _I]),
     "dsp_st_block_forward_train": (_I, [_P, _P, _c.POINTER(BlockWeights), _P, _SZ, _I64, _I64, _I64, _I, _I,
                                         _I, _F, _I, _I, _P]),
@@ -610,6 +613,23 @@ def dsp_st_block_backward(x, dy, weights: dict, saved, H: int, eps: float = 1e-6
                                        _ptr(workspace), workspace.numel(), _ptr(dx), ctypes.byref(gt), B, T, S, C,
                                        H, F, float(eps), flags, code, _stream(stream)), "dsp_st_block_backward")
     return dx, grads
+
+
+def probe_mfma_workspace_bytes() -> int:
+    return int(lib().dsp_probe_mfma_workspace_bytes())
+
+
+def probe_mfma_flops(iters: int) -> float:
+    """Flops one dsp_probe_mfma launch of `iters` iterations issues."""
+    return float(lib().dsp_probe_mfma_flops(iters))
+
+
+def dsp_probe_mfma(iters: int, workspace, stream=None):
+    """Launch the sustained-MFMA-rate probe (a measurement aid): time it with
+    events on `stream` and divide probe_mfma_flops(iters) by the time."""
+    _require_device(workspace)
+    _check(lib().dsp_probe_mfma(_ptr(workspace), workspace.numel() * workspace.element_size(), iters,
+                                _stream(stream)), "dsp_probe_mfma")
 
 
 __all__ = ["lib", "status_str", "DspError", "BlockWeights", "dsp_switch", "dsp_spatial_attn",

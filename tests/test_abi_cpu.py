@@ -394,3 +394,14 @@ def test_binding_rejects_host_tensors():
     x = torch.zeros((1, 2, 2, 8), dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         dsp.dsp_switch(x, 1, 2, 1)
+
+
+def test_probe_mfma_validation(lib):
+    need = lib.dsp_probe_mfma_workspace_bytes()
+    assert need == 2048 * 256 * 4
+    assert lib.dsp_probe_mfma_flops(10) == 2048 * 4 * 10 * 8 * 2.0 * 32 * 32 * 16
+    assert lib.dsp_probe_mfma_flops(0) == 0.0
+    assert lib.dsp_probe_mfma(FAKE, need, 0, None) == dsp.DSP_ERR_ARG
+    assert lib.dsp_probe_mfma(None, need, 10, None) == dsp.DSP_ERR_NULL
+    assert lib.dsp_probe_mfma(FAKE, need - 1, 10, None) == dsp.DSP_ERR_WORKSPACE
+    assert lib.dsp_probe_mfma(FAKE + 4, need, 10, None) == dsp.DSP_ERR_ALIGN
