@@ -76,7 +76,7 @@ def parse():
                     choices=["switch", "switch_inv", "spatial", "temporal", "block", "exchange",
                              "temporal_strided", "switch_k3", "split", "gather", "copy",
                              "attn_bwd_spatial", "attn_bwd_temporal", "block_train_fwd", "block_bwd",
-                             "mfma_probe"],
+                             "mfma_probe", "tiny_chain", "tiny_chain_graph"],
                     help="run a single part (for profiling); prints per-kernel times only. "
                          "'copy' is dsp_switch with from_dim == to_dim on the switch tensor: a "
                          "plain 604 MB copy used to calibrate traffic counters")
@@ -182,6 +182,28 @@ def main():
         t["dx_bl"], t["g_bl"] = dsp.dsp_st_block_backward(t["x_bl"], t["dy_bl"], t["w_bl"], t["sv_bl"], wbl.H)
         t["bws_bl"] = torch.empty(int(dsp.lib().dsp_st_block_backward_workspace_bytes(
             wbl.B, wbl.T, wbl.S, wbl.C, wbl.H, wbl.F, dsp.DSP_BF16)), dtype=torch.uint8, device=dev)
+    # the tiny fp32 chain (launch-latency bound): eager calls and a captured HIP graph
+    wtc = W["tiny_chain_f32"]
+    x_tc, p_tc = synth.chain_inputs(wtc)
+    t["x_tc"] = to_dev(x_tc, "f32")
+    t["w_tc"] = {n: to_dev(v, "f32") for n, v in p_tc.items()}
+    t["y_tc"] = torch.empty((wtc.B, wtc.S, wtc.T, wtc.C), dtype=torch.float32, device=dev)
+    t["ws_tc"] = torch.empty(dsp.block_workspace_bytes(wtc.B, wtc.T, wtc.S, wtc.C, wtc.H, 0, dsp.DSP_F32),
+                             dtype=torch.uint8, device=dev)
+
+    def run_tiny():
+        dsp.dsp_st_block_forward(t["x_tc"], t["w_tc"], wtc.H, flags=dsp.DSP_BLOCK_ATTN_ONLY, out=t["y_tc"],
+                                 workspace=t["ws_tc"])
+
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        run_tiny()
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    tiny_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(tiny_graph):
+        run_tiny()
     torch.cuda.synchronize()
 
     def run_switch():
@@ -237,6 +259,9 @@ def main():
 
     probe_ws = torch.empty(dsp.probe_mfma_workspace_bytes(), dtype=torch.uint8, device=dev)
 
+    def run_tiny_graph():
+        tiny_graph.replay()
+
     def run_mfma_probe():
         dsp.dsp_probe_mfma(PROBE_ITERS, probe_ws)
 
@@ -247,7 +272,7 @@ def main():
               ("switch_k3", run_switch_k3), ("split", run_split), ("gather", run_gather),
               ("attn_bwd_spatial", run_attn_bwd_spatial), ("attn_bwd_temporal", run_attn_bwd_temporal),
               ("block_train_fwd", run_block_train_fwd), ("block_bwd", run_block_bwd),
-              ("mfma_probe", run_mfma_probe)]
+              ("mfma_probe", run_mfma_probe), ("tiny_chain", run_tiny), ("tiny_chain_graph", run_tiny_graph)]
     if args.only:
         every = dict(parts + extras)
         parts, extras = [(args.only, run_copy if args.only == "copy" else every[args.only])], []
@@ -332,7 +357,8 @@ def main():
                         "switched T->H (K=3); split along S / gather along T of 8 shards; spatial attn B2 T16 S4096 H16 D72; "
                         "temporal attn B2 S512 T128 H16 D72; ST block B1 T32 S1024 C1152 H16 F4608; "
                         "attention backward of the spatial and temporal workloads; training forward and "
-                        "backward of the ST block",
+                        "backward of the ST block; the tiny fp32 chain B1 T4 S16 C64 H4 D16 (eager and "
+                        "HIP-graph replay, us per call)",
             "attn_frac_mfma_peak": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
             "switch_GBps": round(sw_gbps, 1),
             "switch_frac_hbm_peak": round(sw_gbps / HBM_PEAK_GBPS, 4),
@@ -353,6 +379,8 @@ def main():
             "attn_bwd_temporal_TFLOPs": round(2.5 * F_tp / (ms["attn_bwd_temporal"] * 1e-3) / 1e12, 2),
             "block_train_fwd_TFLOPs": round(F_bl / (ms["block_train_fwd"] * 1e-3) / 1e12, 2),
             "block_bwd_TFLOPs": round(F_bl_bwd / (ms["block_bwd"] * 1e-3) / 1e12, 2),
+            "tiny_chain_us": round(ms["tiny_chain"] * 1e3, 2),
+            "tiny_chain_graph_us": round(ms["tiny_chain_graph"] * 1e3, 2),
             "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
         },
         "roofline": {

@@ -770,12 +770,19 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
   const int64_t shp[4] = {B, T, S, C};
   // the bf16 (or fp32) operand of a projection: LN of the residual stream, or
   // (post-LN, projection-only chain) the stream itself
+  // (fp32 without LN: the stream itself, no copy)
+  const void* hin = h;
   auto operand = [&](const float* r, bool norm) {
-    return norm ? launch_layernorm(r, 0, h, bf, tokens, C, ln_eps, s)
-                : launch_cast(r, 0, h, bf, tokens * C, s);
+    hin = h;
+    if (norm) return launch_layernorm(r, 0, h, bf, tokens, C, ln_eps, s);
+    if (!bf) {
+      hin = r;
+      return (int)DSP_OK;
+    }
+    return launch_cast(r, 0, h, bf, tokens * C, s);
   };
   auto attn_sublayer = [&](const void* wqkv, const void* bqkv, int64_t X, int64_t L) {
-    int r = linear_impl(h, wqkv, bqkv, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s);
+    int r = linear_impl(hin, wqkv, bqkv, nullptr, qkv, tokens, 3 * C, C, DSP_EPI_NONE, dtype, s);
     if (r != DSP_OK) return r;
     return attn_impl(qkvc, qkvc + (size_t)C * es, qkvc + (size_t)2 * C * es, o, B, X, L, H, D, ld3, C,
                      0.0f, dtype, s);
@@ -805,7 +812,7 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
     DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, y_BSTC, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s));
     // ---- MLP (Eq. 5 with GELU or ReLU), residual
     DSP_TRY(operand(y_BSTC, !(flags & DSP_BLOCK_NO_MLP_LN)));
-    DSP_TRY(linear_impl(h, w->w1, w->b1, nullptr, f, tokens, F, C, act, dtype, s));
+    DSP_TRY(linear_impl(hin, w->w1, w->b1, nullptr, f, tokens, F, C, act, dtype, s));
     DSP_TRY(linear_impl(f, w->w2, w->b2, y_BSTC, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
     return DSP_OK;
   }
@@ -822,7 +829,7 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
   DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, x1, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s));
   DSP_TRY(launch_layernorm(y_BSTC, 0, x1, 0, tokens, C, ln_eps, s));           // x1 = r2
   DSP_TRY(operand(x1, false));
-  DSP_TRY(linear_impl(h, w->w1, w->b1, nullptr, f, tokens, F, C, act, dtype, s));
+  DSP_TRY(linear_impl(hin, w->w1, w->b1, nullptr, f, tokens, F, C, act, dtype, s));
   if (flags & DSP_BLOCK_NO_MLP_LN) {
     DSP_TRY(linear_impl(f, w->w2, w->b2, x1, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
     return DSP_OK;

@@ -1,7 +1,9 @@
 // fp32 attention along one sequence dimension (Eq. 3 per head; also grouped
 // key/value heads and a key length of its own for cross-attention), the exact
 // path: fp32 storage, fp32 FMA arithmetic, no reduced-precision operand
-// anywhere.  One thread owns one (unit, query, 32-column slice of the output):
+// anywhere.  Head widths 16, 32, 64, 72, 80 and 96 run one wave per unit
+// (attn_f32_unit_kernel below); any other width runs the general kernel, in
+// which one thread owns one (unit, query, 32-column slice of the output):
 // a first pass over the keys finds the row maximum of the scaled scores, a
 // second pass accumulates exp(score - max) and the weighted values of its
 // slice.  Meant for small problems and for checking; the bf16 MFMA kernel is
@@ -76,6 +78,77 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(ParamsF p) {
     if (c < nc) orow[c] = acc[c] * inv;
 }
 
+// One wave per unit for common head widths: the unit's keys and values pass
+// through LDS in chunks of KC rows (every lane reads the same row: an LDS
+// broadcast), each lane owns queries lane, lane + 64, ... with its query row
+// and its D output columns in registers, and the softmax runs online (the
+// reference maximum moves when a larger score arrives, rescaling the
+// accumulator and the row sum by exp of the difference).  Same arithmetic
+// type (fp32 FMAs, expf) as the kernel above, but no loop waits on global
+// memory per key.
+template <int D>
+__global__ __launch_bounds__(64) void attn_f32_unit_kernel(ParamsF p) {
+  constexpr int KC = 32;
+  __shared__ __attribute__((aligned(16))) float ks[KC * D];
+  __shared__ __attribute__((aligned(16))) float vs[KC * D];
+  const int lane = threadIdx.x;
+  const int64_t unit = blockIdx.x;
+  const int64_t h = unit % p.H;
+  const int64_t bx = unit / p.H;
+  const int64_t xx = bx % p.X;
+  const int64_t bb = bx / p.X;
+  const float* qg = p.q + bb * p.b_in + xx * p.x_in + h * D;
+  const int64_t kv_base = bb * p.b_kv + xx * p.x_kv + (h / p.grp) * D;
+  const float* kg = p.k + kv_base;
+  const float* vg = p.v + kv_base;
+  float* og = p.o + bb * p.b_out + xx * p.x_out + h * D;
+  for (int64_t q0 = 0; q0 < p.L; q0 += 64) {
+    const int64_t qi = q0 + lane;
+    const bool valid = qi < p.L;
+    float qr[D], acc[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      qr[d] = valid ? qg[qi * p.r_in + d] : 0.0f;
+      acc[d] = 0.0f;
+    }
+    float m = -INFINITY, l = 0.0f;
+    for (int64_t k0 = 0; k0 < p.Lk; k0 += KC) {
+      const int nk = (int)min((int64_t)KC, p.Lk - k0);
+      __syncthreads();  // the previous chunk is consumed
+      for (int e = lane; e < nk * D; e += 64) {
+        const int r = e / D, c = e - r * D;
+        ks[e] = kg[(k0 + r) * p.r_kv + c];
+        vs[e] = vg[(k0 + r) * p.r_kv + c];
+      }
+      __syncthreads();
+      for (int j = 0; j < nk; ++j) {
+        float sc = 0.0f;
+#pragma unroll
+        for (int d = 0; d < D; ++d) sc = fmaf(qr[d], ks[j * D + d], sc);
+        sc *= p.scale;
+        if (sc > m) {
+          const float corr = expf(m - sc);  // 0 for the first key
+          l *= corr;
+#pragma unroll
+          for (int d = 0; d < D; ++d) acc[d] *= corr;
+          m = sc;
+        }
+        const float e = expf(sc - m);
+        l += e;
+#pragma unroll
+        for (int d = 0; d < D; ++d) acc[d] = fmaf(e, vs[j * D + d], acc[d]);
+      }
+    }
+    if (valid) {
+      const float inv = 1.0f / l;
+      float* orow = og + qi * p.r_out;
+#pragma unroll
+      for (int d = 0; d < D; ++d) orow[d] = acc[d] * inv;
+      if (p.lse) p.lse[unit * p.L + qi] = m + logf(l);
+    }
+  }
+}
+
 }  // namespace
 
 int launch_attn_f32(const AttnArgs& a, hipStream_t s) {
@@ -104,6 +177,19 @@ int launch_attn_f32(const AttnArgs& a, hipStream_t s) {
   p.total = a.B * a.X * a.H * a.L * p.n_dc;
   p.scale = a.scale;
   if (p.total == 0) return DSP_OK;
+  const int64_t units = a.B * a.X * a.H;
+  if (units < (int64_t(1) << 31)) {
+    const dim3 g((uint32_t)units), b(64);
+    switch (a.D) {
+      case 16: hipLaunchKernelGGL(attn_f32_unit_kernel<16>, g, b, 0, s, p); return last_launch_status();
+      case 32: hipLaunchKernelGGL(attn_f32_unit_kernel<32>, g, b, 0, s, p); return last_launch_status();
+      case 64: hipLaunchKernelGGL(attn_f32_unit_kernel<64>, g, b, 0, s, p); return last_launch_status();
+      case 72: hipLaunchKernelGGL(attn_f32_unit_kernel<72>, g, b, 0, s, p); return last_launch_status();
+      case 80: hipLaunchKernelGGL(attn_f32_unit_kernel<80>, g, b, 0, s, p); return last_launch_status();
+      case 96: hipLaunchKernelGGL(attn_f32_unit_kernel<96>, g, b, 0, s, p); return last_launch_status();
+      default: break;
+    }
+  }
   const int64_t blocks = (p.total + 255) / 256;
   if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
   hipLaunchKernelGGL(attn_f32_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p);

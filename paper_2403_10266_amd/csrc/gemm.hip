@@ -413,7 +413,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
 }
 
 // ---------------------------------------------------------------- fp32 path
-constexpr int FT = 64, FK = 16;
+constexpr int FT = 64, FK = 64;  // one global round trip per 64-wide K slice
 
 // `pre` (GELU/ReLU, may be null): also store the pre-activation there.
 template <int EPI>
@@ -428,11 +428,22 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   const int m0 = blockIdx.y * FT, n0 = blockIdx.x * FT;
   float acc[4][4] = {};
   for (int k0 = 0; k0 < K; k0 += FK) {
-    for (int e = threadIdx.x; e < FT * FK; e += 256) {
+    // all loads of the slice first (one round trip), then the LDS stores
+    constexpr int PER = FT * FK / 256;
+    float la[PER], lb[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + 256 * i;
       const int r = e / FK, kk = e % FK;
       const int gm = m0 + r, gn = n0 + r, gk = k0 + kk;
-      As[kk][r] = (gm < M && gk < K) ? A[(int64_t)gm * K + gk] : 0.0f;
-      Bs[kk][r] = (gn < N && gk < K) ? W[(int64_t)gn * K + gk] : 0.0f;
+      la[i] = (gm < M && gk < K) ? A[(int64_t)gm * K + gk] : 0.0f;
+      lb[i] = (gn < N && gk < K) ? W[(int64_t)gn * K + gk] : 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      As[e % FK][e / FK] = la[i];
+      Bs[e % FK][e / FK] = lb[i];
     }
     __syncthreads();
 #pragma unroll
