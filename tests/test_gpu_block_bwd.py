@@ -145,3 +145,27 @@ def test_block_backward_deterministic_and_finite_full_size(torch):
     assert torch.equal(dx1, dx2)
     for n in g1:
         assert bool(torch.isfinite(g1[n]).all()) and torch.equal(g1[n], g2[n]), n
+
+
+def test_block_backward_homogeneous_full_size(torch):
+    """The bench workload: the backward is linear in dy, and every step of it
+    (bf16 rounding of an operand, fp32 sums in a fixed order, the LayerNorm
+    backward, dZ = P * (dP - Delta) with Delta's hi/lo split, the split-K
+    reductions) commutes exactly with scaling by a power of two, so
+    backward(2 dy) has exactly twice the bits of backward(dy): a property of
+    the whole chain that holds at any size."""
+    import paper_2403_10266_amd as dsp
+    w = synth.WORKLOADS["block_bf16_B1_T32_S1024"]
+    x, p = synth.block_inputs(w)
+    wd = {n: (None if v is None else dev(v, "bf16")) for n, v in p.items()}
+    xd = dev(x, "f32")
+    dy = torch.randn((w.B, w.S, w.T, w.C), generator=torch.Generator(device="cuda").manual_seed(5),
+                     device="cuda")
+    _, saved = dsp.dsp_st_block_forward_train(xd, wd, w.H)
+    dx1, g1 = dsp.dsp_st_block_backward(xd, dy, wd, saved, w.H, with_bias=True)
+    dx2, g2 = dsp.dsp_st_block_backward(xd, dy * 2.0, wd, saved, w.H, with_bias=True)
+    torch.cuda.synchronize()
+    assert torch.equal(dx2, dx1 * 2.0)
+    for n in g1:
+        assert torch.equal(g2[n], g1[n] * 2.0), n
+
