@@ -385,11 +385,29 @@ int launch_colsum_f32(const float* dy, float* db, int64_t M, int N, hipStream_t 
 }
 
 int grad_splits(int64_t M, int64_t N, int64_t K) {
-  // enough work-groups to fill 256 CUs twice, slices of at least 2048
+  // The split count minimising a cost model, in units of one 64-wide K slice
+  // of one tile on a full round of work-groups (two per CU, 256 CUs):
+  //   rounds * (slices per split + 2 for the work-group's set-up and fp32
+  //   store) + s * (the extra write and read of an M x N fp32 partial,
+  //   about 8 M N bytes at 5 TB/s against 2.9 us per slice round).
+  // Splits keep at least 32 slices (a reduction of 2048), so small problems
+  // run unsplit.
   const int64_t tiles = ((M + GBM - 1) / GBM) * ((N + GBN - 1) / GBN);
-  int64_t s = 1;
-  while (tiles * s < 512 && K / (2 * s) >= 2048 && s < 16) s *= 2;
-  return (int)s;
+  const int64_t slices = (K + GBK - 1) / GBK;
+  const double per_split = (double)M * (double)N * 5.5e-7;
+  int best = 1;
+  double best_cost = 0.0;
+  for (int s = 1; s <= 16; ++s) {
+    const int64_t per = (slices + s - 1) / s;
+    if (per < 32 || per * (s - 1) >= slices) break;  // too short, or the last split empty
+    const int64_t rounds = (tiles * s + 511) / 512;
+    const double cost = (double)rounds * (double)(per + 2) + (s > 1 ? s * per_split : 0.0);
+    if (s == 1 || cost < best_cost) {
+      best = s;
+      best_cost = cost;
+    }
+  }
+  return best;
 }
 
 bool grad_gemm_fits(int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb) {
