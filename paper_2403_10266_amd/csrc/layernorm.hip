@@ -170,6 +170,20 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_long_kernel(
   }
 }
 
+// fp32 -> bf16, eight elements per thread and iteration: two 16-byte loads,
+// one 16-byte store (n a multiple of 8, 16-byte aligned buffers)
+__global__ __launch_bounds__(256) void cast_f32_bf16_x8_kernel(const float4* __restrict__ x,
+                                                               uint4* __restrict__ y, int64_t n8) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += stride) {
+    const float4 a = x[2 * i], b = x[2 * i + 1];
+    typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+    bf16x8_t v = {(__bf16)a.x, (__bf16)a.y, (__bf16)a.z, (__bf16)a.w,
+                  (__bf16)b.x, (__bf16)b.y, (__bf16)b.z, (__bf16)b.w};
+    y[i] = __builtin_bit_cast(uint4, v);
+  }
+}
+
 __global__ __launch_bounds__(256) void cast_kernel(const void* __restrict__ x, int x_bf,
                                                    void* __restrict__ y, int y_bf, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -202,6 +216,14 @@ int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16,
 // Element-wise format conversion (fp32 <-> bf16, round to nearest even).
 int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s) {
   if (n == 0) return DSP_OK;
+  if (!x_bf16 && y_bf16 && n % 8 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+      reinterpret_cast<uintptr_t>(y) % 16 == 0) {
+    const int64_t n8 = n / 8;
+    const int64_t blocks = std::min<int64_t>((n8 + 255) / 256, 16384);
+    hipLaunchKernelGGL(cast_f32_bf16_x8_kernel, dim3((uint32_t)blocks), dim3(256), 0, s,
+                       static_cast<const float4*>(x), static_cast<uint4*>(y), n8);
+    return last_launch_status();
+  }
   const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
   hipLaunchKernelGGL(cast_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, x, x_bf16, y, y_bf16, n);
   return last_launch_status();
