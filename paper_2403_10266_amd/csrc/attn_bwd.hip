@@ -11,7 +11,9 @@
 //  * Two deterministic kernels, no atomics: the first owns a block of queries
 //    and loops over key tiles (dQ, and Delta for its queries); the second owns
 //    a block of keys and loops over query tiles (dK and dV).  Each recomputes
-//    the scores it needs.
+//    the scores it needs.  Units of at most 128 queries and keys (temporal
+//    attention) run a third kernel that holds the whole unit in LDS and does
+//    both loops, so its rows are read from HBM once.
 //  * The head width is padded to a multiple of 16 with two spare columns.
 //    They carry the per-row statistics into the score products, as a bf16 hi/lo
 //    pair (|x - hi - lo| <= 2^-16 |x|): the query side holds -lse and the
@@ -33,6 +35,12 @@
 
 #include "attn_bf16_common.h"
 #include "dsp_internal.h"
+
+// Units of at most 128 queries and keys (no grouped heads) run the fused
+// single-pass kernel.
+#ifndef DSP_ATTN_BWD_SHORT
+#define DSP_ATTN_BWD_SHORT 1
+#endif
 
 namespace dsp {
 namespace {
@@ -528,6 +536,224 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// Short units (L, Lk <= 32 NW, one query head per key/value head): one
+// work-group owns a whole unit.  Q', dO, K and V (and dO * O for Delta) are
+// read from global memory once, with coalesced 16-byte loads, into LDS tiles
+// whose bias columns are set as in the two kernels above (K, V: 1.0 on rows
+// below Lk, 0 past it -- so keys past Lk get dZ = 0 without a mask; Q', dO:
+// -lse2 and -Delta on rows below L, 0 past it).  Then, from LDS only, wave w
+// runs the dQ loop for queries 32w .. 32w + 31 over all keys, and the dK/dV
+// loop for keys 32w .. 32w + 31 over all queries (see the wave roles below).  The scores are computed
+// twice, as in the two-kernel path, but the unit's rows cross HBM once.
+// 2 NW waves: waves [0, NW) run the dQ loops, waves [NW, 2 NW) the dK/dV loops.
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 128, 1) void attn_bwd_short_kernel(BwdParams p) {
+  using G = BGeo<D>;
+  constexpr int R = 32 * NW, NT = NW * 128;
+  constexpr int TILE = R * G::P;
+  constexpr int NCH = R * G::CH;                 // 16-byte chunks of one tensor's rows
+  constexpr int NLOAD = (NCH + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) bf16 lds[4 * TILE];
+  __shared__ float dpart[NCH];
+  bf16* qs = lds;             // Q'
+  bf16* os = lds + TILE;      // dO
+  bf16* ks = lds + 2 * TILE;  // K
+  bf16* vs = lds + 3 * TILE;  // V
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l32 = lane & 31, g = lane >> 5;
+  const uint32_t unit = blockIdx.x;  // (b, x, h): query head = key/value head
+  const uint32_t head = unit % p.H, bx = unit / p.H;
+  const uint32_t L = p.L, Lk = p.Lk;
+  const int64_t q_base = bx_base(p, bx, p.b_q, p.x_q) + (int64_t)head * D;
+  const int64_t o_base = bx_base(p, bx, p.b_o, p.x_o) + (int64_t)head * D;
+  const int64_t kv_base = bx_base(p, bx, p.b_kv, p.x_kv) + (int64_t)head * D;
+
+  // ---- rows into LDS: chunk c = row c / CH, 16 bytes at column 8 (c % CH);
+  // rows past L (Lk) fall outside the buffer ranges and read as zero
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + q_base, L * (uint32_t)p.r_q * 2u);
+  const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.dout + o_base, L * (uint32_t)p.r_o * 2u);
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + o_base, L * (uint32_t)p.r_o * 2u);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + kv_base, Lk * (uint32_t)p.r_kv * 2u);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + kv_base, Lk * (uint32_t)p.r_kv * 2u);
+  u32x4 cq[NLOAD], cd[NLOAD], co[NLOAD], ck[NLOAD], cv[NLOAD];
+#pragma unroll
+  for (int i = 0; i < NLOAD; ++i) {
+    const int c = threadIdx.x + i * NT;
+    if (c < NCH) {
+      const uint32_t row = c / G::CH, col = c - row * G::CH;
+      const uint32_t oq = row * (uint32_t)p.r_q * 2u + col * 16u;
+      const uint32_t oo = row * (uint32_t)p.r_o * 2u + col * 16u;
+      const uint32_t okv = row * (uint32_t)p.r_kv * 2u + col * 16u;
+      cq[i] = __builtin_amdgcn_raw_buffer_load_b128(rq, oq, 0, 0);
+      cd[i] = __builtin_amdgcn_raw_buffer_load_b128(rd, oo, 0, 0);
+      co[i] = __builtin_amdgcn_raw_buffer_load_b128(ro, oo, 0, 0);
+      ck[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, okv, 0, 0);
+      cv[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, okv, 0, 0);
+    }
+  }
+  // padding columns (the bias pair of Q' and dO is written below)
+  for (int r = threadIdx.x; r < R; r += NT) {
+    const bf16 kb = (bf16)((uint32_t)r < Lk ? 1.0f : 0.0f);
+    ks[r * G::P + D] = ks[r * G::P + D + 1] = kb;
+    vs[r * G::P + D] = vs[r * G::P + D + 1] = kb;
+    for (int c = D + 2; c < G::P; ++c)
+      qs[r * G::P + c] = os[r * G::P + c] = ks[r * G::P + c] = vs[r * G::P + c] = (bf16)0.0f;
+  }
+#pragma unroll
+  for (int i = 0; i < NLOAD; ++i) {
+    const int c = threadIdx.x + i * NT;
+    if (c < NCH) {
+      const int row = c / G::CH, col = c - row * G::CH;
+      const int off = row * G::P + col * 8;
+      bf16x8 x = __builtin_bit_cast(bf16x8, cq[i]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = (bf16)((float)x[e] * p.c);  // Q' as in the forward
+      *reinterpret_cast<bf16x8*>(qs + off) = x;
+      *reinterpret_cast<u32x4*>(os + off) = cd[i];
+      *reinterpret_cast<u32x4*>(ks + off) = ck[i];
+      *reinterpret_cast<u32x4*>(vs + off) = cv[i];
+      const bf16x8 dv8 = __builtin_bit_cast(bf16x8, cd[i]), ov8 = __builtin_bit_cast(bf16x8, co[i]);
+      float d = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d += (float)dv8[e] * (float)ov8[e];
+      dpart[c] = d;
+    }
+  }
+  __syncthreads();
+  // Delta = rowsum(dO * O) and the bias pairs: -(lse * log2 e) on Q', -Delta on dO
+  for (int r = threadIdx.x; r < R; r += NT) {
+    float delta = 0.0f, lse2 = 0.0f;
+    if ((uint32_t)r < L) {
+#pragma unroll
+      for (int col = 0; col < G::CH; ++col) delta += dpart[r * G::CH + col];
+      lse2 = p.lse[(int64_t)unit * L + r] * kLog2e;
+      p.delta[(int64_t)unit * L + r] = delta;
+    }
+    const bf16 lh = (bf16)lse2, dh = (bf16)delta;
+    qs[r * G::P + D] = (bf16)(-(float)lh);
+    qs[r * G::P + D + 1] = (bf16)(-(lse2 - (float)lh));
+    os[r * G::P + D] = (bf16)(-(float)dh);
+    os[r * G::P + D + 1] = (bf16)(-(delta - (float)dh));
+  }
+  __syncthreads();
+
+  const int row0 = 32 * (wave % NW);
+  // ---- dQ for queries row0 .. row0 + 31 over all keys:
+  //   S^T = K Q'^T - lse2 -> P^T;  dP^T = V dO^T - Delta;  dZ^T = P^T * dP^T;  dQ^T += K^T dZ^T
+  if (wave < NW && (uint32_t)row0 < L) {
+    bf16x8 qf[G::NDK], df[G::NDK];
+#pragma unroll
+    for (int st = 0; st < G::NDK; ++st) {
+      qf[st] = *reinterpret_cast<const bf16x8*>(qs + (row0 + l32) * G::P + 16 * st + 8 * g);
+      df[st] = *reinterpret_cast<const bf16x8*>(os + (row0 + l32) * G::P + 16 * st + 8 * g);
+    }
+    floatx16 dqt[G::NT32 > 0 ? G::NT32 : 1];
+    floatx4 dqs[2];
+#pragma unroll
+    for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dqt[t][r] = 0.0f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dqs[h][r] = 0.0f;
+    for (uint32_t k0 = 0; k0 < Lk; k0 += 32) {
+      floatx16 sc, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.0f;
+#pragma unroll
+      for (int st = 0; st < G::NDK; ++st) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(ks + (k0 + l32) * G::P + 16 * st + 8 * g);
+        const bf16x8 va = *reinterpret_cast<const bf16x8*>(vs + (k0 + l32) * G::P + 16 * st + 8 * g);
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], sc, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, df[st], dp, 0, 0, 0);
+      }
+      bf16x8 zb[2];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zb[r / 8][r % 8] = (bf16)(__builtin_amdgcn_exp2f(sc[r]) * dp[r]);
+#pragma unroll
+      for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+          dqt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(ks, G::P, k0 + 16 * kk, 32 * t, lane),
+                                                           zb[kk], dqt[t], 0, 0, 0);
+      if constexpr (G::SLAB) {
+        const bf16x8 a = tr_slab(ks, G::P, k0, 32 * G::NT32, lane);
+        bf16x8 b0, b1;
+        slab_b(zb[0], zb[1], b0, b1);
+        dqs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, dqs[0], 0, 0, 0);
+        dqs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, dqs[1], 0, 0, 0);
+      }
+    }
+    store_rows<D>(p.dq + q_base, p.r_q, row0, L, lane, dqt, dqs, p.scale);
+  }
+
+  // ---- dK, dV for keys row0 .. row0 + 31 over all queries:
+  //   S = Q' K^T - lse2 -> P;  dP = dO V^T - Delta;  dZ = P * dP;  dV^T += dO^T P;  dK^T += Q'^T dZ
+  if (wave >= NW && (uint32_t)row0 < Lk) {
+    bf16x8 kf[G::NDK], vf[G::NDK];
+#pragma unroll
+    for (int st = 0; st < G::NDK; ++st) {
+      kf[st] = *reinterpret_cast<const bf16x8*>(ks + (row0 + l32) * G::P + 16 * st + 8 * g);
+      vf[st] = *reinterpret_cast<const bf16x8*>(vs + (row0 + l32) * G::P + 16 * st + 8 * g);
+    }
+    floatx16 dvt[G::NT32 > 0 ? G::NT32 : 1], dkt[G::NT32 > 0 ? G::NT32 : 1];
+    floatx4 dvs[2], dks[2];
+#pragma unroll
+    for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dvt[t][r] = dkt[t][r] = 0.0f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dvs[h][r] = dks[h][r] = 0.0f;
+    for (uint32_t q0 = 0; q0 < L; q0 += 32) {
+      floatx16 sc, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.0f;
+#pragma unroll
+      for (int st = 0; st < G::NDK; ++st) {
+        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qs + (q0 + l32) * G::P + 16 * st + 8 * g);
+        const bf16x8 da = *reinterpret_cast<const bf16x8*>(os + (q0 + l32) * G::P + 16 * st + 8 * g);
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[st], sc, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[st], dp, 0, 0, 0);
+      }
+      bf16x8 pb[2], zb[2];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pr = __builtin_amdgcn_exp2f(sc[r]);
+        pb[r / 8][r % 8] = (bf16)pr;
+        zb[r / 8][r % 8] = (bf16)(pr * dp[r]);
+      }
+#pragma unroll
+      for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          dvt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(os, G::P, q0 + 16 * kk, 32 * t, lane),
+                                                           pb[kk], dvt[t], 0, 0, 0);
+          dkt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(qs, G::P, q0 + 16 * kk, 32 * t, lane),
+                                                           zb[kk], dkt[t], 0, 0, 0);
+        }
+      if constexpr (G::SLAB) {
+        bf16x8 b0, b1;
+        const bf16x8 ao = tr_slab(os, G::P, q0, 32 * G::NT32, lane);
+        slab_b(pb[0], pb[1], b0, b1);
+        dvs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b0, dvs[0], 0, 0, 0);
+        dvs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b1, dvs[1], 0, 0, 0);
+        const bf16x8 aq = tr_slab(qs, G::P, q0, 32 * G::NT32, lane);
+        slab_b(zb[0], zb[1], b0, b1);
+        dks[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b0, dks[0], 0, 0, 0);
+        dks[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b1, dks[1], 0, 0, 0);
+      }
+    }
+    store_rows<D>(p.dv + kv_base, p.r_kv, row0, Lk, lane, dvt, dvs, 1.0f);
+    store_rows<D>(p.dk + kv_base, p.r_kv, row0, Lk, lane, dkt, dks, kLn2);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // fp32 path: plain FMA loops.  One thread per (unit, row, 32-column slice):
 // the dQ kernel's units are query heads (rows: queries), the dK/dV kernel's
 // key/value heads (rows: keys; it visits every query head of the group).
@@ -678,9 +904,44 @@ int launch_bwd_nw(const AttnBwdArgs& a, hipStream_t s) {
   return last_launch_status();
 }
 
+template <int D, int NW>
+int launch_bwd_short(const AttnBwdArgs& a, hipStream_t s) {
+  BwdParams p;
+  p.q = static_cast<const bf16*>(a.q);
+  p.k = static_cast<const bf16*>(a.k);
+  p.v = static_cast<const bf16*>(a.v);
+  p.o = static_cast<const bf16*>(a.o);
+  p.dout = static_cast<const bf16*>(a.dout);
+  p.dq = static_cast<bf16*>(a.dq);
+  p.dk = static_cast<bf16*>(a.dk);
+  p.dv = static_cast<bf16*>(a.dv);
+  fill_common(p, a);
+  p.X = (uint32_t)a.X;
+  p.H = (uint32_t)a.H;
+  p.L = (uint32_t)a.L;
+  p.Lk = (uint32_t)a.Lk;
+  p.grp = 1;
+  p.c = a.scale * kLog2e;
+  p.scale = a.scale;
+  const int64_t units = a.B * a.X * a.H;
+  if (units == 0) return DSP_OK;
+  p.n_blk = 1;
+  p.n_blocks = (uint32_t)units;
+  hipLaunchKernelGGL((attn_bwd_short_kernel<D, NW>), dim3((uint32_t)units), dim3(NW * 128), 0, s, p);
+  return last_launch_status();
+}
+
 template <int D>
 int launch_bwd_d(const AttnBwdArgs& a, hipStream_t s) {
   const int64_t L = std::max(a.L, a.Lk);
+#if DSP_ATTN_BWD_SHORT
+  // short units with one query head per key/value head: one work-group per unit
+  if (a.H == a.Hkv && L <= 128 && a.L > 0 && a.Lk > 0) {
+    if (L <= 32) return launch_bwd_short<D, 1>(a, s);
+    if (L <= 64) return launch_bwd_short<D, 2>(a, s);
+    return launch_bwd_short<D, 4>(a, s);
+  }
+#endif
   if (L <= 64) return launch_bwd_nw<D, 2>(a, s);
   if (L <= 128) return launch_bwd_nw<D, 4>(a, s);
   return launch_bwd_nw<D, 8>(a, s);
