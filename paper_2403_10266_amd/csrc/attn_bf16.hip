@@ -93,6 +93,17 @@
 #define DSP_ATTN_BIAS_COLUMN 1
 #endif
 
+// Row padding (elements) of the K and V tiles in LDS.
+#ifndef DSP_ATTN_KP_PAD
+#define DSP_ATTN_KP_PAD 8
+#endif
+#ifndef DSP_ATTN_VP_PAD
+#define DSP_ATTN_VP_PAD 16
+#endif
+#ifndef DSP_ATTN_VP_PAD_WIDE
+#define DSP_ATTN_VP_PAD_WIDE 0
+#endif
+
 namespace dsp {
 namespace {
 
@@ -104,8 +115,10 @@ struct Geo {
   static constexpr int NDV = (D + 31) / 32;       // 32-row d tiles of P V
   static constexpr bool ONES = (D % 32) != 0;     // spare V column carries the row sum
   static constexpr bool BIAS = DSP_ATTN_BIAS_COLUMN && (D % 16) == 8;  // spare Q K^T column
-  static constexpr int KP = NDK * 16 + 8;         // K row pitch (elements)
-  static constexpr int VP = NDV * 32 + 16;        // V row pitch (elements)
+  static constexpr int KP = NDK * 16 + DSP_ATTN_KP_PAD;  // K row pitch (elements)
+  // V row pitch (elements): 192 bytes for three or more 32-row d tiles (measured:
+  // half the LDS bank conflicts of 224), else padded by 16
+  static constexpr int VP = NDV * 32 + (NDV >= 3 ? DSP_ATTN_VP_PAD_WIDE : DSP_ATTN_VP_PAD);
   static constexpr int CH = D / 8;                // 16-byte chunks per row
   static constexpr int TILE_ELEMS = KB * (KP + VP);
   static constexpr int NKT = KB / 32;             // 32-key MFMA tiles per LDS tile
