@@ -41,6 +41,10 @@
 #ifndef DSP_ATTN_BWD_SHORT
 #define DSP_ATTN_BWD_SHORT 1
 #endif
+// Row pad (elements) of the backward's LDS tiles.
+#ifndef DSP_ATTN_BWD_PAD
+#define DSP_ATTN_BWD_PAD 24
+#endif
 
 namespace dsp {
 namespace {
@@ -53,7 +57,7 @@ struct BGeo {
   static constexpr int NDK = (D + 2 + 15) / 16;  // 16-wide d steps of the score products
   static constexpr int NT32 = D / 32;            // 32-row tiles of the d-row products
   static constexpr bool SLAB = (D % 32) != 0;    // rows 32 NT32 .. + 15 on 16x16x32
-  static constexpr int P = NDK * 16 + 24;        // LDS row pitch (elements): an odd multiple of 16 B
+  static constexpr int P = NDK * 16 + DSP_ATTN_BWD_PAD;  // LDS row pitch (elements): an odd multiple of 16 B
   static constexpr int CH = D / 8;               // 16-byte chunks of a row
   static constexpr int SB = D / 16;              // d step holding the bias columns D, D + 1
   static constexpr int GB = (D % 16) / 8;        // ... in lanes with g == GB, elements 0 and 1
