@@ -294,10 +294,15 @@ int attn_impl(const void* q, const void* k, const void* v, void* o, int64_t B, i
 }
 
 // pre (GELU/ReLU epilogue, may be null): also receives the pre-activation.
+// rs (optional): the output rows permuted from (B, T, S) to (B, S, T) token order
+// (the switch T -> S in the epilogue); the residual is read in the input's order,
+// so out must not alias it.
 int linear_impl(const void* a, const void* w, const void* bias, const float* residual, void* out,
-                int64_t M, int N, int K, int epilogue, int dtype, hipStream_t s, void* pre = nullptr) {
+                int64_t M, int N, int K, int epilogue, int dtype, hipStream_t s, void* pre = nullptr,
+                RowSwap rs = RowSwap()) {
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
   if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
+  if (rs.outer && (rs.inner == 0 || M % ((int64_t)rs.outer * rs.inner) || residual == out)) return DSP_ERR_ARG;
   if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_RELU) return DSP_ERR_ARG;
   if (!w) return DSP_ERR_NULL;
   if (M == 0) return DSP_OK;
@@ -322,12 +327,12 @@ int linear_impl(const void* a, const void* w, const void* bias, const float* res
     if (epilogue == DSP_EPI_RESID && !aligned(residual, 16)) return DSP_ERR_ALIGN;
     if (pre && !aligned(pre, 16)) return DSP_ERR_ALIGN;
     return launch_linear_bf16(a, w, bias, epilogue == DSP_EPI_RESID ? residual : nullptr, out, M, N,
-                              K, epilogue, s, pre);
+                              K, epilogue, s, pre, rs);
   }
   return launch_linear_f32(static_cast<const float*>(a), static_cast<const float*>(w),
                            static_cast<const float*>(bias),
                            epilogue == DSP_EPI_RESID ? residual : nullptr,
-                           static_cast<float*>(out), M, N, K, epilogue, s, static_cast<float*>(pre));
+                           static_cast<float*>(out), M, N, K, epilogue, s, static_cast<float*>(pre), rs);
 }
 
 // Workspace regions of the block (each 256-byte aligned).
@@ -767,7 +772,9 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
 
   const bool post = (flags & DSP_BLOCK_POST_LN) != 0 && !attn_only;
   const int act = (flags & DSP_BLOCK_RELU) ? DSP_EPI_RELU : DSP_EPI_GELU;
-  const int64_t shp[4] = {B, T, S, C};
+  RowSwap swap;  // (B, T, S) token rows -> (B, S, T)
+  swap.outer = (uint32_t)T;
+  swap.inner = (uint32_t)S;
   // the bf16 (or fp32) operand of a projection: LN of the residual stream, or
   // (post-LN, projection-only chain) the stream itself
   // (fp32 without LN: the stream itself, no copy)
@@ -791,8 +798,8 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
     // y = Wo_t * TemporalAttn(Switch(Wo_s * SpatialAttn(x * Wqkv_s)) * Wqkv_t)
     DSP_TRY(operand(x_BTSC, false));
     DSP_TRY(attn_sublayer(w->wqkv_s, w->bqkv_s, T, S));
-    DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, nullptr, x1, tokens, C, C, DSP_EPI_F32, dtype, s));
-    DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+    // the Switch T -> S folded into the out-projection's epilogue (rows written in (B, S, T) order)
+    DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, nullptr, y_BSTC, tokens, C, C, DSP_EPI_F32, dtype, s, nullptr, swap));
     DSP_TRY(operand(y_BSTC, false));
     DSP_TRY(attn_sublayer(w->wqkv_t, w->bqkv_t, S, T));
     DSP_TRY(linear_impl(o, w->wo_t, w->bo_t, nullptr, y_BSTC, tokens, C, C, DSP_EPI_F32, dtype, s));
@@ -803,9 +810,10 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
     // ---- spatial half on (B, T, S, C): attention over S inside each frame
     DSP_TRY(operand(x_BTSC, true));
     DSP_TRY(attn_sublayer(w->wqkv_s, w->bqkv_s, T, S));
-    DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, x_BTSC, x1, tokens, C, C, DSP_EPI_RESID, dtype, s));
-    // ---- the Switch T -> S on one GPU: (B, T, S, C) -> (B, S, T, C)
-    DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+    // ---- the Switch T -> S on one GPU, (B, T, S, C) -> (B, S, T, C), folded into the
+    // out-projection's epilogue: row (b, t, s) of x + o Wo is written at (b, s, t)
+    DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, x_BTSC, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s, nullptr,
+                        swap));
     // ---- temporal half on (B, S, T, C): attention over T at each location
     DSP_TRY(operand(y_BSTC, true));
     DSP_TRY(attn_sublayer(w->wqkv_t, w->bqkv_t, S, T));
@@ -820,9 +828,9 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
   // stream alternates between x1 and y_BSTC (LN is never run in place).
   DSP_TRY(operand(x_BTSC, false));
   DSP_TRY(attn_sublayer(w->wqkv_s, w->bqkv_s, T, S));
-  DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, x_BTSC, x1, tokens, C, C, DSP_EPI_RESID, dtype, s));
-  // switch first, then LN: LN acts per token, so LN(Switch(v)) = Switch(LN(v))
-  DSP_TRY(switch_impl(x1, y_BSTC, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+  // switch first (in the out-projection's epilogue), then LN: LN acts per token,
+  // so LN(Switch(v)) = Switch(LN(v))
+  DSP_TRY(linear_impl(o, w->wo_s, w->bo_s, x_BTSC, y_BSTC, tokens, C, C, DSP_EPI_RESID, dtype, s, nullptr, swap));
   DSP_TRY(launch_layernorm(y_BSTC, 0, x1, 0, tokens, C, ln_eps, s));           // x1 = r1 (B,S,T,C)
   DSP_TRY(operand(x1, false));
   DSP_TRY(attn_sublayer(w->wqkv_t, w->bqkv_t, S, T));
@@ -908,7 +916,9 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
   const size_t es = elem_size(dtype);
   const int D = C / H;
   const int act = (flags & DSP_BLOCK_RELU) ? DSP_EPI_RELU : DSP_EPI_GELU;
-  const int64_t shp[4] = {B, T, S, C};
+  RowSwap swap;  // (B, T, S) token rows -> (B, S, T)
+  swap.outer = (uint32_t)T;
+  swap.inner = (uint32_t)S;
 #define DSP_TRY(expr)            \
   do {                           \
     st = (expr);                 \
@@ -931,8 +941,8 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
     float* r3 = reinterpret_cast<float*>(base + sv.r3);
     DSP_TRY(launch_cast(x_BTSC, 0, h1, bf, tokens * C, s));
     DSP_TRY(attn_sub(h1, w->wqkv_s, w->bqkv_s, qkv1, a1, lse1, T, S));
-    DSP_TRY(linear_impl(a1, w->wo_s, w->bo_s, x_BTSC, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));
-    DSP_TRY(switch_impl(y1, y0, shp, 4, 1, 2, 1, DSP_F32, 0, s));                 // y0 slot: r1 (B,S,T,C)
+    DSP_TRY(linear_impl(a1, w->wo_s, w->bo_s, x_BTSC, y0, tokens, C, C, DSP_EPI_RESID, dtype, s, nullptr,
+                        swap));                                                  // y0 slot: r1 (B,S,T,C)
     DSP_TRY(launch_layernorm(y0, 0, y_BSTC, 0, tokens, C, ln_eps, s));           // stream y0 = LN(r1)
     DSP_TRY(launch_cast(y_BSTC, 0, h2, bf, tokens * C, s));
     DSP_TRY(attn_sub(h2, w->wqkv_t, w->bqkv_t, qkv2, a2, lse2, S, T));
@@ -951,9 +961,8 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
   // spatial half on (B, T, S, C); y1's slot holds the pre-switch stream x1
   DSP_TRY(launch_layernorm(x_BTSC, 0, h1, bf, tokens, C, ln_eps, s));
   DSP_TRY(attn_sub(h1, w->wqkv_s, w->bqkv_s, qkv1, a1, lse1, T, S));
-  DSP_TRY(linear_impl(a1, w->wo_s, w->bo_s, x_BTSC, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));
-  // the Switch T -> S
-  DSP_TRY(switch_impl(y1, y0, shp, 4, 1, 2, 1, DSP_F32, 0, s));
+  // the Switch T -> S in the out-projection's epilogue: y0 = Switch(x + a1 Wo_s)
+  DSP_TRY(linear_impl(a1, w->wo_s, w->bo_s, x_BTSC, y0, tokens, C, C, DSP_EPI_RESID, dtype, s, nullptr, swap));
   // temporal half on (B, S, T, C)
   DSP_TRY(launch_layernorm(y0, 0, h2, bf, tokens, C, ln_eps, s));
   DSP_TRY(attn_sub(h2, w->wqkv_t, w->bqkv_t, qkv2, a2, lse2, S, T));

@@ -114,12 +114,27 @@ int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16,
 
 int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s);
 
+// Output row of GEMM row m when the rows are (b, t, s) tokens of a (B, T, S)
+// sequence and the output is wanted in (B, S, T) order: the switch T -> S
+// folded into the epilogue (outer = T, inner = S; outer = 0: no swap).
+struct RowSwap {
+  uint32_t outer = 0, inner = 0;
+  __host__ __device__ int64_t map(int m) const {
+    if (outer == 0) return m;
+    const uint32_t per = outer * inner, r = (uint32_t)m % per;
+    return (int64_t)((uint32_t)m - r) + (int64_t)(r % inner) * outer + r / inner;
+  }
+};
+
 // out = epilogue(a W^T + bias) (gemm.hip).  pre (GELU or ReLU epilogue only,
-// else null): also receives the pre-activation, in the output's dtype.
+// else null): also receives the pre-activation, in the output's dtype.  rs:
+// output rows permuted as above (the residual is read in the input's order).
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
-                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre = nullptr);
+                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre = nullptr,
+                       RowSwap rs = RowSwap());
 int launch_linear_f32(const float* a, const float* w, const float* bias, const float* residual,
-                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre = nullptr);
+                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre = nullptr,
+                      RowSwap rs = RowSwap());
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? DSP_OK : DSP_ERR_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }

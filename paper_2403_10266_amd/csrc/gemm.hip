@@ -95,16 +95,20 @@ __device__ __forceinline__ uint2 pack_bf16x4(const float v[4]) {
 // bf16, into `keep_out` at the output's offsets -- what a training forward keeps
 // for the activation's backward.  The activation itself still reads the fp32
 // sum, so `out` has the bits of the plain epilogue.
+// The residual is read at row m, the outputs are written at row om (m itself,
+// or its place after a row swap, see RowSwap).
 template <int EPI, bool KEEP>
-__device__ __forceinline__ void epilogue4(float v[4], int m, int n, int N, const bf16* __restrict__ bias,
-                                          const float* resid, void* out, bf16* keep_out) {
+__device__ __forceinline__ void epilogue4(float v[4], int m, int64_t om, int n, int N,
+                                          const bf16* __restrict__ bias, const float* resid, void* out,
+                                          bf16* keep_out) {
   const bool full = (n + 3 < N) && ((N & 3) == 0);
   if (bias) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       if (n + i < N) v[i] += bf2f(bias[n + i]);
   }
-  const int64_t off = (int64_t)m * N + n;
+  const int64_t roff = (int64_t)m * N + n;
+  const int64_t off = om * N + n;
   if (KEEP) {
     if (full) {
       *reinterpret_cast<uint2*>(keep_out + off) = pack_bf16x4(v);
@@ -125,11 +129,11 @@ __device__ __forceinline__ void epilogue4(float v[4], int m, int n, int N, const
     float* o = static_cast<float*>(out);
     if (EPI == DSP_EPI_RESID) {
       if (full) {
-        const float4 rv = *reinterpret_cast<const float4*>(resid + off);
+        const float4 rv = *reinterpret_cast<const float4*>(resid + roff);
         v[0] += rv.x; v[1] += rv.y; v[2] += rv.z; v[3] += rv.w;
       } else {
         for (int i = 0; i < 4; ++i)
-          if (n + i < N) v[i] += resid[off + i];
+          if (n + i < N) v[i] += resid[roff + i];
       }
     }
     if (full) {
@@ -152,7 +156,8 @@ __device__ __forceinline__ void epilogue4(float v[4], int m, int n, int N, const
 template <int EPI, bool KEEP>
 __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
     const bf16* __restrict__ A, const bf16* __restrict__ W, const bf16* __restrict__ bias,
-    const float* resid, void* out, bf16* keep_out, int M, int N, int K, int n_ntiles, int n_tiles) {
+    const float* resid, void* out, bf16* keep_out, int M, int N, int K, int n_ntiles, int n_tiles,
+    RowSwap rs) {
   __shared__ __attribute__((aligned(16))) bf16 As[BM * PITCH];
   __shared__ __attribute__((aligned(16))) bf16 Ws[BN * PITCH];
 
@@ -253,7 +258,7 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
         float v[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[i] = acc[a][b][4 * r4 + i];
-        epilogue4<EPI, KEEP>(v, m, n, N, bias, resid, out, keep_out);
+        epilogue4<EPI, KEEP>(v, m, rs.map(m), n, N, bias, resid, out, keep_out);
       }
   }
 }
@@ -270,7 +275,8 @@ constexpr int BIG_BM = 256, BIG_GROUP = 8;
 template <int EPI, bool KEEP, int TN>
 __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
     const bf16* __restrict__ A, const bf16* __restrict__ W, const bf16* __restrict__ bias,
-    const float* resid, void* out, bf16* keep_out, int M, int N, int K, int n_ntiles, int n_tiles) {
+    const float* resid, void* out, bf16* keep_out, int M, int N, int K, int n_ntiles, int n_tiles,
+    RowSwap rs) {
   constexpr int TM = 4;
   constexpr int BNB = 2 * TN * 32;
   constexpr int STAGE = (BIG_BM + BNB) * PITCH;
@@ -407,7 +413,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
         float v[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[i] = acc[a][bb][4 * r4 + i];
-        epilogue4<EPI, KEEP>(v, m, n, N, bias, resid, out, keep_out);
+        epilogue4<EPI, KEEP>(v, m, rs.map(m), n, N, bias, resid, out, keep_out);
       }
   }
 }
@@ -421,7 +427,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
                                                         const float* __restrict__ W,
                                                         const float* __restrict__ bias,
                                                         const float* resid, float* out, float* pre,
-                                                        int M, int N, int K) {
+                                                        int M, int N, int K, RowSwap rs) {
   __shared__ float As[FK][FT + 1];
   __shared__ float Bs[FK][FT + 1];
   const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
@@ -470,11 +476,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
       if (n >= N) continue;
       float v = acc[i][j];
       if (bias) v += bias[n];
-      const int64_t off = (int64_t)m * N + n;
+      const int64_t off = rs.map(m) * N + n;
       if ((EPI == DSP_EPI_GELU || EPI == DSP_EPI_RELU) && pre) pre[off] = v;
       if (EPI == DSP_EPI_GELU) v = 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
       if (EPI == DSP_EPI_RELU) v = fmaxf(v, 0.0f);
-      if (EPI == DSP_EPI_RESID) v += resid[off];
+      if (EPI == DSP_EPI_RESID) v += resid[(int64_t)m * N + n];
       out[off] = v;
     }
   }
@@ -483,7 +489,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 }  // namespace
 
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
-                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre) {
+                       void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre, RowSwap rs) {
   if (M == 0) return DSP_OK;
   const int64_t n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN;
   const int64_t tiles = n_mt * n_nt;
@@ -506,13 +512,13 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
   do {                                                                                                        \
     if (!big) {                                                                                               \
       hipLaunchKernelGGL((gemm_bf16_kernel<E, KP>), dim3((uint32_t)tiles), dim3(NTHR), 0, s, A, Wt, bs, residual, \
-                         out, pb, (int)M, N, K, (int)n_nt, (int)tiles);                                        \
+                         out, pb, (int)M, N, K, (int)n_nt, (int)tiles, rs);                                        \
     } else if (big_bn == 256) {                                                                               \
       hipLaunchKernelGGL((gemm_bf16_big_kernel<E, KP, 4>), dim3((uint32_t)big_tiles), dim3(NTHR), 0, s, A, Wt,  \
-                         bs, residual, out, pb, (int)M, N, K, (int)big_nt, (int)big_tiles);                    \
+                         bs, residual, out, pb, (int)M, N, K, (int)big_nt, (int)big_tiles, rs);                    \
     } else {                                                                                                  \
       hipLaunchKernelGGL((gemm_bf16_big_kernel<E, KP, 3>), dim3((uint32_t)big_tiles), dim3(NTHR), 0, s, A, Wt,  \
-                         bs, residual, out, pb, (int)M, N, K, (int)big_nt, (int)big_tiles);                    \
+                         bs, residual, out, pb, (int)M, N, K, (int)big_nt, (int)big_tiles, rs);                    \
     }                                                                                                         \
   } while (0)
   switch (epilogue) {
@@ -533,14 +539,14 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
 }
 
 int launch_linear_f32(const float* a, const float* w, const float* bias, const float* residual,
-                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre) {
+                      float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre, RowSwap rs) {
   if (M == 0) return DSP_OK;
   const int64_t gy = (M + FT - 1) / FT;
   if (gy >= 65536 * 1024) return DSP_ERR_SHAPE;
   if (pre && epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) return DSP_ERR_ARG;
   const dim3 grid((uint32_t)((N + FT - 1) / FT), (uint32_t)gy), block(256);
 #define DSP_GEMM_LAUNCH(E) \
-  hipLaunchKernelGGL(gemm_f32_kernel<E>, grid, block, 0, s, a, w, bias, residual, out, pre, (int)M, N, K)
+  hipLaunchKernelGGL(gemm_f32_kernel<E>, grid, block, 0, s, a, w, bias, residual, out, pre, (int)M, N, K, rs)
   switch (epilogue) {
     case DSP_EPI_NONE: DSP_GEMM_LAUNCH(DSP_EPI_NONE); break;
     case DSP_EPI_GELU: DSP_GEMM_LAUNCH(DSP_EPI_GELU); break;
