@@ -1028,7 +1028,9 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
   const int D = C / H;
   const int act_epi = bf ? DSP_GRAD_EPI_BF16 : DSP_GRAD_EPI_F32;   // gradients fed to bf16 / fp32 operands
   const int act_bwd = (flags & DSP_BLOCK_RELU) ? DSP_GRAD_EPI_RELU_BWD : DSP_GRAD_EPI_GELU_BWD;
-  const int64_t shp_bstc[4] = {B, S, T, C};
+  RowSwap back;  // (B, S, T) token rows -> (B, T, S): the Switch's adjoint
+  back.outer = (uint32_t)S;
+  back.inner = (uint32_t)T;
 #define DSP_TRY(expr)            \
   do {                           \
     st = (expr);                 \
@@ -1058,30 +1060,30 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
     const float* r1 = y0;   // (B, S, T, C)
     const float* r2 = y1;
     const float* dr3 = dy_BSTC;
-    if (!(flags & DSP_BLOCK_NO_MLP_LN)) {
-      DSP_TRY(launch_layernorm_bwd(sb + sv.r3, 0, dy_BSTC, 0, nullptr, dcur, tokens, C, ln_eps, s));
-      dr3 = dcur;
-    }
     // ---- MLP: r3 = y1 + act(y1 W1 + b1) W2 + b2
-    DSP_TRY(operand(dr3));
+    if (!(flags & DSP_BLOCK_NO_MLP_LN)) {
+      DSP_TRY(launch_layernorm_bwd(sb + sv.r3, 0, dy_BSTC, 0, nullptr, dcur, tokens, C, ln_eps, s, RowSwap(),
+                                   dyb, bf));
+      dr3 = dcur;
+    } else {
+      DSP_TRY(operand(dr3));
+    }
     DSP_TRY(dsp_linear_bwd_weight(dyb, g, grads->w2, grads->b2, wg, bw.wg_bytes, tokens, C, F, dtype, stream));
     DSP_TRY(dsp_linear_bwd_data(dyb, w->w2, u, du, tokens, C, F, act_bwd, dtype, stream));
     DSP_TRY(dsp_linear_bwd_weight(du, h3, grads->w1, grads->b1, wg, bw.wg_bytes, tokens, F, C, dtype, stream));
     DSP_TRY(dsp_linear_bwd_data(du, w->w1, nullptr, dh, tokens, F, C, DSP_GRAD_EPI_F32, dtype, stream));
     DSP_TRY(launch_add_f32(dr3, dh, dcur, tokens * C, s));                           // dy1
     // ---- temporal half: r2 = y0 + Attn_T(y0 Wqkv_t) Wo_t, y1 = LN(r2)
-    DSP_TRY(launch_layernorm_bwd(r2, 0, dcur, 0, nullptr, dx1, tokens, C, ln_eps, s));  // dr2
-    DSP_TRY(operand(dx1));
+    DSP_TRY(launch_layernorm_bwd(r2, 0, dcur, 0, nullptr, dx1, tokens, C, ln_eps, s, RowSwap(), dyb, bf));  // dr2
     DSP_TRY(attn_sub_bwd(h2, qkv2, a2, lse2, w->wqkv_t, w->wo_t, grads->wqkv_t, grads->bqkv_t, grads->wo_t,
                          grads->bo_t, S, T));
     DSP_TRY(launch_add_f32(dx1, dh, dcur, tokens * C, s));                           // dy0
     // ---- spatial half: r1 = x + Attn_S(x Wqkv_s) Wo_s, y0 = LN(Switch(r1))
-    DSP_TRY(launch_layernorm_bwd(r1, 0, dcur, 0, nullptr, dx1, tokens, C, ln_eps, s));  // dr1 (B,S,T,C)
-    DSP_TRY(switch_impl(dx1, dcur, shp_bstc, 4, 1, 2, 1, DSP_F32, 0, s));               // dr1 (B,T,S,C)
-    DSP_TRY(operand(dcur));
+    // dr1, written back in (B, T, S, C) order (the Switch's adjoint) with its operand copy
+    DSP_TRY(launch_layernorm_bwd(r1, 0, dcur, 0, nullptr, dx1, tokens, C, ln_eps, s, back, dyb, bf));
     DSP_TRY(attn_sub_bwd(h1, qkv1, a1, lse1, w->wqkv_s, w->wo_s, grads->wqkv_s, grads->bqkv_s, grads->wo_s,
                          grads->bo_s, T, S));
-    DSP_TRY(launch_add_f32(dcur, dh, dx_BTSC, tokens * C, s));
+    DSP_TRY(launch_add_f32(dx1, dh, dx_BTSC, tokens * C, s));
     return DSP_OK;
   }
   // ---- MLP: y = y1 + act(h3 W1 + b1) W2 + b2
@@ -1092,18 +1094,16 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
   DSP_TRY(dsp_linear_bwd_data(du, w->w1, nullptr, dh, tokens, F, C, DSP_GRAD_EPI_F32, dtype, stream));
   if (flags & DSP_BLOCK_NO_MLP_LN) {
     DSP_TRY(launch_add_f32(dy_BSTC, dh, dcur, tokens * C, s));
+    DSP_TRY(operand(dcur));
   } else {
-    DSP_TRY(launch_layernorm_bwd(y1, 0, dh, 0, dy_BSTC, dcur, tokens, C, ln_eps, s));
+    DSP_TRY(launch_layernorm_bwd(y1, 0, dh, 0, dy_BSTC, dcur, tokens, C, ln_eps, s, RowSwap(), dyb, bf));
   }
   // ---- temporal half: y1 = y0 + Attn_T(LN(y0) Wqkv_t) Wo_t
-  DSP_TRY(operand(dcur));
   DSP_TRY(attn_sub_bwd(h2, qkv2, a2, lse2, w->wqkv_t, w->wo_t, grads->wqkv_t, grads->bqkv_t, grads->wo_t,
                        grads->bo_t, S, T));
-  DSP_TRY(launch_layernorm_bwd(y0, 0, dh, 0, dcur, dcur, tokens, C, ln_eps, s));
-  // ---- the Switch's adjoint: (B, S, T, C) -> (B, T, S, C)
-  DSP_TRY(switch_impl(dcur, dx1, shp_bstc, 4, 1, 2, 1, DSP_F32, 0, s));
+  // dy0, written back in (B, T, S, C) order (the Switch's adjoint) with its operand copy
+  DSP_TRY(launch_layernorm_bwd(y0, 0, dh, 0, dcur, dx1, tokens, C, ln_eps, s, back, dyb, bf));
   // ---- spatial half: x1 = x + Attn_S(LN(x) Wqkv_s) Wo_s
-  DSP_TRY(operand(dx1));
   DSP_TRY(attn_sub_bwd(h1, qkv1, a1, lse1, w->wqkv_s, w->wo_s, grads->wqkv_s, grads->bqkv_s, grads->wo_s,
                        grads->bo_s, T, S));
   DSP_TRY(launch_layernorm_bwd(x_BTSC, 0, dh, 0, dx1, dx_BTSC, tokens, C, ln_eps, s));

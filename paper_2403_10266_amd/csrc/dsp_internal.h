@@ -108,9 +108,6 @@ int launch_add_f32(const float* a, const float* b, float* out, int64_t n, hipStr
 int launch_colsum_bf16(const void* dy, float* db, int64_t M, int N, hipStream_t s);
 int launch_colsum_f32(const float* dy, float* db, int64_t M, int N, hipStream_t s);
 
-// dx = dres (if not null) + the LayerNorm backward of dy at x (layernorm.hip).
-int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16, const float* dres, float* dx,
-                         int64_t rows, int C, float eps, hipStream_t s);
 
 int launch_cast(const void* x, int x_bf16, void* y, int y_bf16, int64_t n, hipStream_t s);
 
@@ -125,6 +122,14 @@ struct RowSwap {
     return (int64_t)((uint32_t)m - r) + (int64_t)(r % inner) * outer + r / inner;
   }
 };
+
+// dx = dres (if not null) + the LayerNorm backward of dy at x (layernorm.hip).
+// x, dy and dres are read at row r, dx (and dx2, a second copy in fp32 or
+// bf16, if not null) written at row rs.map(r); with a swap, dres may not
+// alias an output.
+int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16, const float* dres, float* dx,
+                         int64_t rows, int C, float eps, hipStream_t s, RowSwap rs = RowSwap(),
+                         void* dx2 = nullptr, int dx2_bf16 = 0);
 
 // out = epilogue(a W^T + bias) (gemm.hip).  pre (GELU or ReLU epilogue only,
 // else null): also receives the pre-activation, in the output's dtype.  rs:

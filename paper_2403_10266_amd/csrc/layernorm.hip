@@ -96,7 +96,7 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_long_kernel(
 template <int VPL>
 __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_kernel(
     const void* __restrict__ x, int x_bf, const void* __restrict__ dy, int dy_bf, const float* dres,
-    float* dx, int64_t rows, int C, float eps) {
+    float* dx, void* dx2, int dx2_bf, RowSwap rs, int64_t rows, int C, float eps) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (row >= rows) return;
@@ -127,13 +127,15 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_kernel(
     sgy = fmaf(g[i], v[i], sgy);
   }
   const float mg = wave_sum(sg) / (float)C, mgy = wave_sum(sgy) / (float)C;
+  const int64_t obase = rs.outer ? rs.map((int)row) * C : base;
 #pragma unroll
   for (int i = 0; i < VPL; ++i) {
     const int c = lane + 64 * i;
     if (c < C) {
       float d = (g[i] - mg - v[i] * mgy) * rstd;
       if (dres) d += dres[base + c];
-      dx[base + c] = d;
+      dx[obase + c] = d;
+      if (dx2) store_elem(dx2, obase + c, d, dx2_bf);
     }
   }
 }
@@ -141,7 +143,7 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_kernel(
 // Rows longer than the register budget: passes over global memory.
 __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_long_kernel(
     const void* __restrict__ x, int x_bf, const void* __restrict__ dy, int dy_bf, const float* dres,
-    float* dx, int64_t rows, int C, float eps) {
+    float* dx, void* dx2, int dx2_bf, RowSwap rs, int64_t rows, int C, float eps) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (row >= rows) return;
@@ -162,11 +164,13 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_bwd_long_kernel(
     sgy = fmaf(gv, (load_elem(x, base + c, x_bf) - mean) * rstd, sgy);
   }
   const float mg = wave_sum(sg) / (float)C, mgy = wave_sum(sgy) / (float)C;
+  const int64_t obase = rs.outer ? rs.map((int)row) * C : base;
   for (int c = lane; c < C; c += 64) {
     const float yv = (load_elem(x, base + c, x_bf) - mean) * rstd;
     float d = (load_elem(dy, base + c, dy_bf) - mg - yv * mgy) * rstd;
     if (dres) d += dres[base + c];
-    dx[base + c] = d;
+    dx[obase + c] = d;
+    if (dx2) store_elem(dx2, obase + c, d, dx2_bf);
   }
 }
 
@@ -194,22 +198,26 @@ __global__ __launch_bounds__(256) void cast_kernel(const void* __restrict__ x, i
 }  // namespace
 
 int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16, const float* dres, float* dx,
-                         int64_t rows, int C, float eps, hipStream_t s) {
+                         int64_t rows, int C, float eps, hipStream_t s, RowSwap rs, void* dx2, int dx2_bf16) {
   if (rows == 0) return DSP_OK;
+  if (rs.outer && (rs.inner == 0 || rows > INT32_MAX || rows % ((int64_t)rs.outer * rs.inner) ||
+                   (const void*)dres == (const void*)dx || (dx2 && (const void*)dres == dx2)))
+    return DSP_ERR_ARG;
   const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
   if (blocks >= (int64_t(1) << 31)) return DSP_ERR_SHAPE;
   const dim3 grid((uint32_t)blocks), block(64 * kRowsPerBlock);
   const int vpl = (C + 63) / 64;
+#define DSP_LN_BWD_ARGS x, x_bf16, dy, dy_bf16, dres, dx, dx2, dx2_bf16, rs, rows, C, eps
   if (vpl <= 4) {
-    hipLaunchKernelGGL(layernorm_bwd_kernel<4>, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C, eps);
+    hipLaunchKernelGGL(layernorm_bwd_kernel<4>, grid, block, 0, s, DSP_LN_BWD_ARGS);
   } else if (vpl <= 8) {
-    hipLaunchKernelGGL(layernorm_bwd_kernel<8>, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C, eps);
+    hipLaunchKernelGGL(layernorm_bwd_kernel<8>, grid, block, 0, s, DSP_LN_BWD_ARGS);
   } else if (vpl <= 18) {
-    hipLaunchKernelGGL(layernorm_bwd_kernel<18>, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C, eps);
+    hipLaunchKernelGGL(layernorm_bwd_kernel<18>, grid, block, 0, s, DSP_LN_BWD_ARGS);
   } else {
-    hipLaunchKernelGGL(layernorm_bwd_long_kernel, grid, block, 0, s, x, x_bf16, dy, dy_bf16, dres, dx, rows, C,
-                       eps);
+    hipLaunchKernelGGL(layernorm_bwd_long_kernel, grid, block, 0, s, DSP_LN_BWD_ARGS);
   }
+#undef DSP_LN_BWD_ARGS
   return last_launch_status();
 }
 
