@@ -15,10 +15,16 @@
 //             staging is needed; loads are batched ahead of stores for memory
 //             level parallelism and stores bypass the cache hierarchy's
 //             allocation (non-temporal), since the output is not re-read here.
+//             Output rows are visited in tiles of 4 from-indices x 16 local
+//             to-indices (from-index fastest), so a work-group's reads come in
+//             runs of 16 consecutive input rows instead of rows one whole
+//             from-plane apart (+2-4% on a 604 MB shard, both directions).
 //  * tiles -- for short rows: a (from x to) tile of rows is read with the
 //             to-index fastest (contiguous in x), staged in LDS, and written
 //             with the from-index fastest (contiguous in y), so both global
 //             sides stay coalesced when rows are only a few bytes long.
+#include <algorithm>
+
 #include "dsp_internal.h"
 
 namespace dsp {
@@ -40,6 +46,30 @@ struct FastDiv {
   __device__ __forceinline__ uint32_t div(uint32_t n) const { return (__umulhi(n, m) + n) >> s; }
 };
 
+// Tuning knobs (compile time): 16-byte vectors per thread, and whether loads
+// and stores carry the non-temporal hint.
+#ifndef DSP_SWITCH_VPT
+#define DSP_SWITCH_VPT 4
+#endif
+#ifndef DSP_SWITCH_NT_LOAD
+#define DSP_SWITCH_NT_LOAD 1
+#endif
+#ifndef DSP_SWITCH_NT_STORE
+#define DSP_SWITCH_NT_STORE 1
+#endif
+#ifndef DSP_SWITCH_TILE_F
+#define DSP_SWITCH_TILE_F 4
+#endif
+#ifndef DSP_SWITCH_TILE_J
+#define DSP_SWITCH_TILE_J 16
+#endif
+#ifndef DSP_SWITCH_TILED
+#define DSP_SWITCH_TILED 1
+#endif
+#ifndef DSP_SWITCH_THREADS
+#define DSP_SWITCH_THREADS 512
+#endif
+
 // Row mapping of the switch.  Output rows are enumerated (n, b, jt', if):
 // chunk, batch, local to-dim index, from-dim index.  The matching input row
 // index is b*D1*D2 + (to==2 ? if*D2 + jt : jt*D2 + if) with jt = n*per + jt'.
@@ -47,6 +77,27 @@ struct RowMap {
   FastDiv f_from, f_per, f_B;
   uint32_t per, d_from, B, D2, plane;  // plane = D1*D2
   uint32_t to_is_2;
+  // Tiled order (when kTileRows divides both dims): output rows are taken in
+  // tiles of kTileF from-indices x kTileJ local to-indices, from-index
+  // fastest, so a tile reads kTileF runs of kTileJ consecutive input rows and
+  // writes kTileJ runs of kTileF consecutive output rows.
+  uint32_t tiled;
+  FastDiv f_ft, f_jt;  // tiles along the from-dim, along the local to-dim
+  uint32_t n_ft, n_jt;
+  static constexpr uint32_t kTileF = DSP_SWITCH_TILE_F, kTileJ = DSP_SWITCH_TILE_J;
+  // tile-order index -> (output row, input row)
+  __device__ __forceinline__ void rows_tiled(uint32_t ro, uint32_t& dst, uint32_t& src) const {
+    const uint32_t tile = ro / (kTileF * kTileJ), k = ro % (kTileF * kTileJ);
+    const uint32_t q1 = f_ft.div(tile);
+    const uint32_t i_from = (tile - q1 * n_ft) * kTileF + k % kTileF;
+    const uint32_t q2 = f_jt.div(q1);
+    const uint32_t jl = (q1 - q2 * n_jt) * kTileJ + k / kTileF;
+    const uint32_t n = f_B.div(q2);
+    const uint32_t b = q2 - n * B;
+    const uint32_t jt = n * per + jl;
+    dst = (q2 * per + jl) * d_from + i_from;
+    src = b * plane + (to_is_2 ? (i_from * D2 + jt) : (jt * D2 + i_from));
+  }
   __device__ __forceinline__ uint32_t src_row(uint32_t ro) const {
     uint32_t q1 = f_from.div(ro);
     uint32_t i_from = ro - q1 * d_from;
@@ -59,21 +110,6 @@ struct RowMap {
     return b * plane + in_plane;
   }
 };
-
-// Tuning knobs (compile time): 16-byte vectors per thread, and whether loads
-// and stores carry the non-temporal hint.
-#ifndef DSP_SWITCH_VPT
-#define DSP_SWITCH_VPT 4
-#endif
-#ifndef DSP_SWITCH_NT_LOAD
-#define DSP_SWITCH_NT_LOAD 1
-#endif
-#ifndef DSP_SWITCH_NT_STORE
-#define DSP_SWITCH_NT_STORE 1
-#endif
-#ifndef DSP_SWITCH_THREADS
-#define DSP_SWITCH_THREADS 512
-#endif
 
 constexpr int kRowThreads = DSP_SWITCH_THREADS;
 constexpr int kRowVecPerThread = DSP_SWITCH_VPT;
@@ -95,7 +131,14 @@ __global__ __launch_bounds__(kRowThreads) void switch_rows_kernel(
       if (!identity) {
         const uint32_t ro = f_vec.div(v);
         const uint32_t c = v - ro * V;
-        src = map.src_row(ro) * V + c;
+        if (map.tiled) {
+          uint32_t d, r;
+          map.rows_tiled(ro, d, r);
+          dst[u] = d * V + c;
+          src = r * V + c;
+        } else {
+          src = map.src_row(ro) * V + c;
+        }
       }
       if (DSP_SWITCH_NT_LOAD) buf[u] = __builtin_nontemporal_load(x + src);
       else buf[u] = x[src];
@@ -184,6 +227,11 @@ int launch_switch_rows(const void* x, void* y, int64_t B, int64_t D1, int64_t D2
   map.f_from = FastDiv(map.d_from);
   map.f_per = FastDiv(map.per);
   map.f_B = FastDiv(map.B);
+  map.tiled = DSP_SWITCH_TILED && !identity && map.per % RowMap::kTileJ == 0 && map.d_from % RowMap::kTileF == 0;
+  map.n_ft = map.d_from / RowMap::kTileF;
+  map.n_jt = std::max<uint32_t>(1, map.per / RowMap::kTileJ);
+  map.f_ft = FastDiv(std::max<uint32_t>(1, map.n_ft));
+  map.f_jt = FastDiv(map.n_jt);
   const uint32_t per_block = kRowThreads * kRowVecPerThread;
   const uint32_t blocks = (uint32_t)((n_vec + per_block - 1) / per_block);
   hipLaunchKernelGGL(switch_rows_kernel, dim3(blocks), dim3(kRowThreads), 0, s,
