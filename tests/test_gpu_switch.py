@@ -70,6 +70,9 @@ def test_full_size_switch_and_inverse(torch, variant):
     ((2, 6, 5, 16), 2, 1, 3, np.uint16),      # from=2, to=1 (slice only)
     ((2, 3, 4, 24), 1, 1, 1, np.uint16),      # from == to: copy
     ((1, 1, 1, 1152), 1, 2, 1, np.uint16),    # single row
+    ((2, 8, 64, 32), 1, 2, 2, np.uint16),     # row kernel in 4 x 16 tiles, B > 1, 2 chunks
+    ((2, 40, 24, 32), 1, 2, 3, np.uint16),    # local to-extent 8: plain row order
+    ((2, 64, 12, 32), 2, 1, 4, np.uint16),    # from=2, to=1 in tiles
 ])
 def test_small_and_ragged(torch, shape, fd, td, n, dt):
     rng = np.random.default_rng(5)
