@@ -270,7 +270,10 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
 // the current slice, and each 16-wide K step's fragments are read from LDS
 // during the previous step's MFMAs.  The MFMAs and their k order are those of
 // gemm_bf16_kernel, so both kernels give the same bits.
-constexpr int BIG_BM = 256, BIG_GROUP = 8;
+#ifndef DSP_GEMM_BIG_GROUP
+#define DSP_GEMM_BIG_GROUP 4
+#endif
+constexpr int BIG_BM = 256, BIG_GROUP = DSP_GEMM_BIG_GROUP;
 
 template <int EPI, bool KEEP, int TN>
 __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
