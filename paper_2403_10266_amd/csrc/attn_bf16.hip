@@ -21,10 +21,12 @@
 //    the bf16 probabilities actually used.
 //  * The softmax scale and log2(e) are folded into Q once (Q' = Q * scale *
 //    log2 e, rounded to bf16), so the MFMA produces scores in the exp2
-//    domain.  When D leaves a spare column in the Q K^T contraction (D % 16
-//    == 8, e.g. 72), K's padding column D is 1.0 and Q's is -m (the running
-//    reference maximum, as bf16): the MFMA then also subtracts the maximum
-//    and the VALU only evaluates exp2 -- no per-score FMA.
+//    domain.  When D leaves spare columns in the Q K^T contraction (D % 16
+//    == 8, e.g. 72), K's padding columns D and D + 1 are 1.0 and Q's hold
+//    -m as a bf16 pair (-hi, -lo) with m = hi + lo exactly in fp32 (the
+//    running reference maximum, within 2^-17 |m| of the tile maximum it was
+//    taken from): the MFMA then also subtracts the maximum and the VALU only
+//    evaluates exp2 -- no per-score FMA.
 //  * Online softmax with a lazily moved reference maximum: a lane moves it
 //    only when a tile maximum exceeds it by more than 2^8, and O is rescaled
 //    only when some lane of the wave moved; the result does not depend on
@@ -185,19 +187,21 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   const uint32_t L = p.L;     // queries of the unit
   const uint32_t Lk = p.Lk;   // keys and values of the unit
 
-  // ---- padding columns of the LDS buffers.  K: column D is 1.0 when it
-  // carries the bias, the rest 0.  V: column D is 1.0 (row sum), the rest 0.
+  // ---- padding columns of the LDS buffers.  K: columns D and D + 1 are 1.0
+  // when they carry the bias pair, the rest 0.  V: column D is 1.0 (row sum),
+  // the rest 0.
   for (int e = threadIdx.x; e < NBUF * KB; e += NT) {
     bf16* t = lds + (e / KB) * G::TILE_ELEMS;
     const int r = e % KB;
-    for (int c = D; c < G::KP; ++c) t[r * G::KP + c] = (bf16)((G::BIAS && c == D) ? 1.0f : 0.0f);
+    for (int c = D; c < G::KP; ++c) t[r * G::KP + c] = (bf16)((G::BIAS && c <= D + 1) ? 1.0f : 0.0f);
     bf16* vt = t + KB * G::KP;
     for (int c = D; c < G::VP; ++c) vt[r * G::VP + c] = (bf16)((G::ONES && c == D) ? 1.0f : 0.0f);
   }
 
   // ---- Q' = Q * scale * log2(e) as bf16 B fragments: lane (n + 32g) holds
-  // Q'[q][16s + 8g .. +7].  With the bias column, element D of Q' is the
-  // negated reference maximum (0 until the first tile sets it).
+  // Q'[q][16s + 8g .. +7].  With the bias columns, elements D and D + 1 of Q'
+  // are the negated reference maximum as a hi/lo pair (0 until the first tile
+  // sets it).
   const uint32_t q_wave = um.qb * QB + wave * 32 * QT;
   const bf16* qg = p.q + um.in_base;
   bf16x8 qf[QT][G::NDK];
@@ -392,7 +396,16 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
       for (int j = 0; j < QT; ++j) {
         const bool mv = !(mx[j] <= m_ref[j] + kLazyRescale);
         float m_new = mv ? mx[j] : m_ref[j];
-        if (G::BIAS) m_new = -(float)(bf16)(-m_new);  // the applied reference is a bf16 value
+        // the applied reference is the pair hi + lo of bf16 values, exact in
+        // fp32 (8 + 8 significant bits) and within 2^-17 |m| of the maximum, so
+        // the exponentials stay below 2^(8 + 2^-17 |m|): finite up to |m| ~ 2^23,
+        // where fp32 no longer resolves a score to one unit anyway
+        bf16 m_hi = (bf16)0.0f, m_lo = (bf16)0.0f;
+        if (G::BIAS) {
+          m_hi = (bf16)m_new;
+          m_lo = (bf16)(m_new - (float)m_hi);
+          m_new = (float)m_hi + (float)m_lo;
+        }
         const float alpha = m_ref[j] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_ref[j] - m_new);
         const float applied = m_ref[j] == -INFINITY ? 0.0f : m_ref[j];
         m_ref[j] = m_new;
@@ -402,10 +415,14 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[t][j][r] *= alpha;
         if (SLAB) {
+          // the 16x16 slab of half h holds query 16 h + lane % 16 in every
+          // lane, not the lane's own query lane % 32: take that query's factor
 #pragma unroll
-          for (int h = 0; h < 2; ++h)
+          for (int h = 0; h < 2; ++h) {
+            const float alpha_h = __shfl(alpha, 16 * h + (lane & 15));
 #pragma unroll
-            for (int r = 0; r < 4; ++r) os[j][h][r] *= alpha;
+            for (int r = 0; r < 4; ++r) os[j][h][r] *= alpha_h;
+          }
         }
         if (G::BIAS) {
           const float sub = m_new - applied;
@@ -413,7 +430,10 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
           for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) s[kt][j][r] -= sub;
-          if (g == 1) qf[j][BS][0] = (bf16)(-m_new);
+          if (g == 1) {
+            qf[j][BS][0] = (bf16)(-(float)m_hi);
+            qf[j][BS][1] = (bf16)(-(float)m_lo);
+          }
         }
       }
     }

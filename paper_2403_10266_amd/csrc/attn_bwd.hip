@@ -14,12 +14,13 @@
 //    the scores it needs.  Units of at most 128 queries and keys (temporal
 //    attention) run a third kernel that holds the whole unit in LDS and does
 //    both loops, so its rows are read from HBM once.
-//  * The head width is padded to a multiple of 16 with two spare columns.
-//    They carry the per-row statistics into the score products, as a bf16 hi/lo
-//    pair (|x - hi - lo| <= 2^-16 |x|): the query side holds -lse and the
-//    key side 1.0, so the MFMA yields z' - lse directly and P = exp2 of the
-//    accumulator.  In the same way the dO side holds -Delta and the V side 1.0,
-//    so the dP product yields dP - Delta.
+//  * The head width is padded to a multiple of 16 with three spare columns.
+//    They carry the per-row statistics into the score products as three bf16
+//    terms whose sum is the fp32 value exactly (8 significant bits each): the
+//    query side holds -lse and the key side 1.0, so the MFMA yields z' - lse
+//    directly and P = exp2 of the accumulator, at any magnitude of lse.  In
+//    the same way the dO side holds -Delta and the V side 1.0, so the dP
+//    product yields dP - Delta.
 //  * Scores use Q' = Q * scale * log2(e), rounded to bf16 exactly as in the
 //    forward, so P matches the probabilities whose log-sum-exp was saved.
 //  * The d-row products (dQ^T = K^T dZ^T, dV^T = dO^T P, dK^T = Q'^T dZ) take
@@ -54,13 +55,13 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 template <int D>
 struct BGeo {
-  static constexpr int NDK = (D + 2 + 15) / 16;  // 16-wide d steps of the score products
+  static constexpr int NDK = (D + 3 + 15) / 16;  // 16-wide d steps of the score products
   static constexpr int NT32 = D / 32;            // 32-row tiles of the d-row products
   static constexpr bool SLAB = (D % 32) != 0;    // rows 32 NT32 .. + 15 on 16x16x32
   static constexpr int P = NDK * 16 + DSP_ATTN_BWD_PAD;  // LDS row pitch (elements): an odd multiple of 16 B
   static constexpr int CH = D / 8;               // 16-byte chunks of a row
-  static constexpr int SB = D / 16;              // d step holding the bias columns D, D + 1
-  static constexpr int GB = (D % 16) / 8;        // ... in lanes with g == GB, elements 0 and 1
+  static constexpr int SB = D / 16;              // d step holding the bias columns D .. D + 2
+  static constexpr int GB = (D % 16) / 8;        // ... in lanes with g == GB, elements 0 .. 2
   static_assert(D % 8 == 0 && D % 32 <= 16, "head width");
 };
 
@@ -143,6 +144,19 @@ __device__ __forceinline__ void slab_b(const bf16x8& x8, const bf16x8& y8, bf16x
   }
   b0 = __builtin_bit_cast(bf16x8, r0);
   b1 = __builtin_bit_cast(bf16x8, r1);
+}
+
+// -x as three bf16 terms t0 + t1 + t2 == -x exactly for any normal fp32 x:
+// each round to nearest leaves an exact residual of at most 16, then 8,
+// significant bits, and the last term holds the final 8.
+struct Bf16x3 {
+  bf16 t[3];
+};
+__device__ __forceinline__ Bf16x3 neg_split3(float x) {
+  const bf16 hi = (bf16)x;
+  const float r1 = x - (float)hi;
+  const bf16 mid = (bf16)r1;
+  return {{(bf16)(-(float)hi), (bf16)(-(float)mid), (bf16)(-(r1 - (float)mid))}};
 }
 
 // Row fragment (B operand of a score product) of one row of a bf16 tensor:
@@ -231,11 +245,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
   const int64_t o_base = bx_base(p, um.bx, p.b_o, p.x_o) + (int64_t)um.head * D;
   const int64_t kv_base = bx_base(p, um.bx, p.b_kv, p.x_kv) + (int64_t)(um.head / p.grp) * D;
 
-  // padding columns of both buffers: D and D + 1 are 1.0 (they multiply the
+  // padding columns of both buffers: D .. D + 2 are 1.0 (they multiply the
   // bias columns of the query side), the rest 0
   for (int e = threadIdx.x; e < 4 * KB; e += NT) {
     bf16* row = lds + (e / (2 * KB)) * TILE + (e % (2 * KB)) * G::P;
-    for (int c = D; c < G::P; ++c) row[c] = (bf16)(c < D + 2 ? 1.0f : 0.0f);
+    for (int c = D; c < G::P; ++c) row[c] = (bf16)(c < D + 3 ? 1.0f : 0.0f);
   }
 
   // this wave's 32 queries: Q' and dO row fragments with the bias columns,
@@ -258,11 +272,12 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
   const float lse2 = qv ? p.lse[(int64_t)um.unit * L + q] * kLog2e : 0.0f;
   if (qv && g == 0) p.delta[(int64_t)um.unit * L + q] = delta;
   if (g == G::GB) {
-    const bf16 lh = (bf16)lse2, dh = (bf16)delta;
-    qf[G::SB][0] = (bf16)(-(float)lh);
-    qf[G::SB][1] = (bf16)(-(lse2 - (float)lh));
-    df[G::SB][0] = (bf16)(-(float)dh);
-    df[G::SB][1] = (bf16)(-(delta - (float)dh));
+    const Bf16x3 nl = neg_split3(lse2), nd = neg_split3(delta);
+#pragma unroll
+    for (int e = 0; e < 3; ++e) {
+      qf[G::SB][e] = nl.t[e];
+      df[G::SB][e] = nd.t[e];
+    }
   }
 
   // tile fetch: waves [0, NW/2) K, the others V; rows past L read as zero
@@ -395,10 +410,10 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
   const int64_t q_bx = bx_base(p, um.bx, p.b_q, p.x_q), o_bx = bx_base(p, um.bx, p.b_o, p.x_o);
   const uint32_t hq0 = um.head * p.grp;                 // first query head of the group
 
-  // padding columns past the bias pair: 0 (the bias columns are rewritten per tile)
+  // padding columns past the bias terms: 0 (the bias columns are rewritten per tile)
   for (int e = threadIdx.x; e < 4 * QB; e += NT) {
     bf16* row = lds + (e / (2 * QB)) * TILE + (e % (2 * QB)) * G::P;
-    for (int c = D + 2; c < G::P; ++c) row[c] = (bf16)0.0f;
+    for (int c = D + 3; c < G::P; ++c) row[c] = (bf16)0.0f;
   }
 
   // this wave's 32 keys: K and V row fragments, bias columns 1.0
@@ -409,7 +424,8 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
   row_frags<D>(kv ? p.k + kv_base + (int64_t)key * p.r_kv : nullptr, g, kf);
   row_frags<D>(kv ? p.v + kv_base + (int64_t)key * p.r_kv : nullptr, g, vf);
   if (g == G::GB) {
-    kf[G::SB][0] = kf[G::SB][1] = vf[G::SB][0] = vf[G::SB][1] = (bf16)1.0f;
+    kf[G::SB][0] = kf[G::SB][1] = kf[G::SB][2] = (bf16)1.0f;
+    vf[G::SB][0] = vf[G::SB][1] = vf[G::SB][2] = (bf16)1.0f;
   }
 
   // tile fetch: waves [0, NW/2) Q (scaled to Q' when stashed), the others dO;
@@ -458,12 +474,13 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
         }
         *reinterpret_cast<u32x4*>(t + lofs[i]) = v;
       }
-    if (ft < QB) {  // bias pair of row ft: -(lse * log2 e) for Q', -Delta for dO
+    if (ft < QB) {  // bias terms of row ft: -(lse * log2 e) for Q', -Delta for dO
       const float x = fetch_do ? pstat : pstat * kLog2e;
-      const bf16 hi = (bf16)x;
       bf16* row = t + (fetch_do ? QB * G::P : 0) + ft * G::P;
-      row[D] = (bf16)(-(float)hi);
-      row[D + 1] = (bf16)(-(x - (float)hi));
+      const Bf16x3 nx = neg_split3(x);
+      row[D] = nx.t[0];
+      row[D + 1] = nx.t[1];
+      row[D + 2] = nx.t[2];
     }
   };
 
@@ -597,12 +614,12 @@ __global__ __launch_bounds__(NW * 128, 1) void attn_bwd_short_kernel(BwdParams p
       cv[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, okv, 0, 0);
     }
   }
-  // padding columns (the bias pair of Q' and dO is written below)
+  // padding columns (the bias terms of Q' and dO are written below)
   for (int r = threadIdx.x; r < R; r += NT) {
     const bf16 kb = (bf16)((uint32_t)r < Lk ? 1.0f : 0.0f);
-    ks[r * G::P + D] = ks[r * G::P + D + 1] = kb;
-    vs[r * G::P + D] = vs[r * G::P + D + 1] = kb;
-    for (int c = D + 2; c < G::P; ++c)
+    ks[r * G::P + D] = ks[r * G::P + D + 1] = ks[r * G::P + D + 2] = kb;
+    vs[r * G::P + D] = vs[r * G::P + D + 1] = vs[r * G::P + D + 2] = kb;
+    for (int c = D + 3; c < G::P; ++c)
       qs[r * G::P + c] = os[r * G::P + c] = ks[r * G::P + c] = vs[r * G::P + c] = (bf16)0.0f;
   }
 #pragma unroll
@@ -626,7 +643,7 @@ __global__ __launch_bounds__(NW * 128, 1) void attn_bwd_short_kernel(BwdParams p
     }
   }
   __syncthreads();
-  // Delta = rowsum(dO * O) and the bias pairs: -(lse * log2 e) on Q', -Delta on dO
+  // Delta = rowsum(dO * O) and the bias terms: -(lse * log2 e) on Q', -Delta on dO
   for (int r = threadIdx.x; r < R; r += NT) {
     float delta = 0.0f, lse2 = 0.0f;
     if ((uint32_t)r < L) {
@@ -635,11 +652,12 @@ __global__ __launch_bounds__(NW * 128, 1) void attn_bwd_short_kernel(BwdParams p
       lse2 = p.lse[(int64_t)unit * L + r] * kLog2e;
       p.delta[(int64_t)unit * L + r] = delta;
     }
-    const bf16 lh = (bf16)lse2, dh = (bf16)delta;
-    qs[r * G::P + D] = (bf16)(-(float)lh);
-    qs[r * G::P + D + 1] = (bf16)(-(lse2 - (float)lh));
-    os[r * G::P + D] = (bf16)(-(float)dh);
-    os[r * G::P + D + 1] = (bf16)(-(delta - (float)dh));
+    const Bf16x3 nl = neg_split3(lse2), nd = neg_split3(delta);
+#pragma unroll
+    for (int e = 0; e < 3; ++e) {
+      qs[r * G::P + D + e] = nl.t[e];
+      os[r * G::P + D + e] = nd.t[e];
+    }
   }
   __syncthreads();
 

@@ -1,0 +1,257 @@
+"""Attention when the softmax's dynamic range is large, on the GPU against the
+fp64 oracle (Eq. 3: the softmax is invariant to subtracting any per-row
+constant; the kernels subtract a running reference maximum).
+
+Three input families, each built from seeded N(0, 1) tensors (bf16-rounded on
+the host, so the oracle sees exactly the values the kernels see):
+
+* ramp: the keys of the 64-key tile t are shifted by gamma * t along one unit
+  direction u per head.  Queries with q.u > 0 see every later tile's maximum
+  beat the running reference by more than 2^8 (exp2 units), so the tiled
+  kernel's rescale after the first tile runs thousands of times (checked on
+  the host before the launch); queries with q.u < 0 keep the first tile's.
+* offset: every score of a row carries a common term of magnitude
+  2^15 .. 2^17 (exp2 units) while the softmax itself stays soft.  Either
+  column d0 of every key holds a large constant A and the query's column d0
+  holds +-U(0.8, 1.2) ("key column"), or two columns of every query hold
+  large values +-A U(0.8, 1.2) and the keys hold 1.0 there ("query
+  columns").  The row maxima are then far from any bf16 value: a reference
+  rounded to one bf16 value (half an ulp is 128 .. 512 there) lets exp2
+  overflow, whereas the hi + lo pair of the forward and the three-term
+  statistics of the backward are exact.  The backward takes the query-column
+  form: with a key column, dq's component d0 is A times the row sum of dZ,
+  exactly 0, which a bf16 dZ (any bf16 backward rounds dZ before the dZ K
+  product) leaves at A times its rounding residue.
+* hard max: the keys are the queries in permuted order and the scale is 800,
+  as in the oracle's pin "a huge scale gives V at the arg-max" (the own
+  query is the unique best key by a wide margin): every output row is V at
+  the arg-max, bit for bit, with scores near 2^16 .. 2^17.
+
+Tolerances are the standard ones (bf16 2e-2 max-abs / 1e-2 relative L2,
+fp32 1e-5).  The fp32 path sees the ramp and the hard max; at the offset
+magnitudes fp32 itself resolves a score only to ~2^-24 * 2^17, which no fp32
+implementation can bring within 1e-5 of the exact result.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import assert_close, dev, host, say, bits16
+
+pytestmark = pytest.mark.gpu
+
+LOG2E = 1.4426950408889634
+H, D = 2, 72
+C = H * D
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    return torch
+
+
+def _normal(rng, shape, dtype):
+    a = rng.standard_normal(shape, dtype=np.float32)
+    return synth.bf16_round(a) if dtype == "bf16" else a
+
+
+def _round(a, dtype):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return synth.bf16_round(a) if dtype == "bf16" else a
+
+
+def ramp_inputs(L, dtype, seed, gamma=30.0, X=2):
+    rng = np.random.default_rng(seed)
+    q, k, v, do = (_normal(rng, (1, X, L, C), dtype) for _ in range(4))
+    u = rng.standard_normal((H, D)).astype(np.float32)
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    shift = gamma * (np.arange(L) // 64).astype(np.float32)
+    k = _round(k + (shift[:, None] * u.reshape(1, C))[None, None], dtype)
+    return q, k, v, do
+
+
+def offset_inputs(L, dtype, seed, A, d0, X=2):
+    rng = np.random.default_rng(seed)
+    q, k, v, do = (_normal(rng, (1, X, L, C), dtype) for _ in range(4))
+    for h in range(H):
+        sign = np.where(rng.random((1, X, L)) < 0.5, -1.0, 1.0)
+        q[..., h * D + d0] = _round(sign * rng.uniform(0.8, 1.2, (1, X, L)), dtype)
+        k[..., h * D + d0] = _round(np.float32(A), dtype)
+    return q, k, v, do
+
+
+def offset_q_inputs(L, dtype, seed, A, cols=(D - 2, D - 1), X=2):
+    rng = np.random.default_rng(seed)
+    q, k, v, do = (_normal(rng, (1, X, L, C), dtype) for _ in range(4))
+    for h in range(H):
+        sign = np.where(rng.random((1, X, L)) < 0.5, -1.0, 1.0)
+        for c in cols:
+            q[..., h * D + c] = _round(sign * A * rng.uniform(0.8, 1.2, (1, X, L)), dtype)
+            k[..., h * D + c] = 1.0
+    return q, k, v, do
+
+
+def hardmax_inputs(L, dtype, seed, X=2):
+    rng = np.random.default_rng(seed)
+    q, v, do = (_normal(rng, (1, X, L, C), dtype) for _ in range(3))
+    perm = rng.permutation(L)
+    k = np.ascontiguousarray(q[:, :, perm])
+    return q, k, v, do, perm
+
+
+def _scores_exp2(q, k, scale):
+    """Exact scores in exp2 units, [X, H, L, L] (host-side precondition checks)."""
+    qh = q[0].reshape(q.shape[1], q.shape[2], H, D).transpose(0, 2, 1, 3).astype(np.float64)
+    kh = k[0].reshape(k.shape[1], k.shape[2], H, D).transpose(0, 2, 1, 3).astype(np.float64)
+    return np.matmul(qh, np.swapaxes(kh, -1, -2)) * scale * LOG2E
+
+
+def late_moves(q, k, scale, KB=64):
+    """How often a 64-key tile after the first beats the running maximum by more
+    than 2^8 (+1 of slack), over all rows."""
+    s = _scores_exp2(q, k, scale)
+    ref = s[..., :KB].max(-1)
+    n = 0
+    for kb in range(KB, s.shape[-1], KB):
+        mx = s[..., kb:kb + KB].max(-1)
+        mv = mx > ref + 9.0
+        n += int(mv.sum())
+        ref = np.where(mv, mx, ref)
+    return n
+
+
+def _fwd(torch, q, k, v, dtype, scale, layout):
+    import paper_2403_10266_amd as dsp
+    fn = dsp.dsp_spatial_attn if layout == "spatial" else dsp.dsp_temporal_attn
+    o = fn(dev(q, dtype), dev(k, dtype), dev(v, dtype), H, scale=scale)
+    torch.cuda.synchronize()
+    return o
+
+
+# ---------------------------------------------------------------- forward
+
+@pytest.mark.parametrize("dtype,L", [("bf16", 1024), ("bf16", 128), ("f32", 256)])
+def test_ramp_forward(torch, dtype, L):
+    q, k, v, _ = ramp_inputs(L, dtype, seed=700 + L)
+    scale = 1.0 / math.sqrt(D)
+    moves = late_moves(q, k, scale)
+    say(f"ramp forward {dtype} L={L}: {moves} late reference moves in the input")
+    assert moves > (100 if L > 128 else 10)
+    o = _fwd(torch, q, k, v, dtype, 0.0, "spatial" if L > 128 else "temporal")
+    want = oracle.spatial_attention(q, k, v, H)
+    assert_close(host(o), want, dtype, f"ramp L={L}")
+
+
+@pytest.mark.parametrize("L", [1024, 320, 128, 100])
+@pytest.mark.parametrize("form,A,d0", [("key column", 470000.0, D - 1), ("key column", 250000.0, 0),
+                                       ("query columns", 240000.0, None)])
+def test_offset_forward(torch, L, form, A, d0):
+    if form == "key column":
+        q, k, v, _ = offset_inputs(L, "bf16", seed=800 + L, A=A, d0=d0)
+    else:
+        q, k, v, _ = offset_q_inputs(L, "bf16", seed=850 + L, A=A)
+    scale = 1.0 / math.sqrt(D)
+    m = np.abs(_scores_exp2(q, k, scale).max(-1))
+    say(f"offset forward L={L} A={A:g} d0={d0}: |row max| in [{m.min():.0f}, {m.max():.0f}] (exp2 units)")
+    assert m.min() >= 2.0 ** 15
+    o = _fwd(torch, q, k, v, "bf16", 0.0, "spatial" if L > 128 else "temporal")
+    want = oracle.spatial_attention(q, k, v, H)
+    assert_close(host(o), want, "bf16", f"offset L={L} A={A:g} d0={d0}")
+
+
+@pytest.mark.parametrize("dtype,L", [("bf16", 1024), ("bf16", 200), ("bf16", 128), ("bf16", 40),
+                                     ("f32", 256), ("f32", 64)])
+def test_hard_max_forward(torch, dtype, L):
+    q, k, v, _, perm = hardmax_inputs(L, dtype, seed=900 + L)
+    scale = 800.0
+    s = _scores_exp2(q, k, scale)
+    top2 = np.sort(s, axis=-1)[..., -2:]
+    margin = (top2[..., 1] - top2[..., 0]).min()
+    say(f"hard max {dtype} L={L}: row max up to {s.max():.0f}, margin >= {margin:.0f} (exp2 units)")
+    inv = np.argsort(perm)
+    assert (s.argmax(-1) == inv[None, None, :]).all() and margin > 1000
+    o = _fwd(torch, q, k, v, dtype, scale, "spatial" if L > 128 else "temporal")
+    want = oracle.spatial_attention(q, k, v, H, scale=scale)
+    assert_close(host(o), want, dtype, f"hard max L={L}")
+    # V at the arg-max key (key j holds query perm[j]), bit for bit
+    v_at = v[:, :, inv]
+    assert np.array_equal(bits16(o) if dtype == "bf16" else host(o).astype(np.float32).view(np.int32),
+                          bits16(dev(v_at, dtype)) if dtype == "bf16" else v_at.view(np.int32))
+
+
+# ---------------------------------------------------------------- backward
+
+def _assert_grad_scaled(got, want, dtype, what):
+    """Each gradient divided by its largest magnitude in the oracle, then the
+    forward's bar of its dtype (the ramp's shifted keys make dq several times
+    larger than the forward's outputs)."""
+    mx = float(np.abs(want).max())
+    assert_close(got / mx, want / mx, dtype, f"{what} (/max {mx:.3e})")
+
+
+def _bwd(torch, q, k, v, do, dtype, scale):
+    import paper_2403_10266_amd as dsp
+    qd, kd, vd, dd = (dev(a, dtype) for a in (q, k, v, do))
+    o, lse = dsp.dsp_attn_fwd_lse(qd, kd, vd, H, scale=scale)
+    dq, dk, dv = dsp.dsp_attn_bwd(qd, kd, vd, o, dd, lse, H, scale=scale)
+    torch.cuda.synchronize()
+    return o, lse, dq, dk, dv
+
+
+# the tiled forward at L = 256 with a smaller shift: the keys' common shift
+# within a tile cancels in dq = scale dZ K only up to the bf16 rounding of dZ
+@pytest.mark.parametrize("dtype,L,gamma", [("bf16", 256, 12.0), ("bf16", 128, 30.0), ("f32", 256, 30.0)])
+def test_ramp_backward(torch, dtype, L, gamma):
+    q, k, v, do = ramp_inputs(L, dtype, seed=1000 + L, gamma=gamma)
+    assert late_moves(q, k, 1.0 / math.sqrt(D)) > (50 if L > 128 else 10)
+    say(f"ramp backward {dtype} L={L}")
+    o, lse, dq, dk, dv = _bwd(torch, q, k, v, do, dtype, 0.0)
+    want = oracle.attention_bwd_units(q, k, v, do, H)
+    for got, w, name in zip((dq, dk, dv), want, ("dq", "dk", "dv")):
+        _assert_grad_scaled(host(got), w, dtype, f"ramp {name} L={L}")
+
+
+@pytest.mark.parametrize("L", [256, 128])
+def test_offset_backward(torch, L):
+    q, k, v, do = offset_q_inputs(L, "bf16", seed=1100 + L, A=240000.0)
+    m = np.abs(_scores_exp2(q, k, 1.0 / math.sqrt(D)).max(-1))
+    say(f"offset backward L={L}: |row max| in [{m.min():.0f}, {m.max():.0f}] (exp2 units)")
+    assert m.min() >= 2.0 ** 15
+    o, lse, dq, dk, dv = _bwd(torch, q, k, v, do, "bf16", 0.0)
+    want = oracle.attention_bwd_units(q, k, v, do, H)
+    for got, w, name in zip((dq, dk, dv), want, ("dq", "dk", "dv")):
+        _assert_grad_scaled(host(got), w, "bf16", f"offset {name} L={L}")
+    # the row log-sum-exp carries the common term; the query's rounding to
+    # Q * scale * log2(e) in bf16 moves it by up to 2^-9 of its size
+    lse_want = oracle.attention_lse_units(q, k, H)
+    rel = np.abs(host(lse).reshape(lse_want.shape) - lse_want) / np.abs(lse_want)
+    say(f"  lse: max relative error {rel.max():.2e}")
+    assert rel.max() <= 2.0 ** -8
+
+
+@pytest.mark.parametrize("L", [256, 128])
+def test_hard_max_backward(torch, L):
+    """A saturated softmax: dv = P^T dout with P one-hot (the key that holds the
+    row's own query), so dv of key j is dout of that query.  dq and dk are 0
+    in exact arithmetic; on the GPU they are what fp32 rounding leaves of
+    dP - Delta, each a dot product of length D evaluated twice: bounded by
+    scale * max|k or q| * 2 D 2^-24 * sum_d |dout_d v_d| per entry."""
+    q, k, v, do, perm = hardmax_inputs(L, "bf16", seed=1200 + L)
+    scale = 800.0
+    say(f"hard max backward L={L}")
+    o, lse, dq, dk, dv = _bwd(torch, q, k, v, do, "bf16", scale)
+    want = oracle.attention_bwd_units(q, k, v, do, H, scale=scale)
+    _assert_grad_scaled(host(dv), want[2], "bf16", f"hard max dv L={L}")
+    inv = np.argsort(perm)
+    # key j holds query perm[j]: its dv is dout[perm[j]]
+    assert np.allclose(want[2], do[:, :, perm].astype(np.float64), atol=1e-12)
+    dot_abs = np.abs(do.astype(np.float64) * v[:, :, inv].astype(np.float64)).reshape(1, -1, L, H, D).sum(-1)
+    bound = scale * float(np.abs(q).max()) * 2 * D * 2.0 ** -24 * float(dot_abs.max()) * 4
+    for g, name in ((dq, "dq"), (dk, "dk")):
+        got = host(g)
+        say(f"  {name}: max |got| {np.abs(got).max():.3e} (exact 0, bound {bound:.3e})")
+        assert np.isfinite(got).all() and np.abs(got).max() <= bound
