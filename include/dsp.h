@@ -15,7 +15,9 @@
  * Conventions shared by every entry point
  *   - All tensor arguments are DEVICE pointers owned by the caller.  The
  *     library allocates nothing, keeps no pointer after returning and holds no
- *     mutable global state; calls are thread-safe.
+ *     mutable global state; calls are thread-safe.  The one exception is
+ *     dsp_attn_bwd_noalloc, whose scratch is a static per-device array (calls
+ *     that overlap on one GPU race on it).
  *   - Work is enqueued asynchronously on `stream` (a hipStream_t passed as an
  *     opaque pointer; NULL means the default stream).  Device faults surface at
  *     the caller's next synchronisation.
@@ -256,6 +258,28 @@ int dsp_attn_bwd(const void* q, const void* k, const void* v, const void* o, con
                  const float* lse, void* dq, void* dk, void* dv, float* delta, int64_t B, int64_t X,
                  int64_t L, int H, int D, const int64_t* qkv_strides, const int64_t* o_strides,
                  float scale, int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * dsp_attn_bwd_noalloc -- dsp_attn_bwd for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  It takes no `delta` workspace: the Delta rows live in
+ * a library-owned static device array of dsp_attn_bwd_noalloc_max_rows()
+ * fp32 values (4194304 values, 16 MiB), one copy per GPU, loaded with the
+ * library's code and held until the process ends.  The call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine); its first call on a
+ * device looks up that device's copy (hipGetSymbolAddress).
+ * Every call on one GPU uses that GPU's array, and its contents are those of
+ * the last call: calls that overlap on one GPU (several streams or host
+ * threads) race and must be serialised by the caller.  Delta is not returned.
+ * B * X * H * L above the maximum: DSP_ERR_WORKSPACE, nothing launched.
+ * Everything else -- arguments, layouts, dtypes, errors and the bits of dq,
+ * dk, dv -- as dsp_attn_bwd.
+ * ------------------------------------------------------------------------ */
+int64_t dsp_attn_bwd_noalloc_max_rows(void);
+int dsp_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                         const float* lse, void* dq, void* dk, void* dv, int64_t B, int64_t X, int64_t L, int H,
+                         int D, const int64_t* qkv_strides, const int64_t* o_strides, float scale, int dtype,
+                         void* stream);
 
 /* ------------------------------------------------------------------------
  * dsp_attn_general / dsp_attn_general_bwd -- the attention variants the

@@ -70,6 +70,9 @@ _SIGNATURES = {
                               _c.POINTER(_I64), _F, _I, _P]),
     "dsp_attn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _I,
                           _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
+    "dsp_attn_bwd_noalloc_max_rows": (_I64, []),
+    "dsp_attn_bwd_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _I,
+                                  _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
     "dsp_layernorm": (_I, [_P, _I, _P, _I, _I64, _I, _F, _P]),
     "dsp_attn_general": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I, _I, _I, _c.POINTER(_I64),
                               _c.POINTER(_I64), _c.POINTER(_I64), _F, _I, _P]),
@@ -466,6 +469,36 @@ def dsp_attn_bwd(q, k, v, o, dout, lse, H: int, dq=None, dk=None, dv=None, delta
         _check_status(lib().dsp_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
                                          _ptr(dk), _ptr(dv), _ptr(delta), B, X, L, H, C // H, qs, os_,
                                          float(scale), _dtype_code(q), s), w)
+    return dq, dk, dv
+
+
+def attn_bwd_noalloc_max_rows() -> int:
+    """Largest B*X*H*L that dsp_attn_bwd_noalloc accepts."""
+    return int(lib().dsp_attn_bwd_noalloc_max_rows())
+
+
+def dsp_attn_bwd_noalloc(q, k, v, o, dout, lse, H: int, dq, dk, dv, scale: float = 0.0, stream=None):
+    """dsp_attn_bwd for callers that cannot allocate: no Delta workspace (the
+    library keeps Delta in a static per-device array; calls overlapping on one
+    GPU race) and caller-given dq, dk, dv (views with the strides of q)."""
+    torch = _torch()
+    w = "dsp_attn_bwd_noalloc"
+    B, X, L, C = _qkv_views(w, q, k, v, H)
+    _like_view(w, o, q, "o")
+    _like_view(w, dout, q, "dout")
+    if dout.stride() != o.stride():
+        raise ValueError(f"{w}: dout must have the strides of o")
+    _check(w, "lse", lse, dtype=torch.float32, numel=B * X * H * L, like=q)
+    for g, name in ((dq, "dq"), (dk, "dk"), (dv, "dv")):
+        _like_view(w, g, q, name)
+        if tuple(g.stride()) != tuple(q.stride()):
+            raise ValueError(f"{w}: {name} must have the strides of q, k, v")
+    with _on(stream) as s:
+        qs = (ctypes.c_int64 * 3)(*q.stride()[:3])
+        os_ = (ctypes.c_int64 * 3)(*o.stride()[:3])
+        _check_status(lib().dsp_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse),
+                                                 _ptr(dq), _ptr(dk), _ptr(dv), B, X, L, H, C // H, qs, os_,
+                                                 float(scale), _dtype_code(q), s), w)
     return dq, dk, dv
 
 

@@ -5,6 +5,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <utility>
 
 #include "dsp_internal.h"
@@ -430,6 +431,42 @@ bool block_bwd_ws_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, i
   return true;
 }
 
+// ---- dsp_attn_bwd_noalloc: the attention backward with its Delta rows in a
+// library-owned device array instead of a caller workspace.  Each device holds
+// its own copy of `scratch` (loaded with the code object, kept until the
+// process ends); host code must never pass the array's name to a kernel or a
+// copy (in host code it is a host-side stand-in), only the device address
+// hipGetSymbolAddress returns for the device that is current.
+constexpr int64_t kNoallocDeltaRows = int64_t(1) << 22;  // fp32 Delta values: 16 MiB
+__device__ __align__(256) float scratch[kNoallocDeltaRows];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the device the stream belongs to, looked
+// up once per device with that device current; nullptr if HIP fails.
+float* noalloc_scratch(hipStream_t s) {
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return nullptr;
+  int dev = cur;
+  if (s && hipStreamGetDevice(s, &dev) != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) return nullptr;
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (dev != cur && hipSetDevice(cur) != hipSuccess) return nullptr;
+    if (e != hipSuccess || !ptr) {
+      (void)hipGetLastError();  // leave no error behind for the next launch check
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = static_cast<float*>(ptr);
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -584,6 +621,26 @@ int dsp_attn_bwd(const void* q, const void* k, const void* v, const void* o, con
                  float scale, int dtype, void* stream) {
   return attn_bwd_impl(q, k, v, o, dout, lse, dq, dk, dv, delta, B, X, L, H, D, qkv_strides, o_strides,
                        scale, dtype, stream);
+}
+
+int64_t dsp_attn_bwd_noalloc_max_rows(void) { return kNoallocDeltaRows; }
+
+int dsp_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                         const float* lse, void* dq, void* dk, void* dv, int64_t B, int64_t X, int64_t L, int H,
+                         int D, const int64_t* qkv_strides, const int64_t* o_strides, float scale, int dtype,
+                         void* stream) {
+  int64_t rows;
+  if (B < 0 || X < 0 || L < 0 || H < 1 || !mul_ok(B, X, &rows) || !mul_ok(rows, H, &rows) ||
+      !mul_ok(rows, L, &rows))
+    return DSP_ERR_SHAPE;
+  if (rows > kNoallocDeltaRows) return DSP_ERR_WORKSPACE;
+  if (rows == 0)  // nothing to compute: validate without touching the device
+    return attn_bwd_impl(q, k, v, o, dout, lse, dq, dk, dv, nullptr, B, X, L, H, D, qkv_strides, o_strides,
+                         scale, dtype, stream);
+  float* delta = noalloc_scratch(as_stream(stream));
+  if (!delta) return DSP_ERR_HIP;
+  return attn_bwd_impl(q, k, v, o, dout, lse, dq, dk, dv, delta, B, X, L, H, D, qkv_strides, o_strides, scale,
+                       dtype, stream);
 }
 
 int dsp_attn_general(const void* q, const void* k, const void* v, void* o, float* lse, int64_t B, int64_t X,
