@@ -293,8 +293,7 @@ def main():
             ev[s][i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = {name: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(K)]))
-          for i, (name, _) in enumerate(parts)}
+    samples = {name: [ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(K)] for i, (name, _) in enumerate(parts)}
     for name, fn in extras:
         for _ in range(args.warmup):
             fn()
@@ -305,10 +304,33 @@ def main():
             fn()
             xev[s + 1].record(stream)
         torch.cuda.synchronize()
-        ms[name] = float(np.mean([xev[s].elapsed_time(xev[s + 1]) for s in range(K)]))
+        samples[name] = [xev[s].elapsed_time(xev[s + 1]) for s in range(K)]
+    ms = {name: float(np.mean(v)) for name, v in samples.items()}
+    ms_median = {name: float(np.median(v)) for name, v in samples.items()}
+    ms_min = {name: float(np.min(v)) for name, v in samples.items()}
     if args.only:
         print(json.dumps({"only": args.only, "steps": K, "kernel_ms": ms}), flush=True)
         return
+
+    # the practical HBM ceiling of a streaming copy: a device-to-device copy of
+    # the 604 MB switch tensor (torch copy_, one call per event pair)
+    d2d = None
+    if "switch" in wanted:
+        dst = torch.empty_like(t["x_sw"])
+        for _ in range(args.warmup):
+            dst.copy_(t["x_sw"])
+        cev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+        torch.cuda.synchronize()
+        cev[0].record(stream)
+        for s_ in range(K):
+            dst.copy_(t["x_sw"])
+            cev[s_ + 1].record(stream)
+        torch.cuda.synchronize()
+        cs = [cev[i].elapsed_time(cev[i + 1]) for i in range(K)]
+        nb = 2.0 * t["x_sw"].numel() * t["x_sw"].element_size()
+        d2d = {"bytes": int(nb), "GBps_median": round(nb / (np.median(cs) * 1e-3) / 1e9, 1),
+               "GBps_max": round(nb / (np.min(cs) * 1e-3) / 1e9, 1)}
+        del dst
 
     # ---- accounting
     sw_bytes = 2.0 * t["x_sw"].numel() * t["x_sw"].element_size()
@@ -382,6 +404,11 @@ def main():
             "tiny_chain_us": round(ms["tiny_chain"] * 1e3, 2),
             "tiny_chain_graph_us": round(ms["tiny_chain_graph"] * 1e3, 2),
             "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
+            "kernel_ms_median": {k: round(v, 4) for k, v in ms_median.items()},
+            "kernel_ms_min": {k: round(v, 4) for k, v in ms_min.items()},
+            "d2d_copy": d2d,
+            "switch_frac_of_d2d_copy": round(sw_gbps / d2d["GBps_median"], 4) if d2d else None,
+            "clocks": gpu_clocks(),
         },
         "roofline": {
             "kernel": "spatial attention attn_fwd_kernel<72,8,2,64,2,2> (B2 T16 S4096 H16 D72)",
@@ -408,6 +435,19 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def gpu_clocks():
+    """The current shader / memory / fabric clocks as rocm-smi reports them (a
+    child process; None when the tool is not there or fails)."""
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=30)
+        d = json.loads(r.stdout)
+    except Exception:
+        return None
+    card = next(iter(d.values()), {}) if isinstance(d, dict) else {}
+    return {k: v for k, v in card.items() if "clock" in k.lower() or "clk" in k.lower()} or None
+
+
 def measured_traffic(path):
     """HBM bytes per launch of the spatial kernel from the committed counter
     summary, or None when the summary is missing or the kernel source has
@@ -430,56 +470,93 @@ def measured_traffic(path):
     return int(kv["spatial_bytes_per_launch"])
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(budget_s: float) -> dict:
-    """The fp64 oracle on this host's cores, on a bounded sample of the same
-    attention workloads (independent units, so throughput is per-unit exact)."""
+    """The fp64 oracle on this host's cores, on bounded samples of the same
+    workloads (independent units, so throughput is per-unit exact): attention
+    with BLAS threads equal to the CPUs this process may run on (capped by
+    OMP_NUM_THREADS, the host's share per GPU), the same with one thread, and
+    the switch oracle (a uint16 gather) on a slice of the switch shard."""
     import oracle
     import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
+    from threadpoolctl import threadpool_limits
+    affinity = len(os.sched_getaffinity(0))
+    threads = min(affinity, int(os.environ.get("OMP_NUM_THREADS", affinity) or affinity))
     W = synth.WORKLOADS
-    wsp, wtp = W["spatial_bf16_B2_T16_S4096"], W["temporal_bf16_B2_S512_T128"]
-    rng = np.random.default_rng(0)
+    wsp, wtp, wsw = W["spatial_bf16_B2_T16_S4096"], W["temporal_bf16_B2_S512_T128"], W["switch_bf16_T64_S4096"]
     D = wsp.D
 
     def unit_set(w, L, n):
         g = synth.rng(w.seed)
-        q = synth.bf16_round(synth.normal_f32(g, (n, L, D))).astype(np.float64)
-        k = synth.bf16_round(synth.normal_f32(g, (n, L, D))).astype(np.float64)
-        v = synth.bf16_round(synth.normal_f32(g, (n, L, D))).astype(np.float64)
-        return q, k, v
+        return tuple(synth.bf16_round(synth.normal_f32(g, (n, L, D))).astype(np.float64) for _ in range(3))
 
-    # spatial: whole units of L = 4096, as many as fit in half the budget
-    t_sp = f_sp = 0.0
-    n_sp = 0
-    q, k, v = unit_set(wsp, wsp.S, 1)
-    while t_sp < budget_s / 2 and n_sp < 512:
+    def attention_rate(budget, max_sp, max_tp):
+        """(TFLOP/s, spatial units, temporal units, seconds, per-unit spatial times)"""
+        t_sp = f_sp = 0.0
+        n_sp = 0
+        per_unit = []
+        q, k, v = unit_set(wsp, wsp.S, 1)
+        while t_sp < budget / 2 and n_sp < max_sp:
+            t0 = time.perf_counter()
+            oracle.attention(q[0], k[0], v[0])
+            per_unit.append(time.perf_counter() - t0)
+            t_sp += per_unit[-1]
+            f_sp += attn_flops(1, wsp.S, D)
+            n_sp += 1
+        t_tp = f_tp = 0.0
+        n_tp = 0
+        q, k, v = unit_set(wtp, wtp.T, 256)
+        while t_tp < budget / 2 and n_tp < max_tp:
+            t0 = time.perf_counter()
+            oracle.attention(q, k, v)
+            t_tp += time.perf_counter() - t0
+            f_tp += attn_flops(256, wtp.T, D)
+            n_tp += 256
+        return (f_sp + f_tp) / (t_sp + t_tp) / 1e12, n_sp, n_tp, t_sp + t_tp, per_unit
+
+    with threadpool_limits(limits=threads):
+        rate, n_sp, n_tp, secs, per_unit = attention_rate(0.6 * budget_s, 512, 16384)
+    with threadpool_limits(limits=1):
+        rate1, n_sp1, n_tp1, secs1, per_unit1 = attention_rate(0.25 * budget_s, 512, 16384)
+    # the switch oracle on the first 8 of the shard's 64 frames (75.5 MB), T -> S into 8 chunks
+    frames = 8
+    # (the generator's first draws: the same values as those frames of the full shard)
+    xb = synth.f32_to_bf16_bits(synth.activations(wsw, synth.rng(wsw.seed), (wsw.B, frames, wsw.S, wsw.C)))
+    sw_times = []
+    for _ in range(3):
         t0 = time.perf_counter()
-        oracle.attention(q[0], k[0], v[0])
-        t_sp += time.perf_counter() - t0
-        f_sp += attn_flops(1, wsp.S, D)
-        n_sp += 1
-    # temporal: batches of 256 units of L = 128
-    t_tp = f_tp = 0.0
-    n_tp = 0
-    q, k, v = unit_set(wtp, wtp.T, 256)
-    while t_tp < budget_s / 2 and n_tp < 16384:
-        t0 = time.perf_counter()
-        oracle.attention(q, k, v)
-        t_tp += time.perf_counter() - t0
-        f_tp += attn_flops(256, wtp.T, D)
-        n_tp += 256
+        oracle.switch(xb, 1, 2, wsw.n_chunks)
+        sw_times.append(time.perf_counter() - t0)
+    sw_bytes = 2.0 * xb.nbytes
+    del xb
     return {
-        "value": round((f_sp + f_tp) / (t_sp + t_tp) / 1e12, 6),
+        "value": round(rate, 6),
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"fp64 NumPy oracle attention: {n_sp} of 512 spatial units (L=4096, D=72) and "
-                  f"{n_tp} of 16384 temporal units (L=128, D=72), same 4*L^2*D accounting; "
-                  f"{t_sp + t_tp:.1f} s of host time",
+        "sample": f"fp64 NumPy oracle attention, {threads} BLAS threads: {n_sp} of 512 spatial units (L=4096, D=72) "
+                  f"and {n_tp} of 16384 temporal units (L=128, D=72), same 4*L^2*D accounting; {secs:.1f} s of "
+                  f"host time",
+        "cpu_model": cpu_model(),
+        "affinity_cpus": affinity,
+        "one_thread": {"value": round(rate1, 6), "unit": "TFLOP/s",
+                       "sample": f"{n_sp1} spatial and {n_tp1} temporal units, {secs1:.1f} s"},
+        "spatial_unit_s": {"median": round(float(np.median(per_unit)), 4), "min": round(float(np.min(per_unit)), 4),
+                           "one_thread_median": round(float(np.median(per_unit1)), 4)},
+        "switch": {"GBps_median": round(sw_bytes / np.median(sw_times) / 1e9, 3),
+                   "GBps_max": round(sw_bytes / np.min(sw_times) / 1e9, 3),
+                   "sample": f"oracle.switch (uint16 gather, single-threaded NumPy) of frames 0-{frames - 1} of the "
+                             f"1x64x4096x1152 shard, T -> S into 8 chunks, {sw_bytes / 1e6:.0f} MB moved, 3 runs"},
     }
 
 
