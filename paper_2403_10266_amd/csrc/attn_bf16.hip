@@ -27,10 +27,13 @@
 //    running reference maximum, within 2^-17 |m| of the tile maximum it was
 //    taken from): the MFMA then also subtracts the maximum and the VALU only
 //    evaluates exp2 -- no per-score FMA.
-//  * Online softmax with a lazily moved reference maximum: a lane moves it
-//    only when a tile maximum exceeds it by more than 2^8, and O is rescaled
-//    only when some lane of the wave moved; the result does not depend on
-//    the reference point (the row sum uses the same reference).
+//  * Online softmax with a lazily moved reference: the bias subtracted from
+//    the scores is the first tile's maximum plus 64, and the exponentials are
+//    clamped to 1.  A later score above the bias shows as a row sum above
+//    1/2 (probabilities below the bias sum to far less); only then is the
+//    bias moved, O rescaled and the clamped probabilities corrected, after
+//    the tile's P V product.  The result does not depend on the reference
+//    point (the row sum uses the same one).
 //  * K and V tiles of 64 keys are staged in LDS, double-buffered, with the
 //    next tile prefetched into registers during the current tile's math.
 //    Tiles are fetched with buffer loads through a per-tile buffer resource:
@@ -46,6 +49,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "attn_bf16_common.h"
 #include "dsp_internal.h"
@@ -109,7 +113,10 @@
 namespace dsp {
 namespace {
 
-constexpr float kLazyRescale = 8.0f;       // log2 headroom before the reference moves
+// log2 headroom of the bias over the reference maximum: probabilities stay at
+// most 2^-64 of the reference's (still normal in bf16 and fp32) until a score
+// beats the bias, so the reference rarely moves
+constexpr float kLazyRescale = 64.0f;
 
 template <int D, int KB>
 struct Geo {
@@ -296,10 +303,14 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int r = 0; r < 4; ++r) os[j][h][r] = 0.0f;
-  // m_ref: reference maximum currently applied (exp2 domain); -inf before the first tile
-  float m_ref[QT], l_run[QT];
+  // b_ref: the bias subtracted from every score of a query (exp2 domain): the
+  // reference maximum plus kLazyRescale, as the exact sum of the bf16 pair
+  // (b_hi, b_lo) when the Q K^T MFMA applies it.  Probabilities are
+  // exp2(s - b_ref) clamped to 1: at most 2^-kLazyRescale of the reference
+  // maximum's until a score beats the bias.
+  float b_ref[QT], l_run[QT];
 #pragma unroll
-  for (int j = 0; j < QT; ++j) { m_ref[j] = -INFINITY; l_run[j] = 0.0f; }
+  for (int j = 0; j < QT; ++j) { b_ref[j] = 0.0f; l_run[j] = 0.0f; }
 
   const uint32_t n_kb = (Lk + KB - 1) / KB;
   if (SPLIT) {
@@ -310,14 +321,66 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   }
   __syncthreads();
 
-  for (uint32_t it = 0; it < n_kb; ++it) {
-    const uint32_t kb = it * KB;
-    const bool more = NBUF > 1 && it + 1 < n_kb;
-    if (SPLIT && more) fetch(kb + KB);
-    const bf16* k_lds = lds + (NBUF > 1 ? (it & 1) : 0) * G::TILE_ELEMS;
+  // ---- O^T += V^T F^T for bf16 probability fragments F (the P V product, and
+  // the correction of a moved reference)
+  const int j16 = lane & 15;
+  const int mbase = 16 * ((lane >> 4) & 1);
+  auto pv = [&](const bf16* v_lds, const bf16x8 (&f)[NKT][2][QT]) {
+#pragma unroll
+    for (int t = 0; t < NT32; ++t) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int row = 32 * kt + 16 * kk + 4 * g + (j16 >> 2);
+          const int col = 32 * t + mbase + 4 * (j16 & 3);
+          const shortx4 lo = lds_read_tr(v_lds + row * G::VP + col);
+          const shortx4 hi = lds_read_tr(v_lds + (row + 8) * G::VP + col);
+          const shortx8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          const bf16x8 a = __builtin_bit_cast(bf16x8, both);
+#pragma unroll
+          for (int j = 0; j < QT; ++j)
+            o[t][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, f[kt][kk][j], o[t][j], 0, 0, 0);
+        }
+    }
+    if constexpr (SLAB) {
+      // rows d = 32 NT32 .. + 15 over each 32-key tile with 16x16x32 MFMAs.
+      // B operand (keys x 16 queries): lane group c = lane / 16 holds 8 keys
+      // for queries lane % 16.  One permlane16 swap of the two 16-key halves
+      // of a 32x32 probability tile yields it: group c then holds keys
+      // kb(c) + {0..3, 8..11} with kb = {0, 16, 4, 20}, for queries 0-15 of
+      // the tile in the first register and 16-31 in the second.
+      const int c = lane >> 4;
+      const int kbase = ((c & 1) ? 16 : 0) + ((c & 2) ? 4 : 0);
+      const int col = 32 * NT32 + 4 * (j16 & 3);
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        // A operand: lane (d + 16 c) holds V^T[d][keys of group c]
+        const int row = 32 * kt + kbase + (j16 >> 2);
+        const shortx4 lo = lds_read_tr(v_lds + row * G::VP + col);
+        const shortx4 hi = lds_read_tr(v_lds + (row + 8) * G::VP + col);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int j = 0; j < QT; ++j) {
+          u32x4 x = __builtin_bit_cast(u32x4, f[kt][0][j]);
+          u32x4 y = __builtin_bit_cast(u32x4, f[kt][1][j]);
+          u32x4 b0, b1;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
+            b0[w] = r[0];
+            b1[w] = r[1];
+          }
+          os[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, b0), os[j][0], 0, 0, 0);
+          os[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, b1), os[j][1], 0, 0, 0);
+        }
+      }
+    }
+  };
 
-    // ---- S'^T = K Q'^T (exp2-domain scores, minus the reference with BIAS)
-    floatx16 s[NKT][QT];
+  // ---- S'^T = K Q'^T (exp2-domain scores, minus the bias with BIAS) for the
+  // key tile at kb, keys past Lk at -inf
+  auto qk = [&](const bf16* k_lds, uint32_t kb, floatx16 (&s)[NKT][QT]) {
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
@@ -369,76 +432,70 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
           }
         }
     }
+  };
 
-    // ---- online softmax with a lazily moved reference
-    float mx[QT];
-    bool need = false;
+  // the maximum of query j's scores in a tile (the lane's query, both halves)
+  auto tile_max = [&](const floatx16 (&s)[NKT][QT], int j) {
+    float m = s[0][j][0];
 #pragma unroll
-    for (int j = 0; j < QT; ++j) {
-      float m = s[0][j][0];
+    for (int r = 1; r < 16; ++r) m = fmaxf(m, s[0][j][r]);
 #pragma unroll
-      for (int r = 1; r < 16; ++r) m = fmaxf(m, s[0][j][r]);
+    for (int kt = 1; kt < NKT; ++kt)
 #pragma unroll
-      for (int kt = 1; kt < NKT; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[kt][j][r]);
-      m = fmaxf(m, swap_halves(m));
-      // with BIAS the scores are relative to the reference the MFMA applied
-      // (0 before the first tile); mx is the absolute tile maximum
-      const float applied = m_ref[j] == -INFINITY ? 0.0f : m_ref[j];
-      mx[j] = G::BIAS ? m + applied : m;
-      need |= !(mx[j] <= m_ref[j] + kLazyRescale);
+      for (int r = 0; r < 16; ++r) m = fmaxf(m, s[kt][j][r]);
+    return fmaxf(m, swap_halves(m));
+  };
+  // whether this lane holds the running row sum of a query of tile j and it
+  // exceeds thr (the lanes and registers the normalisation reads it from)
+  auto row_sum_over = [&](int j, float thr) -> bool {
+    if constexpr (SLAB) {
+      return lane >= 32 && lane < 48 && (os[j][0][0] > thr || os[j][1][0] > thr);
+    } else if constexpr (G::ONES) {
+      constexpr int tl = D / 32, ml = D % 32;
+      constexpr int gl = (ml / 4) % 2, rl = (ml / 8) * 4 + ml % 4;
+      return g == gl && o[tl][j][rl] > thr;
+    } else {
+      return l_run[j] > thr;
     }
-    if (__any(need)) {
-      // rare path (the first tile, occasionally later): move the references,
-      // rescale O, and re-base this tile's scores on the new reference
+  };
+
+  // One key tile, up to (not including) its barrier.  FIRST: the first tile
+  // sets the reference from its exact maximum (nothing is applied in the MFMA
+  // yet).  Later tiles take their probabilities against the current bias and
+  // return whether, afterwards, some query's row sum shows a clamped
+  // probability (a score at or above the bias): then fix() moves the reference
+  // before the tile's barrier.  The fix runs outside the loop of ordinary
+  // tiles, so its code does not weigh on that loop.
+  auto tile = [&](uint32_t it, auto first_c) -> bool {
+    constexpr bool FIRST = decltype(first_c)::value;
+    const uint32_t kb = it * KB;
+    const bool more = NBUF > 1 && it + 1 < n_kb;
+    if (SPLIT && more) fetch(kb + KB);
+    const bf16* k_lds = lds + (NBUF > 1 ? (it & 1) : 0) * G::TILE_ELEMS;
+
+    // ---- S'^T = K Q'^T (exp2-domain scores, minus the bias with BIAS)
+    floatx16 s[NKT][QT];
+    qk(k_lds, kb, s);
+
+    if constexpr (FIRST) {
+      // the bias: the exact maximum plus the headroom, as a bf16 pair whose sum
+      // (exact in fp32, within 2^-17 of its size) is what the MFMA subtracts
 #pragma unroll
       for (int j = 0; j < QT; ++j) {
-        const bool mv = !(mx[j] <= m_ref[j] + kLazyRescale);
-        float m_new = mv ? mx[j] : m_ref[j];
-        // the applied reference is the pair hi + lo of bf16 values, exact in
-        // fp32 (8 + 8 significant bits) and within 2^-17 |m| of the maximum, so
-        // the exponentials stay below 2^(8 + 2^-17 |m|): finite up to |m| ~ 2^23,
-        // where fp32 no longer resolves a score to one unit anyway
-        bf16 m_hi = (bf16)0.0f, m_lo = (bf16)0.0f;
-        if (G::BIAS) {
-          m_hi = (bf16)m_new;
-          m_lo = (bf16)(m_new - (float)m_hi);
-          m_new = (float)m_hi + (float)m_lo;
-        }
-        const float alpha = m_ref[j] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_ref[j] - m_new);
-        const float applied = m_ref[j] == -INFINITY ? 0.0f : m_ref[j];
-        m_ref[j] = m_new;
-        l_run[j] *= alpha;
-#pragma unroll
-        for (int t = 0; t < NT32; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[t][j][r] *= alpha;
-        if (SLAB) {
-          // the 16x16 slab of half h holds query 16 h + lane % 16 in every
-          // lane, not the lane's own query lane % 32: take that query's factor
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const float alpha_h = __shfl(alpha, 16 * h + (lane & 15));
-#pragma unroll
-            for (int r = 0; r < 4; ++r) os[j][h][r] *= alpha_h;
-          }
-        }
-        if (G::BIAS) {
-          const float sub = m_new - applied;
-#pragma unroll
-          for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) s[kt][j][r] -= sub;
-          if (g == 1) {
-            qf[j][BS][0] = (bf16)(-(float)m_hi);
-            qf[j][BS][1] = (bf16)(-(float)m_lo);
-          }
+        const float bt = tile_max(s, j) + kLazyRescale;
+        const bf16 hi = (bf16)bt;
+        const bf16 lo = (bf16)(bt - (float)hi);
+        b_ref[j] = (float)hi + (float)lo;
+        if (G::BIAS && g == 1) {
+          qf[j][BS][0] = (bf16)(-(float)hi);
+          qf[j][BS][1] = (bf16)(-(float)lo);
         }
       }
     }
-    // probabilities as bf16 B fragments (with BIAS the scores are already
-    // relative to the reference; otherwise subtract it here)
+
+    // ---- probabilities exp2(s - bias) clamped to 1 (the clamp only acts when
+    // a score reached the bias; fix() then restores it), as bf16 B fragments
+    // of the P V product
     bf16x8 pf[NKT][2][QT];
 #pragma unroll
     for (int j = 0; j < QT; ++j) {
@@ -447,69 +504,16 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = G::BIAS ? __builtin_amdgcn_exp2f(s[kt][j][r])
-                                  : __builtin_amdgcn_exp2f(s[kt][j][r] - m_ref[j]);
+          const float x = (FIRST || !G::BIAS) ? s[kt][j][r] - b_ref[j] : s[kt][j][r];
+          const float e = __builtin_amdgcn_fmed3f(__builtin_amdgcn_exp2f(x), 0.0f, 1.0f);
           if (!G::ONES) ls += e;
           pf[kt][r / 8][j][r % 8] = (bf16)e;
         }
       if (!G::ONES) l_run[j] += ls;
     }
 
-    // ---- O^T += V^T P^T, V fragments read transposed from row-major LDS
-    const bf16* v_lds = k_lds + KB * G::KP;
-    const int j16 = lane & 15;
-    const int mbase = 16 * ((lane >> 4) & 1);
-#pragma unroll
-    for (int t = 0; t < NT32; ++t) {
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          const int row = 32 * kt + 16 * kk + 4 * g + (j16 >> 2);
-          const int col = 32 * t + mbase + 4 * (j16 & 3);
-          const shortx4 lo = lds_read_tr(v_lds + row * G::VP + col);
-          const shortx4 hi = lds_read_tr(v_lds + (row + 8) * G::VP + col);
-          const shortx8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          const bf16x8 a = __builtin_bit_cast(bf16x8, both);
-#pragma unroll
-          for (int j = 0; j < QT; ++j)
-            o[t][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[kt][kk][j], o[t][j], 0, 0, 0);
-        }
-    }
-    if constexpr (SLAB) {
-      // rows d = 32 NT32 .. + 15 over each 32-key tile with 16x16x32 MFMAs.
-      // B operand (keys x 16 queries): lane group c = lane / 16 holds 8 keys
-      // for queries lane % 16.  One permlane16 swap of the two 16-key halves
-      // of a 32x32 probability tile yields it: group c then holds keys
-      // kb(c) + {0..3, 8..11} with kb = {0, 16, 4, 20}, for queries 0-15 of
-      // the tile in the first register and 16-31 in the second.
-      const int c = lane >> 4;
-      const int kbase = ((c & 1) ? 16 : 0) + ((c & 2) ? 4 : 0);
-      const int col = 32 * NT32 + 4 * (j16 & 3);
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt) {
-        // A operand: lane (d + 16 c) holds V^T[d][keys of group c]
-        const int row = 32 * kt + kbase + (j16 >> 2);
-        const shortx4 lo = lds_read_tr(v_lds + row * G::VP + col);
-        const shortx4 hi = lds_read_tr(v_lds + (row + 8) * G::VP + col);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-        for (int j = 0; j < QT; ++j) {
-          u32x4 x = __builtin_bit_cast(u32x4, pf[kt][0][j]);
-          u32x4 y = __builtin_bit_cast(u32x4, pf[kt][1][j]);
-          u32x4 b0, b1;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
-            b0[w] = r[0];
-            b1[w] = r[1];
-          }
-          os[j][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, b0), os[j][0], 0, 0, 0);
-          os[j][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, b1), os[j][1], 0, 0, 0);
-        }
-      }
-    }
-
+    // the next tile's prefetched rows into the other LDS buffer (no wave reads
+    // it during this tile), so the registers are free for the rest of it
     if (more) {
       if (SPLIT) {
         stash((it + 1) & 1);
@@ -517,7 +521,101 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
         fetch_single(kb + KB, (it + 1) & 1);
       }
     }
+
+    // ---- O^T += V^T P^T, V fragments read transposed from row-major LDS
+    pv(k_lds + KB * G::KP, pf);
+
+    // a clamped probability puts its query's row sum at 1 or more, while
+    // probabilities below the bias sum to far less than 1/2 (each is under
+    // 2^-kLazyRescale of the reference maximum's, unless scores crept up to
+    // within ~kLazyRescale of the bias: then the reference moves early, which
+    // is harmless)
+    bool need = false;
+    if constexpr (!FIRST) {
+#pragma unroll
+      for (int j = 0; j < QT; ++j) need |= row_sum_over(j, 0.5f);
+    }
+    return __any(need);
+  };
+
+  // The rare move of the reference in tile it, after its P V product: the
+  // scores again (against the bias still in place), the tile maximum; for
+  // each query with a score above its bias, the bias becomes that maximum
+  // plus the headroom (d higher), O and the row sum are rescaled by 2^-d, and
+  // every key gets, in a second P V pass, the difference between its exact
+  // probability against the new bias and the clamped one already summed:
+  // exp2(x - d) - exp2(min(x, 0) - d), x the score minus the old bias (0 for
+  // keys below the old bias and for queries that keep theirs).
+  auto fix = [&](uint32_t it) {
+    const uint32_t kb = it * KB;
+    const bf16* k_lds = lds + (NBUF > 1 ? (it & 1) : 0) * G::TILE_ELEMS;
+    floatx16 s[NKT][QT];
+    qk(k_lds, kb, s);
+    bf16x8 pf[NKT][2][QT];
+#pragma unroll
+    for (int j = 0; j < QT; ++j) {
+      const float mrel = G::BIAS ? tile_max(s, j) : tile_max(s, j) - b_ref[j];
+      const bool mv = mrel > 0.0f;
+      float d = 0.0f;
+      if (mv) {
+        const float bt = b_ref[j] + mrel + kLazyRescale;
+        const bf16 hi = (bf16)bt;
+        const bf16 lo = (bf16)(bt - (float)hi);
+        const float bn = (float)hi + (float)lo;
+        d = bn - b_ref[j];
+        b_ref[j] = bn;
+        if (G::BIAS && g == 1) {
+          qf[j][BS][0] = (bf16)(-(float)hi);
+          qf[j][BS][1] = (bf16)(-(float)lo);
+        }
+      }
+      const float alpha = __builtin_amdgcn_exp2f(-d);
+      l_run[j] *= alpha;
+#pragma unroll
+      for (int t = 0; t < NT32; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][j][r] *= alpha;
+      if (SLAB) {
+        // the 16x16 slab of half h holds query 16 h + lane % 16 in every
+        // lane, not the lane's own query lane % 32: take that query's factor
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const float alpha_h = __shfl(alpha, 16 * h + (lane & 15));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) os[j][h][r] *= alpha_h;
+        }
+      }
+      float ls = 0.0f;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float x = G::BIAS ? s[kt][j][r] : s[kt][j][r] - (b_ref[j] - d);
+          const float cx = __builtin_amdgcn_exp2f(x - d) - __builtin_amdgcn_exp2f(fminf(x, 0.0f) - d);
+          if (!G::ONES) ls += cx;
+          pf[kt][r / 8][j][r % 8] = (bf16)cx;
+        }
+      if (!G::ONES) l_run[j] += ls;
+    }
+    pv(k_lds + KB * G::KP, pf);
+  };
+
+  tile(0, std::true_type{});
+  __syncthreads();
+  uint32_t it = 1;
+  while (it < n_kb) {
+    bool moved = false;
+    for (; it < n_kb; ++it) {
+      if (tile(it, std::false_type{})) {
+        moved = true;
+        break;
+      }
+      __syncthreads();
+    }
+    if (!moved) break;
+    fix(it);
     __syncthreads();
+    ++it;
   }
 
   // ---- normalise and store: lane (n + 32g) holds O^T[32t + 8(r/4) + 4g + r%4][q]
@@ -543,10 +641,10 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
     }
     const float inv = 1.0f / l;
     if (p.lse && g == 0) {
-      // natural-log row log-sum-exp: the scores were exp2(s' - m_ref) with s'
-      // the log2-domain score, summing to l
+      // natural-log row log-sum-exp: the probabilities were exp2(s' - b_ref)
+      // with s' the log2-domain score, summing to l
       const uint32_t q = q_wave + 32 * j + l32;
-      if (q < L) p.lse[(int64_t)um.unit * L + q] = 0.6931471805599453f * (m_ref[j] + log2f(l));
+      if (q < L) p.lse[(int64_t)um.unit * L + q] = 0.6931471805599453f * (b_ref[j] + log2f(l));
     }
     if constexpr (SLAB) {
       // slab rows d < D: lanes 0-31 hold d = 32 NT32 + 4 (lane / 16) + r for

@@ -266,9 +266,10 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
 // Large-tile variant for problems with many tiles: 256 x (64 TN) output tile,
 // 4 waves of 128 x (32 TN), one work-group per CU (one wave per SIMD) with the
 // accumulators in AGPRs.  Two LDS buffers, so one barrier per 64-wide K slice;
-// the next slice's global loads and LDS stores are spread between the MFMAs of
-// the current slice, and each 16-wide K step's fragments are read from LDS
-// during the previous step's MFMAs.  The MFMAs and their k order are those of
+// the next slice's LDS stores, each followed by the global load that refills
+// its register, are spread between the MFMAs of the current slice's first
+// step, and each 16-wide K step's fragments are read from LDS during the
+// previous step's MFMAs.  The MFMAs and their k order are those of
 // gemm_bf16_kernel, so both kernels give the same bits.
 #ifndef DSP_GEMM_BIG_GROUP
 #define DSP_GEMM_BIG_GROUP 4
@@ -351,8 +352,9 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
   };
 
   // One K slice from LDS buffer kt & 1.  ST: store the prefetched slice kt + 1
-  // into the other buffer (during step 0); LD: load slice kt + 2 from global
-  // memory into the prefetch registers (during step 1).
+  // into the other buffer; LD: reload each prefetch register with its part of
+  // slice kt + 2 right after its store (both spread over the MFMAs of step 0),
+  // which gives the loads a whole slice of MFMAs before their store.
   auto slice = [&](int kt, auto st_c, auto ld_c) {
     constexpr bool ST = decltype(st_c)::value, LD = decltype(ld_c)::value;
     constexpr int NMF = TM * TN;
@@ -368,11 +370,10 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
         acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][a], af[cur][bb], acc[a][bb], 0, 0, 0);
         if (ks == 0 && ST) {
 #pragma unroll
-          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) lstore(i, b ^ 1);
-        }
-        if (ks == 1 && LD) {
-#pragma unroll
-          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) gload(i, (kt + 2) * BK);
+          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) {
+            lstore(i, b ^ 1);
+            if (LD) gload(i, (kt + 2) * BK);
+          }
         }
         __builtin_amdgcn_sched_barrier(0);
       }
