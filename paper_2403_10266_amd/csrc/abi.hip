@@ -853,6 +853,21 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
   };
   if (attn_only) {
     // y = Wo_t * TemporalAttn(Switch(Wo_s * SpatialAttn(x * Wqkv_s)) * Wqkv_t)
+    if (!bf && chain_sublayer_f32_fits(S, C, H) && chain_sublayer_f32_fits(T, C, H) && aligned(x_BTSC, 16) &&
+        aligned(y_BSTC, 16) && aligned(w->wqkv_s, 16) && aligned(w->wo_s, 16) && aligned(w->wqkv_t, 16) &&
+        aligned(w->wo_t, 16)) {
+      // small fp32 shapes: each sublayer in one kernel (one work-group per frame,
+      // then per location); the spatial one writes its rows in (B, S, T) order
+      const float scl = (float)(1.0 / sqrt((double)D));
+      DSP_TRY(launch_chain_sublayer_f32(x_BTSC, static_cast<const float*>(w->wqkv_s),
+                                        static_cast<const float*>(w->bqkv_s), static_cast<const float*>(w->wo_s),
+                                        static_cast<const float*>(w->bo_s), y_BSTC, B * T, (int)S, C, H, scl, swap, s));
+      DSP_TRY(launch_chain_sublayer_f32(y_BSTC, static_cast<const float*>(w->wqkv_t),
+                                        static_cast<const float*>(w->bqkv_t), static_cast<const float*>(w->wo_t),
+                                        static_cast<const float*>(w->bo_t), y_BSTC, B * S, (int)T, C, H, scl,
+                                        RowSwap(), s));
+      return DSP_OK;
+    }
     DSP_TRY(operand(x_BTSC, false));
     DSP_TRY(attn_sublayer(w->wqkv_s, w->bqkv_s, T, S));
     // the Switch T -> S folded into the out-projection's epilogue (rows written in (B, S, T) order)

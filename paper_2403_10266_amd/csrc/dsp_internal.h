@@ -141,6 +141,15 @@ int launch_linear_f32(const float* a, const float* w, const float* bias, const f
                       float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre = nullptr,
                       RowSwap rs = RowSwap());
 
+// One attention sublayer of the fp32 projection-only chain in one kernel
+// (chain_f32.hip), for groups of L <= 64 rows and C <= 64:
+//   y[rs.map(g L + r)] = (Attn(x[g L + r] Wqkv^T + bqkv)) Wo^T + bo
+// per group g (the heads' softmax attention over the group's rows); y may
+// alias x.  fits() tells whether the shape is in range.
+bool chain_sublayer_f32_fits(int64_t L, int C, int H);
+int launch_chain_sublayer_f32(const float* x, const float* wqkv, const float* bqkv, const float* wo, const float* bo,
+                              float* y, int64_t groups, int L, int C, int H, float scale, RowSwap rs, hipStream_t s);
+
 inline int hip_status(hipError_t e) { return e == hipSuccess ? DSP_OK : DSP_ERR_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }
 

@@ -32,6 +32,44 @@ def test_tiny_chain_fp32(torch):
     assert_close(host(y), want, "f32", "tiny chain")
 
 
+@pytest.mark.parametrize("B,T,S,C,H,bias", [
+    (1, 4, 16, 64, 4, False),    # the tiny configuration (one kernel per sublayer)
+    (2, 3, 20, 32, 2, True),     # biases, B > 1
+    (1, 7, 5, 48, 3, True),      # C not a divisor of the work-group: partial row bands
+    (1, 64, 64, 64, 8, True),    # the largest one-kernel shape
+    (1, 2, 70, 64, 4, True),     # S > 64: the general path (GEMM and attention launches)
+    (1, 3, 8, 96, 4, True),      # C > 64: the general path
+])
+def test_projection_chain_fp32(torch, B, T, S, C, H, bias):
+    """The projection-only chain (DSP_BLOCK_ATTN_ONLY) in fp32 against the
+    oracle's pieces: Wqkv_s, spatial attention, Wo_s, the switch, Wqkv_t,
+    temporal attention, Wo_t, each linear map with its bias when given."""
+    import paper_2403_10266_amd as dsp
+    rng = np.random.default_rng(B * 1000 + T * 100 + S + C)
+    x = rng.standard_normal((B, T, S, C), dtype=np.float32)
+    p = {"wqkv_s": 0.05 * rng.standard_normal((3 * C, C), dtype=np.float32),
+         "wo_s": 0.05 * rng.standard_normal((C, C), dtype=np.float32),
+         "wqkv_t": 0.05 * rng.standard_normal((3 * C, C), dtype=np.float32),
+         "wo_t": 0.05 * rng.standard_normal((C, C), dtype=np.float32)}
+    if bias:
+        for n, k in (("bqkv_s", 3 * C), ("bo_s", C), ("bqkv_t", 3 * C), ("bo_t", C)):
+            p[n] = 0.1 * rng.standard_normal(k, dtype=np.float32)
+    p = {n: v.astype(np.float32) for n, v in p.items()}
+    say(f"projection chain fp32 B={B} T={T} S={S} C={C} H={H} bias={bias}")
+    y = dsp.dsp_st_block_forward(dev(x, "f32"), {n: dev(v, "f32") for n, v in p.items()}, H,
+                                 flags=dsp.DSP_BLOCK_ATTN_ONLY)
+    torch.cuda.synchronize()
+
+    def sub(h, tag, attn):
+        qkv = oracle.linear(h, p["wqkv_" + tag].T, p.get("bqkv_" + tag))
+        o = attn(qkv[..., :C], qkv[..., C:2 * C], qkv[..., 2 * C:], H)
+        return oracle.linear(o, p["wo_" + tag].T, p.get("bo_" + tag))
+
+    ys = sub(x.astype(np.float64), "s", oracle.spatial_attention)
+    want = sub(np.ascontiguousarray(ys.transpose(0, 2, 1, 3)), "t", oracle.temporal_attention)
+    assert_close(host(y), want, "f32", "projection chain")
+
+
 def _block_case(torch, w, with_bias, flags=0):
     import paper_2403_10266_amd as dsp
     x, p = synth.block_inputs(w, with_bias=with_bias)

@@ -169,3 +169,39 @@ def test_block_backward_homogeneous_full_size(torch):
     for n in g1:
         assert torch.equal(g2[n], g1[n] * 2.0), n
 
+
+
+def test_block_backward_full_size_sampled_against_oracle(torch):
+    """The bench workload (B1 T32 S1024, C 1152, 16 heads, MLP 4608, the
+    split-K weight-gradient counts chosen at 32768 tokens) against the fp64
+    oracle's chain rule: 8 whole rows of dx and 128 entries of every weight
+    gradient, stored by tests/golden/make_block_bwd_samples.py (oracle only).
+    Errors are taken relative to each tensor's largest magnitude, as in the
+    smaller cases above."""
+    import json
+    from pathlib import Path
+    import paper_2403_10266_amd as dsp
+    gold = json.loads((Path(__file__).parent / "golden" / "block_bwd_B1_T32_S1024_samples.json").read_text())
+    w = synth.WORKLOADS["block_bf16_B1_T32_S1024"]
+    x, p = synth.block_inputs(w)
+    dy = np.random.default_rng(w.seed + 1).standard_normal((w.B, w.S, w.T, w.C), dtype=np.float32)
+    say(f"block backward sampled {w.name}")
+    wd = {n: (None if v is None else dev(v, "bf16")) for n, v in p.items()}
+    xd = dev(x, "f32")
+    _, saved = dsp.dsp_st_block_forward_train(xd, wd, w.H)
+    dx, g = dsp.dsp_st_block_backward(xd, dev(dy, "f32"), wd, saved, w.H)
+    torch.cuda.synchronize()
+    dxh = host(dx)
+    # dx is returned in the input's (B, T, S, C) order
+    got = np.stack([dxh[b, t, s] for b, t, s in gold["dx_rows"]])
+    mx = gold["dx_max_abs"]
+    a, r = errors(got / mx, np.asarray(gold["dx"]) / mx)
+    say(f"  dx rows: max_abs/max={a:.2e} rel_l2={r:.2e}")
+    assert a <= 2e-2 and r <= 1e-2, "dx"
+    for n, e in gold["grads"].items():
+        gh = host(g[n])
+        got = np.array([gh[i, j] for i, j in e["pos"]])
+        mx = e["max_abs"]
+        a, r = errors(got / mx, np.asarray(e["val"]) / mx)
+        say(f"  {n} ({len(got)} entries): max_abs/max={a:.2e} rel_l2={r:.2e}")
+        assert a <= 2e-2 and r <= 1e-2, n
