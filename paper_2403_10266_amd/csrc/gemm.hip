@@ -36,6 +36,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int BM = 256, BN = 128, BK = 64;
 constexpr int PITCH = BK + 8;                 // 144-byte rows
@@ -269,7 +270,10 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
 // the next slice's LDS stores, each followed by the global load that refills
 // its register, are spread between the MFMAs of the current slice's first
 // step, and each 16-wide K step's fragments are read from LDS during the
-// previous step's MFMAs.  The MFMAs and their k order are those of
+// previous step's MFMAs.  The barrier sits before the slice's last step: by
+// then every wave has stored the next slice (step 0) and read this slice's
+// last fragments, so the next slice's first fragments are read during the
+// last step's MFMAs instead of after a barrier at the slice's end.  The MFMAs and their k order are those of
 // gemm_bf16_kernel, so both kernels give the same bits.
 #ifndef DSP_GEMM_BIG_GROUP
 #define DSP_GEMM_BIG_GROUP 4
@@ -362,7 +366,12 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int cur = ks & 1;
-      if (ks + 1 < BK / 16) fread(cur ^ 1, b, ks + 1);
+      if (ks + 1 < BK / 16) {
+        fread(cur ^ 1, b, ks + 1);
+      } else if (ST) {
+        __syncthreads();
+        fread(cur ^ 1, b ^ 1, 0);
+      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < NMF; ++j) {
@@ -378,8 +387,6 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    __syncthreads();
-    if (ST) fread(0, b ^ 1, 0);
   };
 
   const int nk = (K + BK - 1) / BK;
@@ -403,7 +410,79 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
   }
   slice(kt, no{}, no{});
 
-  // epilogue: lane owns row m = .. + l32 and columns n = .. + 8*r4 + 4g + {0..3}
+  // epilogue: lane owns rows m = .. + 32 bb + l32 and, in each, the column
+  // groups n = .. + 32 a + 8 r4 + 4 g + {0..3}
+  if ((EPI == DSP_EPI_RESID || EPI == DSP_EPI_GELU || EPI == DSP_EPI_RELU) && (N & 3) == 0) {
+    // Every global read of the epilogue (bias, residual) is issued before the
+    // first one is used, through buffer resources whose ranges end at the
+    // last valid row and column (reads past them return zero), so the loads
+    // overlap instead of costing one memory round trip per column group.
+    constexpr int NG = TN * 4;
+    int ncol[NG];
+#pragma unroll
+    for (int j = 0; j < NG; ++j) ncol[j] = n0 + wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
+    float4 bv[NG];
+    if (bias) {
+      const __amdgpu_buffer_rsrc_t rb = make_rsrc(bias, (uint32_t)N * 2u);
+#pragma unroll
+      for (int j = 0; j < NG; ++j) {
+        const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(rb, ncol[j] < N ? (uint32_t)ncol[j] * 2u : 0xFFFFFFF0u, 0, 0);
+        bv[j] = make_float4(__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xFFFF0000u),
+                            __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xFFFF0000u));
+      }
+    }
+    u32x4 rv[EPI == DSP_EPI_RESID ? TM : 1][NG];
+    if constexpr (EPI == DSP_EPI_RESID) {
+      const uint32_t rrow = (uint32_t)N * 4u;
+      const __amdgpu_buffer_rsrc_t rr = make_rsrc(resid + (int64_t)m0 * N, a_rows * rrow);
+#pragma unroll
+      for (int bb = 0; bb < TM; ++bb)
+#pragma unroll
+        for (int j = 0; j < NG; ++j) {
+          const uint32_t r = (uint32_t)(wm * TM * 32 + 32 * bb + l32);
+          rv[bb][j] = __builtin_amdgcn_raw_buffer_load_b128(
+              rr, ncol[j] < N ? r * rrow + (uint32_t)ncol[j] * 4u : 0xFFFFFFF0u, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int bb = 0; bb < TM; ++bb) {
+      const int m = m0 + wm * TM * 32 + 32 * bb + l32;
+      if (m >= M) continue;
+      const int64_t orow = rs.map(m) * N;
+#pragma unroll
+      for (int j = 0; j < NG; ++j) {
+        const int n = ncol[j];
+        if (n >= N) continue;
+        const int a = j / 4, r4 = j % 4;
+        float v[4] = {acc[a][bb][4 * r4 + 0], acc[a][bb][4 * r4 + 1], acc[a][bb][4 * r4 + 2],
+                      acc[a][bb][4 * r4 + 3]};
+        if (bias) {
+          v[0] += bv[j].x;
+          v[1] += bv[j].y;
+          v[2] += bv[j].z;
+          v[3] += bv[j].w;
+        }
+        if (KEEP) *reinterpret_cast<uint2*>(keep_out + orow + n) = pack_bf16x4(v);
+        if (EPI == DSP_EPI_GELU) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
+        }
+        if (EPI == DSP_EPI_RELU) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
+        }
+        if constexpr (EPI == DSP_EPI_RESID) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] += __uint_as_float(rv[bb][j][i]);
+        }
+        if (EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32)
+          *reinterpret_cast<float4*>(static_cast<float*>(out) + orow + n) = make_float4(v[0], v[1], v[2], v[3]);
+        else
+          *reinterpret_cast<uint2*>(static_cast<bf16*>(out) + orow + n) = pack_bf16x4(v);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int bb = 0; bb < TM; ++bb) {
     const int m = m0 + wm * TM * 32 + 32 * bb + l32;
@@ -511,7 +590,9 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
   const int big_bn = N >= 2048 ? 256 : 192;
   const int64_t big_nt = (N + big_bn - 1) / big_bn;
   const int64_t big_tiles = ((M + BIG_BM - 1) / BIG_BM) * big_nt;
-  const bool big = DSP_GEMM_BIG && big_tiles >= 256;
+  // (the large-tile epilogue addresses a tile's 256 rows of fp32 residual
+  // with 32-bit offsets)
+  const bool big = DSP_GEMM_BIG && big_tiles >= 256 && (int64_t)BIG_BM * N * 4 < (int64_t(1) << 31);
 #define DSP_GEMM_LAUNCH(E, KP)                                                                                  \
   do {                                                                                                        \
     if (!big) {                                                                                               \
