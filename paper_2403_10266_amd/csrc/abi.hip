@@ -401,7 +401,7 @@ bool block_saved_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, in
 
 // Scratch of the block backward.
 struct BlockBwdWs {
-  size_t dyb, du, dh, dcur, dx1, da, dqkv, delta, wg, wg_bytes, total;
+  size_t dyb, du, dh, dcur, dx1, da, dqkv, delta, wg, wg_bytes, wt, total;
 };
 
 bool block_bwd_ws_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, int dtype, BlockBwdWs* ws) {
@@ -427,6 +427,9 @@ bool block_bwd_ws_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, i
   ws->delta = off; off += up((size_t)th * 4);
   ws->wg = off;    off += up(wg);
   ws->wg_bytes = wg;
+  // bf16: one weight matrix transposed, for the input gradients on the
+  // forward's GEMM
+  ws->wt = off;    off += dtype == DSP_BF16 ? up((size_t)std::max(3 * (int64_t)C, (int64_t)F) * C * es) : 0;
   ws->total = off;
   return true;
 }
@@ -1095,6 +1098,7 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
   float* dx1 = reinterpret_cast<float*>(wb + bw.dx1);
   float* delta = reinterpret_cast<float*>(wb + bw.delta);
   void* wg = bw.wg_bytes ? wb + bw.wg : nullptr;
+  void* wt = wb + bw.wt;
   const int bf = dtype == DSP_BF16;
   const size_t es = elem_size(dtype);
   const int D = C / H;
@@ -1110,13 +1114,27 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
   } while (0)
   // the upstream fp32 gradient as an operand of the block dtype
   auto operand = [&](const float* d) { return launch_cast(d, 0, dyb, bf, tokens * C, s); };
+  // dx = dy W (+ the activation's derivative) for W stored [N][K]: in bf16 at
+  // sizes the forward's large-tile GEMM takes, W is transposed into the
+  // workspace and dx = dy (W^T)^T runs on that GEMM; else the gradient GEMM
+  auto bwd_data = [&](const void* dyp, const void* wp, const void* up, void* dxp, int N, int K, int epi) -> int {
+    if (bf && linear_bf16_large_tiles(tokens, K)) {
+      const int r = launch_transpose_bf16(wp, wt, N, K, s);
+      if (r != DSP_OK) return r;
+      const int e = epi == DSP_GRAD_EPI_F32 ? DSP_EPI_F32
+                    : epi == DSP_GRAD_EPI_BF16 ? DSP_EPI_NONE
+                    : epi == DSP_GRAD_EPI_GELU_BWD ? DSP_EPI_GELU_BWD : DSP_EPI_RELU_BWD;
+      return launch_linear_bf16(dyp, wt, nullptr, nullptr, dxp, tokens, K, N, e, s, const_cast<void*>(up));
+    }
+    return dsp_linear_bwd_data(dyp, wp, up, dxp, tokens, N, K, epi, dtype, stream);
+  };
   // backward of one attention sublayer: d_out (in dyb) -> dh (fp32), weight gradients
   auto attn_sub_bwd = [&](const char* h, const char* qkv, const char* a, const float* lse, const void* wqkv,
                           const void* wo, float* g_wqkv, float* g_bqkv, float* g_wo, float* g_bo, int64_t X,
                           int64_t L) {
     int r = dsp_linear_bwd_weight(dyb, a, g_wo, g_bo, wg, bw.wg_bytes, tokens, C, C, dtype, stream);
     if (r != DSP_OK) return r;
-    r = dsp_linear_bwd_data(dyb, wo, nullptr, da, tokens, C, C, act_epi, dtype, stream);
+    r = bwd_data(dyb, wo, nullptr, da, C, C, act_epi);
     if (r != DSP_OK) return r;
     const int64_t q_st[3] = {X * L * 3 * C, L * 3 * C, 3 * (int64_t)C}, o_st[3] = {X * L * C, L * C, C};
     r = attn_bwd_impl(qkv, qkv + (size_t)C * es, qkv + (size_t)2 * C * es, a, da, lse, dqkv, dqkv + (size_t)C * es,
@@ -1124,7 +1142,7 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
     if (r != DSP_OK) return r;
     r = dsp_linear_bwd_weight(dqkv, h, g_wqkv, g_bqkv, wg, bw.wg_bytes, tokens, 3 * C, C, dtype, stream);
     if (r != DSP_OK) return r;
-    return dsp_linear_bwd_data(dqkv, wqkv, nullptr, dh, tokens, 3 * C, C, DSP_GRAD_EPI_F32, dtype, stream);
+    return bwd_data(dqkv, wqkv, nullptr, dh, 3 * C, C, DSP_GRAD_EPI_F32);
   };
   if (flags & DSP_BLOCK_POST_LN) {
     // post-LN: the gradient passes each LayerNorm before its sublayer, and the
@@ -1141,9 +1159,9 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
       DSP_TRY(operand(dr3));
     }
     DSP_TRY(dsp_linear_bwd_weight(dyb, g, grads->w2, grads->b2, wg, bw.wg_bytes, tokens, C, F, dtype, stream));
-    DSP_TRY(dsp_linear_bwd_data(dyb, w->w2, u, du, tokens, C, F, act_bwd, dtype, stream));
+    DSP_TRY(bwd_data(dyb, w->w2, u, du, C, F, act_bwd));
     DSP_TRY(dsp_linear_bwd_weight(du, h3, grads->w1, grads->b1, wg, bw.wg_bytes, tokens, F, C, dtype, stream));
-    DSP_TRY(dsp_linear_bwd_data(du, w->w1, nullptr, dh, tokens, F, C, DSP_GRAD_EPI_F32, dtype, stream));
+    DSP_TRY(bwd_data(du, w->w1, nullptr, dh, F, C, DSP_GRAD_EPI_F32));
     DSP_TRY(launch_add_f32(dr3, dh, dcur, tokens * C, s));                           // dy1
     // ---- temporal half: r2 = y0 + Attn_T(y0 Wqkv_t) Wo_t, y1 = LN(r2)
     DSP_TRY(launch_layernorm_bwd(r2, 0, dcur, 0, nullptr, dx1, tokens, C, ln_eps, s, RowSwap(), dyb, bf));  // dr2
@@ -1161,9 +1179,9 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
   // ---- MLP: y = y1 + act(h3 W1 + b1) W2 + b2
   DSP_TRY(operand(dy_BSTC));
   DSP_TRY(dsp_linear_bwd_weight(dyb, g, grads->w2, grads->b2, wg, bw.wg_bytes, tokens, C, F, dtype, stream));
-  DSP_TRY(dsp_linear_bwd_data(dyb, w->w2, u, du, tokens, C, F, act_bwd, dtype, stream));
+  DSP_TRY(bwd_data(dyb, w->w2, u, du, C, F, act_bwd));
   DSP_TRY(dsp_linear_bwd_weight(du, h3, grads->w1, grads->b1, wg, bw.wg_bytes, tokens, F, C, dtype, stream));
-  DSP_TRY(dsp_linear_bwd_data(du, w->w1, nullptr, dh, tokens, F, C, DSP_GRAD_EPI_F32, dtype, stream));
+  DSP_TRY(bwd_data(du, w->w1, nullptr, dh, F, C, DSP_GRAD_EPI_F32));
   if (flags & DSP_BLOCK_NO_MLP_LN) {
     DSP_TRY(launch_add_f32(dy_BSTC, dh, dcur, tokens * C, s));
     DSP_TRY(operand(dcur));

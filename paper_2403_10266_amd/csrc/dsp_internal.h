@@ -137,6 +137,14 @@ int launch_layernorm_bwd(const void* x, int x_bf16, const void* dy, int dy_bf16,
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
                        void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre = nullptr,
                        RowSwap rs = RowSwap());
+// Internal epilogues of launch_linear_bf16 (not in the public header): the
+// backward of an activation, out = (a W^T) * act'(u), u the saved
+// pre-activation passed as `pre` (read, at the output's offsets; no row swap).
+constexpr int DSP_EPI_GELU_BWD = 5, DSP_EPI_RELU_BWD = 6;
+// Whether launch_linear_bf16 runs (M, N) on its large-tile kernel.
+bool linear_bf16_large_tiles(int64_t M, int N);
+// y[c][r] = x[r][c] for a rows x cols bf16 matrix (gemm.hip).
+int launch_transpose_bf16(const void* x, void* y, int64_t rows, int64_t cols, hipStream_t s);
 int launch_linear_f32(const float* a, const float* w, const float* bias, const float* residual,
                       float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre = nullptr,
                       RowSwap rs = RowSwap());

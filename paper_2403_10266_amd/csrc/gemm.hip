@@ -81,6 +81,29 @@ __device__ __forceinline__ float gelu_bf16out(float v) {
   return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f));
 }
 
+// its derivative Phi(u) + u phi(u), for the backward epilogue.  The
+// exp(-z^2) of erf's tail at z = u / sqrt(2) is exp(-u^2 / 2) = sqrt(2 pi)
+// phi(u), so one exponential serves both terms.
+__device__ __forceinline__ float gelu_grad_bf16(float u) {
+  const float z = u * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, fabsf(z), 1.0f));
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  poly *= t;
+  const float e = __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);
+  const float erf = copysignf(1.0f - poly * e, z);
+  return fmaf(0.5f, erf, 0.5f) + u * (0.3989422804014327f * e);
+}
+
+// the activation's derivative at the saved pre-activation u (backward
+// epilogues: the output is the GEMM sum times it)
+template <int EPI>
+__device__ __forceinline__ float act_grad(float u) {
+  return EPI == DSP_EPI_GELU_BWD ? gelu_grad_bf16(u) : (u > 0.0f ? 1.0f : 0.0f);
+}
+
 __device__ __forceinline__ uint2 pack_bf16x4(const float v[4]) {
   bf16x2 lo = {(bf16)v[0], (bf16)v[1]};
   bf16x2 hi = {(bf16)v[2], (bf16)v[3]};
@@ -103,6 +126,12 @@ __device__ __forceinline__ void epilogue4(float v[4], int m, int64_t om, int n, 
                                           const bf16* __restrict__ bias, const float* resid, void* out,
                                           bf16* keep_out) {
   const bool full = (n + 3 < N) && ((N & 3) == 0);
+  if (EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD) {
+    // keep_out holds the saved pre-activation u, read at the output's offsets
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (n + i < N) v[i] *= act_grad<EPI>(bf2f(keep_out[om * N + n + i]));
+  }
   if (bias) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -412,7 +441,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
 
   // epilogue: lane owns rows m = .. + 32 bb + l32 and, in each, the column
   // groups n = .. + 32 a + 8 r4 + 4 g + {0..3}
-  if ((EPI == DSP_EPI_RESID || EPI == DSP_EPI_GELU || EPI == DSP_EPI_RELU) && (N & 3) == 0) {
+  constexpr bool BWD = EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD;
+  if ((EPI == DSP_EPI_RESID || EPI == DSP_EPI_GELU || EPI == DSP_EPI_RELU || BWD) && (N & 3) == 0) {
     // Every global read of the epilogue (bias, residual) is issued before the
     // first one is used, through buffer resources whose ranges end at the
     // last valid row and column (reads past them return zero), so the loads
@@ -430,6 +460,21 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
         bv[j] = make_float4(__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xFFFF0000u),
                             __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xFFFF0000u));
       }
+    }
+    // backward epilogues: the saved pre-activation (bf16, in keep_out, at the
+    // output's offsets: no row swap with them)
+    u32x2 uv[BWD ? TM : 1][NG];
+    if constexpr (BWD) {
+      const uint32_t urow = (uint32_t)N * 2u;
+      const __amdgpu_buffer_rsrc_t ru = make_rsrc(keep_out + (int64_t)m0 * N, a_rows * urow);
+#pragma unroll
+      for (int bb = 0; bb < TM; ++bb)
+#pragma unroll
+        for (int j = 0; j < NG; ++j) {
+          const uint32_t r = (uint32_t)(wm * TM * 32 + 32 * bb + l32);
+          uv[bb][j] = __builtin_amdgcn_raw_buffer_load_b64(
+              ru, ncol[j] < N ? r * urow + (uint32_t)ncol[j] * 2u : 0xFFFFFFF0u, 0, 0);
+        }
     }
     u32x4 rv[EPI == DSP_EPI_RESID ? TM : 1][NG];
     if constexpr (EPI == DSP_EPI_RESID) {
@@ -463,6 +508,13 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
           v[3] += bv[j].w;
         }
         if (KEEP) *reinterpret_cast<uint2*>(keep_out + orow + n) = pack_bf16x4(v);
+        if constexpr (BWD) {
+          const uint32_t w0 = uv[bb][j][0], w1 = uv[bb][j][1];
+          v[0] *= act_grad<EPI>(__uint_as_float(w0 << 16));
+          v[1] *= act_grad<EPI>(__uint_as_float(w0 & 0xFFFF0000u));
+          v[2] *= act_grad<EPI>(__uint_as_float(w1 << 16));
+          v[3] *= act_grad<EPI>(__uint_as_float(w1 & 0xFFFF0000u));
+        }
         if (EPI == DSP_EPI_GELU) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
@@ -569,17 +621,52 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
+// bf16 transpose through a padded 64 x 64 LDS tile: rows of 64 consecutive
+// elements read and written (the weight transposes of the backward)
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ x, uint16_t* y, int R,
+                                                             int C) {
+  __shared__ uint16_t t[64][66];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int r = i / 64, c = i % 64;
+    if (r0 + r < R && c0 + c < C) t[r][c] = x[(int64_t)(r0 + r) * C + c0 + c];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int c = i / 64, r = i % 64;
+    if (r0 + r < R && c0 + c < C) y[(int64_t)(c0 + c) * R + r0 + r] = t[r][c];
+  }
+}
+
 }  // namespace
+
+int launch_transpose_bf16(const void* x, void* y, int64_t rows, int64_t cols, hipStream_t s) {
+  if (rows == 0 || cols == 0) return DSP_OK;
+  if (rows >= (int64_t(1) << 31) || cols >= (int64_t(1) << 31) || (rows + 63) / 64 >= 65536) return DSP_ERR_SHAPE;
+  const dim3 grid((uint32_t)((cols + 63) / 64), (uint32_t)((rows + 63) / 64));
+  hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, s, static_cast<const uint16_t*>(x),
+                     static_cast<uint16_t*>(y), (int)rows, (int)cols);
+  return last_launch_status();
+}
+
+bool linear_bf16_large_tiles(int64_t M, int N) {
+  const int big_bn = N >= 2048 ? 256 : 192;
+  const int64_t big_tiles = ((M + BIG_BM - 1) / BIG_BM) * ((N + big_bn - 1) / big_bn);
+  return DSP_GEMM_BIG && big_tiles >= 256 && (int64_t)BIG_BM * N * 4 < (int64_t(1) << 31);
+}
 
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
                        void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre, RowSwap rs) {
   if (M == 0) return DSP_OK;
+  // backward epilogues: `pre` is the saved pre-activation, read (not written)
+  const bool bwd = epilogue == DSP_EPI_GELU_BWD || epilogue == DSP_EPI_RELU_BWD;
+  if (bwd && (!pre || rs.outer != 0)) return DSP_ERR_ARG;
   const int64_t n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN;
   const int64_t tiles = n_mt * n_nt;
   // a tile's buffer resources address BM rows of K bf16 with 32-bit offsets
   if (tiles >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) || (int64_t)BM * K * 2 >= (int64_t(1) << 31))
     return DSP_ERR_SHAPE;
-  const bool keep = pre != nullptr;
+  const bool keep = pre != nullptr && !bwd;
   if (keep && epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) return DSP_ERR_ARG;
   const bf16* A = static_cast<const bf16*>(a);
   const bf16* Wt = static_cast<const bf16*>(w);
@@ -592,7 +679,7 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
   const int64_t big_tiles = ((M + BIG_BM - 1) / BIG_BM) * big_nt;
   // (the large-tile epilogue addresses a tile's 256 rows of fp32 residual
   // with 32-bit offsets)
-  const bool big = DSP_GEMM_BIG && big_tiles >= 256 && (int64_t)BIG_BM * N * 4 < (int64_t(1) << 31);
+  const bool big = linear_bf16_large_tiles(M, N);
 #define DSP_GEMM_LAUNCH(E, KP)                                                                                  \
   do {                                                                                                        \
     if (!big) {                                                                                               \
@@ -616,6 +703,8 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
     case DSP_EPI_RELU:
       if (keep) DSP_GEMM_LAUNCH(DSP_EPI_RELU, true); else DSP_GEMM_LAUNCH(DSP_EPI_RELU, false);
       break;
+    case DSP_EPI_GELU_BWD: DSP_GEMM_LAUNCH(DSP_EPI_GELU_BWD, false); break;
+    case DSP_EPI_RELU_BWD: DSP_GEMM_LAUNCH(DSP_EPI_RELU_BWD, false); break;
     default:
       return DSP_ERR_ARG;
   }

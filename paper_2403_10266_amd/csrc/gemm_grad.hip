@@ -45,24 +45,20 @@ struct TPitch {
   static constexpr int P = ROWS + 8;  // transposed tiles: an odd multiple of 16 bytes
 };
 
-// erf by Abramowitz and Stegun 7.1.26 (|error| <= 1.5e-7)
-__device__ __forceinline__ float erf_as(float z) {
-  const float a = fabsf(z);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
+// d/du (u Phi(u)) = Phi(u) + u phi(u), with erf by Abramowitz and Stegun
+// 7.1.26 (|error| <= 1.5e-7).  The exp(-z^2) of erf's tail at z = u / sqrt(2)
+// is exp(-u^2 / 2) = sqrt(2 pi) phi(u): one exponential serves both terms.
+__device__ __forceinline__ float gelu_grad(float u) {
+  const float z = u * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, fabsf(z), 1.0f));
   float poly = fmaf(1.061405429f, t, -1.453152027f);
   poly = fmaf(poly, t, 1.421413741f);
   poly = fmaf(poly, t, -0.284496736f);
   poly = fmaf(poly, t, 0.254829592f);
   poly *= t;
-  const float e = __builtin_amdgcn_exp2f(-a * a * 1.4426950408889634f);
-  return copysignf(1.0f - poly * e, z);
-}
-
-// d/du (u Phi(u)) = Phi(u) + u phi(u)
-__device__ __forceinline__ float gelu_grad(float u) {
-  const float cdf = 0.5f * (1.0f + erf_as(u * 0.70710678118654752f));
-  const float pdf = 0.3989422804014327f * __builtin_amdgcn_exp2f(-0.5f * u * u * 1.4426950408889634f);
-  return cdf + u * pdf;
+  const float e = __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);
+  const float erf = copysignf(1.0f - poly * e, z);
+  return fmaf(0.5f, erf, 0.5f) + u * (0.3989422804014327f * e);
 }
 
 struct GradArgs {
