@@ -18,7 +18,6 @@
 namespace dsp {
 namespace {
 
-constexpr int CH_NT = 256;
 constexpr int CH_CMAX = 64, CH_LMAX = 64;
 // LDS floats for the largest shape: rows, W_qkv (pitch C + 4), qkv (pitch 3C + 4)
 constexpr int CH_LDS = CH_LMAX * CH_CMAX + 3 * CH_CMAX * (CH_CMAX + 4) + CH_LMAX * (3 * CH_CMAX + 4);
@@ -63,10 +62,14 @@ __device__ __forceinline__ void chain_gemm_col(const float* a, int C, const floa
   }
 }
 
-template <int DT>
-__global__ __launch_bounds__(CH_NT) void chain_sublayer_f32_kernel(ChainParams p) {
+// NTH threads: 1024 for head widths up to 32 (more threads for the two
+// GEMMs' output columns and row bands; the attention's per-thread registers
+// still fit), 256 for 64
+template <int DT, int NTH>
+__global__ __launch_bounds__(NTH) void chain_sublayer_f32_kernel(ChainParams p) {
   const int L = p.L, C = p.C, H = p.H;
   constexpr int D = DT;
+  constexpr int CH_NT = NTH;
   const int C3 = 3 * C;
   const int WP = C + 4;     // weight row pitch (floats): float4 rows
   const int QP = C3 + 4;    // qkv row pitch: float4 rows
@@ -224,10 +227,10 @@ int launch_chain_sublayer_f32(const float* x, const float* wqkv, const float* bq
   p.scale = scale;
   p.rs = rs;
   switch (p.D) {
-    case 8: hipLaunchKernelGGL(chain_sublayer_f32_kernel<8>, dim3((uint32_t)groups), dim3(CH_NT), 0, s, p); break;
-    case 16: hipLaunchKernelGGL(chain_sublayer_f32_kernel<16>, dim3((uint32_t)groups), dim3(CH_NT), 0, s, p); break;
-    case 32: hipLaunchKernelGGL(chain_sublayer_f32_kernel<32>, dim3((uint32_t)groups), dim3(CH_NT), 0, s, p); break;
-    case 64: hipLaunchKernelGGL(chain_sublayer_f32_kernel<64>, dim3((uint32_t)groups), dim3(CH_NT), 0, s, p); break;
+    case 8: hipLaunchKernelGGL((chain_sublayer_f32_kernel<8, 1024>), dim3((uint32_t)groups), dim3(1024), 0, s, p); break;
+    case 16: hipLaunchKernelGGL((chain_sublayer_f32_kernel<16, 1024>), dim3((uint32_t)groups), dim3(1024), 0, s, p); break;
+    case 32: hipLaunchKernelGGL((chain_sublayer_f32_kernel<32, 1024>), dim3((uint32_t)groups), dim3(1024), 0, s, p); break;
+    case 64: hipLaunchKernelGGL((chain_sublayer_f32_kernel<64, 256>), dim3((uint32_t)groups), dim3(256), 0, s, p); break;
     default: return DSP_ERR_SHAPE;
   }
   return last_launch_status();
