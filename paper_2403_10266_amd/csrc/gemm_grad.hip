@@ -29,6 +29,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "attn_bf16_common.h"
 #include "dsp_internal.h"
@@ -296,6 +297,187 @@ __global__ __launch_bounds__(256) void colsum_bf16_kernel(const bf16* __restrict
   *reinterpret_cast<float4*>(db + 4 * n4) = make_float4(s[0], s[1], s[2], s[3]);
 }
 
+// ---------------------------------------------------------------------------
+// Large-tile weight gradient: out[M][N] = sum over k of a[k][m] b[k][n] (both
+// operands stored with the reduction index as rows: dW = dy^T x), fp32, with
+// the reduction split over blockIdx.z into fp32 partials.  The schedule of
+// gemm_bf16_big_kernel (gemm.hip): 256 x (64 TN) output tiles, 4 waves of
+// 128 x (32 TN) on one SIMD each with the accumulators in AGPRs, two LDS
+// buffers and one barrier per 64-wide k slice (before its last 16-wide step),
+// the next slice's LDS stores and the loads after it spread over the MFMAs of
+// step 0, each step's fragments read during the previous step's MFMAs.  Tiles
+// hold k rows of the tile's columns as they lie in memory; fragments are read
+// with ds_read_b64_tr_b16 (k order {4g..4g+3, 8+4g..8+4g+3} on both sides).
+constexpr int GB_BM = 256;
+#ifndef DSP_GRAD_BIG
+#define DSP_GRAD_BIG 1
+#endif
+
+template <int TN>
+__global__ __launch_bounds__(GNTHR, 1) void gemm_grad_tt_big_kernel(GradArgs p) {
+  constexpr int TM = 4;
+  constexpr int BNB = 2 * TN * 32;
+  constexpr int PA = GB_BM + 8, PB = BNB + 8;   // k-row pitches: odd multiples of 16 bytes
+  constexpr int A_EL = GBK * PA, STAGE = A_EL + GBK * PB;
+  constexpr int CA = GB_BM / 8, CB = BNB / 8;   // 16-byte chunks per k row
+  constexpr int A_LOADS = GBK * CA / GNTHR, B_LOADS = GBK * CB / GNTHR, NL = A_LOADS + B_LOADS;
+  static_assert(GBK * CA % GNTHR == 0 && GBK * CB % GNTHR == 0, "loader shape");
+  __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
+
+  // tile order: contiguous ranges per XCD, then groups of 4 m-tiles (m fastest)
+  uint32_t bid = blockIdx.x;
+  if ((p.n_tiles & 7) == 0) bid = (bid & 7u) * ((uint32_t)p.n_tiles >> 3) + (bid >> 3);
+  const int n_mt = p.n_tiles / p.n_ntiles;
+  const int per_group = 4 * p.n_ntiles;
+  const int grp = (int)bid / per_group;
+  const int first_m = grp * 4;
+  const int gm = min(4, n_mt - first_m);
+  const int rem = (int)bid - grp * per_group;
+  const int m0 = (first_m + rem % gm) * GB_BM, n0 = (rem / gm) * BNB;
+  const int kb = blockIdx.z * p.k_per_split;
+  const int ke = min(p.K, kb + p.k_per_split);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int l32 = lane & 31, g = lane >> 5;
+  const int j16 = lane & 15, mbase = 16 * ((lane >> 4) & 1);
+
+  // loader: chunk e = t + 256 i of a tensor's slice is k row e / C, columns
+  // 8 (e % C) .. + 7 of the tile; columns past M (N) read zero
+  uint32_t off[NL];
+  int lofs[NL];
+  bool ok[NL];
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const bool is_a = i < A_LOADS;
+    const int e = threadIdx.x + GNTHR * (is_a ? i : i - A_LOADS);
+    const int C = is_a ? CA : CB;
+    const int r = e / C, c = e % C;
+    off[i] = (uint32_t)r * (uint32_t)((is_a ? p.lda : p.ldb) * 2) + (uint32_t)c * 16u;
+    lofs[i] = is_a ? r * PA + c * 8 : A_EL + r * PB + c * 8;
+    ok[i] = is_a ? m0 + 8 * c < p.M : n0 + 8 * c < p.N;
+  }
+  u32x4 pre[NL];
+  __amdgpu_buffer_rsrc_t ra, rb;
+  auto rsrcs = [&](int k0) {  // the slice's k rows below ke (rows past it read zero)
+    const uint32_t krows = (uint32_t)max(0, min(GBK, ke - k0));
+    ra = make_rsrc(p.a + (int64_t)k0 * p.lda + m0, krows * (uint32_t)(p.lda * 2));
+    rb = make_rsrc(p.b + (int64_t)k0 * p.ldb + n0, krows * (uint32_t)(p.ldb * 2));
+  };
+  auto gload = [&](int i) {
+    pre[i] = __builtin_amdgcn_raw_buffer_load_b128(i < A_LOADS ? ra : rb, ok[i] ? off[i] : 0xFFFFFFF0u, 0, 0);
+  };
+  auto lstore = [&](int i, int buf) { *reinterpret_cast<u32x4*>(lds + buf * STAGE + lofs[i]) = pre[i]; };
+
+  floatx16 acc[TN][TM];
+#pragma unroll
+  for (int a = 0; a < TN; ++a)
+#pragma unroll
+    for (int b = 0; b < TM; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+  auto frag = [&](const bf16* t, int P, int rbase, int ks) {
+    const int row = 16 * ks + 4 * g + (j16 >> 2);
+    const int col = rbase + mbase + 4 * (j16 & 3);
+    const shortx4 lo = lds_read_tr(t + row * P + col);
+    const shortx4 hi = lds_read_tr(t + (row + 8) * P + col);
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  bf16x8 af[2][TM], wf[2][TN];
+  auto fread = [&](int slot, int buf, int ks) {
+    const bf16* As = lds + buf * STAGE;
+    const bf16* Bs = As + A_EL;
+#pragma unroll
+    for (int b = 0; b < TM; ++b) af[slot][b] = frag(As, PA, wm * TM * 32 + 32 * b, ks);
+#pragma unroll
+    for (int a = 0; a < TN; ++a) wf[slot][a] = frag(Bs, PB, wn * TN * 32 + 32 * a, ks);
+  };
+
+  auto slice = [&](int kt, auto st_c, auto ld_c) {
+    constexpr bool ST = decltype(st_c)::value, LD = decltype(ld_c)::value;
+    constexpr int NMF = TM * TN;
+    const int b = kt & 1;
+    if (LD) rsrcs(kb + (kt + 2) * GBK);
+#pragma unroll
+    for (int ks = 0; ks < GBK / 16; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < GBK / 16) {
+        fread(cur ^ 1, b, ks + 1);
+      } else if (ST) {
+        __syncthreads();
+        fread(cur ^ 1, b ^ 1, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < NMF; ++j) {
+        const int a = j / TM, bb = j % TM;
+        acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][a], af[cur][bb], acc[a][bb], 0, 0, 0);
+        if (ks == 0 && ST) {
+#pragma unroll
+          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) {
+            lstore(i, b ^ 1);
+            if (LD) gload(i);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+
+  const int nk = (ke - kb + GBK - 1) / GBK;
+  if (nk > 0) {
+    rsrcs(kb);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) gload(i);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) lstore(i, 0);
+    if (nk > 1) {
+      rsrcs(kb + GBK);
+#pragma unroll
+      for (int i = 0; i < NL; ++i) gload(i);
+    }
+    __syncthreads();
+    fread(0, 0, 0);
+    using yes = std::true_type;
+    using no = std::false_type;
+    int kt = 0;
+    for (; kt + 2 < nk; ++kt) slice(kt, yes{}, yes{});
+    if (kt + 1 < nk) {
+      slice(kt, yes{}, no{});
+      ++kt;
+    }
+    slice(kt, no{}, no{});
+  }
+
+  // fp32 partial (or the result, unsplit): lane owns rows m = .. + 32 bb + l32
+  // and column groups n = .. + 32 a + 8 r4 + 4 g + {0..3}
+  float* out = static_cast<float*>(p.out) + (int64_t)blockIdx.z * p.M * p.N;
+#pragma unroll
+  for (int bb = 0; bb < TM; ++bb) {
+    const int m = m0 + wm * TM * 32 + 32 * bb + l32;
+    if (m >= p.M) continue;
+#pragma unroll
+    for (int a = 0; a < TN; ++a)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int n = n0 + wn * TN * 32 + 32 * a + 8 * r4 + 4 * g;
+        if (n < p.N)
+          *reinterpret_cast<float4*>(out + (int64_t)m * p.N + n) =
+              make_float4(acc[a][bb][4 * r4], acc[a][bb][4 * r4 + 1], acc[a][bb][4 * r4 + 2], acc[a][bb][4 * r4 + 3]);
+      }
+  }
+}
+
+// Whether the weight gradient out[M][N] (reduction K, row strides lda, ldb)
+// runs on the large-tile kernel, and with which tile width.
+bool grad_big_ok(int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb) {
+  return DSP_GRAD_BIG && M >= 512 && N >= 512 && M % 8 == 0 && N % 8 == 0 && K >= 2048 &&
+         (int64_t)GBK * lda * 2 < (int64_t(1) << 31) && (int64_t)GBK * ldb * 2 < (int64_t(1) << 31) &&
+         M * N < (int64_t(1) << 31);
+}
+int grad_big_tn(int64_t N) { return N >= 2048 ? 4 : 3; }
+
 template <bool TA, bool TB, int EPI>
 int launch_grad(const GradArgs& p0, int splits, float* ws, hipStream_t s) {
   GradArgs p = p0;
@@ -381,6 +563,28 @@ int launch_colsum_f32(const float* dy, float* db, int64_t M, int N, hipStream_t 
 }
 
 int grad_splits(int64_t M, int64_t N, int64_t K) {
+  if (grad_big_ok(M, N, K, M, N)) {
+    // the large-tile kernel: one work-group per CU (256 slots), in units of
+    // one 64-wide slice of a tile on a full round; a split's extra fp32
+    // partial (8 M N bytes at 5 TB/s) against ~2 us per slice round
+    const int bnb = grad_big_tn(N) * 64;
+    const int64_t tiles = ((M + GB_BM - 1) / GB_BM) * ((N + bnb - 1) / bnb);
+    const int64_t slices = (K + GBK - 1) / GBK;
+    const double per_split = (double)M * (double)N * 8e-7;
+    int best = 1;
+    double best_cost = 0.0;
+    for (int s = 1; s <= 16; ++s) {
+      const int64_t per = (slices + s - 1) / s;
+      if (per < 32 || per * (s - 1) >= slices) break;
+      const int64_t rounds = (tiles * s + 255) / 256;
+      const double cost = (double)rounds * (double)(per + 2) + (s > 1 ? s * per_split : 0.0);
+      if (s == 1 || cost < best_cost) {
+        best = s;
+        best_cost = cost;
+      }
+    }
+    return best;
+  }
   // The split count minimising a cost model, in units of one 64-wide K slice
   // of one tile on a full round of work-groups (two per CU, 256 CUs):
   //   rounds * (slices per split + 2 for the work-group's set-up and fp32
@@ -426,6 +630,29 @@ int launch_gemm_grad(const void* a, int ta, int64_t lda, const void* b, int tb, 
   p.M = (int)M;
   p.N = (int)N;
   p.K = (int)K;
+  if (ta == 1 && tb == 1 && epi == DSP_GRAD_EPI_F32 && grad_big_ok(M, N, K, lda, ldb) &&
+      (splits == 1 || ws)) {
+    const int tn = grad_big_tn(N);
+    const int bnb = tn * 64;
+    const int64_t n_nt = (N + bnb - 1) / bnb;
+    const int64_t tiles = ((M + GB_BM - 1) / GB_BM) * n_nt;
+    p.n_ntiles = (int)n_nt;
+    p.n_tiles = (int)tiles;
+    p.k_per_split = ((p.K + splits - 1) / splits + GBK - 1) / GBK * GBK;
+    if (splits > 1) p.out = ws;
+    if (tn == 4)
+      hipLaunchKernelGGL((gemm_grad_tt_big_kernel<4>), dim3((uint32_t)tiles, 1, (uint32_t)splits), dim3(GNTHR), 0, s,
+                         p);
+    else
+      hipLaunchKernelGGL((gemm_grad_tt_big_kernel<3>), dim3((uint32_t)tiles, 1, (uint32_t)splits), dim3(GNTHR), 0, s,
+                         p);
+    int st = last_launch_status();
+    if (st != DSP_OK || splits == 1) return st;
+    const int64_t n4 = M * N / 4;
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((uint32_t)((n4 + 255) / 256)), dim3(256), 0, s,
+                       reinterpret_cast<const float4*>(ws), reinterpret_cast<float4*>(out), n4, splits);
+    return last_launch_status();
+  }
 #define DSP_GRAD_CASE(TA_, TB_)                                                                    \
   if (ta == TA_ && tb == TB_) {                                                                   \
     switch (epi) {                                                                                \

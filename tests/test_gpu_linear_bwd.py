@@ -67,7 +67,10 @@ def test_linear_bwd_data_activation(torch, dtype, act):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("M,N,K", [(1, 8, 8), (300, 72, 136), (1000, 1152, 264), (4100, 3456, 1152)])
+@pytest.mark.parametrize("M,N,K", [(1, 8, 8), (300, 72, 136), (1000, 1152, 264), (4100, 3456, 1152),
+                                    # the large-tile weight-gradient kernel: ragged tiles in both output
+                                    # dimensions and in the token reduction, split-K partials
+                                    (4100, 1160, 520), (12000, 1152, 4608)])
 def test_linear_bwd_weight(torch, dtype, M, N, K):
     import paper_2403_10266_amd as dsp
     if dtype == "f32" and M * N * K > 3e8:
