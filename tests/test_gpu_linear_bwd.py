@@ -66,15 +66,17 @@ def test_linear_bwd_data_activation(torch, dtype, act):
     _close(host(got), want, "f32" if dtype == "f32" else "bf16", f"{act} backward")
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("M,N,K", [(1, 8, 8), (300, 72, 136), (1000, 1152, 264), (4100, 3456, 1152),
-                                    # the large-tile weight-gradient kernel: ragged tiles in both output
-                                    # dimensions and in the token reduction, split-K partials
-                                    (4100, 1160, 520), (12000, 1152, 4608)])
+_SMALL_W = [(1, 8, 8), (300, 72, 136), (1000, 1152, 264)]
+# bf16 only (the fp32 path is for small problems): the 256 x 128 gradient
+# kernel, then the large-tile one with ragged tiles in both output dimensions
+# and in the token reduction, and split-K partials
+_LARGE_W = [(4100, 3456, 1152), (4100, 1160, 520), (12000, 1152, 4608)]
+
+
+@pytest.mark.parametrize("dtype,M,N,K", [(d, *m) for d in ("f32", "bf16") for m in _SMALL_W] +
+                         [("bf16", *m) for m in _LARGE_W])
 def test_linear_bwd_weight(torch, dtype, M, N, K):
     import paper_2403_10266_amd as dsp
-    if dtype == "f32" and M * N * K > 3e8:
-        pytest.skip("the fp32 path is for small problems")
     x, dy = _draw((M, K), dtype, M + K), _draw((M, N), dtype, N)
     say(f"bwd_weight {dtype} M={M} N={N} K={K}")
     _, dw_paper, db = oracle.linear_bwd(x, np.zeros((K, N)), dy)
