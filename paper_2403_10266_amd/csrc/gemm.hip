@@ -298,12 +298,13 @@ __global__ __launch_bounds__(NTHR, 2) void gemm_bf16_kernel(
 // accumulators in AGPRs.  Two LDS buffers, so one barrier per 64-wide K slice;
 // the next slice's LDS stores, each followed by the global load that refills
 // its register, are spread between the MFMAs of the current slice's first
-// step, and each 16-wide K step's fragments are read from LDS during the
-// previous step's MFMAs.  The barrier sits before the slice's last step: by
-// then every wave has stored the next slice (step 0) and read this slice's
+// three steps, and each 16-wide K step's fragments are read from LDS during
+// the previous step's MFMAs.  The barrier sits before the slice's last step: by
+// then every wave has stored the next slice (steps 0-2) and read this slice's
 // last fragments, so the next slice's first fragments are read during the
-// last step's MFMAs instead of after a barrier at the slice's end.  The MFMAs and their k order are those of
-// gemm_bf16_kernel, so both kernels give the same bits.
+// last step's MFMAs instead of after a barrier at the slice's end.  The MFMAs
+// and their k order are those of gemm_bf16_kernel, so both kernels give the
+// same bits.
 #ifndef DSP_GEMM_BIG_GROUP
 #define DSP_GEMM_BIG_GROUP 4
 #endif
@@ -386,11 +387,14 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
 
   // One K slice from LDS buffer kt & 1.  ST: store the prefetched slice kt + 1
   // into the other buffer; LD: reload each prefetch register with its part of
-  // slice kt + 2 right after its store (both spread over the MFMAs of step 0),
-  // which gives the loads a whole slice of MFMAs before their store.
+  // slice kt + 2 right after its store, which gives the loads a slice of MFMAs
+  // before their store.  The stores are spread over the MFMAs of the first
+  // three steps: in one step, they and the next step's fragment reads
+  // together needed more LDS bandwidth than the CU has (~190 of 128 B/clk).
   auto slice = [&](int kt, auto st_c, auto ld_c) {
     constexpr bool ST = decltype(st_c)::value, LD = decltype(ld_c)::value;
     constexpr int NMF = TM * TN;
+    constexpr int NSPREAD = 3;  // steps that carry the next slice's LDS stores
     const int b = kt & 1;
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
@@ -406,9 +410,9 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
       for (int j = 0; j < NMF; ++j) {
         const int a = j / TM, bb = j % TM;
         acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][a], af[cur][bb], acc[a][bb], 0, 0, 0);
-        if (ks == 0 && ST) {
+        if (ks < NSPREAD && ST) {
 #pragma unroll
-          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) {
+          for (int i = (ks * NMF + j) * NL / (NSPREAD * NMF); i < (ks * NMF + j + 1) * NL / (NSPREAD * NMF); ++i) {
             lstore(i, b ^ 1);
             if (LD) gload(i, (kt + 2) * BK);
           }

@@ -304,8 +304,8 @@ __global__ __launch_bounds__(256) void colsum_bf16_kernel(const bf16* __restrict
 // gemm_bf16_big_kernel (gemm.hip): 256 x (64 TN) output tiles, 4 waves of
 // 128 x (32 TN) on one SIMD each with the accumulators in AGPRs, two LDS
 // buffers and one barrier per 64-wide k slice (before its last 16-wide step),
-// the next slice's LDS stores and the loads after it spread over the MFMAs of
-// step 0, each step's fragments read during the previous step's MFMAs.  Tiles
+// the next slice's LDS stores and the loads after them spread over the MFMAs
+// of steps 0-2, each step's fragments read during the previous step's MFMAs.  Tiles
 // hold k rows of the tile's columns as they lie in memory; fragments are read
 // with ds_read_b64_tr_b16 (k order {4g..4g+3, 8+4g..8+4g+3} on both sides).
 constexpr int GB_BM = 256;
@@ -397,6 +397,7 @@ __global__ __launch_bounds__(GNTHR, 1) void gemm_grad_tt_big_kernel(GradArgs p) 
   auto slice = [&](int kt, auto st_c, auto ld_c) {
     constexpr bool ST = decltype(st_c)::value, LD = decltype(ld_c)::value;
     constexpr int NMF = TM * TN;
+    constexpr int NSPREAD = 3;  // steps that carry the next slice's LDS stores
     const int b = kt & 1;
     if (LD) rsrcs(kb + (kt + 2) * GBK);
 #pragma unroll
@@ -413,9 +414,9 @@ __global__ __launch_bounds__(GNTHR, 1) void gemm_grad_tt_big_kernel(GradArgs p) 
       for (int j = 0; j < NMF; ++j) {
         const int a = j / TM, bb = j % TM;
         acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][a], af[cur][bb], acc[a][bb], 0, 0, 0);
-        if (ks == 0 && ST) {
+        if (ks < NSPREAD && ST) {
 #pragma unroll
-          for (int i = j * NL / NMF; i < (j + 1) * NL / NMF; ++i) {
+          for (int i = (ks * NMF + j) * NL / (NSPREAD * NMF); i < (ks * NMF + j + 1) * NL / (NSPREAD * NMF); ++i) {
             lstore(i, b ^ 1);
             if (LD) gload(i);
           }
