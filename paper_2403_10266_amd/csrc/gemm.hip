@@ -443,77 +443,138 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
   }
   slice(kt, no{}, no{});
 
-  // epilogue: lane owns rows m = .. + 32 bb + l32 and, in each, the column
-  // groups n = .. + 32 a + 8 r4 + 4 g + {0..3}
+  // Epilogue (N is a multiple of 8 here).  The accumulators hold, per lane,
+  // rows m = .. + 32 bb + l32 and in each the column groups
+  // n = .. + 32 a + 8 r4 + 4 g + {0..3}: stored from there, one store
+  // instruction would write 16-byte pieces of 32 rows, and the L2 would take
+  // a request per piece.  So the tile goes through LDS (free once every wave
+  // has read its last fragments) and leaves in whole rows: 64 lanes write
+  // consecutive 16-byte chunks of one or two rows.
   constexpr bool BWD = EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD;
-  if ((EPI == DSP_EPI_RESID || EPI == DSP_EPI_GELU || EPI == DSP_EPI_RELU || BWD) && (N & 3) == 0) {
-    // Every global read of the epilogue (bias, residual) is issued before the
-    // first one is used, through buffer resources whose ranges end at the
-    // last valid row and column (reads past them return zero), so the loads
-    // overlap instead of costing one memory round trip per column group.
-    constexpr int NG = TN * 4;
-    int ncol[NG];
+  constexpr bool F32OUT = EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32;
+  constexpr int NG = TN * 4;  // column groups of 4 per lane and row
+  // Bias of each column group, kept as bf16 pairs until used.  Without a
+  // bias the loads read nothing (empty range) and the pairs become -0, the
+  // one addend that leaves every value, -0 included, unchanged: the adds stay
+  // unconditional, with no branch for the accumulators to be copied across.
+  u32x2 braw[NG];
+  {
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(bias, bias ? (uint32_t)N * 2u : 0u);
+    const uint32_t neg0 = bias ? 0u : 0x80008000u;
 #pragma unroll
-    for (int j = 0; j < NG; ++j) ncol[j] = n0 + wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
-    float4 bv[NG];
-    if (bias) {
-      const __amdgpu_buffer_rsrc_t rb = make_rsrc(bias, (uint32_t)N * 2u);
+    for (int j = 0; j < NG; ++j) {
+      const int n = n0 + wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
+      braw[j] = __builtin_amdgcn_raw_buffer_load_b64(rb, n < N ? (uint32_t)n * 2u : 0xFFFFFFF0u, 0, 0);
+      braw[j][0] |= neg0;
+      braw[j][1] |= neg0;
+    }
+  }
+  // a W + bias of accumulator row block bb, column group j
+  auto sum4 = [&](int bb, int j, float v[4]) {
+    const int a = j / 4, r4 = j % 4;
+    v[0] = acc[a][bb][4 * r4 + 0] + __uint_as_float(braw[j][0] << 16);
+    v[1] = acc[a][bb][4 * r4 + 1] + __uint_as_float(braw[j][0] & 0xFFFF0000u);
+    v[2] = acc[a][bb][4 * r4 + 2] + __uint_as_float(braw[j][1] << 16);
+    v[3] = acc[a][bb][4 * r4 + 3] + __uint_as_float(braw[j][1] & 0xFFFF0000u);
+  };
+  // output row of each tile row (the row swap evaluated once per row), at
+  // the end of the LDS buffers, past every staged row
+  uint32_t* orows = reinterpret_cast<uint32_t*>(lds + 2 * STAGE) - BIG_BM;
+  auto put_orow = [&]() {
+    const int m = m0 + (int)threadIdx.x;
+    orows[threadIdx.x] = (uint32_t)rs.map(m < M ? m : 0);
+  };
+  if constexpr (!F32OUT && !BWD && !KEEP) {
+    // bf16 results, activation applied in registers: the whole tile is
+    // staged as bf16 in one pass and leaves in 16-byte chunks of 8 columns
+    constexpr int SP = BNB + 8;  // staged row pitch (bf16): a 16-byte pad
+    static_assert(BIG_BM * SP * 2 + BIG_BM * 4 <= 2 * STAGE * 2, "bf16 staging fits the LDS buffers");
+    constexpr int CPR = BNB / 8;  // chunks per row
+    bf16* st = lds;
+    __syncthreads();
+    put_orow();
+#pragma unroll
+    for (int bb = 0; bb < TM; ++bb)
 #pragma unroll
       for (int j = 0; j < NG; ++j) {
-        const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(rb, ncol[j] < N ? (uint32_t)ncol[j] * 2u : 0xFFFFFFF0u, 0, 0);
-        bv[j] = make_float4(__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xFFFF0000u),
-                            __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xFFFF0000u));
+        float v[4];
+        sum4(bb, j, v);
+        if (EPI == DSP_EPI_GELU) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
+        }
+        if (EPI == DSP_EPI_RELU) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
+        }
+        const int col = wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
+        *reinterpret_cast<uint2*>(st + (wm * TM * 32 + 32 * bb + l32) * SP + col) = pack_bf16x4(v);
       }
+    __syncthreads();
+#pragma unroll 8
+    for (int q = 0; q < CPR; ++q) {
+      const int c = (int)threadIdx.x + NTHR * q;
+      const int tr = c / CPR, cc = c % CPR;
+      const int m = m0 + tr, n = n0 + 8 * cc;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(st + tr * SP + 8 * cc);
+      if (m < M && n < N) *reinterpret_cast<u32x4*>(static_cast<bf16*>(out) + (int64_t)orows[tr] * N + n) = w;
     }
-    // backward epilogues: the saved pre-activation (bf16, in keep_out, at the
-    // output's offsets: no row swap with them)
-    u32x2 uv[BWD ? TM : 1][NG];
-    if constexpr (BWD) {
-      const uint32_t urow = (uint32_t)N * 2u;
-      const __amdgpu_buffer_rsrc_t ru = make_rsrc(keep_out + (int64_t)m0 * N, a_rows * urow);
+  } else {
+    // fp32 staging in NP passes of RPP rows (pass p: rows HR p + [0, HR) of
+    // each wave row half), 16-byte chunks of 4 columns; the residual or saved
+    // pre-activation reads of a pass are issued before its staging.  Four
+    // passes where two would hold more of those reads than the registers do.
+    constexpr int NP = (TN == 4 && (EPI == DSP_EPI_RESID || BWD)) ? 4 : 2;
+    constexpr int RPP = BIG_BM / NP, HR = RPP / 2, BPP = TM / NP;
+    constexpr int SPF = BNB + 4;  // staged row pitch (fp32): a 16-byte pad
+    static_assert(RPP * SPF * 4 + BIG_BM * 4 <= 2 * STAGE * 2, "fp32 staging fits the LDS buffers");
+    constexpr int CPR = BNB / 4;
+    constexpr int PER = RPP * CPR / NTHR;  // chunks per thread and pass
+    float* sf = reinterpret_cast<float*>(lds);
+    const uint32_t rrow = (uint32_t)N * 4u, urow = (uint32_t)N * 2u;
+    __amdgpu_buffer_rsrc_t rr, ru;
+    if constexpr (EPI == DSP_EPI_RESID) rr = make_rsrc(resid + (int64_t)m0 * N, a_rows * rrow);
+    if constexpr (BWD) ru = make_rsrc(keep_out + (int64_t)m0 * N, a_rows * urow);
 #pragma unroll
-      for (int bb = 0; bb < TM; ++bb)
+    for (int p = 0; p < NP; ++p) {
+      u32x4 rv[EPI == DSP_EPI_RESID ? PER : 1];
+      u32x2 uv[BWD ? PER : 1];
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int c = (int)threadIdx.x + NTHR * q;
+        const int sr = c / CPR, cc = c % CPR;
+        const uint32_t tr = (uint32_t)((sr / HR) * 128 + HR * p + sr % HR);
+        const int n = n0 + 4 * cc;
+        if constexpr (EPI == DSP_EPI_RESID)
+          rv[q] = __builtin_amdgcn_raw_buffer_load_b128(rr, n < N ? tr * rrow + (uint32_t)n * 4u : 0xFFFFFFF0u, 0, 0);
+        if constexpr (BWD)
+          uv[q] = __builtin_amdgcn_raw_buffer_load_b64(ru, n < N ? tr * urow + (uint32_t)n * 2u : 0xFFFFFFF0u, 0, 0);
+      }
+      __syncthreads();  // p = 0: last fragments read; p > 0: the previous pass's rows read
+      if (p == 0) put_orow();
+#pragma unroll
+      for (int h = 0; h < BPP; ++h)
 #pragma unroll
         for (int j = 0; j < NG; ++j) {
-          const uint32_t r = (uint32_t)(wm * TM * 32 + 32 * bb + l32);
-          uv[bb][j] = __builtin_amdgcn_raw_buffer_load_b64(
-              ru, ncol[j] < N ? r * urow + (uint32_t)ncol[j] * 2u : 0xFFFFFFF0u, 0, 0);
+          float v[4];
+          sum4(BPP * p + h, j, v);
+          const int col = wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
+          *reinterpret_cast<float4*>(sf + (wm * HR + 32 * h + l32) * SPF + col) = make_float4(v[0], v[1], v[2], v[3]);
         }
-    }
-    u32x4 rv[EPI == DSP_EPI_RESID ? TM : 1][NG];
-    if constexpr (EPI == DSP_EPI_RESID) {
-      const uint32_t rrow = (uint32_t)N * 4u;
-      const __amdgpu_buffer_rsrc_t rr = make_rsrc(resid + (int64_t)m0 * N, a_rows * rrow);
+      __syncthreads();
 #pragma unroll
-      for (int bb = 0; bb < TM; ++bb)
-#pragma unroll
-        for (int j = 0; j < NG; ++j) {
-          const uint32_t r = (uint32_t)(wm * TM * 32 + 32 * bb + l32);
-          rv[bb][j] = __builtin_amdgcn_raw_buffer_load_b128(
-              rr, ncol[j] < N ? r * rrow + (uint32_t)ncol[j] * 4u : 0xFFFFFFF0u, 0, 0);
-        }
-    }
-#pragma unroll
-    for (int bb = 0; bb < TM; ++bb) {
-      const int m = m0 + wm * TM * 32 + 32 * bb + l32;
-      if (m >= M) continue;
-      const int64_t orow = rs.map(m) * N;
-#pragma unroll
-      for (int j = 0; j < NG; ++j) {
-        const int n = ncol[j];
-        if (n >= N) continue;
-        const int a = j / 4, r4 = j % 4;
-        float v[4] = {acc[a][bb][4 * r4 + 0], acc[a][bb][4 * r4 + 1], acc[a][bb][4 * r4 + 2],
-                      acc[a][bb][4 * r4 + 3]};
-        if (bias) {
-          v[0] += bv[j].x;
-          v[1] += bv[j].y;
-          v[2] += bv[j].z;
-          v[3] += bv[j].w;
-        }
+      for (int q = 0; q < PER; ++q) {
+        const int c = (int)threadIdx.x + NTHR * q;
+        const int sr = c / CPR, cc = c % CPR;
+        const int tr = (sr / HR) * 128 + HR * p + sr % HR;
+        const int m = m0 + tr, n = n0 + 4 * cc;
+        const float4 s4 = *reinterpret_cast<const float4*>(sf + sr * SPF + 4 * cc);
+        if (m >= M || n >= N) continue;
+        float v[4] = {s4.x, s4.y, s4.z, s4.w};
+        const int64_t orow = (int64_t)orows[tr] * N;
         if (KEEP) *reinterpret_cast<uint2*>(keep_out + orow + n) = pack_bf16x4(v);
         if constexpr (BWD) {
-          const uint32_t w0 = uv[bb][j][0], w1 = uv[bb][j][1];
+          const uint32_t w0 = uv[q][0], w1 = uv[q][1];
           v[0] *= act_grad<EPI>(__uint_as_float(w0 << 16));
           v[1] *= act_grad<EPI>(__uint_as_float(w0 & 0xFFFF0000u));
           v[2] *= act_grad<EPI>(__uint_as_float(w1 << 16));
@@ -529,31 +590,14 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
         }
         if constexpr (EPI == DSP_EPI_RESID) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] += __uint_as_float(rv[bb][j][i]);
+          for (int i = 0; i < 4; ++i) v[i] += __uint_as_float(rv[q][i]);
         }
-        if (EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32)
+        if (F32OUT)
           *reinterpret_cast<float4*>(static_cast<float*>(out) + orow + n) = make_float4(v[0], v[1], v[2], v[3]);
         else
           *reinterpret_cast<uint2*>(static_cast<bf16*>(out) + orow + n) = pack_bf16x4(v);
       }
     }
-    return;
-  }
-#pragma unroll
-  for (int bb = 0; bb < TM; ++bb) {
-    const int m = m0 + wm * TM * 32 + 32 * bb + l32;
-    if (m >= M) continue;
-#pragma unroll
-    for (int a = 0; a < TN; ++a)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int n = n0 + wn * TN * 32 + 32 * a + 8 * r4 + 4 * g;
-        if (n >= N) continue;
-        float v[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = acc[a][bb][4 * r4 + i];
-        epilogue4<EPI, KEEP>(v, m, rs.map(m), n, N, bias, resid, out, keep_out);
-      }
   }
 }
 
@@ -656,7 +700,7 @@ int launch_transpose_bf16(const void* x, void* y, int64_t rows, int64_t cols, hi
 bool linear_bf16_large_tiles(int64_t M, int N) {
   const int big_bn = N >= 2048 ? 256 : 192;
   const int64_t big_tiles = ((M + BIG_BM - 1) / BIG_BM) * ((N + big_bn - 1) / big_bn);
-  return DSP_GEMM_BIG && big_tiles >= 256 && (int64_t)BIG_BM * N * 4 < (int64_t(1) << 31);
+  return DSP_GEMM_BIG && big_tiles >= 256 && N % 8 == 0 && (int64_t)BIG_BM * N * 4 < (int64_t(1) << 31);
 }
 
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,

@@ -58,7 +58,7 @@ def test_linear_bf16(torch, M, N, K, epi, bias):
 
 # Problems of at least 256 output tiles of 256 x 192 (N < 2048) or 256 x 256
 # run the large-tile kernel: ragged M, N and K (a partial last 64-wide slice).
-LARGE = [(16421, 1000, 1176), (8292, 2056, 136)]
+LARGE = [(16421, 1000, 1176), (8292, 2056, 136), (8292, 1004, 136)]
 
 
 @pytest.mark.parametrize("M,N,K", LARGE)
