@@ -63,22 +63,25 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 // 1 - (a1 t + ... + a5 t^5) exp(-z^2) with t = 1 / (1 + p |z|), |error| <=
 // 1.5e-7 -- far below the bf16 rounding of the GEMM output, and a reciprocal,
 // an exp2 and five FMAs instead of a general erf.
-__device__ __forceinline__ float erf_as7126(float z) {
-  const float a = fabsf(z);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
-  float poly = fmaf(1.061405429f, t, -1.453152027f);
-  poly = fmaf(poly, t, 1.421413741f);
-  poly = fmaf(poly, t, -0.284496736f);
-  poly = fmaf(poly, t, 0.254829592f);
-  poly *= t;
-  // exp(-a^2) = exp2(-a^2 log2 e); the raw exp2 flushes tiny results to 0
-  const float e = __builtin_amdgcn_exp2f(-a * a * 1.4426950408889634f);
-  return copysignf(1.0f - poly * e, z);
-}
+constexpr float AS_P = 0.3275911f, AS_A1 = 0.254829592f, AS_A2 = -0.284496736f, AS_A3 = 1.421413741f,
+                AS_A4 = -1.453152027f, AS_A5 = 1.061405429f;
 
-// GELU x * Phi(x) for the bf16 path (output rounded to bf16)
+// GELU x Phi(x) for the bf16 path (output rounded to bf16).  Phi(x) is
+// 1 - erfc(|x| / sqrt 2) / 2 for x >= 0 and erfc(|x| / sqrt 2) / 2 for x < 0, so
+// x Phi(x) = max(x, 0) - |x| erfc(|x| / sqrt 2) / 2, with erfc(a) = 1 - erf(a)
+// from 7.1.26 above.  The 1 / sqrt 2 of the argument and the 1 / 2 are folded
+// into the constants, and the negative tail keeps its relative accuracy (no
+// 1 + erf cancellation).
 __device__ __forceinline__ float gelu_bf16out(float v) {
-  return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f));
+  const float av = fabsf(v);
+  const float t = __builtin_amdgcn_rcpf(fmaf(AS_P * 0.70710678118654752f, av, 1.0f));
+  float poly = fmaf(0.5f * AS_A5, t, 0.5f * AS_A4);
+  poly = fmaf(poly, t, 0.5f * AS_A3);
+  poly = fmaf(poly, t, 0.5f * AS_A2);
+  poly = fmaf(poly, t, 0.5f * AS_A1);
+  // exp(-x^2 / 2) = exp2(-x^2 log2(e) / 2); the raw exp2 flushes tiny results to 0
+  const float e = __builtin_amdgcn_exp2f(av * (av * (-0.5f * 1.4426950408889634f)));
+  return fmaf(-(av * t) * poly, e, fmaxf(v, 0.0f));
 }
 
 // its derivative Phi(u) + u phi(u), for the backward epilogue.  The
@@ -86,11 +89,11 @@ __device__ __forceinline__ float gelu_bf16out(float v) {
 // phi(u), so one exponential serves both terms.
 __device__ __forceinline__ float gelu_grad_bf16(float u) {
   const float z = u * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, fabsf(z), 1.0f));
-  float poly = fmaf(1.061405429f, t, -1.453152027f);
-  poly = fmaf(poly, t, 1.421413741f);
-  poly = fmaf(poly, t, -0.284496736f);
-  poly = fmaf(poly, t, 0.254829592f);
+  const float t = __builtin_amdgcn_rcpf(fmaf(AS_P, fabsf(z), 1.0f));
+  float poly = fmaf(AS_A5, t, AS_A4);
+  poly = fmaf(poly, t, AS_A3);
+  poly = fmaf(poly, t, AS_A2);
+  poly = fmaf(poly, t, AS_A1);
   poly *= t;
   const float e = __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);
   const float erf = copysignf(1.0f - poly * e, z);
@@ -441,6 +444,41 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
     slice(kt, yes{}, no{});
     ++kt;
   }
+  // Epilogue layout of the fp32-staged results (fp32 output, backward
+  // epilogues, pre-activation copy): NP passes of RPP rows (pass p: rows
+  // HR p + [0, HR) of each wave row half), 16-byte chunks of 4 columns, PER
+  // chunks per thread and pass.  Four passes where two would hold more
+  // residual or pre-activation reads than the registers do.
+  constexpr bool BWD = EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD;
+  constexpr bool F32OUT = EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32;
+  constexpr int NP = (TN == 4 && (EPI == DSP_EPI_RESID || BWD)) ? 4 : 2;
+  constexpr int RPP = BIG_BM / NP, HR = RPP / 2, BPP = TM / NP;
+  constexpr int CPR4 = BNB / 4;
+  constexpr int PER = RPP * CPR4 / NTHR;
+  const uint32_t rrow = (uint32_t)N * 4u, urow = (uint32_t)N * 2u;
+  __amdgpu_buffer_rsrc_t rr, ru;
+  if constexpr (EPI == DSP_EPI_RESID) rr = make_rsrc(resid + (int64_t)m0 * N, a_rows * rrow);
+  if constexpr (BWD) ru = make_rsrc(keep_out + (int64_t)m0 * N, a_rows * urow);
+  constexpr int NRV = EPI == DSP_EPI_RESID ? PER : 1, NUV = BWD ? PER : 1;
+  // the residual or saved pre-activation chunks of pass p
+  auto side_loads = [&](int p, u32x4 (&rv)[NRV], u32x2 (&uv)[NUV]) {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int c = (int)threadIdx.x + NTHR * q;
+      const int sr = c / CPR4, cc = c % CPR4;
+      const uint32_t tr = (uint32_t)((sr / HR) * 128 + HR * p + sr % HR);
+      const int n = n0 + 4 * cc;
+      if constexpr (EPI == DSP_EPI_RESID)
+        rv[q] = __builtin_amdgcn_raw_buffer_load_b128(rr, n < N ? tr * rrow + (uint32_t)n * 4u : 0xFFFFFFF0u, 0, 0);
+      if constexpr (BWD)
+        uv[q] = __builtin_amdgcn_raw_buffer_load_b64(ru, n < N ? tr * urow + (uint32_t)n * 2u : 0xFFFFFFF0u, 0, 0);
+    }
+  };
+  // the first pass's reads go out before the last slice, whose MFMAs then
+  // hide their latency
+  u32x4 rv0[NRV];
+  u32x2 uv0[NUV];
+  if constexpr (EPI == DSP_EPI_RESID || BWD) side_loads(0, rv0, uv0);
   slice(kt, no{}, no{});
 
   // Epilogue (N is a multiple of 8 here).  The accumulators hold, per lane,
@@ -450,8 +488,6 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
   // a request per piece.  So the tile goes through LDS (free once every wave
   // has read its last fragments) and leaves in whole rows: 64 lanes write
   // consecutive 16-byte chunks of one or two rows.
-  constexpr bool BWD = EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD;
-  constexpr bool F32OUT = EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32;
   constexpr int NG = TN * 4;  // column groups of 4 per lane and row
   // Bias of each column group, kept as bf16 pairs until used.  Without a
   // bias the loads read nothing (empty range) and the pairs become -0, the
@@ -485,8 +521,11 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
     orows[threadIdx.x] = (uint32_t)rs.map(m < M ? m : 0);
   };
   if constexpr (!F32OUT && !BWD && !KEEP) {
-    // bf16 results, activation applied in registers: the whole tile is
-    // staged as bf16 in one pass and leaves in 16-byte chunks of 8 columns
+    // bf16 results, activation applied in registers, staged as bf16 and
+    // stored in 16-byte chunks of 8 columns.  Two halves (accumulator row
+    // blocks 0-1, then 2-3, i.e. tile rows 64 h + [0, 64) of each wave row
+    // half): the first half's stores are in flight while the second half's
+    // activation is computed.
     constexpr int SP = BNB + 8;  // staged row pitch (bf16): a 16-byte pad
     static_assert(BIG_BM * SP * 2 + BIG_BM * 4 <= 2 * STAGE * 2, "bf16 staging fits the LDS buffers");
     constexpr int CPR = BNB / 8;  // chunks per row
@@ -494,61 +533,52 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
     __syncthreads();
     put_orow();
 #pragma unroll
-    for (int bb = 0; bb < TM; ++bb)
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
-      for (int j = 0; j < NG; ++j) {
-        float v[4];
-        sum4(bb, j, v);
-        if (EPI == DSP_EPI_GELU) {
+      for (int bb = 2 * h; bb < 2 * h + 2; ++bb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
+        for (int j = 0; j < NG; ++j) {
+          float v[4];
+          sum4(bb, j, v);
+          if (EPI == DSP_EPI_GELU) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
+          }
+          if (EPI == DSP_EPI_RELU) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
+          }
+          const int col = wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
+          *reinterpret_cast<uint2*>(st + (wm * TM * 32 + 32 * bb + l32) * SP + col) = pack_bf16x4(v);
         }
-        if (EPI == DSP_EPI_RELU) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
-        }
-        const int col = wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
-        *reinterpret_cast<uint2*>(st + (wm * TM * 32 + 32 * bb + l32) * SP + col) = pack_bf16x4(v);
-      }
-    __syncthreads();
-#pragma unroll 8
-    for (int q = 0; q < CPR; ++q) {
-      const int c = (int)threadIdx.x + NTHR * q;
-      const int tr = c / CPR, cc = c % CPR;
-      const int m = m0 + tr, n = n0 + 8 * cc;
-      const u32x4 w = *reinterpret_cast<const u32x4*>(st + tr * SP + 8 * cc);
-      if (m < M && n < N) *reinterpret_cast<u32x4*>(static_cast<bf16*>(out) + (int64_t)orows[tr] * N + n) = w;
-    }
-  } else {
-    // fp32 staging in NP passes of RPP rows (pass p: rows HR p + [0, HR) of
-    // each wave row half), 16-byte chunks of 4 columns; the residual or saved
-    // pre-activation reads of a pass are issued before its staging.  Four
-    // passes where two would hold more of those reads than the registers do.
-    constexpr int NP = (TN == 4 && (EPI == DSP_EPI_RESID || BWD)) ? 4 : 2;
-    constexpr int RPP = BIG_BM / NP, HR = RPP / 2, BPP = TM / NP;
-    constexpr int SPF = BNB + 4;  // staged row pitch (fp32): a 16-byte pad
-    static_assert(RPP * SPF * 4 + BIG_BM * 4 <= 2 * STAGE * 2, "fp32 staging fits the LDS buffers");
-    constexpr int CPR = BNB / 4;
-    constexpr int PER = RPP * CPR / NTHR;  // chunks per thread and pass
-    float* sf = reinterpret_cast<float*>(lds);
-    const uint32_t rrow = (uint32_t)N * 4u, urow = (uint32_t)N * 2u;
-    __amdgpu_buffer_rsrc_t rr, ru;
-    if constexpr (EPI == DSP_EPI_RESID) rr = make_rsrc(resid + (int64_t)m0 * N, a_rows * rrow);
-    if constexpr (BWD) ru = make_rsrc(keep_out + (int64_t)m0 * N, a_rows * urow);
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      u32x4 rv[EPI == DSP_EPI_RESID ? PER : 1];
-      u32x2 uv[BWD ? PER : 1];
-#pragma unroll
-      for (int q = 0; q < PER; ++q) {
+      __syncthreads();
+#pragma unroll 4
+      for (int q = 0; q < CPR / 2; ++q) {
         const int c = (int)threadIdx.x + NTHR * q;
         const int sr = c / CPR, cc = c % CPR;
-        const uint32_t tr = (uint32_t)((sr / HR) * 128 + HR * p + sr % HR);
-        const int n = n0 + 4 * cc;
-        if constexpr (EPI == DSP_EPI_RESID)
-          rv[q] = __builtin_amdgcn_raw_buffer_load_b128(rr, n < N ? tr * rrow + (uint32_t)n * 4u : 0xFFFFFFF0u, 0, 0);
-        if constexpr (BWD)
-          uv[q] = __builtin_amdgcn_raw_buffer_load_b64(ru, n < N ? tr * urow + (uint32_t)n * 2u : 0xFFFFFFF0u, 0, 0);
+        const int tr = (sr / 64) * 128 + 64 * h + sr % 64;
+        const int m = m0 + tr, n = n0 + 8 * cc;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(st + tr * SP + 8 * cc);
+        if (m < M && n < N) *reinterpret_cast<u32x4*>(static_cast<bf16*>(out) + (int64_t)orows[tr] * N + n) = w;
+      }
+    }
+  } else {
+    // fp32 staging: the reads of pass p > 0 are issued before its staging
+    constexpr int SPF = BNB + 4;  // staged row pitch (fp32): a 16-byte pad
+    static_assert(RPP * SPF * 4 + BIG_BM * 4 <= 2 * STAGE * 2, "fp32 staging fits the LDS buffers");
+    constexpr int CPR = CPR4;
+    float* sf = reinterpret_cast<float*>(lds);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      u32x4 rv[NRV];
+      u32x2 uv[NUV];
+      if (p == 0) {
+#pragma unroll
+        for (int q = 0; q < NRV; ++q) rv[q] = rv0[q];
+#pragma unroll
+        for (int q = 0; q < NUV; ++q) uv[q] = uv0[q];
+      } else if constexpr (EPI == DSP_EPI_RESID || BWD) {
+        side_loads(p, rv, uv);
       }
       __syncthreads();  // p = 0: last fragments read; p > 0: the previous pass's rows read
       if (p == 0) put_orow();
