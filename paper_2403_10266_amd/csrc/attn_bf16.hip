@@ -620,6 +620,13 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
 
   // ---- normalise and store: lane (n + 32g) holds O^T[32t + 8(r/4) + 4g + r%4][q]
   bf16* og = p.o + um.out_base;
+  // staged output row pitch (elements): padded so that the rows of 16
+  // consecutive queries start on distinct banks for the 8-byte staging writes,
+  // where the padded rows fit the tile buffers
+  constexpr int SOP_PAD = (D % 16 == 8) ? D : D + 8;
+  constexpr int SOP = NW * 32 * SOP_PAD <= NBUF * G::TILE_ELEMS ? SOP_PAD : D;
+  static_assert(NW * 32 * SOP <= NBUF * G::TILE_ELEMS, "the output staging fits the LDS tile buffers");
+  __syncthreads();  // every wave is done with the K and V tiles
 #pragma unroll
   for (int j = 0; j < QT; ++j) {
     float l;
@@ -646,6 +653,14 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
       const uint32_t q = q_wave + 32 * j + l32;
       if (q < L) p.lse[(int64_t)um.unit * L + q] = 0.6931471805599453f * (b_ref[j] + log2f(l));
     }
+    // The output rows leave through LDS: this wave's 32 rows of query tile j
+    // are staged (bf16, row pitch SOP) in its own LDS region and stored as
+    // whole 16-byte chunks, CH consecutive lanes per row.  From the
+    // accumulator layout a store instruction would write 8-byte pieces of 32
+    // rows, one L2 request each.  Only this wave touches its region, and one
+    // wave's LDS accesses complete in order, so no barrier is needed between
+    // the staging and the reads.
+    bf16* so = lds + wave * 32 * SOP;
     if constexpr (SLAB) {
       // slab rows d < D: lanes 0-31 hold d = 32 NT32 + 4 (lane / 16) + r for
       // query 16 h + lane % 16; their row sum is that query's
@@ -653,35 +668,40 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const float inv_h = __shfl(inv, 16 * h + sl);
-        const uint32_t qs = q_wave + 32 * j + 16 * h + sl;
-        if (lane < 32 && qs < L) {
+        if (lane < 32) {
           const int d0 = 32 * NT32 + 4 * (lane >> 4);
           bf16x2 lo = {(bf16)(os[j][h][0] * inv_h), (bf16)(os[j][h][1] * inv_h)};
           bf16x2 hi = {(bf16)(os[j][h][2] * inv_h), (bf16)(os[j][h][3] * inv_h)};
           uint2 w;
           w.x = __builtin_bit_cast(uint32_t, lo);
           w.y = __builtin_bit_cast(uint32_t, hi);
-          *reinterpret_cast<uint2*>(og + (int64_t)qs * p.r_out + d0) = w;
+          *reinterpret_cast<uint2*>(so + (16 * h + sl) * SOP + d0) = w;
         }
       }
     }
-    const uint32_t q = q_wave + 32 * j + l32;
-    if (q < L) {
-      bf16* orow = og + (int64_t)q * p.r_out;
 #pragma unroll
-      for (int t = 0; t < NT32; ++t)
+    for (int t = 0; t < NT32; ++t)
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          const int d0 = 32 * t + 8 * r4 + 4 * g;
-          if (d0 < D) {
-            bf16x2 lo = {(bf16)(o[t][j][4 * r4 + 0] * inv), (bf16)(o[t][j][4 * r4 + 1] * inv)};
-            bf16x2 hi = {(bf16)(o[t][j][4 * r4 + 2] * inv), (bf16)(o[t][j][4 * r4 + 3] * inv)};
-            uint2 w;
-            w.x = __builtin_bit_cast(uint32_t, lo);
-            w.y = __builtin_bit_cast(uint32_t, hi);
-            *reinterpret_cast<uint2*>(orow + d0) = w;
-          }
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int d0 = 32 * t + 8 * r4 + 4 * g;
+        if (d0 < D) {
+          bf16x2 lo = {(bf16)(o[t][j][4 * r4 + 0] * inv), (bf16)(o[t][j][4 * r4 + 1] * inv)};
+          bf16x2 hi = {(bf16)(o[t][j][4 * r4 + 2] * inv), (bf16)(o[t][j][4 * r4 + 3] * inv)};
+          uint2 w;
+          w.x = __builtin_bit_cast(uint32_t, lo);
+          w.y = __builtin_bit_cast(uint32_t, hi);
+          *reinterpret_cast<uint2*>(so + l32 * SOP + d0) = w;
         }
+      }
+    constexpr int OCH = 32 * G::CH;  // 16-byte chunks of the 32 rows
+#pragma unroll
+    for (int i = 0; i < (OCH + 63) / 64; ++i) {
+      const int c = lane + 64 * i;
+      const int row = c / G::CH, col = c - row * G::CH;
+      const uint32_t q = q_wave + 32 * j + row;
+      if (c < OCH && q < L)
+        *reinterpret_cast<u32x4*>(og + (int64_t)q * p.r_out + col * 8) =
+            *reinterpret_cast<const u32x4*>(so + row * SOP + col * 8);
     }
   }
 }
