@@ -219,6 +219,65 @@ __device__ __forceinline__ void store_rows(bf16* base, int64_t r_st, uint32_t ro
   }
 }
 
+// store_rows through LDS: the wave's 32 rows are staged (bf16, row pitch SP)
+// in `so`, a region only this wave touches, and leave as whole 16-byte
+// chunks, D / 8 consecutive lanes per row.  From the accumulator layout a
+// store instruction would write 8-byte pieces of 32 rows, one L2 request
+// each.  One wave's LDS accesses complete in order, so no barrier separates
+// the staging from the reads.
+template <int D, int SP>
+__device__ __forceinline__ void store_rows_lds(bf16* so, bf16* base, int64_t r_st, uint32_t row0, uint32_t L,
+                                               int lane,
+                                               const floatx16 (&t32)[BGeo<D>::NT32 > 0 ? BGeo<D>::NT32 : 1],
+                                               const floatx4 (&sl)[2], float mul) {
+  using G = BGeo<D>;
+  static_assert(D % 8 == 0, "rows leave in 16-byte chunks");
+  const int l32 = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int d0 = 32 * t + 8 * r4 + 4 * g;
+      bf16x2 lo = {(bf16)(t32[t][4 * r4 + 0] * mul), (bf16)(t32[t][4 * r4 + 1] * mul)};
+      bf16x2 hi = {(bf16)(t32[t][4 * r4 + 2] * mul), (bf16)(t32[t][4 * r4 + 3] * mul)};
+      uint2 w;
+      w.x = __builtin_bit_cast(uint32_t, lo);
+      w.y = __builtin_bit_cast(uint32_t, hi);
+      *reinterpret_cast<uint2*>(so + l32 * SP + d0) = w;
+    }
+  if constexpr (G::SLAB) {
+    const int d0 = 32 * G::NT32 + 4 * (lane >> 4);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (d0 < D) {
+        bf16x2 lo = {(bf16)(sl[h][0] * mul), (bf16)(sl[h][1] * mul)};
+        bf16x2 hi = {(bf16)(sl[h][2] * mul), (bf16)(sl[h][3] * mul)};
+        uint2 w;
+        w.x = __builtin_bit_cast(uint32_t, lo);
+        w.y = __builtin_bit_cast(uint32_t, hi);
+        *reinterpret_cast<uint2*>(so + (16 * h + (lane & 15)) * SP + d0) = w;
+      }
+    }
+  }
+  constexpr int CH = D / 8, OCH = 32 * CH;
+#pragma unroll
+  for (int i = 0; i < (OCH + 63) / 64; ++i) {
+    const int c = lane + 64 * i;
+    const int row = c / CH, col = c - row * CH;
+    if (c < OCH && row0 + (uint32_t)row < L)
+      *reinterpret_cast<u32x4*>(base + (int64_t)(row0 + row) * r_st + col * 8) =
+          *reinterpret_cast<const u32x4*>(so + row * SP + col * 8);
+  }
+}
+
+// staged output row pitch (elements) for NW waves within `elems` of LDS:
+// padded so that the rows of 16 consecutive lanes start on distinct banks,
+// where the padded rows fit
+template <int D, int NW>
+constexpr int staged_pitch(int elems) {
+  return NW * 32 * ((D % 16 == 8) ? D : D + 8) <= elems ? ((D % 16 == 8) ? D : D + 8) : D;
+}
+
 // ---------------------------------------------------------------------------
 // dQ (and Delta): a work-group owns 32 NW queries of one unit and loops over
 // the unit's keys in LDS tiles of 64 (K and V, double-buffered, the next tile
@@ -377,7 +436,10 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
     if (more) stash((it + 1) & 1);
     __syncthreads();
   }
-  store_rows<D>(p.dq + q_base, p.r_q, um.blk * 32 * NW + 32 * wave, L, lane, dqt, dqs, p.scale);
+  constexpr int SP = staged_pitch<D, NW>(2 * TILE);
+  static_assert(NW * 32 * SP <= 2 * TILE, "the output staging fits the LDS tiles");
+  store_rows_lds<D, SP>(lds + wave * 32 * SP, p.dq + q_base, p.r_q, um.blk * 32 * NW + 32 * wave, L, lane, dqt,
+                        dqs, p.scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -552,8 +614,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
     __syncthreads();
   }
   // dK = scale * dZ^T Q = ln 2 * dZ^T Q'
-  store_rows<D>(p.dv + kv_base, p.r_kv, key0, Lk, lane, dvt, dvs, 1.0f);
-  store_rows<D>(p.dk + kv_base, p.r_kv, key0, Lk, lane, dkt, dks, kLn2);
+  constexpr int SP = staged_pitch<D, NW>(2 * TILE);
+  static_assert(NW * 32 * SP <= 2 * TILE, "the output staging fits the LDS tiles");
+  bf16* so = lds + wave * 32 * SP;
+  store_rows_lds<D, SP>(so, p.dv + kv_base, p.r_kv, key0, Lk, lane, dvt, dvs, 1.0f);
+  store_rows_lds<D, SP>(so, p.dk + kv_base, p.r_kv, key0, Lk, lane, dkt, dks, kLn2);
 }
 
 // ---------------------------------------------------------------------------
