@@ -630,7 +630,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dkv_kernel(BwdParams p) {
 // -lse2 and -Delta on rows below L, 0 past it).  Then, from LDS only, wave w
 // runs the dQ loop for queries 32w .. 32w + 31 over all keys, and the dK/dV
 // loop for keys 32w .. 32w + 31 over all queries (see the wave roles below).  The scores are computed
-// twice, as in the two-kernel path, but the unit's rows cross HBM once.
+// twice, as in the two-kernel path, but the unit's rows cross HBM once.  The
+// grid is persistent: while a unit is computed from LDS, the next unit's rows
+// are already in flight in registers.
 // 2 NW waves: waves [0, NW) run the dQ loops, waves [NW, 2 NW) the dK/dV loops.
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 128, 1) void attn_bwd_short_kernel(BwdParams p) {
@@ -649,37 +651,28 @@ __global__ __launch_bounds__(NW * 128, 1) void attn_bwd_short_kernel(BwdParams p
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, g = lane >> 5;
-  const uint32_t unit = blockIdx.x;  // (b, x, h): query head = key/value head
-  const uint32_t head = unit % p.H, bx = unit / p.H;
   const uint32_t L = p.L, Lk = p.Lk;
-  const int64_t q_base = bx_base(p, bx, p.b_q, p.x_q) + (int64_t)head * D;
-  const int64_t o_base = bx_base(p, bx, p.b_o, p.x_o) + (int64_t)head * D;
-  const int64_t kv_base = bx_base(p, bx, p.b_kv, p.x_kv) + (int64_t)head * D;
 
-  // ---- rows into LDS: chunk c = row c / CH, 16 bytes at column 8 (c % CH);
-  // rows past L (Lk) fall outside the buffer ranges and read as zero
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + q_base, L * (uint32_t)p.r_q * 2u);
-  const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.dout + o_base, L * (uint32_t)p.r_o * 2u);
-  const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + o_base, L * (uint32_t)p.r_o * 2u);
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + kv_base, Lk * (uint32_t)p.r_kv * 2u);
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + kv_base, Lk * (uint32_t)p.r_kv * 2u);
-  u32x4 cq[NLOAD], cd[NLOAD], co[NLOAD], ck[NLOAD], cv[NLOAD];
-#pragma unroll
-  for (int i = 0; i < NLOAD; ++i) {
-    const int c = threadIdx.x + i * NT;
-    if (c < NCH) {
-      const uint32_t row = c / G::CH, col = c - row * G::CH;
-      const uint32_t oq = row * (uint32_t)p.r_q * 2u + col * 16u;
-      const uint32_t oo = row * (uint32_t)p.r_o * 2u + col * 16u;
-      const uint32_t okv = row * (uint32_t)p.r_kv * 2u + col * 16u;
-      cq[i] = __builtin_amdgcn_raw_buffer_load_b128(rq, oq, 0, 0);
-      cd[i] = __builtin_amdgcn_raw_buffer_load_b128(rd, oo, 0, 0);
-      co[i] = __builtin_amdgcn_raw_buffer_load_b128(ro, oo, 0, 0);
-      ck[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, okv, 0, 0);
-      cv[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, okv, 0, 0);
-    }
+  // Persistent: this work-group's units are 8 contiguous ranges, one per XCD
+  // (work-group i runs on XCD i % 8), the work-groups of an XCD interleaved
+  // over its range, so neighbouring heads of a token row share an L2.  While
+  // one unit is computed from LDS, the next unit's rows are in flight in
+  // registers.
+  const uint32_t nb = gridDim.x, n_units = p.n_blocks;
+  uint32_t u, u_end, u_step;
+  if ((nb & 7u) == 0) {
+    const uint32_t xcd = blockIdx.x & 7u;
+    u = (uint32_t)(((uint64_t)n_units * xcd) >> 3) + (blockIdx.x >> 3);
+    u_end = (uint32_t)(((uint64_t)n_units * (xcd + 1)) >> 3);
+    u_step = nb >> 3;
+  } else {
+    u = blockIdx.x;
+    u_end = n_units;
+    u_step = nb;
   }
-  // padding columns (the bias terms of Q' and dO are written below)
+
+  // padding columns, the same for every unit (the bias terms of Q' and dO are
+  // written per unit): K, V columns D .. D + 2 are 1.0 on rows below Lk
   for (int r = threadIdx.x; r < R; r += NT) {
     const bf16 kb = (bf16)((uint32_t)r < Lk ? 1.0f : 0.0f);
     ks[r * G::P + D] = ks[r * G::P + D + 1] = ks[r * G::P + D + 2] = kb;
@@ -687,156 +680,196 @@ __global__ __launch_bounds__(NW * 128, 1) void attn_bwd_short_kernel(BwdParams p
     for (int c = D + 3; c < G::P; ++c)
       qs[r * G::P + c] = os[r * G::P + c] = ks[r * G::P + c] = vs[r * G::P + c] = (bf16)0.0f;
   }
-#pragma unroll
-  for (int i = 0; i < NLOAD; ++i) {
-    const int c = threadIdx.x + i * NT;
-    if (c < NCH) {
-      const int row = c / G::CH, col = c - row * G::CH;
-      const int off = row * G::P + col * 8;
-      bf16x8 x = __builtin_bit_cast(bf16x8, cq[i]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = (bf16)((float)x[e] * p.c);  // Q' as in the forward
-      *reinterpret_cast<bf16x8*>(qs + off) = x;
-      *reinterpret_cast<u32x4*>(os + off) = cd[i];
-      *reinterpret_cast<u32x4*>(ks + off) = ck[i];
-      *reinterpret_cast<u32x4*>(vs + off) = cv[i];
-      const bf16x8 dv8 = __builtin_bit_cast(bf16x8, cd[i]), ov8 = __builtin_bit_cast(bf16x8, co[i]);
-      float d = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) d += (float)dv8[e] * (float)ov8[e];
-      dpart[c] = d;
-    }
-  }
-  __syncthreads();
-  // Delta = rowsum(dO * O) and the bias terms: -(lse * log2 e) on Q', -Delta on dO
-  for (int r = threadIdx.x; r < R; r += NT) {
-    float delta = 0.0f, lse2 = 0.0f;
-    if ((uint32_t)r < L) {
-#pragma unroll
-      for (int col = 0; col < G::CH; ++col) delta += dpart[r * G::CH + col];
-      lse2 = p.lse[(int64_t)unit * L + r] * kLog2e;
-      p.delta[(int64_t)unit * L + r] = delta;
-    }
-    const Bf16x3 nl = neg_split3(lse2), nd = neg_split3(delta);
-#pragma unroll
-    for (int e = 0; e < 3; ++e) {
-      qs[r * G::P + D + e] = nl.t[e];
-      os[r * G::P + D + e] = nd.t[e];
-    }
-  }
-  __syncthreads();
 
-  const int row0 = 32 * (wave % NW);
-  // ---- dQ for queries row0 .. row0 + 31 over all keys:
-  //   S^T = K Q'^T - lse2 -> P^T;  dP^T = V dO^T - Delta;  dZ^T = P^T * dP^T;  dQ^T += K^T dZ^T
-  if (wave < NW && (uint32_t)row0 < L) {
-    bf16x8 qf[G::NDK], df[G::NDK];
+  // ---- a unit's rows: chunk c = row c / CH, 16 bytes at column 8 (c % CH);
+  // rows past L (Lk) fall outside the buffer ranges and read as zero
+  u32x4 cq[NLOAD], cd[NLOAD], co[NLOAD], ck[NLOAD], cv[NLOAD];
+  auto issue = [&](uint32_t unit) {
+    const uint32_t head = unit % p.H, bx = unit / p.H;  // (b, x, h): query head = key/value head
+    const int64_t qb = bx_base(p, bx, p.b_q, p.x_q) + (int64_t)head * D;
+    const int64_t ob = bx_base(p, bx, p.b_o, p.x_o) + (int64_t)head * D;
+    const int64_t kb = bx_base(p, bx, p.b_kv, p.x_kv) + (int64_t)head * D;
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + qb, L * (uint32_t)p.r_q * 2u);
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(p.dout + ob, L * (uint32_t)p.r_o * 2u);
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + ob, L * (uint32_t)p.r_o * 2u);
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + kb, Lk * (uint32_t)p.r_kv * 2u);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + kb, Lk * (uint32_t)p.r_kv * 2u);
 #pragma unroll
-    for (int st = 0; st < G::NDK; ++st) {
-      qf[st] = *reinterpret_cast<const bf16x8*>(qs + (row0 + l32) * G::P + 16 * st + 8 * g);
-      df[st] = *reinterpret_cast<const bf16x8*>(os + (row0 + l32) * G::P + 16 * st + 8 * g);
+    for (int i = 0; i < NLOAD; ++i) {
+      const int c = threadIdx.x + i * NT;
+      if (c < NCH) {
+        const uint32_t row = c / G::CH, col = c - row * G::CH;
+        const uint32_t oq = row * (uint32_t)p.r_q * 2u + col * 16u;
+        const uint32_t oo = row * (uint32_t)p.r_o * 2u + col * 16u;
+        const uint32_t okv = row * (uint32_t)p.r_kv * 2u + col * 16u;
+        cq[i] = __builtin_amdgcn_raw_buffer_load_b128(rq, oq, 0, 0);
+        cd[i] = __builtin_amdgcn_raw_buffer_load_b128(rd, oo, 0, 0);
+        co[i] = __builtin_amdgcn_raw_buffer_load_b128(ro, oo, 0, 0);
+        ck[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, okv, 0, 0);
+        cv[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, okv, 0, 0);
+      }
     }
-    floatx16 dqt[G::NT32 > 0 ? G::NT32 : 1];
-    floatx4 dqs[2];
+  };
+  if (u < u_end) issue(u);
+  for (; u < u_end; u += u_step) {
+    const uint32_t unit = u;
+    const uint32_t head = unit % p.H, bx = unit / p.H;
+    const int64_t q_base = bx_base(p, bx, p.b_q, p.x_q) + (int64_t)head * D;
+    const int64_t o_base = bx_base(p, bx, p.b_o, p.x_o) + (int64_t)head * D;
+    const int64_t kv_base = bx_base(p, bx, p.b_kv, p.x_kv) + (int64_t)head * D;
+    __syncthreads();  // the previous unit's LDS reads are done (and the padding is written)
 #pragma unroll
-    for (int t = 0; t < G::NT32; ++t)
+    for (int i = 0; i < NLOAD; ++i) {
+      const int c = threadIdx.x + i * NT;
+      if (c < NCH) {
+        const int row = c / G::CH, col = c - row * G::CH;
+        const int off = row * G::P + col * 8;
+        bf16x8 x = __builtin_bit_cast(bf16x8, cq[i]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dqt[t][r] = 0.0f;
+        for (int e = 0; e < 8; ++e) x[e] = (bf16)((float)x[e] * p.c);  // Q' as in the forward
+        *reinterpret_cast<bf16x8*>(qs + off) = x;
+        *reinterpret_cast<u32x4*>(os + off) = cd[i];
+        *reinterpret_cast<u32x4*>(ks + off) = ck[i];
+        *reinterpret_cast<u32x4*>(vs + off) = cv[i];
+        const bf16x8 dv8 = __builtin_bit_cast(bf16x8, cd[i]), ov8 = __builtin_bit_cast(bf16x8, co[i]);
+        float d = 0.0f;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+        for (int e = 0; e < 8; ++e) d += (float)dv8[e] * (float)ov8[e];
+        dpart[c] = d;
+      }
+    }
+    __syncthreads();
+    // Delta = rowsum(dO * O) and the bias terms: -(lse * log2 e) on Q', -Delta on dO
+    for (int r = threadIdx.x; r < R; r += NT) {
+      float delta = 0.0f, lse2 = 0.0f;
+      if ((uint32_t)r < L) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) dqs[h][r] = 0.0f;
-    for (uint32_t k0 = 0; k0 < Lk; k0 += 32) {
-      floatx16 sc, dp;
+        for (int col = 0; col < G::CH; ++col) delta += dpart[r * G::CH + col];
+        lse2 = p.lse[(int64_t)unit * L + r] * kLog2e;
+        p.delta[(int64_t)unit * L + r] = delta;
+      }
+      const Bf16x3 nl = neg_split3(lse2), nd = neg_split3(delta);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.0f;
+      for (int e = 0; e < 3; ++e) {
+        qs[r * G::P + D + e] = nl.t[e];
+        os[r * G::P + D + e] = nd.t[e];
+      }
+    }
+    __syncthreads();
+    if (u + u_step < u_end) issue(u + u_step);
+
+    const int row0 = 32 * (wave % NW);
+    // ---- dQ for queries row0 .. row0 + 31 over all keys:
+    //   S^T = K Q'^T - lse2 -> P^T;  dP^T = V dO^T - Delta;  dZ^T = P^T * dP^T;  dQ^T += K^T dZ^T
+    if (wave < NW && (uint32_t)row0 < L) {
+      bf16x8 qf[G::NDK], df[G::NDK];
 #pragma unroll
       for (int st = 0; st < G::NDK; ++st) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(ks + (k0 + l32) * G::P + 16 * st + 8 * g);
-        const bf16x8 va = *reinterpret_cast<const bf16x8*>(vs + (k0 + l32) * G::P + 16 * st + 8 * g);
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], sc, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, df[st], dp, 0, 0, 0);
+        qf[st] = *reinterpret_cast<const bf16x8*>(qs + (row0 + l32) * G::P + 16 * st + 8 * g);
+        df[st] = *reinterpret_cast<const bf16x8*>(os + (row0 + l32) * G::P + 16 * st + 8 * g);
       }
-      bf16x8 zb[2];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) zb[r / 8][r % 8] = (bf16)(__builtin_amdgcn_exp2f(sc[r]) * dp[r]);
+      floatx16 dqt[G::NT32 > 0 ? G::NT32 : 1];
+      floatx4 dqs[2];
 #pragma unroll
       for (int t = 0; t < G::NT32; ++t)
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-          dqt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(ks, G::P, k0 + 16 * kk, 32 * t, lane),
-                                                           zb[kk], dqt[t], 0, 0, 0);
-      if constexpr (G::SLAB) {
-        const bf16x8 a = tr_slab(ks, G::P, k0, 32 * G::NT32, lane);
-        bf16x8 b0, b1;
-        slab_b(zb[0], zb[1], b0, b1);
-        dqs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, dqs[0], 0, 0, 0);
-        dqs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, dqs[1], 0, 0, 0);
-      }
-    }
-    store_rows<D>(p.dq + q_base, p.r_q, row0, L, lane, dqt, dqs, p.scale);
-  }
-
-  // ---- dK, dV for keys row0 .. row0 + 31 over all queries:
-  //   S = Q' K^T - lse2 -> P;  dP = dO V^T - Delta;  dZ = P * dP;  dV^T += dO^T P;  dK^T += Q'^T dZ
-  if (wave >= NW && (uint32_t)row0 < Lk) {
-    bf16x8 kf[G::NDK], vf[G::NDK];
+        for (int r = 0; r < 16; ++r) dqt[t][r] = 0.0f;
 #pragma unroll
-    for (int st = 0; st < G::NDK; ++st) {
-      kf[st] = *reinterpret_cast<const bf16x8*>(ks + (row0 + l32) * G::P + 16 * st + 8 * g);
-      vf[st] = *reinterpret_cast<const bf16x8*>(vs + (row0 + l32) * G::P + 16 * st + 8 * g);
-    }
-    floatx16 dvt[G::NT32 > 0 ? G::NT32 : 1], dkt[G::NT32 > 0 ? G::NT32 : 1];
-    floatx4 dvs[2], dks[2];
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int t = 0; t < G::NT32; ++t)
+        for (int r = 0; r < 4; ++r) dqs[h][r] = 0.0f;
+      for (uint32_t k0 = 0; k0 < Lk; k0 += 32) {
+        floatx16 sc, dp;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dvt[t][r] = dkt[t][r] = 0.0f;
+        for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.0f;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) dvs[h][r] = dks[h][r] = 0.0f;
-    for (uint32_t q0 = 0; q0 < L; q0 += 32) {
-      floatx16 sc, dp;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.0f;
-#pragma unroll
-      for (int st = 0; st < G::NDK; ++st) {
-        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qs + (q0 + l32) * G::P + 16 * st + 8 * g);
-        const bf16x8 da = *reinterpret_cast<const bf16x8*>(os + (q0 + l32) * G::P + 16 * st + 8 * g);
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[st], sc, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[st], dp, 0, 0, 0);
-      }
-      bf16x8 pb[2], zb[2];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pr = __builtin_amdgcn_exp2f(sc[r]);
-        pb[r / 8][r % 8] = (bf16)pr;
-        zb[r / 8][r % 8] = (bf16)(pr * dp[r]);
-      }
-#pragma unroll
-      for (int t = 0; t < G::NT32; ++t)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          dvt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(os, G::P, q0 + 16 * kk, 32 * t, lane),
-                                                           pb[kk], dvt[t], 0, 0, 0);
-          dkt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(qs, G::P, q0 + 16 * kk, 32 * t, lane),
-                                                           zb[kk], dkt[t], 0, 0, 0);
+        for (int st = 0; st < G::NDK; ++st) {
+          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(ks + (k0 + l32) * G::P + 16 * st + 8 * g);
+          const bf16x8 va = *reinterpret_cast<const bf16x8*>(vs + (k0 + l32) * G::P + 16 * st + 8 * g);
+          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], sc, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, df[st], dp, 0, 0, 0);
         }
-      if constexpr (G::SLAB) {
-        bf16x8 b0, b1;
-        const bf16x8 ao = tr_slab(os, G::P, q0, 32 * G::NT32, lane);
-        slab_b(pb[0], pb[1], b0, b1);
-        dvs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b0, dvs[0], 0, 0, 0);
-        dvs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b1, dvs[1], 0, 0, 0);
-        const bf16x8 aq = tr_slab(qs, G::P, q0, 32 * G::NT32, lane);
-        slab_b(zb[0], zb[1], b0, b1);
-        dks[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b0, dks[0], 0, 0, 0);
-        dks[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b1, dks[1], 0, 0, 0);
+        bf16x8 zb[2];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) zb[r / 8][r % 8] = (bf16)(__builtin_amdgcn_exp2f(sc[r]) * dp[r]);
+#pragma unroll
+        for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk)
+            dqt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(ks, G::P, k0 + 16 * kk, 32 * t, lane),
+                                                             zb[kk], dqt[t], 0, 0, 0);
+        if constexpr (G::SLAB) {
+          const bf16x8 a = tr_slab(ks, G::P, k0, 32 * G::NT32, lane);
+          bf16x8 b0, b1;
+          slab_b(zb[0], zb[1], b0, b1);
+          dqs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, dqs[0], 0, 0, 0);
+          dqs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, dqs[1], 0, 0, 0);
+        }
       }
+      store_rows<D>(p.dq + q_base, p.r_q, row0, L, lane, dqt, dqs, p.scale);
     }
-    store_rows<D>(p.dv + kv_base, p.r_kv, row0, Lk, lane, dvt, dvs, 1.0f);
-    store_rows<D>(p.dk + kv_base, p.r_kv, row0, Lk, lane, dkt, dks, kLn2);
+
+    // ---- dK, dV for keys row0 .. row0 + 31 over all queries:
+    //   S = Q' K^T - lse2 -> P;  dP = dO V^T - Delta;  dZ = P * dP;  dV^T += dO^T P;  dK^T += Q'^T dZ
+    if (wave >= NW && (uint32_t)row0 < Lk) {
+      bf16x8 kf[G::NDK], vf[G::NDK];
+#pragma unroll
+      for (int st = 0; st < G::NDK; ++st) {
+        kf[st] = *reinterpret_cast<const bf16x8*>(ks + (row0 + l32) * G::P + 16 * st + 8 * g);
+        vf[st] = *reinterpret_cast<const bf16x8*>(vs + (row0 + l32) * G::P + 16 * st + 8 * g);
+      }
+      floatx16 dvt[G::NT32 > 0 ? G::NT32 : 1], dkt[G::NT32 > 0 ? G::NT32 : 1];
+      floatx4 dvs[2], dks[2];
+#pragma unroll
+      for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dvt[t][r] = dkt[t][r] = 0.0f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dvs[h][r] = dks[h][r] = 0.0f;
+      for (uint32_t q0 = 0; q0 < L; q0 += 32) {
+        floatx16 sc, dp;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.0f;
+#pragma unroll
+        for (int st = 0; st < G::NDK; ++st) {
+          const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qs + (q0 + l32) * G::P + 16 * st + 8 * g);
+          const bf16x8 da = *reinterpret_cast<const bf16x8*>(os + (q0 + l32) * G::P + 16 * st + 8 * g);
+          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[st], sc, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[st], dp, 0, 0, 0);
+        }
+        bf16x8 pb[2], zb[2];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float pr = __builtin_amdgcn_exp2f(sc[r]);
+          pb[r / 8][r % 8] = (bf16)pr;
+          zb[r / 8][r % 8] = (bf16)(pr * dp[r]);
+        }
+#pragma unroll
+        for (int t = 0; t < G::NT32; ++t)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            dvt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(os, G::P, q0 + 16 * kk, 32 * t, lane),
+                                                             pb[kk], dvt[t], 0, 0, 0);
+            dkt[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag32(qs, G::P, q0 + 16 * kk, 32 * t, lane),
+                                                             zb[kk], dkt[t], 0, 0, 0);
+          }
+        if constexpr (G::SLAB) {
+          bf16x8 b0, b1;
+          const bf16x8 ao = tr_slab(os, G::P, q0, 32 * G::NT32, lane);
+          slab_b(pb[0], pb[1], b0, b1);
+          dvs[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b0, dvs[0], 0, 0, 0);
+          dvs[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, b1, dvs[1], 0, 0, 0);
+          const bf16x8 aq = tr_slab(qs, G::P, q0, 32 * G::NT32, lane);
+          slab_b(zb[0], zb[1], b0, b1);
+          dks[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b0, dks[0], 0, 0, 0);
+          dks[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, b1, dks[1], 0, 0, 0);
+        }
+      }
+      store_rows<D>(p.dv + kv_base, p.r_kv, row0, Lk, lane, dvt, dvs, 1.0f);
+      store_rows<D>(p.dk + kv_base, p.r_kv, row0, Lk, lane, dkt, dks, kLn2);
+    }
   }
 }
 
@@ -1014,7 +1047,19 @@ int launch_bwd_short(const AttnBwdArgs& a, hipStream_t s) {
   if (units == 0) return DSP_OK;
   p.n_blk = 1;
   p.n_blocks = (uint32_t)units;
-  hipLaunchKernelGGL((attn_bwd_short_kernel<D, NW>), dim3((uint32_t)units), dim3(NW * 128), 0, s, p);
+  // persistent grid: as many work-groups as are resident at once (the
+  // runtime's occupancy for this kernel: registers and LDS), a multiple of 8
+  // (whole XCD ranges)
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1 ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_short_kernel<D, NW>, NW * 128, 0) !=
+          hipSuccess ||
+      per_cu < 1)
+    return DSP_ERR_HIP;
+  int64_t blocks = std::min<int64_t>(units, (int64_t)cus * per_cu);
+  if (blocks >= 8) blocks &= ~int64_t(7);
+  hipLaunchKernelGGL((attn_bwd_short_kernel<D, NW>), dim3((uint32_t)blocks), dim3(NW * 128), 0, s, p);
   return last_launch_status();
 }
 
