@@ -194,44 +194,6 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   const uint32_t L = p.L;     // queries of the unit
   const uint32_t Lk = p.Lk;   // keys and values of the unit
 
-  // ---- padding columns of the LDS buffers.  K: columns D and D + 1 are 1.0
-  // when they carry the bias pair, the rest 0.  V: column D is 1.0 (row sum),
-  // the rest 0.
-  for (int e = threadIdx.x; e < NBUF * KB; e += NT) {
-    bf16* t = lds + (e / KB) * G::TILE_ELEMS;
-    const int r = e % KB;
-    for (int c = D; c < G::KP; ++c) t[r * G::KP + c] = (bf16)((G::BIAS && c <= D + 1) ? 1.0f : 0.0f);
-    bf16* vt = t + KB * G::KP;
-    for (int c = D; c < G::VP; ++c) vt[r * G::VP + c] = (bf16)((G::ONES && c == D) ? 1.0f : 0.0f);
-  }
-
-  // ---- Q' = Q * scale * log2(e) as bf16 B fragments: lane (n + 32g) holds
-  // Q'[q][16s + 8g .. +7].  With the bias columns, elements D and D + 1 of Q'
-  // are the negated reference maximum as a hi/lo pair (0 until the first tile
-  // sets it).
-  const uint32_t q_wave = um.qb * QB + wave * 32 * QT;
-  const bf16* qg = p.q + um.in_base;
-  bf16x8 qf[QT][G::NDK];
-#pragma unroll
-  for (int j = 0; j < QT; ++j) {
-    const uint32_t q = q_wave + 32 * j + l32;
-#pragma unroll
-    for (int s = 0; s < G::NDK; ++s) {
-      const int d = 16 * s + 8 * g;
-      bf16x8 v;
-      if (q < L && d < D) {
-        v = *reinterpret_cast<const bf16x8*>(qg + (int64_t)q * p.r_in + d);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = (bf16)((float)v[e] * p.c);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = (bf16)0.0f;
-      }
-      qf[j][s] = v;
-    }
-  }
-  constexpr int BS = G::NDK - 1;  // the d step holding column D (lanes g == 1)
-
   // ---- tile fetch through buffer resources covering rows [kb, L) of the
   // unit (rows past L read as zero).  With several waves, waves [0, NW/2)
   // fetch K and the others V; a single wave fetches both.
@@ -313,8 +275,58 @@ __global__ __launch_bounds__(NW * 64, MINW) void attn_fwd_kernel(Params p) {
   for (int j = 0; j < QT; ++j) { b_ref[j] = 0.0f; l_run[j] = 0.0f; }
 
   const uint32_t n_kb = (Lk + KB - 1) / KB;
+  // the first tile's fetch goes out first: the padding columns and the Q
+  // fragments (a global round trip of their own) are prepared while it is in
+  // flight
+  if (SPLIT) fetch(0);
+
+  // ---- padding columns of the LDS buffers.  K: columns D and D + 1 are 1.0
+  // when they carry the bias pair, the rest 0.  V: column D is 1.0 (row sum),
+  // the rest 0.
+  for (int e = threadIdx.x; e < NBUF * KB; e += NT) {
+    bf16* t = lds + (e / KB) * G::TILE_ELEMS;
+    const int r = e % KB;
+    for (int c = D; c < G::KP; ++c) t[r * G::KP + c] = (bf16)((G::BIAS && c <= D + 1) ? 1.0f : 0.0f);
+    bf16* vt = t + KB * G::KP;
+    for (int c = D; c < G::VP; ++c) vt[r * G::VP + c] = (bf16)((G::ONES && c == D) ? 1.0f : 0.0f);
+  }
+
+  // ---- Q' = Q * scale * log2(e) as bf16 B fragments: lane (n + 32g) holds
+  // Q'[q][16s + 8g .. +7].  With the bias columns, elements D and D + 1 of Q'
+  // are the negated reference maximum as a hi/lo pair (0 until the first tile
+  // sets it).
+  const uint32_t q_wave = um.qb * QB + wave * 32 * QT;
+  // Loaded through a buffer resource over this work-group's query rows: rows
+  // past L and columns past D read as zero, so every load goes out at once
+  // (no per-lane branch, no wait between them).
+  const uint32_t q_first = um.qb * QB;
+  const uint32_t q_rows = L > q_first ? min(L - q_first, (uint32_t)QB) : 0u;
+  const __amdgpu_buffer_rsrc_t rq =
+      make_rsrc(p.q + um.in_base + (int64_t)q_first * p.r_in, q_rows * (uint32_t)p.r_in * 2u);
+  u32x4 qraw[QT][G::NDK];
+#pragma unroll
+  for (int j = 0; j < QT; ++j) {
+    const uint32_t qr = (uint32_t)(wave * 32 * QT + 32 * j + l32);  // row within the work-group's
+#pragma unroll
+    for (int s = 0; s < G::NDK; ++s) {
+      const int d = 16 * s + 8 * g;
+      qraw[j][s] = __builtin_amdgcn_raw_buffer_load_b128(
+          rq, d < D ? (qr * (uint32_t)p.r_in + (uint32_t)d) * 2u : 0xFFFFFFF0u, 0, 0);
+    }
+  }
+  bf16x8 qf[QT][G::NDK];
+#pragma unroll
+  for (int j = 0; j < QT; ++j)
+#pragma unroll
+    for (int s = 0; s < G::NDK; ++s) {
+      bf16x8 v = __builtin_bit_cast(bf16x8, qraw[j][s]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (bf16)((float)v[e] * p.c);
+      qf[j][s] = v;
+    }
+  constexpr int BS = G::NDK - 1;  // the d step holding column D (lanes g == 1)
+
   if (SPLIT) {
-    fetch(0);
     stash(0);
   } else {
     fetch_single(0, 0);
@@ -734,7 +746,8 @@ int64_t make_params(const AttnArgs& a, int QB, int KB, Params& p) {
   const int64_t blocks = units * n_qb;
   if (blocks == 0) return 0;
   // a tile's buffer resource addresses its rows with 32-bit byte offsets
-  if (blocks >= (int64_t(1) << 31) || std::min<int64_t>(a.Lk, KB) * a.r_stride_kv * 2 >= (int64_t(1) << 31))
+  if (blocks >= (int64_t(1) << 31) || std::min<int64_t>(a.Lk, KB) * a.r_stride_kv * 2 >= (int64_t(1) << 31) ||
+      std::min<int64_t>(a.L, QB) * a.r_stride_in * 2 >= (int64_t(1) << 31))
     return -1;
   p.n_units = (uint32_t)units;
   p.n_qb = (uint32_t)n_qb;
