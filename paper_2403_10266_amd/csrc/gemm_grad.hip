@@ -451,22 +451,40 @@ __global__ __launch_bounds__(GNTHR, 1) void gemm_grad_tt_big_kernel(GradArgs p) 
     slice(kt, no{}, no{});
   }
 
-  // fp32 partial (or the result, unsplit): lane owns rows m = .. + 32 bb + l32
-  // and column groups n = .. + 32 a + 8 r4 + 4 g + {0..3}
+  // fp32 partial (or the result, unsplit).  The lane holds rows
+  // m = .. + 32 bb + l32 and column groups n = .. + 32 a + 8 r4 + 4 g + {0..3};
+  // stored from there, a store instruction would write 16-byte pieces of 32
+  // rows.  So the tile goes through LDS in two passes of 128 rows (rows
+  // 64 p + [0, 64) of each wave row half) and leaves in whole 16-byte row
+  // chunks, consecutive lanes on consecutive chunks.
   float* out = static_cast<float*>(p.out) + (int64_t)blockIdx.z * p.M * p.N;
+  constexpr int SPF = BNB + 4;  // staged row pitch (fp32): a 16-byte pad
+  static_assert(128 * SPF * 4 <= 2 * STAGE * 2, "the staging fits the LDS buffers");
+  constexpr int CPR = BNB / 4, PER = 128 * CPR / GNTHR;
+  float* sf = reinterpret_cast<float*>(lds);
 #pragma unroll
-  for (int bb = 0; bb < TM; ++bb) {
-    const int m = m0 + wm * TM * 32 + 32 * bb + l32;
-    if (m >= p.M) continue;
+  for (int pass = 0; pass < 2; ++pass) {
+    __syncthreads();  // pass 0: the last fragments are read; pass 1: pass 0's rows are read
 #pragma unroll
-    for (int a = 0; a < TN; ++a)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int n = n0 + wn * TN * 32 + 32 * a + 8 * r4 + 4 * g;
-        if (n < p.N)
-          *reinterpret_cast<float4*>(out + (int64_t)m * p.N + n) =
-              make_float4(acc[a][bb][4 * r4], acc[a][bb][4 * r4 + 1], acc[a][bb][4 * r4 + 2], acc[a][bb][4 * r4 + 3]);
-      }
+      for (int a = 0; a < TN; ++a)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const floatx16& t = acc[a][2 * pass + h];
+          *reinterpret_cast<float4*>(sf + (wm * 64 + 32 * h + l32) * SPF + wn * TN * 32 + 32 * a + 8 * r4 + 4 * g) =
+              make_float4(t[4 * r4], t[4 * r4 + 1], t[4 * r4 + 2], t[4 * r4 + 3]);
+        }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int c = (int)threadIdx.x + GNTHR * q;
+      const int sr = c / CPR, cc = c % CPR;
+      const int m = m0 + (sr / 64) * 128 + 64 * pass + sr % 64, n = n0 + 4 * cc;
+      if (m < p.M && n < p.N)
+        *reinterpret_cast<float4*>(out + (int64_t)m * p.N + n) =
+            *reinterpret_cast<const float4*>(sf + sr * SPF + 4 * cc);
+    }
   }
 }
 
