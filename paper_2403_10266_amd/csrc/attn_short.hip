@@ -10,9 +10,10 @@
 //    there is no online rescaling.
 //  * The kernel is persistent: a grid of two waves per SIMD loops over units,
 //    and while it computes one unit it already holds the loads of the next
-//    one (K, V and this lane's Q fragments) in flight in registers.  Every
-//    work-group therefore keeps ~56 KB of reads outstanding at all times,
-//    instead of paying a full HBM round trip between a unit's fetch and its
+//    one (K, V and this lane's Q fragments) in flight in registers (for
+//    128-key units, K and V of the next two).  Every work-group therefore
+//    keeps one to two units' reads outstanding at all times, instead of
+//    paying a full HBM round trip between a unit's fetch and its
 //    math.
 //  * Units are cut into 8 contiguous ranges, one per XCD, so the 16 heads of
 //    a token row (neighbouring 144-byte segments of one 2304-byte row) are
@@ -22,6 +23,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "attn_bf16_common.h"
 #include "dsp_internal.h"
@@ -148,10 +150,15 @@ __global__ __launch_bounds__(HG * KB / 32 * 64, 2) void attn_short_kernel(ShortP
     qofs[i] = hh * G::HEAD_ELEMS + KB * (G::KP + G::VP) + row * G::KP + col * 8;
   }
 
-  // the next unit's K/V/Q chunks, in registers
-  u32x4 pk[NTS][NLOAD];
+  // K/V chunks of the next units, in registers.  128-key units keep two sets:
+  // set S holds the unit after next while the other set's unit is computed,
+  // so two units' K and V are in flight at a time (266-279 against 273-287 us
+  // on the temporal workload; shorter units measured no gain).  Q's chunks
+  // (one set) are fetched one unit ahead.
+  constexpr int NSET = KB == 128 ? 2 : 1;
+  u32x4 pk[NSET][NTS][NLOAD];
   u32x4 pq[NLQ];
-  auto issue = [&](uint32_t unit) {
+  auto issue_kv = [&](int S, uint32_t unit) {
     const int64_t ib = unit_base(unit, p.b_in, p.x_in);
 #pragma unroll
     for (int t = 0; t < NTS; ++t) {
@@ -160,9 +167,11 @@ __global__ __launch_bounds__(HG * KB / 32 * 64, 2) void attn_short_kernel(ShortP
 #pragma unroll
       for (int i = 0; i < NLOAD; ++i)
         if (ft + i * FT < TCH)
-          pk[t][i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, ShortHints<KB>::kLoadCpol);
+          pk[S][t][i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, ShortHints<KB>::kLoadCpol);
     }
-    const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + ib, unit_bytes);
+  };
+  auto issue_q = [&](uint32_t unit) {
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + unit_base(unit, p.b_in, p.x_in), unit_bytes);
 #pragma unroll
     for (int i = 0; i < NLQ; ++i)
       if ((int)threadIdx.x + i * NT < TCH)
@@ -176,8 +185,10 @@ __global__ __launch_bounds__(HG * KB / 32 * 64, 2) void attn_short_kernel(ShortP
   const bf16* const v_lds = v_of(hw);
   bf16* const q_lds = q_of(hw);
   const uint32_t q_row = 32 * qw + l32;
-  if (u < u_end) issue(u);
-  for (; u < u_end; u += u_step) {
+  // one unit from register set S (compile-time, so the two sets never move
+  // between registers)
+  auto unit_body = [&](auto s_c, uint32_t u) {
+    constexpr int S = decltype(s_c)::value;
     __syncthreads();  // the previous unit's LDS reads are done (and the padding is written)
 #pragma unroll
     for (int t = 0; t < NTS; ++t)
@@ -185,15 +196,16 @@ __global__ __launch_bounds__(HG * KB / 32 * 64, 2) void attn_short_kernel(ShortP
       for (int i = 0; i < NLOAD; ++i)
         if (ft + i * FT < TCH) {
           bf16* dst = lds + ((SPLIT ? fetch_v : t == 1) ? vofs[i] : kofs[i]);
-          *reinterpret_cast<u32x4*>(dst) = pk[t][i];
+          *reinterpret_cast<u32x4*>(dst) = pk[S][t][i];
         }
 #pragma unroll
     for (int i = 0; i < NLQ; ++i)
       if ((int)threadIdx.x + i * NT < TCH) *reinterpret_cast<u32x4*>(lds + qofs[i]) = pq[i];
     __syncthreads();
     const int64_t ob = unit_base(u, p.b_out, p.x_out) + hw * D;
-    if (u + u_step < u_end) issue(u + u_step);
-    if (32 * (uint32_t)qw >= L) continue;  // no queries for this wave (wave-uniform)
+    if (u + NSET * u_step < u_end) issue_kv(S, u + NSET * u_step);
+    if (u + u_step < u_end) issue_q(u + u_step);
+    if (32 * (uint32_t)qw >= L) return;  // no queries for this wave (wave-uniform)
 
     // Q' = Q * scale * log2(e) as bf16 B fragments: lane (n + 32g) holds
     // Q'[32 wave + n][16s + 8g .. +7] (columns >= D are LDS padding, 0)
@@ -371,6 +383,21 @@ __global__ __launch_bounds__(HG * KB / 32 * 64, 2) void attn_short_kernel(ShortP
         if constexpr (ShortHints<KB>::kNtStore) __builtin_nontemporal_store(val, dst);
         else *dst = val;
       }
+    }
+  };
+  using set0 = std::integral_constant<int, 0>;
+  using set1 = std::integral_constant<int, 1>;
+  if (u < u_end) {
+    issue_kv(0, u);
+    issue_q(u);
+  }
+  if constexpr (NSET == 2) {
+    if (u + u_step < u_end) issue_kv(1, u + u_step);
+  }
+  for (; u < u_end; u += NSET * u_step) {
+    unit_body(set0{}, u);
+    if constexpr (NSET == 2) {
+      if (u + u_step < u_end) unit_body(set1{}, u + u_step);
     }
   }
 }
