@@ -520,12 +520,13 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
     const int m = m0 + (int)threadIdx.x;
     orows[threadIdx.x] = (uint32_t)rs.map(m < M ? m : 0);
   };
-  if constexpr (!F32OUT && !BWD && !KEEP) {
+  if constexpr (!F32OUT && !BWD) {
     // bf16 results, activation applied in registers, staged as bf16 and
     // stored in 16-byte chunks of 8 columns.  Two halves (accumulator row
     // blocks 0-1, then 2-3, i.e. tile rows 64 h + [0, 64) of each wave row
     // half): the first half's stores are in flight while the second half's
-    // activation is computed.
+    // activation is computed.  KEEP: the pre-activation copy of a half is
+    // staged in the other half's rows (tile row r ^ 64), free at that time.
     constexpr int SP = BNB + 8;  // staged row pitch (bf16): a 16-byte pad
     static_assert(BIG_BM * SP * 2 + BIG_BM * 4 <= 2 * STAGE * 2, "bf16 staging fits the LDS buffers");
     constexpr int CPR = BNB / 8;  // chunks per row
@@ -534,12 +535,16 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
     put_orow();
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
+      if (KEEP && h == 1) __syncthreads();  // the first half's copies are read
 #pragma unroll
       for (int bb = 2 * h; bb < 2 * h + 2; ++bb)
 #pragma unroll
         for (int j = 0; j < NG; ++j) {
           float v[4];
           sum4(bb, j, v);
+          const int col = wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
+          const int row = wm * TM * 32 + 32 * bb + l32;
+          if (KEEP) *reinterpret_cast<uint2*>(st + (row ^ 64) * SP + col) = pack_bf16x4(v);
           if (EPI == DSP_EPI_GELU) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
@@ -548,8 +553,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
 #pragma unroll
             for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
           }
-          const int col = wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
-          *reinterpret_cast<uint2*>(st + (wm * TM * 32 + 32 * bb + l32) * SP + col) = pack_bf16x4(v);
+          *reinterpret_cast<uint2*>(st + row * SP + col) = pack_bf16x4(v);
         }
       __syncthreads();
 #pragma unroll 4
@@ -559,7 +563,12 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
         const int tr = (sr / 64) * 128 + 64 * h + sr % 64;
         const int m = m0 + tr, n = n0 + 8 * cc;
         const u32x4 w = *reinterpret_cast<const u32x4*>(st + tr * SP + 8 * cc);
-        if (m < M && n < N) *reinterpret_cast<u32x4*>(static_cast<bf16*>(out) + (int64_t)orows[tr] * N + n) = w;
+        const int64_t o = (int64_t)orows[tr] * N + n;
+        if (m < M && n < N) {
+          *reinterpret_cast<u32x4*>(static_cast<bf16*>(out) + o) = w;
+          if (KEEP)
+            *reinterpret_cast<u32x4*>(keep_out + o) = *reinterpret_cast<const u32x4*>(st + (tr ^ 64) * SP + 8 * cc);
+        }
       }
     }
   } else {
