@@ -403,17 +403,21 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_bwd_dq_kernel(BwdParams p) {
         s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s[kt], 0, 0, 0);
         dp[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, df[st], dp[kt], 0, 0, 0);
       }
-    // lane (n + 32g) holds keys kb + 32kt + 8(r/4) + 4g + r%4 of query n
-    const bool tail = kb + KB > Lk;
+    // lane (n + 32g) holds keys kb + 32kt + 8(r/4) + 4g + r%4 of query n.
+    // Keys past Lk (only the last tile holds any) get score -inf, so P = +0
+    // there; the branch keeps the key compares out of every other tile.
+    if (kb + KB > Lk) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (kb + 32 * kt + (r / 4) * 8 + 4 * g + (r % 4) >= Lk) s[kt][r] = -INFINITY;
+    }
     bf16x8 zb[NKT][2];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float pr = __builtin_amdgcn_exp2f(s[kt][r]);
-        if (tail && kb + 32 * kt + (r / 4) * 8 + 4 * g + (r % 4) >= Lk) pr = 0.0f;
-        zb[kt][r / 8][r % 8] = (bf16)(pr * dp[kt][r]);
-      }
+      for (int r = 0; r < 16; ++r) zb[kt][r / 8][r % 8] = (bf16)(__builtin_amdgcn_exp2f(s[kt][r]) * dp[kt][r]);
     // dQ^T += K^T dZ^T
 #pragma unroll
     for (int t = 0; t < G::NT32; ++t)
