@@ -458,7 +458,9 @@ int dsp_st_block_forward(const float* x_BTSC, float* y_BSTC, const dsp_block_wei
  *   residual add) and DSP_BLOCK_RELU; the projection-only chain
  *   (DSP_BLOCK_ATTN_ONLY) gives DSP_ERR_ARG.  y has the bits
  *   dsp_st_block_forward writes for the same arguments (the MLP's first GEMM
- *   stores its pre-activation beside the activation from the same fp32 sum).
+ *   stores, from the same fp32 sum as the activation, what the activation's
+ *   backward needs: the pre-activation, or GELU' there when the block is
+ *   bf16 with GELU at sizes whose backward runs on the large-tile GEMM).
  * dsp_st_block_backward -- given the forward's x (B,T,S,C), its saved
  *   activations, and dy (B,S,T,C) = dL/dy, writes dx = dL/dx (B,T,S,C, fp32)
  *   and the weight gradients into `grads`: fp32 arrays shaped like the weights

@@ -304,7 +304,10 @@ int linear_impl(const void* a, const void* w, const void* bias, const float* res
   if (!valid_dtype(dtype)) return DSP_ERR_DTYPE;
   if (M < 0 || N < 1 || K < 1) return DSP_ERR_SHAPE;
   if (rs.outer && (rs.inner == 0 || M % ((int64_t)rs.outer * rs.inner) || residual == out)) return DSP_ERR_ARG;
-  if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_RELU) return DSP_ERR_ARG;
+  // the public epilogues, and (bf16 only, with `pre`) GELU keeping its derivative
+  const bool keep_grad = epilogue == DSP_EPI_GELU_KEEP_GRAD;
+  if ((epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_RELU) && !keep_grad) return DSP_ERR_ARG;
+  if (keep_grad && (dtype != DSP_BF16 || !pre)) return DSP_ERR_ARG;
   if (!w) return DSP_ERR_NULL;
   if (M == 0) return DSP_OK;
   if (!a || !out) return DSP_ERR_NULL;
@@ -320,7 +323,8 @@ int linear_impl(const void* a, const void* w, const void* bias, const float* res
   if (residual && epilogue == DSP_EPI_RESID && residual != out &&
       overlap(out, out_bytes, residual, (size_t)mn * 4))
     return DSP_ERR_ARG;
-  if (pre && ((epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) || overlap(pre, out_bytes, out, out_bytes) ||
+  if (pre && ((epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU && !keep_grad) ||
+              overlap(pre, out_bytes, out, out_bytes) ||
               overlap(pre, out_bytes, a, (size_t)mk * es)))
     return DSP_ERR_ARG;
   if (dtype == DSP_BF16) {
@@ -366,9 +370,17 @@ bool block_ws_layout(int64_t B, int64_t T, int64_t S, int C, int F, int dtype, B
 // (the inputs of their LayerNorms).  Post-LN: y0 and y1 hold the sums r1
 // (switched to (B, S, T, C)) and r2 that the first two LayerNorms normalise,
 // and r3, the sum the MLP's LayerNorm normalises, gets a slot of its own.
+// u is what the MLP activation's backward needs: the pre-activation, or with
+// GELU in bf16 at sizes whose backward runs on the large-tile GEMM, GELU' at
+// the fp32 pre-activation (block_keeps_act_grad), so that the backward's
+// epilogue is one multiply instead of the derivative's evaluation.
 struct BlockSaved {
   size_t y0, y1, h1, qkv1, a1, lse1, h2, qkv2, a2, lse2, h3, u, g, r3, total;
 };
+
+bool block_keeps_act_grad(int64_t tokens, int F, int dtype, int flags) {
+  return dtype == DSP_BF16 && !(flags & DSP_BLOCK_RELU) && linear_bf16_large_tiles(tokens, F);
+}
 
 bool block_saved_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, int flags, int dtype,
                         BlockSaved* sv) {
@@ -767,6 +779,7 @@ int dsp_layernorm(const void* x, int x_dtype, void* y, int y_dtype, int64_t rows
 
 int dsp_linear(const void* a, const void* w, const void* bias, const float* residual, void* out,
                int64_t M, int N, int K, int epilogue, int dtype, void* stream) {
+  if (epilogue < DSP_EPI_NONE || epilogue > DSP_EPI_RELU) return DSP_ERR_ARG;
   return linear_impl(a, w, bias, residual, out, M, N, K, epilogue, dtype, as_stream(stream));
 }
 
@@ -991,6 +1004,8 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
   const size_t es = elem_size(dtype);
   const int D = C / H;
   const int act = (flags & DSP_BLOCK_RELU) ? DSP_EPI_RELU : DSP_EPI_GELU;
+  // what the MLP's first GEMM keeps in `u` (see block_keeps_act_grad)
+  const int act_keep = block_keeps_act_grad(tokens, F, dtype, flags) ? DSP_EPI_GELU_KEEP_GRAD : act;
   RowSwap swap;  // (B, T, S) token rows -> (B, S, T)
   swap.outer = (uint32_t)T;
   swap.inner = (uint32_t)S;
@@ -1024,7 +1039,7 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
     DSP_TRY(linear_impl(a2, w->wo_t, w->bo_t, y_BSTC, y1, tokens, C, C, DSP_EPI_RESID, dtype, s));  // r2
     DSP_TRY(launch_layernorm(y1, 0, y_BSTC, 0, tokens, C, ln_eps, s));           // stream y1 = LN(r2)
     DSP_TRY(launch_cast(y_BSTC, 0, h3, bf, tokens * C, s));
-    DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, g, tokens, F, C, act, dtype, s, u));
+    DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, g, tokens, F, C, act_keep, dtype, s, u));
     if (flags & DSP_BLOCK_NO_MLP_LN) {
       DSP_TRY(linear_impl(g, w->w2, w->b2, y_BSTC, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
     } else {
@@ -1049,7 +1064,7 @@ int dsp_st_block_forward_train(const float* x_BTSC, float* y_BSTC, const dsp_blo
   } else {
     DSP_TRY(launch_layernorm(y1, 0, h3, bf, tokens, C, ln_eps, s));
   }
-  DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, g, tokens, F, C, act, dtype, s, u));
+  DSP_TRY(linear_impl(h3, w->w1, w->b1, nullptr, g, tokens, F, C, act_keep, dtype, s, u));
   DSP_TRY(linear_impl(g, w->w2, w->b2, y1, y_BSTC, tokens, C, F, DSP_EPI_RESID, dtype, s));
   return DSP_OK;
 #undef DSP_TRY
@@ -1104,6 +1119,7 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
   const int D = C / H;
   const int act_epi = bf ? DSP_GRAD_EPI_BF16 : DSP_GRAD_EPI_F32;   // gradients fed to bf16 / fp32 operands
   const int act_bwd = (flags & DSP_BLOCK_RELU) ? DSP_GRAD_EPI_RELU_BWD : DSP_GRAD_EPI_GELU_BWD;
+  const bool kept_grad = block_keeps_act_grad(tokens, F, dtype, flags);
   RowSwap back;  // (B, S, T) token rows -> (B, T, S): the Switch's adjoint
   back.outer = (uint32_t)S;
   back.inner = (uint32_t)T;
@@ -1123,7 +1139,8 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
       if (r != DSP_OK) return r;
       const int e = epi == DSP_GRAD_EPI_F32 ? DSP_EPI_F32
                     : epi == DSP_GRAD_EPI_BF16 ? DSP_EPI_NONE
-                    : epi == DSP_GRAD_EPI_GELU_BWD ? DSP_EPI_GELU_BWD : DSP_EPI_RELU_BWD;
+                    : epi == DSP_GRAD_EPI_GELU_BWD ? (kept_grad ? DSP_EPI_SCALE_BWD : DSP_EPI_GELU_BWD)
+                                                   : DSP_EPI_RELU_BWD;
       return launch_linear_bf16(dyp, wt, nullptr, nullptr, dxp, tokens, K, N, e, s, const_cast<void*>(up));
     }
     return dsp_linear_bwd_data(dyp, wp, up, dxp, tokens, N, K, epi, dtype, stream);

@@ -141,6 +141,12 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
 // backward of an activation, out = (a W^T) * act'(u), u the saved
 // pre-activation passed as `pre` (read, at the output's offsets; no row swap).
 constexpr int DSP_EPI_GELU_BWD = 5, DSP_EPI_RELU_BWD = 6;
+// DSP_EPI_GELU_KEEP_GRAD: GELU whose `pre` receives GELU'(v), the derivative
+// at the fp32 pre-activation v (rounded to the output dtype), instead of v.
+// DSP_EPI_SCALE_BWD: the backward through such a kept derivative,
+// out = (a W^T) * f with f read from `pre`.  Together they turn the
+// activation's backward epilogue into one multiply.
+constexpr int DSP_EPI_GELU_KEEP_GRAD = 7, DSP_EPI_SCALE_BWD = 8;
 // Whether launch_linear_bf16 runs (M, N) on its large-tile kernel.
 bool linear_bf16_large_tiles(int64_t M, int N);
 // y[c][r] = x[r][c] for a rows x cols bf16 matrix (gemm.hip).

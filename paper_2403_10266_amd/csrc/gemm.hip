@@ -100,11 +100,44 @@ __device__ __forceinline__ float gelu_grad_bf16(float u) {
   return fmaf(0.5f, erf, 0.5f) + u * (0.3989422804014327f * e);
 }
 
-// the activation's derivative at the saved pre-activation u (backward
-// epilogues: the output is the GEMM sum times it)
+// GELU'(v) = Phi(v) + v phi(v) at the fp32 pre-activation, from the same
+// terms as gelu_bf16out (for a forward that keeps the derivative): with
+// q = erfc(|v| / sqrt 2) / 2, Phi(v) is 1 - q for v >= 0 and q for v < 0, and
+// phi(v) = exp(-v^2 / 2) / sqrt(2 pi).
+__device__ __forceinline__ float gelu_grad_fwd(float v) {
+  const float av = fabsf(v);
+  const float t = __builtin_amdgcn_rcpf(fmaf(AS_P * 0.70710678118654752f, av, 1.0f));
+  float poly = fmaf(0.5f * AS_A5, t, 0.5f * AS_A4);
+  poly = fmaf(poly, t, 0.5f * AS_A3);
+  poly = fmaf(poly, t, 0.5f * AS_A2);
+  poly = fmaf(poly, t, 0.5f * AS_A1);
+  const float e = __builtin_amdgcn_exp2f(av * (av * (-0.5f * 1.4426950408889634f)));
+  const float q = (t * poly) * e;
+  return fmaf(v, 0.3989422804014327f * e, v >= 0.0f ? 1.0f - q : q);
+}
+
+// the factor of a backward epilogue (the output is the GEMM sum times it) from
+// the saved value u: the activation's derivative at the pre-activation u, or
+// u itself when the forward kept the derivative
 template <int EPI>
 __device__ __forceinline__ float act_grad(float u) {
+  if constexpr (EPI == DSP_EPI_SCALE_BWD) return u;
   return EPI == DSP_EPI_GELU_BWD ? gelu_grad_bf16(u) : (u > 0.0f ? 1.0f : 0.0f);
+}
+
+template <int EPI>
+constexpr bool epi_is_bwd() {
+  return EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD || EPI == DSP_EPI_SCALE_BWD;
+}
+template <int EPI>
+constexpr bool epi_is_gelu() {
+  return EPI == DSP_EPI_GELU || EPI == DSP_EPI_GELU_KEEP_GRAD;
+}
+// what a keeping forward stores beside the activation
+template <int EPI>
+__device__ __forceinline__ float kept(float v) {
+  if constexpr (EPI == DSP_EPI_GELU_KEEP_GRAD) return gelu_grad_fwd(v);
+  return v;
 }
 
 __device__ __forceinline__ uint2 pack_bf16x4(const float v[4]) {
@@ -129,8 +162,8 @@ __device__ __forceinline__ void epilogue4(float v[4], int m, int64_t om, int n, 
                                           const bf16* __restrict__ bias, const float* resid, void* out,
                                           bf16* keep_out) {
   const bool full = (n + 3 < N) && ((N & 3) == 0);
-  if (EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD) {
-    // keep_out holds the saved pre-activation u, read at the output's offsets
+  if (epi_is_bwd<EPI>()) {
+    // keep_out holds the saved value u, read at the output's offsets
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       if (n + i < N) v[i] *= act_grad<EPI>(bf2f(keep_out[om * N + n + i]));
@@ -143,14 +176,17 @@ __device__ __forceinline__ void epilogue4(float v[4], int m, int64_t om, int n, 
   const int64_t roff = (int64_t)m * N + n;
   const int64_t off = om * N + n;
   if (KEEP) {
+    float k[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) k[i] = kept<EPI>(v[i]);
     if (full) {
-      *reinterpret_cast<uint2*>(keep_out + off) = pack_bf16x4(v);
+      *reinterpret_cast<uint2*>(keep_out + off) = pack_bf16x4(k);
     } else {
       for (int i = 0; i < 4; ++i)
-        if (n + i < N) keep_out[off + i] = (bf16)v[i];
+        if (n + i < N) keep_out[off + i] = (bf16)k[i];
     }
   }
-  if (EPI == DSP_EPI_GELU) {
+  if (epi_is_gelu<EPI>()) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
   }
@@ -449,7 +485,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
   // HR p + [0, HR) of each wave row half), 16-byte chunks of 4 columns, PER
   // chunks per thread and pass.  Four passes where two would hold more
   // residual or pre-activation reads than the registers do.
-  constexpr bool BWD = EPI == DSP_EPI_GELU_BWD || EPI == DSP_EPI_RELU_BWD;
+  constexpr bool BWD = epi_is_bwd<EPI>();
   constexpr bool F32OUT = EPI == DSP_EPI_RESID || EPI == DSP_EPI_F32;
   constexpr int NP = (TN == 4 && (EPI == DSP_EPI_RESID || BWD)) ? 4 : 2;
   constexpr int RPP = BIG_BM / NP, HR = RPP / 2, BPP = TM / NP;
@@ -544,8 +580,13 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
           sum4(bb, j, v);
           const int col = wn * TN * 32 + 32 * (j / 4) + 8 * (j % 4) + 4 * g;
           const int row = wm * TM * 32 + 32 * bb + l32;
-          if (KEEP) *reinterpret_cast<uint2*>(st + (row ^ 64) * SP + col) = pack_bf16x4(v);
-          if (EPI == DSP_EPI_GELU) {
+          if (KEEP) {
+            float k[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) k[i] = kept<EPI>(v[i]);
+            *reinterpret_cast<uint2*>(st + (row ^ 64) * SP + col) = pack_bf16x4(k);
+          }
+          if (epi_is_gelu<EPI>()) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
           }
@@ -611,7 +652,12 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
         if (m >= M || n >= N) continue;
         float v[4] = {s4.x, s4.y, s4.z, s4.w};
         const int64_t orow = (int64_t)orows[tr] * N;
-        if (KEEP) *reinterpret_cast<uint2*>(keep_out + orow + n) = pack_bf16x4(v);
+        if (KEEP) {
+          float k[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) k[i] = kept<EPI>(v[i]);
+          *reinterpret_cast<uint2*>(keep_out + orow + n) = pack_bf16x4(k);
+        }
         if constexpr (BWD) {
           const uint32_t w0 = uv[q][0], w1 = uv[q][1];
           v[0] *= act_grad<EPI>(__uint_as_float(w0 << 16));
@@ -619,7 +665,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_big_kernel(
           v[2] *= act_grad<EPI>(__uint_as_float(w1 << 16));
           v[3] *= act_grad<EPI>(__uint_as_float(w1 & 0xFFFF0000u));
         }
-        if (EPI == DSP_EPI_GELU) {
+        if (epi_is_gelu<EPI>()) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) v[i] = gelu_bf16out(v[i]);
         }
@@ -745,8 +791,8 @@ bool linear_bf16_large_tiles(int64_t M, int N) {
 int launch_linear_bf16(const void* a, const void* w, const void* bias, const float* residual,
                        void* out, int64_t M, int N, int K, int epilogue, hipStream_t s, void* pre, RowSwap rs) {
   if (M == 0) return DSP_OK;
-  // backward epilogues: `pre` is the saved pre-activation, read (not written)
-  const bool bwd = epilogue == DSP_EPI_GELU_BWD || epilogue == DSP_EPI_RELU_BWD;
+  // backward epilogues: `pre` is the saved value, read (not written)
+  const bool bwd = epilogue == DSP_EPI_GELU_BWD || epilogue == DSP_EPI_RELU_BWD || epilogue == DSP_EPI_SCALE_BWD;
   if (bwd && (!pre || rs.outer != 0)) return DSP_ERR_ARG;
   const int64_t n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN;
   const int64_t tiles = n_mt * n_nt;
@@ -754,7 +800,9 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
   if (tiles >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) || (int64_t)BM * K * 2 >= (int64_t(1) << 31))
     return DSP_ERR_SHAPE;
   const bool keep = pre != nullptr && !bwd;
-  if (keep && epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU) return DSP_ERR_ARG;
+  if (keep && epilogue != DSP_EPI_GELU && epilogue != DSP_EPI_RELU && epilogue != DSP_EPI_GELU_KEEP_GRAD)
+    return DSP_ERR_ARG;
+  if (epilogue == DSP_EPI_GELU_KEEP_GRAD && !keep) return DSP_ERR_ARG;
   const bf16* A = static_cast<const bf16*>(a);
   const bf16* Wt = static_cast<const bf16*>(w);
   const bf16* bs = static_cast<const bf16*>(bias);
@@ -790,7 +838,9 @@ int launch_linear_bf16(const void* a, const void* w, const void* bias, const flo
     case DSP_EPI_RELU:
       if (keep) DSP_GEMM_LAUNCH(DSP_EPI_RELU, true); else DSP_GEMM_LAUNCH(DSP_EPI_RELU, false);
       break;
+    case DSP_EPI_GELU_KEEP_GRAD: DSP_GEMM_LAUNCH(DSP_EPI_GELU_KEEP_GRAD, true); break;
     case DSP_EPI_GELU_BWD: DSP_GEMM_LAUNCH(DSP_EPI_GELU_BWD, false); break;
+    case DSP_EPI_SCALE_BWD: DSP_GEMM_LAUNCH(DSP_EPI_SCALE_BWD, false); break;
     case DSP_EPI_RELU_BWD: DSP_GEMM_LAUNCH(DSP_EPI_RELU_BWD, false); break;
     default:
       return DSP_ERR_ARG;
