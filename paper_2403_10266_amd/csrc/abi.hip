@@ -439,9 +439,11 @@ bool block_bwd_ws_layout(int64_t B, int64_t T, int64_t S, int C, int H, int F, i
   ws->delta = off; off += up((size_t)th * 4);
   ws->wg = off;    off += up(wg);
   ws->wg_bytes = wg;
-  // bf16: one weight matrix transposed, for the input gradients on the
+  // bf16: the six weight matrices transposed, for the input gradients on the
   // forward's GEMM
-  ws->wt = off;    off += dtype == DSP_BF16 ? up((size_t)std::max(3 * (int64_t)C, (int64_t)F) * C * es) : 0;
+  ws->wt = off;
+  if (dtype == DSP_BF16)
+    off += 2 * up((size_t)3 * C * C * es) + 2 * up((size_t)C * C * es) + 2 * up((size_t)F * C * es);
   ws->total = off;
   return true;
 }
@@ -1131,17 +1133,47 @@ int dsp_st_block_backward(const float* x_BTSC, const float* dy_BSTC, const dsp_b
   // the upstream fp32 gradient as an operand of the block dtype
   auto operand = [&](const float* d) { return launch_cast(d, 0, dyb, bf, tokens * C, s); };
   // dx = dy W (+ the activation's derivative) for W stored [N][K]: in bf16 at
-  // sizes the forward's large-tile GEMM takes, W is transposed into the
-  // workspace and dx = dy (W^T)^T runs on that GEMM; else the gradient GEMM
+  // sizes the forward's large-tile GEMM takes, dx = dy (W^T)^T runs on that
+  // GEMM with W^T from the workspace; else the gradient GEMM.  The weights
+  // taking the large tiles are transposed first, all in one launch.
+  struct Transposed {
+    const void* w;
+    int N, K;
+    const void* wt;
+  };
+  Transposed tw[6];
+  int n_tw = 0;
+  if (bf) {
+    const void* src[6] = {w->wqkv_s, w->wo_s, w->wqkv_t, w->wo_t, w->w1, w->w2};
+    const int nk[6][2] = {{3 * C, C}, {C, C}, {3 * C, C}, {C, C}, {F, C}, {C, F}};
+    const void* xs[6];
+    void* ys[6];
+    int64_t rows[6], cols[6];
+    size_t off = 0;
+    for (int i = 0; i < 6; ++i) {
+      if (!linear_bf16_large_tiles(tokens, nk[i][1])) continue;
+      void* dst = static_cast<char*>(wt) + off;
+      off += ((size_t)nk[i][0] * nk[i][1] * es + 255) & ~size_t(255);
+      tw[n_tw] = {src[i], nk[i][0], nk[i][1], dst};
+      xs[n_tw] = src[i];
+      ys[n_tw] = dst;
+      rows[n_tw] = nk[i][0];
+      cols[n_tw] = nk[i][1];
+      ++n_tw;
+    }
+    if (n_tw) DSP_TRY(launch_transpose_bf16_batch(xs, ys, rows, cols, n_tw, s));
+  }
   auto bwd_data = [&](const void* dyp, const void* wp, const void* up, void* dxp, int N, int K, int epi) -> int {
     if (bf && linear_bf16_large_tiles(tokens, K)) {
-      const int r = launch_transpose_bf16(wp, wt, N, K, s);
-      if (r != DSP_OK) return r;
+      const void* wtp = nullptr;
+      for (int i = 0; i < n_tw; ++i)
+        if (tw[i].w == wp && tw[i].N == N && tw[i].K == K) wtp = tw[i].wt;
+      if (!wtp) return DSP_ERR_ARG;  // every large-tile weight was transposed above
       const int e = epi == DSP_GRAD_EPI_F32 ? DSP_EPI_F32
                     : epi == DSP_GRAD_EPI_BF16 ? DSP_EPI_NONE
                     : epi == DSP_GRAD_EPI_GELU_BWD ? (kept_grad ? DSP_EPI_SCALE_BWD : DSP_EPI_GELU_BWD)
                                                    : DSP_EPI_RELU_BWD;
-      return launch_linear_bf16(dyp, wt, nullptr, nullptr, dxp, tokens, K, N, e, s, const_cast<void*>(up));
+      return launch_linear_bf16(dyp, wtp, nullptr, nullptr, dxp, tokens, K, N, e, s, const_cast<void*>(up));
     }
     return dsp_linear_bwd_data(dyp, wp, up, dxp, tokens, N, K, epi, dtype, stream);
   };

@@ -149,8 +149,10 @@ constexpr int DSP_EPI_GELU_BWD = 5, DSP_EPI_RELU_BWD = 6;
 constexpr int DSP_EPI_GELU_KEEP_GRAD = 7, DSP_EPI_SCALE_BWD = 8;
 // Whether launch_linear_bf16 runs (M, N) on its large-tile kernel.
 bool linear_bf16_large_tiles(int64_t M, int N);
-// y[c][r] = x[r][c] for a rows x cols bf16 matrix (gemm.hip).
-int launch_transpose_bf16(const void* x, void* y, int64_t rows, int64_t cols, hipStream_t s);
+// y_i[c][r] = x_i[r][c] for n <= 6 bf16 matrices of rows_i x cols_i (multiples
+// of 8, 16-byte aligned), in one launch (gemm.hip).
+int launch_transpose_bf16_batch(const void* const* x, void* const* y, const int64_t* rows, const int64_t* cols,
+                                int n, hipStream_t s);
 int launch_linear_f32(const float* a, const float* w, const float* bias, const float* residual,
                       float* out, int64_t M, int N, int K, int epilogue, hipStream_t s, float* pre = nullptr,
                       RowSwap rs = RowSwap());

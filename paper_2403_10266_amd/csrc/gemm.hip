@@ -754,31 +754,68 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
-// bf16 transpose through a padded 64 x 64 LDS tile: rows of 64 consecutive
-// elements read and written (the weight transposes of the backward)
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ x, uint16_t* y, int R,
-                                                             int C) {
-  __shared__ uint16_t t[64][66];
-  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-    const int r = i / 64, c = i % 64;
-    if (r0 + r < R && c0 + c < C) t[r][c] = x[(int64_t)(r0 + r) * C + c0 + c];
+// bf16 transposes of up to kMaxTranspose matrices in one launch (the weights
+// of the block backward), one 64 x 64 tile per work-group: 16-byte chunks of
+// 8 elements in, through LDS, 16-byte chunks out.  Rows and columns are
+// multiples of 8, so a chunk is either wholly inside a matrix or outside.
+constexpr int kMaxTranspose = 6;
+struct TransposeBatch {
+  const uint16_t* x[kMaxTranspose];
+  uint16_t* y[kMaxTranspose];
+  int rows[kMaxTranspose], cols[kMaxTranspose], col_tiles[kMaxTranspose];
+  int first[kMaxTranspose + 1];  // first tile of each matrix; first[n] = all tiles
+  int n;
+};
+
+__global__ __launch_bounds__(256) void transpose_bf16_batch_kernel(TransposeBatch b) {
+  __shared__ __attribute__((aligned(16))) uint16_t t[64][72];
+  int m = 0;
+  while (m + 1 < b.n && (int)blockIdx.x >= b.first[m + 1]) ++m;
+  const int tile = (int)blockIdx.x - b.first[m];
+  const int R = b.rows[m], C = b.cols[m];
+  const int c0 = (tile % b.col_tiles[m]) * 64, r0 = (tile / b.col_tiles[m]) * 64;
+  const uint16_t* x = b.x[m];
+  uint16_t* y = b.y[m];
+#pragma unroll
+  for (int i = threadIdx.x; i < 512; i += 256) {
+    const int r = i / 8, c = (i % 8) * 8;
+    if (r0 + r < R && c0 + c < C)
+      *reinterpret_cast<u32x4*>(&t[r][c]) = *reinterpret_cast<const u32x4*>(x + (int64_t)(r0 + r) * C + c0 + c);
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-    const int c = i / 64, r = i % 64;
-    if (r0 + r < R && c0 + c < C) y[(int64_t)(c0 + c) * R + r0 + r] = t[r][c];
+#pragma unroll
+  for (int i = threadIdx.x; i < 512; i += 256) {
+    const int c = i / 8, r = (i % 8) * 8;
+    if (c0 + c < C && r0 + r < R) {
+      u32x4 v;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = (uint32_t)t[r + 2 * j][c] | ((uint32_t)t[r + 2 * j + 1][c] << 16);
+      *reinterpret_cast<u32x4*>(y + (int64_t)(c0 + c) * R + r0 + r) = v;
+    }
   }
 }
 
 }  // namespace
 
-int launch_transpose_bf16(const void* x, void* y, int64_t rows, int64_t cols, hipStream_t s) {
-  if (rows == 0 || cols == 0) return DSP_OK;
-  if (rows >= (int64_t(1) << 31) || cols >= (int64_t(1) << 31) || (rows + 63) / 64 >= 65536) return DSP_ERR_SHAPE;
-  const dim3 grid((uint32_t)((cols + 63) / 64), (uint32_t)((rows + 63) / 64));
-  hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, s, static_cast<const uint16_t*>(x),
-                     static_cast<uint16_t*>(y), (int)rows, (int)cols);
+int launch_transpose_bf16_batch(const void* const* x, void* const* y, const int64_t* rows, const int64_t* cols,
+                                int n, hipStream_t s) {
+  if (n < 1 || n > kMaxTranspose) return DSP_ERR_ARG;
+  TransposeBatch b = {};
+  b.n = n;
+  int64_t tiles = 0;
+  for (int i = 0; i < n; ++i) {
+    if (rows[i] < 1 || cols[i] < 1 || rows[i] % 8 || cols[i] % 8 || rows[i] * cols[i] >= (int64_t(1) << 31))
+      return DSP_ERR_SHAPE;
+    b.x[i] = static_cast<const uint16_t*>(x[i]);
+    b.y[i] = static_cast<uint16_t*>(y[i]);
+    b.rows[i] = (int)rows[i];
+    b.cols[i] = (int)cols[i];
+    b.col_tiles[i] = (int)((cols[i] + 63) / 64);
+    b.first[i] = (int)tiles;
+    tiles += ((rows[i] + 63) / 64) * b.col_tiles[i];
+  }
+  b.first[n] = (int)tiles;
+  hipLaunchKernelGGL(transpose_bf16_batch_kernel, dim3((uint32_t)tiles), dim3(256), 0, s, b);
   return last_launch_status();
 }
 
