@@ -97,6 +97,15 @@ def test_block_train_full_width_bf16(torch, flags, T):
     _train_case(torch, w, False, flags)
 
 
+def test_block_train_large_tiles_partial_bf16(torch):
+    """Widths that are not multiples of 64 (C = 864, 12 heads of 72; MLP 3464)
+    on 5120 tokens: the MLP's second weight takes the large-tile input gradient,
+    so its transpose has partial 64 x 64 tiles in both dimensions, and the first
+    GEMM keeps GELU' over a ragged last tile column."""
+    w = synth.Workload("block_ragged", "block", "bf16", B=1, T=20, S=256, C=864, H=12, F=3464, seed=24)
+    _train_case(torch, w, True, 0)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("flags", [0, 1, 4, 5, 12, 13])
 def test_forward_train_output_matches_forward(torch, dtype, flags):
