@@ -15,7 +15,10 @@
 //    vectors.
 //  * Epilogues: none, erf GELU (bf16 out; erf evaluated by Abramowitz-Stegun
 //    7.1.26, abs. error <= 1.5e-7), ReLU (Eq. 5), fp32 output, residual add
-//    (fp32 out, may be in place).
+//    (fp32 out, may be in place); for training, GELU / ReLU that also keep the
+//    pre-activation (or GELU' there), and the activation's backward (the sum
+//    times act'(u), or times a kept GELU').
+//  * A batched bf16 transpose for the block backward's weights.
 // fp32 path: LDS-tiled FMA kernel, 64 x 64 tile, 4 x 4 outputs per thread.
 #include <math.h>
 
